@@ -1,0 +1,162 @@
+/*
+ * CPU oracle for the QUAN hot path -- TEST INFRASTRUCTURE ONLY.
+ *
+ * A plain, slow, obviously correct fp64 reference for what the GPU library
+ * computes.  Only the test suite, the smoke check and the benchmark's CPU
+ * baseline leg load this file; the product path never calls it and shares no
+ * code with it (no headers, tables or helpers in common).
+ *
+ * Paper: "Quaternion Approximate Networks for Enhanced Image Classification
+ * and Oriented Object Detection" (arXiv 2509.05512).
+ *
+ * Logical layouts used here (all row-major, fp64):
+ *   activations  x[n][q][c][h][w]      q in {r=0, i=1, j=2, k=3}
+ *   conv weights w[q][o][c][kh][kw]    the four real kernels W_r, W_i, W_j, W_k
+ *   conv bias    b[q][o]               one quaternion bias per output channel
+ *   IQBN params  gamma[q][c], beta[q][c], mean[q][c], var[q][c]
+ *
+ * Readings of the paper taken here (the paper does not spell these out):
+ *   - the convolution symbol inside eq. 5 is a deep-learning cross-correlation
+ *     (no kernel flip) with zero padding, summed over input channels;
+ *   - the kernel multiplies from the left (W (x) X), as eqs. 5 and 6 write it;
+ *   - IQBN normalises with the biased (population) variance of eq. 11 over the
+ *     batch and both spatial axes, separately for each (component, channel).
+ */
+#include <math.h>
+#include <stddef.h>
+#include <stdint.h>
+
+/* Hamilton product p (x) q, written out term by term as in Section III-A,
+ * eq. 3.  out must not alias p or q. */
+void quan_oracle_hamilton(const double p[4], const double q[4], double out[4])
+{
+    const double pr = p[0], pi = p[1], pj = p[2], pk = p[3];
+    const double qr = q[0], qi = q[1], qj = q[2], qk = q[3];
+    out[0] = pr * qr - pi * qi - pj * qj - pk * qk;
+    out[1] = pr * qi + pi * qr + pj * qk - pk * qj;
+    out[2] = pr * qj - pi * qk + pj * qr + pk * qi;
+    out[3] = pr * qk + pi * qj - pj * qi + pk * qr;
+}
+
+/* Output extent of one spatial axis of a strided, padded, dilated window. */
+int64_t quan_oracle_out_size(int64_t in, int64_t k, int64_t stride, int64_t pad, int64_t dil)
+{
+    return (in + 2 * pad - dil * (k - 1) - 1) / stride + 1;
+}
+
+/* Full quaternion convolution of Section III-B, eq. 5 (equivalently the
+ * Hamilton matrix of eq. 6 applied at every tap):
+ *
+ *   Y[n,o,y,x] = bias[o] + sum_{c,ky,kx} W[o,c,ky,kx] (x) X[n,c,iy,ix]
+ *   iy = y*sh - ph + ky*dh,  ix = x*sw - pw + kx*dw,
+ *
+ * with quaternion-valued W, X, Y and (x) the Hamilton product; taps that fall
+ * outside the image contribute nothing (zero padding).  bias may be NULL. */
+void quan_oracle_qconv2d(const double *x, const double *w, const double *bias, double *y,
+                         int64_t N, int64_t Cin, int64_t H, int64_t W,
+                         int64_t Cout, int64_t KH, int64_t KW,
+                         int64_t sh, int64_t sw, int64_t ph, int64_t pw,
+                         int64_t dh, int64_t dw)
+{
+    const int64_t Ho = quan_oracle_out_size(H, KH, sh, ph, dh);
+    const int64_t Wo = quan_oracle_out_size(W, KW, sw, pw, dw);
+    if (Ho <= 0 || Wo <= 0)
+        return;
+    const int64_t wq = Cout * Cin * KH * KW; /* stride between W_r, W_i, ... */
+    const int64_t xq = Cin * H * W;          /* stride between X_r, X_i, ... */
+
+#pragma omp parallel for collapse(2) schedule(dynamic)
+    for (int64_t n = 0; n < N; ++n) {
+        for (int64_t o = 0; o < Cout; ++o) {
+            for (int64_t oy = 0; oy < Ho; ++oy) {
+                for (int64_t ox = 0; ox < Wo; ++ox) {
+                    double acc[4] = {0.0, 0.0, 0.0, 0.0};
+                    if (bias) {
+                        for (int q = 0; q < 4; ++q)
+                            acc[q] = bias[q * Cout + o];
+                    }
+                    for (int64_t c = 0; c < Cin; ++c) {
+                        for (int64_t ky = 0; ky < KH; ++ky) {
+                            const int64_t iy = oy * sh - ph + ky * dh;
+                            if (iy < 0 || iy >= H)
+                                continue;
+                            for (int64_t kx = 0; kx < KW; ++kx) {
+                                const int64_t ix = ox * sw - pw + kx * dw;
+                                if (ix < 0 || ix >= W)
+                                    continue;
+                                const int64_t widx = ((o * Cin + c) * KH + ky) * KW + kx;
+                                const int64_t xidx = ((n * 4 * Cin + c) * H + iy) * W + ix;
+                                double wv[4], xv[4], prod[4];
+                                for (int q = 0; q < 4; ++q) {
+                                    wv[q] = w[q * wq + widx];
+                                    xv[q] = x[q * xq + xidx];
+                                }
+                                quan_oracle_hamilton(wv, xv, prod);
+                                for (int q = 0; q < 4; ++q)
+                                    acc[q] += prod[q];
+                            }
+                        }
+                    }
+                    for (int q = 0; q < 4; ++q)
+                        y[((n * 4 * Cout + q * Cout + o) * Ho + oy) * Wo + ox] = acc[q];
+                }
+            }
+        }
+    }
+}
+
+/* Independent Quaternion Batch Normalization, Section III-C, eqs. 11 and 12:
+ * for every component q and channel c separately, over the n = N*H*W values
+ * X[:, q, c, :, :],
+ *
+ *   mu     = (1/n) sum x
+ *   sigma2 = (1/n) sum (x - mu)^2                (two passes, biased)
+ *   out    = (x - mu) / sqrt(sigma2 + eps) * gamma[q,c] + beta[q,c]
+ *
+ * followed by a component-wise max(0, .) when relu is non-zero.  mean and var
+ * receive mu and sigma2 (either may be NULL). */
+void quan_oracle_iqbn(const double *x, const double *gamma, const double *beta, double eps,
+                      int relu, double *out, double *mean, double *var,
+                      int64_t N, int64_t C, int64_t H, int64_t W)
+{
+    const int64_t hw = H * W;
+    const double cnt = (double)(N * hw);
+
+#pragma omp parallel for collapse(2) schedule(dynamic)
+    for (int64_t q = 0; q < 4; ++q) {
+        for (int64_t c = 0; c < C; ++c) {
+            double s = 0.0;
+            for (int64_t n = 0; n < N; ++n) {
+                const double *xs = x + (n * 4 * C + q * C + c) * hw;
+                for (int64_t t = 0; t < hw; ++t)
+                    s += xs[t];
+            }
+            const double mu = s / cnt;
+            double ss = 0.0;
+            for (int64_t n = 0; n < N; ++n) {
+                const double *xs = x + (n * 4 * C + q * C + c) * hw;
+                for (int64_t t = 0; t < hw; ++t) {
+                    const double d = xs[t] - mu;
+                    ss += d * d;
+                }
+            }
+            const double sigma2 = ss / cnt;
+            const double inv = 1.0 / sqrt(sigma2 + eps);
+            const double g = gamma[q * C + c], b = beta[q * C + c];
+            for (int64_t n = 0; n < N; ++n) {
+                const double *xs = x + (n * 4 * C + q * C + c) * hw;
+                double *os = out + (n * 4 * C + q * C + c) * hw;
+                for (int64_t t = 0; t < hw; ++t) {
+                    double v = (xs[t] - mu) * inv * g + b;
+                    if (relu && v < 0.0)
+                        v = 0.0;
+                    os[t] = v;
+                }
+            }
+            if (mean)
+                mean[q * C + c] = mu;
+            if (var)
+                var[q * C + c] = sigma2;
+        }
+    }
+}

@@ -1,0 +1,78 @@
+"""Planted mistakes in copies of the CPU oracle must each fail a pin.
+
+Every mutant below is a plausible slip in transcribing the paper (a flipped
+sign or swapped index in eq. 3, the operands of the Hamilton product swapped,
+a wrong padding or dilation term, an unbiased variance, eps outside the square
+root, ...).  Each is compiled from a text substitution of quan_oracle.c into a
+temporary library and run through the pins of oracle_pins.py; the test passes
+only if at least one pin rejects it.  All mutations stay in bounds."""
+import os
+
+import pytest
+
+import oracle
+from oracle import build as obuild
+from oracle_pins import ALL_PINS
+
+SRC = open(obuild.SRC).read()
+
+MUTANTS = [
+    # eq. 3: one sign flipped in each output component
+    ("sign r", "out[0] = pr * qr - pi * qi", "out[0] = pr * qr + pi * qi"),
+    ("sign r2", "- pj * qj - pk * qk", "- pj * qj + pk * qk"),
+    ("sign i", "out[1] = pr * qi + pi * qr", "out[1] = pr * qi - pi * qr"),
+    ("sign i2", "+ pj * qk - pk * qj", "- pj * qk - pk * qj"),
+    ("sign j", "out[2] = pr * qj - pi * qk", "out[2] = pr * qj + pi * qk"),
+    ("sign j2", "+ pj * qr + pk * qi", "+ pj * qr - pk * qi"),
+    ("sign k", "out[3] = pr * qk + pi * qj", "out[3] = pr * qk - pi * qj"),
+    ("sign k2", "- pj * qi + pk * qr", "+ pj * qi + pk * qr"),
+    # eq. 3: a dropped term, a wrong component index
+    ("dropped term", "- pj * qj - pk * qk;", "- pj * qj;"),
+    ("wrong index", "out[1] = pr * qi + pi * qr + pj * qk", "out[1] = pr * qi + pi * qr + pj * qj"),
+    # right instead of left multiplication (X (x) W)
+    ("operands swapped", "quan_oracle_hamilton(wv, xv, prod);", "quan_oracle_hamilton(xv, wv, prod);"),
+    # convolution indexing
+    ("pad sign", "const int64_t iy = oy * sh - ph + ky * dh;", "const int64_t iy = oy * sh + ph + ky * dh;"),
+    ("no dilation", "const int64_t ix = ox * sw - pw + kx * dw;", "const int64_t ix = ox * sw - pw + kx;"),
+    ("stride dropped", "const int64_t iy = oy * sh - ph + ky * dh;", "const int64_t iy = oy - ph + ky * dh;"),
+    ("kernel flipped", "const int64_t widx = ((o * Cin + c) * KH + ky) * KW + kx;",
+     "const int64_t widx = ((o * Cin + c) * KH + (KH - 1 - ky)) * KW + (KW - 1 - kx);"),
+    ("ky/kx swapped", "const int64_t widx = ((o * Cin + c) * KH + ky) * KW + kx;",
+     "const int64_t widx = ((o * Cin + c) * KH + kx) * KW + ky;"),
+    ("output permuted", "y[((n * 4 * Cout + q * Cout + o) * Ho + oy) * Wo + ox]",
+     "y[((n * 4 * Cout + o * 4 + q) * Ho + oy) * Wo + ox]"),
+    ("bias one comp", "acc[q] = bias[q * Cout + o];", "acc[q] = bias[o];"),
+    # IQBN
+    ("unbiased var", "const double sigma2 = ss / cnt;", "const double sigma2 = ss / (cnt - 1.0);"),
+    ("eps outside sqrt", "1.0 / sqrt(sigma2 + eps)", "1.0 / (sqrt(sigma2) + eps)"),
+    ("gamma/beta swapped", "double v = (xs[t] - mu) * inv * g + b;", "double v = (xs[t] - mu) * inv * b + g;"),
+    ("std not var", "1.0 / sqrt(sigma2 + eps)", "1.0 / (sigma2 + eps)"),
+    ("relu inverted", "if (relu && v < 0.0)", "if (relu && v > 0.0)"),
+    ("shared stats across components", "const double *xs = x + (n * 4 * C + q * C + c) * hw;\n                for (int64_t t = 0; t < hw; ++t)\n                    s += xs[t];",
+     "const double *xs = x + (n * 4 * C + 0 * C + c) * hw;\n                for (int64_t t = 0; t < hw; ++t)\n                    s += xs[t];"),
+]
+
+
+@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_mutant_is_caught(tmp_path, name, old, new):
+    assert SRC.count(old) == 1, f"mutation anchor not unique/found: {old!r}"
+    src = tmp_path / "mutant.c"
+    src.write_text(SRC.replace(old, new))
+    lib = obuild.build(str(src), str(tmp_path / "libmutant.so"))
+    orc = oracle.Oracle(lib)
+    failed = []
+    for pin in ALL_PINS:
+        try:
+            pin(orc)
+        except AssertionError:
+            failed.append(pin.__name__)
+            break
+    assert failed, f"mutant '{name}' passed every pin"
+
+
+def test_unmutated_copy_passes(tmp_path):
+    src = tmp_path / "copy.c"
+    src.write_text(SRC)
+    orc = oracle.Oracle(obuild.build(str(src), str(tmp_path / "libcopy.so")))
+    for pin in ALL_PINS:
+        pin(orc)
