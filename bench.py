@@ -1,0 +1,263 @@
+#!/usr/bin/env python3
+"""Benchmark of the QUAN hot path on one MI355X.
+
+One step = one pass of the whole hot path over one batch of a workload: for
+every layer, pack the four real kernels, run the quaternion (Hamilton)
+convolution, then IQBN (+ReLU where the layer has it), each through libquan's
+C ABI on torch's current stream.  Inputs are seeded synthetic tensors already
+resident in HBM when the timed region starts.
+
+Prints ONE JSON line:
+  value        useful convolution TFLOP/s over whole steps (pack + conv + IQBN);
+               useful FLOPs = 2 * N*Ho*Wo * 4Cout * 4Cin * k^2 per layer
+  qconv2d      the convolution kernel alone: TFLOP/s and fraction of the bf16
+               dense MFMA peak (2516.6 TFLOP/s)
+  iqbn         IQBN (stats + finalize + affine): GB/s of algorithmic traffic
+               (two reads + one write of the tensor) and fraction of 8 TB/s
+  roofline     the dominant kernel (the convolution) against its roofline,
+               timed with HIP events on the stream it runs on
+  cpu_baseline the CPU oracle timed on a bounded sample of the same workload
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+MFMA_PEAK_TFLOPS = {"bf16": 2516.6, "fp32": 157.3}
+HBM_PEAK_GBPS = 8000.0
+METRIC = "qconv2d bf16 TFLOP/s + % MFMA peak; IQBN GB/s + % HBM peak"
+DEFAULT_WORKLOAD = "imagenet_stage"
+# Measured HBM-byte counters of the convolution kernel, from the committed
+# rocprofv3 --pmc summaries (profiles/); None until taken for the current kernel.
+CONV_TRAFFIC_BYTES = {}
+
+
+def parse_args():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--no-cpu-baseline", action="store_true",
+                    help="skip the CPU oracle leg (profiling runs)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="target duration of the CPU oracle sample")
+    return ap.parse_args()
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def build_layers(wl, tens, dev, quan, torch):
+    """Device tensors and preallocated outputs for every layer."""
+    layers = []
+    n, h, w = wl.n, wl.h, wl.w
+    x = quan.to_device_layout(tens.x.to(dev))
+    for L, lt, d in zip(wl.layers, tens.layers, wl.layer_dims()):
+        ws = [lt.weight[q].contiguous().to(dev) for q in range(4)]
+        layer = dict(
+            spec=L, dims=d, x=x, w=ws,
+            bias=lt.bias.contiguous().to(dev) if lt.bias is not None else None,
+            gamma=lt.gamma.to(dev), beta=lt.beta.to(dev),
+            packed=torch.empty(quan.quan_qconv2d_packed_bytes(L.c_in, L.c_out, L.k, L.k, x.dtype),
+                               dtype=torch.uint8, device=dev),
+            y=quan.empty_qmap(n, L.c_out, d["ho"], d["wo"], x.dtype, dev),
+            z=quan.empty_qmap(n, L.c_out, d["ho"], d["wo"], x.dtype, dev),
+            mean=torch.empty(4, L.c_out, device=dev), var=torch.empty(4, L.c_out, device=dev),
+        )
+        layers.append(layer)
+        x = layer["z"]
+    return layers
+
+
+def run_step(layers, quan, events=None, eps=1e-5):
+    for li, ly in enumerate(layers):
+        L = ly["spec"]
+        if events is not None:
+            events[li][0].record()
+        quan.quan_qconv2d_pack_weights(*ly["w"], packed=ly["packed"])
+        if events is not None:
+            events[li][1].record()
+        quan.quan_qconv2d_forward_packed(ly["x"], ly["packed"], (L.c_out, L.c_in, L.k, L.k),
+                                         bias=ly["bias"], stride=L.stride, pad=L.pad,
+                                         dilation=L.dilation, out=ly["y"])
+        if events is not None:
+            events[li][2].record()
+        fn = quan.quan_iqbn_relu_forward if L.relu else quan.quan_iqbn_forward
+        fn(ly["y"], ly["gamma"], ly["beta"], eps, out=ly["z"], mean=ly["mean"], var=ly["var"])
+        if events is not None:
+            events[li][3].record()
+
+
+def cpu_baseline(wl, tens, target_s):
+    """The oracle on the first images of the batch (all layers, conv + IQBN),
+    timed on this host's cores.  Returns the oracle's useful-FLOP rate."""
+    import numpy as np
+    import oracle
+    import torch
+
+    def run(n_img):
+        x = tens.x[:n_img].to(torch.float64).numpy()
+        flops = 0
+        t0 = time.perf_counter()
+        for L, lt in zip(wl.layers, tens.layers):
+            w = lt.weight.to(torch.float64).numpy()
+            b = lt.bias.to(torch.float64).numpy() if lt.bias is not None else None
+            y = oracle.qconv2d(x, w, b, L.stride, L.pad, L.dilation)
+            flops += 2 * y.shape[0] * y.shape[3] * y.shape[4] * 4 * L.c_out * 4 * L.c_in * L.k * L.k
+            x, _, _ = oracle.iqbn(y, lt.gamma.double().numpy(), lt.beta.double().numpy(),
+                                  wl.eps, L.relu)
+        return time.perf_counter() - t0, flops
+
+    oracle.default()  # build/load outside the timed region
+    t1, f1 = run(1)
+    n_img = int(max(1, min(wl.n, round(target_s / max(t1, 1e-6)))))
+    if n_img > 1:
+        t, f = run(n_img)
+    else:
+        t, f = t1, f1
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or len(os.sched_getaffinity(0))
+    return {
+        "value": f / t / 1e12,
+        "unit": "TFLOP/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": f"first {n_img} of {wl.n} images through every layer (conv + IQBN), fp64, "
+                  f"{t:.1f} s, {f / 1e9:.2f} GFLOP",
+    }
+
+
+def main():
+    args = parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs on exactly one GPU: the QUAN hot path here is the single-GPU "
+              "kernel pair (quaternion conv + IQBN); multi-GPU data parallelism (one all-reduce "
+              "of IQBN statistics per layer) is not built.  Use --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2509_05512_amd import quan, workloads
+
+    quan.load_library()  # fails loudly if the HIP library is missing
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    wl = workloads.WORKLOADS[args.workload]
+    log(f"[bench] workload {wl.name}: {wl.description}")
+    tens = workloads.generate(wl)
+    layers = build_layers(wl, tens, dev, quan, torch)
+    torch.cuda.synchronize()
+
+    dims = wl.layer_dims()
+    conv_flops = [d["useful_flops"] for d in dims]
+    esz = 2 if wl.dtype == "bf16" else 4
+    iqbn_bytes = [3 * wl.n * d["ho"] * d["wo"] * 4 * L.c_out * esz for d, L in zip(dims, wl.layers)]
+
+    for _ in range(args.warmup):
+        run_step(layers, quan, eps=wl.eps)
+    torch.cuda.synchronize()
+    log(f"[bench] warmup {args.warmup} done; timing {args.steps} steps")
+
+    events = [[[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in layers]
+              for _ in range(args.steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall0 = time.perf_counter()
+    start.record()
+    for s in range(args.steps):
+        run_step(layers, quan, events=events[s], eps=wl.eps)
+    end.record()
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall0
+    total_ms = start.elapsed_time(end)
+    ms_per_step = total_ms / args.steps
+
+    pack_ms = [sum(events[s][li][0].elapsed_time(events[s][li][1]) for s in range(args.steps)) / args.steps
+               for li in range(len(layers))]
+    conv_ms = [sum(events[s][li][1].elapsed_time(events[s][li][2]) for s in range(args.steps)) / args.steps
+               for li in range(len(layers))]
+    iqbn_ms = [sum(events[s][li][2].elapsed_time(events[s][li][3]) for s in range(args.steps)) / args.steps
+               for li in range(len(layers))]
+    log(f"[bench] {args.steps} steps: {ms_per_step:.4f} ms/step (wall {1e3 * t_wall / args.steps:.4f})")
+
+    step_flops = sum(conv_flops)
+    value = step_flops / (ms_per_step * 1e-3) / 1e12
+    conv_tflops = step_flops / (sum(conv_ms) * 1e-3) / 1e12
+    peak = MFMA_PEAK_TFLOPS[wl.dtype]
+    iqbn_gbps = sum(iqbn_bytes) / (sum(iqbn_ms) * 1e-3) / 1e9
+    per_layer = []
+    for li, L in enumerate(wl.layers):
+        per_layer.append({
+            "layer": li, "c_in": L.c_in, "c_out": L.c_out, "k": L.k, "stride": L.stride,
+            "pad": L.pad, "h_out": dims[li]["ho"], "w_out": dims[li]["wo"],
+            "pack_us": round(pack_ms[li] * 1e3, 3),
+            "qconv2d_us": round(conv_ms[li] * 1e3, 3),
+            "qconv2d_tflops": round(conv_flops[li] / (conv_ms[li] * 1e-3) / 1e12, 2),
+            "iqbn_us": round(iqbn_ms[li] * 1e3, 3),
+            "iqbn_gbps": round(iqbn_bytes[li] / (iqbn_ms[li] * 1e-3) / 1e9, 1),
+        })
+    for pl in per_layer:
+        log(f"[bench] layer {pl}")
+
+    traffic = CONV_TRAFFIC_BYTES.get(wl.name)
+    result = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic",
+        "config": {
+            "workload": wl.name, "description": wl.description, "batch": wl.n,
+            "height": wl.h, "width": wl.w,
+            "layers": [{"c_in": L.c_in, "c_out": L.c_out, "k": L.k, "stride": L.stride,
+                        "pad": L.pad, "iqbn_relu": L.relu} for L in wl.layers],
+            "useful_gflop_per_step": round(step_flops / 1e9, 3),
+        },
+        "qconv2d": {
+            "tflops": round(conv_tflops, 2),
+            "frac_mfma_peak": round(conv_tflops / peak, 4),
+            "us_per_step": round(sum(conv_ms) * 1e3, 3),
+            "pack_us_per_step": round(sum(pack_ms) * 1e3, 3),
+        },
+        "iqbn": {
+            "gbps": round(iqbn_gbps, 1),
+            "frac_hbm_peak": round(iqbn_gbps / HBM_PEAK_GBPS, 4),
+            "us_per_step": round(sum(iqbn_ms) * 1e3, 3),
+        },
+        "per_layer": per_layer,
+        "roofline": {
+            "bound": "mfma",
+            "kernel": "qconv2d_igemm",
+            "achieved": round(conv_tflops, 2),
+            "peak": peak,
+            "unit": "TFLOP/s",
+            "frac": round(conv_tflops / peak, 4),
+            "traffic": traffic,
+        },
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] CPU oracle baseline ...")
+        result["cpu_baseline"] = cpu_baseline(wl, tens, args.cpu_seconds)
+        log(f"[bench] cpu baseline {result['cpu_baseline']}")
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,184 @@
+/*
+ * libquan -- the QUAN hot path on AMD Instinct MI355X (gfx950).
+ *
+ * Paper: "Quaternion Approximate Networks for Enhanced Image Classification
+ * and Oriented Object Detection" (arXiv 2509.05512).
+ *
+ * Two operations, each a plain C entry point over device pointers:
+ *   - the quaternion 2-D convolution as a Hamilton product (Section III-B,
+ *     eqs. 5 and 6), and
+ *   - Independent Quaternion Batch Normalization (Section III-C, eqs. 11, 12).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Quaternion components are ordered q = r, i, j, k (0..3).  A quaternion
+ * feature map of C channels has the logical shape [N, 4, C, H, W]; in memory
+ * it is channels-last by component, i.e. the dense array [N][H][W][4][C]: for
+ * each pixel the 4*C reals are contiguous, component-major.  The same tensor
+ * seen by PyTorch is x.permute(0, 3, 4, 1, 2) of a contiguous [N, H, W, 4, C].
+ *
+ * All tensor pointers are device pointers owned by the caller; the library
+ * never frees or retains them.  Activation and output pointers must be 16-byte
+ * aligned; every other pointer must be aligned to its element size.  No tensor
+ * may hold 2^31 or more elements.
+ *
+ * dtype is QUAN_F32 or QUAN_BF16 and applies to activations, weights, bias and
+ * outputs of the convolution and to the IQBN input/output; accumulation is
+ * always fp32, and IQBN's gamma, beta, mean and var are always fp32.
+ *
+ * Every call validates its arguments on the host before it touches the device
+ * and returns QUAN_OK (0) or a negative QUAN_ERR_* code; quan_last_error()
+ * then describes the failure (per thread).  A successful call has only
+ * enqueued its kernels on `stream` (a hipStream_t; NULL is the default
+ * stream): errors raised while they run surface at the next synchronisation.
+ *
+ * The library keeps a small per-(device, stream) workspace (the packed
+ * convolution weights and IQBN partial statistics), allocated with hipMalloc
+ * on first use and grown on demand; quan_release() frees it.  Calls issued to
+ * different streams never share a workspace.
+ */
+#ifndef QUAN_H
+#define QUAN_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define QUAN_API __attribute__((visibility("default")))
+
+enum quan_dtype { QUAN_F32 = 0, QUAN_BF16 = 1 };
+
+enum quan_status {
+    QUAN_OK = 0,
+    QUAN_ERR_NULL = -1,        /* a required pointer is NULL */
+    QUAN_ERR_SHAPE = -2,       /* a size is <= 0, or the output would be empty */
+    QUAN_ERR_DTYPE = -3,       /* dtype is not QUAN_F32 / QUAN_BF16 */
+    QUAN_ERR_ALIGN = -4,       /* a pointer violates its alignment requirement */
+    QUAN_ERR_ALIAS = -5,       /* an output overlaps an input it may not overlap */
+    QUAN_ERR_UNSUPPORTED = -6, /* a size exceeds the library's limits */
+    QUAN_ERR_HIP = -7,         /* the HIP runtime reported an error */
+    QUAN_ERR_NOMEM = -8        /* the workspace could not be allocated */
+};
+
+/*
+ * Quaternion convolution Y = W (x) X + b  (Section III-B, eq. 5; the signed
+ * 4x4 block of eq. 6 at every tap).
+ *
+ * With W = W_r + W_i i + W_j j + W_k k and (x) the Hamilton product of eq. 3
+ * with the kernel on the left, for every image n, output channel o and output
+ * pixel (y, x):
+ *
+ *   Y[n,o,y,x] = b[o] + sum_{c, ky, kx} W[o,c,ky,kx] (x) X[n,c,iy,ix],
+ *   iy = y*stride_h - pad_h + ky*dilation_h,  ix = x*stride_w - pad_w + kx*dilation_w,
+ *
+ * a cross-correlation (no kernel flip) in which taps outside the image read
+ * zero.  Ho = (h + 2*pad_h - dilation_h*(k_h-1) - 1)/stride_h + 1, likewise Wo.
+ *
+ *   x       [n, 4, c_in, h, w] channels-last by component (see above)
+ *   w_r..w_k  the four real kernels, each dense [c_out, c_in, k_h, k_w] (OIHW)
+ *   bias    [4, c_out] (component-major), or NULL for no bias
+ *   out     [n, 4, c_out, Ho, Wo] channels-last by component; written in full.
+ *           It must not overlap x, a kernel or the bias.
+ *   stride, dilation >= 1; pad >= 0; all sizes >= 1.
+ *
+ * bf16 outputs are the fp32 accumulator rounded to nearest even.
+ * Returns QUAN_ERR_SHAPE when Ho or Wo would be < 1.
+ */
+QUAN_API int quan_qconv2d_forward(const void *x,
+                                  const void *w_r, const void *w_i,
+                                  const void *w_j, const void *w_k,
+                                  const void *bias,
+                                  int32_t stride_h, int32_t stride_w,
+                                  int32_t pad_h, int32_t pad_w,
+                                  int32_t dilation_h, int32_t dilation_w,
+                                  void *out,
+                                  int32_t n, int32_t c_in, int32_t h, int32_t w,
+                                  int32_t c_out, int32_t k_h, int32_t k_w,
+                                  int32_t dtype, void *stream);
+
+/*
+ * The same convolution split in two, for callers whose kernels stay fixed
+ * across calls (inference): pack W_r..W_k once, then run the convolution on
+ * the packed weights.  quan_qconv2d_forward is exactly
+ * quan_qconv2d_pack_weights into a library workspace followed by
+ * quan_qconv2d_forward_packed.
+ *
+ * quan_qconv2d_packed_bytes returns the size in bytes of the packed weights
+ * for (c_in, c_out, k_h, k_w, dtype), or a negative QUAN_ERR_* code.  The
+ * packed layout is private to the library but depends only on these five
+ * values: weights packed once serve every later call with the same ones.
+ *
+ * quan_qconv2d_pack_weights reads w_r..w_k (as in quan_qconv2d_forward) and
+ * writes `packed`, a caller-owned, 16-byte-aligned device buffer of at least
+ * quan_qconv2d_packed_bytes(...) bytes (`packed_bytes` states its size) that
+ * must not overlap the kernels.
+ *
+ * quan_qconv2d_forward_packed takes the packed buffer in place of the four
+ * kernels; every other argument is as in quan_qconv2d_forward, and out must
+ * not overlap `packed` either.
+ */
+QUAN_API int64_t quan_qconv2d_packed_bytes(int32_t c_in, int32_t c_out, int32_t k_h, int32_t k_w,
+                                           int32_t dtype);
+
+QUAN_API int quan_qconv2d_pack_weights(const void *w_r, const void *w_i,
+                                       const void *w_j, const void *w_k,
+                                       int32_t c_in, int32_t c_out, int32_t k_h, int32_t k_w,
+                                       int32_t dtype, void *packed, int64_t packed_bytes,
+                                       void *stream);
+
+QUAN_API int quan_qconv2d_forward_packed(const void *x, const void *packed, const void *bias,
+                                         int32_t stride_h, int32_t stride_w,
+                                         int32_t pad_h, int32_t pad_w,
+                                         int32_t dilation_h, int32_t dilation_w,
+                                         void *out,
+                                         int32_t n, int32_t c_in, int32_t h, int32_t w,
+                                         int32_t c_out, int32_t k_h, int32_t k_w,
+                                         int32_t dtype, void *stream);
+
+/*
+ * Independent Quaternion Batch Normalization (Section III-C, eqs. 11, 12).
+ *
+ * For every component q and channel ch separately, over the P = n*h*w values
+ * x[:, q, ch, :, :]:
+ *
+ *   mean[q,ch] = (1/P) sum x
+ *   var[q,ch]  = (1/P) sum (x - mean)^2          (biased, as in eq. 11)
+ *   out = (x - mean) / sqrt(var + eps) * gamma[q,ch] + beta[q,ch]
+ *
+ *   x, out        [n, 4, c, h, w] channels-last by component; out may equal x
+ *                 (in place) but may not otherwise overlap it.
+ *   gamma, beta   [4, c] fp32 device arrays.
+ *   mean, var     [4, c] fp32 device arrays receiving the batch statistics used
+ *                 for normalisation.  Running statistics are the caller's.
+ *   eps           > 0.
+ */
+QUAN_API int quan_iqbn_forward(const void *x, const float *gamma, const float *beta,
+                               float eps, void *out, float *mean, float *var,
+                               int32_t n, int32_t c, int32_t h, int32_t w,
+                               int32_t dtype, void *stream);
+
+/* As quan_iqbn_forward, followed by a component-wise max(0, .) on out (the
+ * IQBN + ReLU pairing of the quaternion networks of Section IV). */
+QUAN_API int quan_iqbn_relu_forward(const void *x, const float *gamma, const float *beta,
+                                    float eps, void *out, float *mean, float *var,
+                                    int32_t n, int32_t c, int32_t h, int32_t w,
+                                    int32_t dtype, void *stream);
+
+/* Message describing the last failure of a quan_* call on this thread
+ * ("" if none).  The pointer stays valid until the next call on the thread. */
+QUAN_API const char *quan_last_error(void);
+
+/* Synchronise every device the library has used and free its workspaces.
+ * Returns QUAN_OK or QUAN_ERR_HIP.  Later calls allocate afresh. */
+QUAN_API int quan_release(void);
+
+/* Library version string. */
+QUAN_API const char *quan_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* QUAN_H */

@@ -1,0 +1,314 @@
+// Independent Quaternion Batch Normalization (Section III-C, eqs. 11 and 12)
+// for gfx950.
+//
+// The tensor is channels-last by component: P = N*H*W rows of L = 4*C reals,
+// and every one of the L columns (component q, channel c) is normalised on
+// its own with its batch mean and biased variance.  Three launches on the
+// caller's stream, no host synchronisation:
+//
+//   1. iqbn_stats     streams x once.  Each thread owns one 16-byte column
+//                     chunk and a strided set of rows and accumulates shifted
+//                     sums  s1 = sum(x - K), s2 = sum((x - K)^2)  in fp32, with
+//                     K the column's value in row 0 (so the variance does not
+//                     cancel when |mean| >> std).  A fixed-order LDS reduction
+//                     gives one (s1, s2) per column per block.
+//   2. iqbn_finalize  merges the per-block partials in fp64, in block order
+//                     (deterministic: no atomics), and writes mean, var and the
+//                     per-column affine  scale = gamma / sqrt(var + eps),
+//                     shift = beta - mean * scale.
+//   3. iqbn_affine    streams x again: out = x * scale + shift, optional ReLU.
+#include <hip/hip_runtime.h>
+
+#include "quan_launch.h"
+
+namespace quan {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kMaxBlocks = 1024;
+constexpr int kFinalizeCols = 16;
+
+template <typename T, int VW>
+struct alignas(sizeof(T) * VW) Vec {
+    T v[VW];
+};
+
+// Thread layout shared by the stats and affine passes.
+struct Layout {
+    int64_t pixels;          // rows
+    int row_len;             // L = 4*C
+    int vw;                  // elements per column chunk
+    int chunks;              // L / vw
+    int cg;                  // chunk columns per block (grid.y splits the rest)
+    int rpi;                 // rows a block advances per iteration
+    int col_groups;          // grid.y
+    int blocks;              // grid.x
+    int64_t rows_per_block;  // contiguous rows of one block
+};
+
+Layout make_layout(int64_t pixels, int c, int vw)
+{
+    Layout l;
+    l.pixels = pixels;
+    l.row_len = 4 * c;
+    l.vw = vw;
+    l.chunks = l.row_len / vw;
+    l.cg = l.chunks < kThreads ? l.chunks : kThreads;
+    l.rpi = kThreads / l.cg;
+    l.col_groups = (l.chunks + l.cg - 1) / l.cg;
+    int64_t want = (pixels + int64_t(l.rpi) * 16 - 1) / (int64_t(l.rpi) * 16);
+    int max_blocks = kMaxBlocks / l.col_groups;
+    if (max_blocks < 1)
+        max_blocks = 1;
+    if (want > max_blocks)
+        want = max_blocks;
+    if (want < 1)
+        want = 1;
+    l.rows_per_block = (pixels + want - 1) / want;
+    l.blocks = int((pixels + l.rows_per_block - 1) / l.rows_per_block);
+    return l;
+}
+
+int vec_width(int c, DType dt)
+{
+    const int epc = dt == DType::BF16 ? 8 : 4;
+    return (4 * c) % epc == 0 ? epc : 1;
+}
+
+template <typename T, int VW>
+__global__ __launch_bounds__(kThreads) void iqbn_stats(const T *__restrict__ x, Layout l,
+                                                       float *__restrict__ part)
+{
+    __shared__ float red[2][kThreads][VW];
+    const int tid = threadIdx.x;
+    const int cl = tid % l.cg;
+    const int rl = tid / l.cg;
+    const int col = blockIdx.y * l.cg + cl;
+    const bool active = rl < l.rpi && col < l.chunks;
+    const int64_t r0 = int64_t(blockIdx.x) * l.rows_per_block;
+    int64_t r1 = r0 + l.rows_per_block;
+    if (r1 > l.pixels)
+        r1 = l.pixels;
+
+    float s1[VW], s2[VW], k[VW];
+#pragma unroll
+    for (int e = 0; e < VW; ++e)
+        s1[e] = s2[e] = k[e] = 0.0f;
+
+    if (active) {
+        const Vec<T, VW> kv = *reinterpret_cast<const Vec<T, VW> *>(x + col * VW);
+#pragma unroll
+        for (int e = 0; e < VW; ++e)
+            k[e] = float(kv.v[e]);
+        const T *base = x + col * VW;
+        const int64_t step = l.rpi;
+        int64_t r = r0 + rl;
+        // Four independent loads in flight per thread.
+        for (; r + 3 * step < r1; r += 4 * step) {
+            Vec<T, VW> v[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                v[u] = *reinterpret_cast<const Vec<T, VW> *>(base + (r + u * step) * l.row_len);
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+#pragma unroll
+                for (int e = 0; e < VW; ++e) {
+                    const float d = float(v[u].v[e]) - k[e];
+                    s1[e] += d;
+                    s2[e] = fmaf(d, d, s2[e]);
+                }
+        }
+        for (; r < r1; r += step) {
+            const Vec<T, VW> v = *reinterpret_cast<const Vec<T, VW> *>(base + r * l.row_len);
+#pragma unroll
+            for (int e = 0; e < VW; ++e) {
+                const float d = float(v.v[e]) - k[e];
+                s1[e] += d;
+                s2[e] = fmaf(d, d, s2[e]);
+            }
+        }
+    }
+#pragma unroll
+    for (int e = 0; e < VW; ++e) {
+        red[0][tid][e] = s1[e];
+        red[1][tid][e] = s2[e];
+    }
+    __syncthreads();
+    if (rl == 0 && col < l.chunks) {
+        float t1[VW], t2[VW];
+#pragma unroll
+        for (int e = 0; e < VW; ++e)
+            t1[e] = t2[e] = 0.0f;
+        for (int j = 0; j < l.rpi; ++j) {
+#pragma unroll
+            for (int e = 0; e < VW; ++e) {
+                t1[e] += red[0][j * l.cg + cl][e];
+                t2[e] += red[1][j * l.cg + cl][e];
+            }
+        }
+        float *p1 = part + (size_t(blockIdx.x) * 2) * l.row_len + col * VW;
+        float *p2 = p1 + l.row_len;
+#pragma unroll
+        for (int e = 0; e < VW; ++e) {
+            p1[e] = t1[e];
+            p2[e] = t2[e];
+        }
+    }
+}
+
+template <typename T>
+__global__ __launch_bounds__(kThreads) void iqbn_finalize(const T *__restrict__ x, Layout l,
+                                                          const float *__restrict__ part,
+                                                          const float *__restrict__ gamma,
+                                                          const float *__restrict__ beta, float eps,
+                                                          float *__restrict__ mean, float *__restrict__ var,
+                                                          float *__restrict__ affine)
+{
+    __shared__ double red[2][kThreads];
+    const int tid = threadIdx.x;
+    const int cl = tid % kFinalizeCols;
+    const int gl = tid / kFinalizeCols;
+    const int col = blockIdx.x * kFinalizeCols + cl;
+    double s1 = 0.0, s2 = 0.0;
+    if (col < l.row_len) {
+        for (int b = gl; b < l.blocks; b += kThreads / kFinalizeCols) {
+            const float *p = part + size_t(b) * 2 * l.row_len + col;
+            s1 += double(p[0]);
+            s2 += double(p[l.row_len]);
+        }
+    }
+    red[0][tid] = s1;
+    red[1][tid] = s2;
+    __syncthreads();
+    if (gl == 0 && col < l.row_len) {
+        double t1 = 0.0, t2 = 0.0;
+        for (int j = 0; j < kThreads / kFinalizeCols; ++j) {
+            t1 += red[0][j * kFinalizeCols + cl];
+            t2 += red[1][j * kFinalizeCols + cl];
+        }
+        const double n = double(l.pixels);
+        const double d = t1 / n;          // mean - K
+        double v = t2 / n - d * d;        // biased variance
+        if (v < 0.0)
+            v = 0.0;
+        const double mu = double(float(x[col])) + d;
+        const double sc = double(gamma[col]) / sqrt(v + double(eps));
+        mean[col] = float(mu);
+        var[col] = float(v);
+        affine[col] = float(sc);
+        affine[l.row_len + col] = float(double(beta[col]) - mu * sc);
+    }
+}
+
+template <typename T, int VW, bool RELU>
+__global__ __launch_bounds__(kThreads) void iqbn_affine(const T *x, T *out, Layout l,
+                                                        const float *__restrict__ affine)
+{
+    const int tid = threadIdx.x;
+    const int cl = tid % l.cg;
+    const int rl = tid / l.cg;
+    const int col = blockIdx.y * l.cg + cl;
+    if (rl >= l.rpi || col >= l.chunks)
+        return;
+    float sc[VW], sh[VW];
+#pragma unroll
+    for (int e = 0; e < VW; ++e) {
+        sc[e] = affine[col * VW + e];
+        sh[e] = affine[l.row_len + col * VW + e];
+    }
+    const int64_t r0 = int64_t(blockIdx.x) * l.rows_per_block;
+    int64_t r1 = r0 + l.rows_per_block;
+    if (r1 > l.pixels)
+        r1 = l.pixels;
+    const int64_t step = l.rpi;
+    const T *src = x + col * VW;
+    T *dst = out + col * VW;
+    int64_t r = r0 + rl;
+    for (; r + 3 * step < r1; r += 4 * step) {
+        Vec<T, VW> v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            v[u] = *reinterpret_cast<const Vec<T, VW> *>(src + (r + u * step) * l.row_len);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            Vec<T, VW> o;
+#pragma unroll
+            for (int e = 0; e < VW; ++e) {
+                float y = fmaf(float(v[u].v[e]), sc[e], sh[e]);
+                if (RELU)
+                    y = fmaxf(y, 0.0f);
+                o.v[e] = T(y);
+            }
+            *reinterpret_cast<Vec<T, VW> *>(dst + (r + u * step) * l.row_len) = o;
+        }
+    }
+    for (; r < r1; r += step) {
+        const Vec<T, VW> v = *reinterpret_cast<const Vec<T, VW> *>(src + r * l.row_len);
+        Vec<T, VW> o;
+#pragma unroll
+        for (int e = 0; e < VW; ++e) {
+            float y = fmaf(float(v.v[e]), sc[e], sh[e]);
+            if (RELU)
+                y = fmaxf(y, 0.0f);
+            o.v[e] = T(y);
+        }
+        *reinterpret_cast<Vec<T, VW> *>(dst + r * l.row_len) = o;
+    }
+}
+
+template <typename T, int VW>
+hipError_t launch_all(const void *x, const float *gamma, const float *beta, float eps, bool relu,
+                      void *out, float *mean, float *var, int64_t pixels, int c, void *work,
+                      hipStream_t stream)
+{
+    const Layout l = make_layout(pixels, c, VW);
+    float *part = static_cast<float *>(work);
+    float *affine = part + size_t(l.blocks) * 2 * l.row_len;
+    const T *xt = static_cast<const T *>(x);
+    const dim3 grid(l.blocks, l.col_groups);
+    hipLaunchKernelGGL((iqbn_stats<T, VW>), grid, dim3(kThreads), 0, stream, xt, l, part);
+    const int fin_blocks = (l.row_len + kFinalizeCols - 1) / kFinalizeCols;
+    hipLaunchKernelGGL((iqbn_finalize<T>), dim3(fin_blocks), dim3(kThreads), 0, stream, xt, l, part,
+                       gamma, beta, eps, mean, var, affine);
+    if (relu)
+        hipLaunchKernelGGL((iqbn_affine<T, VW, true>), grid, dim3(kThreads), 0, stream, xt,
+                           static_cast<T *>(out), l, (const float *)affine);
+    else
+        hipLaunchKernelGGL((iqbn_affine<T, VW, false>), grid, dim3(kThreads), 0, stream, xt,
+                           static_cast<T *>(out), l, (const float *)affine);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+size_t iqbn_workspace_bytes(int64_t pixels, int c)
+{
+    // Largest over the vector widths the dispatcher may pick.
+    size_t best = 0;
+    for (int vw : {1, 4, 8}) {
+        if ((4 * c) % vw)
+            continue;
+        const Layout l = make_layout(pixels, c, vw);
+        const size_t b = (size_t(l.blocks) * 2 + 2) * size_t(l.row_len) * sizeof(float);
+        if (b > best)
+            best = b;
+    }
+    return best;
+}
+
+hipError_t iqbn_run(const void *x, const float *gamma, const float *beta, float eps, bool relu,
+                    void *out, float *mean, float *var, int64_t pixels, int c, DType dt, void *work,
+                    hipStream_t stream)
+{
+    const int vw = vec_width(c, dt);
+    if (dt == DType::BF16) {
+        if (vw == 8)
+            return launch_all<__bf16, 8>(x, gamma, beta, eps, relu, out, mean, var, pixels, c, work, stream);
+        return launch_all<__bf16, 1>(x, gamma, beta, eps, relu, out, mean, var, pixels, c, work, stream);
+    }
+    if (vw == 4)
+        return launch_all<float, 4>(x, gamma, beta, eps, relu, out, mean, var, pixels, c, work, stream);
+    return launch_all<float, 1>(x, gamma, beta, eps, relu, out, mean, var, pixels, c, work, stream);
+}
+
+}  // namespace quan

@@ -1,0 +1,384 @@
+// C ABI of libquan: argument validation, workspace management and dispatch.
+//
+// Every entry point validates all of its arguments on the host before the
+// first HIP call, so a rejected call never touches the device.  Kernels run
+// asynchronously on the caller's stream.
+#include <hip/hip_runtime_api.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <utility>
+
+#include "../../include/quan.h"
+#include "quan_launch.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const char *fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return code;
+}
+
+int fail_hip(hipError_t e, const char *what)
+{
+    return fail(QUAN_ERR_HIP, "%s: %s (%d)", what, hipGetErrorString(e), int(e));
+}
+
+// Library-owned device memory, one buffer per (device, stream, purpose), so
+// that calls on different streams never race on a shared scratch buffer.
+struct Workspace {
+    void *ptr = nullptr;
+    size_t bytes = 0;
+};
+
+std::mutex g_ws_mutex;
+std::map<std::pair<int, std::pair<void *, int>>, Workspace> g_ws;
+
+enum Purpose { kWeightPack = 0, kIqbnPartials = 1 };
+
+// Returns a device buffer of at least `bytes` for (current device, stream,
+// purpose).  Growing it first waits for the device to finish with the old one.
+int workspace(void *stream, Purpose purpose, size_t bytes, void **out)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return fail_hip(e, "hipGetDevice");
+    std::lock_guard<std::mutex> lock(g_ws_mutex);
+    Workspace &ws = g_ws[{dev, {stream, int(purpose)}}];
+    if (ws.bytes < bytes) {
+        if (ws.ptr) {
+            e = hipDeviceSynchronize();
+            if (e != hipSuccess)
+                return fail_hip(e, "hipDeviceSynchronize");
+            e = hipFree(ws.ptr);
+            ws.ptr = nullptr;
+            ws.bytes = 0;
+            if (e != hipSuccess)
+                return fail_hip(e, "hipFree");
+        }
+        size_t want = bytes + bytes / 4;  // headroom for slightly larger calls
+        want = (want + 4095) & ~size_t(4095);
+        e = hipMalloc(&ws.ptr, want);
+        if (e != hipSuccess) {
+            ws.ptr = nullptr;
+            return fail(QUAN_ERR_NOMEM, "hipMalloc(%zu) for workspace: %s", want, hipGetErrorString(e));
+        }
+        ws.bytes = want;
+    }
+    *out = ws.ptr;
+    return QUAN_OK;
+}
+
+constexpr int64_t kMaxElems = (int64_t(1) << 31) - 1;
+
+bool misaligned(const void *p, size_t a)
+{
+    return (reinterpret_cast<uintptr_t>(p) % a) != 0;
+}
+
+bool overlaps(const void *a, size_t abytes, const void *b, size_t bbytes)
+{
+    const uintptr_t a0 = reinterpret_cast<uintptr_t>(a), b0 = reinterpret_cast<uintptr_t>(b);
+    return a0 < b0 + bbytes && b0 < a0 + abytes;
+}
+
+size_t elem_size(int32_t dtype)
+{
+    return dtype == QUAN_BF16 ? 2 : 4;
+}
+
+int check_dtype(int32_t dtype)
+{
+    if (dtype != QUAN_F32 && dtype != QUAN_BF16)
+        return fail(QUAN_ERR_DTYPE, "dtype %d is neither QUAN_F32 (0) nor QUAN_BF16 (1)", dtype);
+    return QUAN_OK;
+}
+
+quan::DType to_dt(int32_t dtype)
+{
+    return dtype == QUAN_BF16 ? quan::DType::BF16 : quan::DType::F32;
+}
+
+// Validation shared by the two convolution entry points (everything except
+// the weights): sizes, output extent, limits, alignment of x/out/bias and
+// overlap of out with x and the bias.  Fills the geometry on success.
+int check_conv(const void *x, const void *bias, int32_t stride_h, int32_t stride_w, int32_t pad_h,
+               int32_t pad_w, int32_t dilation_h, int32_t dilation_w, const void *out, int32_t n,
+               int32_t c_in, int32_t h, int32_t w, int32_t c_out, int32_t k_h, int32_t k_w,
+               int32_t dtype, quan::ConvGeom *g, size_t *xb, size_t *ob)
+{
+    if (int rc = check_dtype(dtype))
+        return rc;
+    if (n < 1 || c_in < 1 || h < 1 || w < 1 || c_out < 1 || k_h < 1 || k_w < 1)
+        return fail(QUAN_ERR_SHAPE,
+                    "qconv2d: sizes must be >= 1 (n=%d c_in=%d h=%d w=%d c_out=%d k=%dx%d)", n, c_in,
+                    h, w, c_out, k_h, k_w);
+    if (stride_h < 1 || stride_w < 1 || dilation_h < 1 || dilation_w < 1 || pad_h < 0 || pad_w < 0)
+        return fail(QUAN_ERR_SHAPE, "qconv2d: stride/dilation must be >= 1 and pad >= 0");
+    const int64_t span_h = int64_t(h) + 2 * int64_t(pad_h) - int64_t(dilation_h) * (k_h - 1) - 1;
+    const int64_t span_w = int64_t(w) + 2 * int64_t(pad_w) - int64_t(dilation_w) * (k_w - 1) - 1;
+    if (span_h < 0 || span_w < 0)
+        return fail(QUAN_ERR_SHAPE, "qconv2d: empty output (kernel span exceeds padded input)");
+    const int64_t ho = span_h / stride_h + 1, wo = span_w / stride_w + 1;
+    const int64_t x_elems = int64_t(n) * h * w * 4 * c_in;
+    const int64_t o_elems = int64_t(n) * ho * wo * 4 * c_out;
+    const int64_t w_elems = int64_t(c_out) * c_in * k_h * k_w;
+    if (x_elems > kMaxElems || o_elems > kMaxElems || w_elems * 4 * 4 > kMaxElems)
+        return fail(QUAN_ERR_UNSUPPORTED, "qconv2d: a tensor exceeds 2^31-1 elements");
+    const size_t es = elem_size(dtype);
+    if (misaligned(x, 16) || misaligned(out, 16))
+        return fail(QUAN_ERR_ALIGN, "qconv2d: x and out must be 16-byte aligned");
+    if (bias && misaligned(bias, es))
+        return fail(QUAN_ERR_ALIGN, "qconv2d: weights and bias must be aligned to their element size");
+    *xb = size_t(x_elems) * es;
+    *ob = size_t(o_elems) * es;
+    if (overlaps(out, *ob, x, *xb) || (bias && overlaps(out, *ob, bias, size_t(4) * c_out * es)))
+        return fail(QUAN_ERR_ALIAS, "qconv2d: out overlaps x, a kernel or the bias");
+    g->n = n;
+    g->c_in = c_in;
+    g->h = h;
+    g->w = w;
+    g->c_out = c_out;
+    g->k_h = k_h;
+    g->k_w = k_w;
+    g->s_h = stride_h;
+    g->s_w = stride_w;
+    g->p_h = pad_h;
+    g->p_w = pad_w;
+    g->d_h = dilation_h;
+    g->d_w = dilation_w;
+    g->h_out = int(ho);
+    g->w_out = int(wo);
+    return QUAN_OK;
+}
+
+int iqbn_common(const void *x, const float *gamma, const float *beta, float eps, void *out,
+                float *mean, float *var, int32_t n, int32_t c, int32_t h, int32_t w, int32_t dtype,
+                void *stream, bool relu)
+{
+    g_last_error.clear();
+    if (!x || !gamma || !beta || !out || !mean || !var)
+        return fail(QUAN_ERR_NULL, "iqbn: x, gamma, beta, out, mean and var must be non-NULL");
+    if (int rc = check_dtype(dtype))
+        return rc;
+    if (n < 1 || c < 1 || h < 1 || w < 1)
+        return fail(QUAN_ERR_SHAPE, "iqbn: sizes must be >= 1 (n=%d c=%d h=%d w=%d)", n, c, h, w);
+    if (!(eps > 0.0f) || eps != eps)
+        return fail(QUAN_ERR_SHAPE, "iqbn: eps must be > 0 (got %g)", double(eps));
+    const int64_t pixels = int64_t(n) * h * w;
+    const int64_t elems = pixels * 4 * c;
+    if (elems > kMaxElems)
+        return fail(QUAN_ERR_UNSUPPORTED, "iqbn: tensor of %lld elements exceeds 2^31-1",
+                    (long long)elems);
+    const size_t es = elem_size(dtype);
+    if (misaligned(x, 16) || misaligned(out, 16))
+        return fail(QUAN_ERR_ALIGN, "iqbn: x and out must be 16-byte aligned");
+    if (misaligned(gamma, 4) || misaligned(beta, 4) || misaligned(mean, 4) || misaligned(var, 4))
+        return fail(QUAN_ERR_ALIGN, "iqbn: gamma, beta, mean and var must be 4-byte aligned");
+    const size_t xbytes = size_t(elems) * es, sbytes = size_t(4) * c * sizeof(float);
+    if (out != x && overlaps(out, xbytes, x, xbytes))
+        return fail(QUAN_ERR_ALIAS, "iqbn: out partially overlaps x (only out == x is allowed)");
+    if (overlaps(mean, sbytes, var, sbytes) || overlaps(mean, sbytes, x, xbytes) ||
+        overlaps(var, sbytes, x, xbytes) || overlaps(mean, sbytes, out, xbytes) ||
+        overlaps(var, sbytes, out, xbytes))
+        return fail(QUAN_ERR_ALIAS, "iqbn: mean/var overlap each other or a tensor");
+
+    const quan::DType dt = to_dt(dtype);
+    void *work = nullptr;
+    if (int rc = workspace(stream, kIqbnPartials, quan::iqbn_workspace_bytes(pixels, c), &work))
+        return rc;
+    hipError_t e = quan::iqbn_run(x, gamma, beta, eps, relu, out, mean, var, pixels, c, dt, work,
+                                  static_cast<hipStream_t>(stream));
+    if (e != hipSuccess)
+        return fail_hip(e, "iqbn launch");
+    return QUAN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+QUAN_API int64_t quan_qconv2d_packed_bytes(int32_t c_in, int32_t c_out, int32_t k_h, int32_t k_w,
+                                           int32_t dtype)
+{
+    g_last_error.clear();
+    if (int rc = check_dtype(dtype))
+        return rc;
+    if (c_in < 1 || c_out < 1 || k_h < 1 || k_w < 1)
+        return fail(QUAN_ERR_SHAPE, "qconv2d_packed_bytes: sizes must be >= 1");
+    const quan::PackGeom pg = quan::qconv2d_pack_geom(c_in, c_out, k_h, k_w, to_dt(dtype));
+    if (pg.bytes / elem_size(dtype) > size_t(kMaxElems))
+        return fail(QUAN_ERR_UNSUPPORTED, "qconv2d: packed weights exceed 2^31-1 elements");
+    return int64_t(pg.bytes);
+}
+
+QUAN_API int quan_qconv2d_pack_weights(const void *w_r, const void *w_i, const void *w_j,
+                                       const void *w_k, int32_t c_in, int32_t c_out, int32_t k_h,
+                                       int32_t k_w, int32_t dtype, void *packed,
+                                       int64_t packed_bytes, void *stream)
+{
+    g_last_error.clear();
+    if (!w_r || !w_i || !w_j || !w_k || !packed)
+        return fail(QUAN_ERR_NULL, "qconv2d_pack_weights: w_r..w_k and packed must be non-NULL");
+    const int64_t need = quan_qconv2d_packed_bytes(c_in, c_out, k_h, k_w, dtype);
+    if (need < 0)
+        return int(need);
+    if (packed_bytes < need)
+        return fail(QUAN_ERR_SHAPE, "qconv2d_pack_weights: packed holds %lld bytes, needs %lld",
+                    (long long)packed_bytes, (long long)need);
+    const size_t es = elem_size(dtype);
+    if (misaligned(packed, 16))
+        return fail(QUAN_ERR_ALIGN, "qconv2d_pack_weights: packed must be 16-byte aligned");
+    if (misaligned(w_r, es) || misaligned(w_i, es) || misaligned(w_j, es) || misaligned(w_k, es))
+        return fail(QUAN_ERR_ALIGN, "qconv2d_pack_weights: kernels must be aligned to their element size");
+    const size_t wb = size_t(c_out) * c_in * k_h * k_w * es;
+    if (overlaps(packed, size_t(need), w_r, wb) || overlaps(packed, size_t(need), w_i, wb) ||
+        overlaps(packed, size_t(need), w_j, wb) || overlaps(packed, size_t(need), w_k, wb))
+        return fail(QUAN_ERR_ALIAS, "qconv2d_pack_weights: packed overlaps a kernel");
+    const quan::PackGeom pg = quan::qconv2d_pack_geom(c_in, c_out, k_h, k_w, to_dt(dtype));
+    hipError_t e = quan::qconv2d_pack_weights(pg, c_in, c_out, k_h, k_w, to_dt(dtype), w_r, w_i,
+                                              w_j, w_k, packed, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess)
+        return fail_hip(e, "qconv2d weight pack launch");
+    return QUAN_OK;
+}
+
+QUAN_API int quan_qconv2d_forward_packed(const void *x, const void *packed, const void *bias,
+                                         int32_t stride_h, int32_t stride_w, int32_t pad_h,
+                                         int32_t pad_w, int32_t dilation_h, int32_t dilation_w,
+                                         void *out, int32_t n, int32_t c_in, int32_t h, int32_t w,
+                                         int32_t c_out, int32_t k_h, int32_t k_w, int32_t dtype,
+                                         void *stream)
+{
+    g_last_error.clear();
+    if (!x || !packed || !out)
+        return fail(QUAN_ERR_NULL, "qconv2d_forward_packed: x, packed and out must be non-NULL");
+    quan::ConvGeom g;
+    size_t xb = 0, ob = 0;
+    if (int rc = check_conv(x, bias, stride_h, stride_w, pad_h, pad_w, dilation_h, dilation_w, out,
+                            n, c_in, h, w, c_out, k_h, k_w, dtype, &g, &xb, &ob))
+        return rc;
+    const int64_t need = quan_qconv2d_packed_bytes(c_in, c_out, k_h, k_w, dtype);
+    if (need < 0)
+        return int(need);
+    if (misaligned(packed, 16))
+        return fail(QUAN_ERR_ALIGN, "qconv2d_forward_packed: packed must be 16-byte aligned");
+    if (overlaps(out, ob, packed, size_t(need)))
+        return fail(QUAN_ERR_ALIAS, "qconv2d_forward_packed: out overlaps the packed weights");
+    const quan::DType dt = to_dt(dtype);
+    const quan::PackGeom pg = quan::qconv2d_pack_geom(c_in, c_out, k_h, k_w, dt);
+    const quan::ConvPlan plan = quan::qconv2d_plan(g, dt);
+    hipError_t e = quan::qconv2d_run(plan, pg, g, dt, x, packed, bias, out,
+                                     static_cast<hipStream_t>(stream));
+    if (e != hipSuccess)
+        return fail_hip(e, "qconv2d launch");
+    return QUAN_OK;
+}
+
+QUAN_API int quan_qconv2d_forward(const void *x, const void *w_r, const void *w_i, const void *w_j,
+                                  const void *w_k, const void *bias, int32_t stride_h,
+                                  int32_t stride_w, int32_t pad_h, int32_t pad_w, int32_t dilation_h,
+                                  int32_t dilation_w, void *out, int32_t n, int32_t c_in, int32_t h,
+                                  int32_t w, int32_t c_out, int32_t k_h, int32_t k_w, int32_t dtype,
+                                  void *stream)
+{
+    g_last_error.clear();
+    if (!x || !w_r || !w_i || !w_j || !w_k || !out)
+        return fail(QUAN_ERR_NULL, "qconv2d: x, w_r, w_i, w_j, w_k and out must be non-NULL");
+    quan::ConvGeom g;
+    size_t xb = 0, ob = 0;
+    if (int rc = check_conv(x, bias, stride_h, stride_w, pad_h, pad_w, dilation_h, dilation_w, out,
+                            n, c_in, h, w, c_out, k_h, k_w, dtype, &g, &xb, &ob))
+        return rc;
+    const size_t es = elem_size(dtype);
+    if (misaligned(w_r, es) || misaligned(w_i, es) || misaligned(w_j, es) || misaligned(w_k, es))
+        return fail(QUAN_ERR_ALIGN, "qconv2d: weights and bias must be aligned to their element size");
+    const size_t wb = size_t(c_out) * c_in * k_h * k_w * es;
+    if (overlaps(out, ob, w_r, wb) || overlaps(out, ob, w_i, wb) || overlaps(out, ob, w_j, wb) ||
+        overlaps(out, ob, w_k, wb))
+        return fail(QUAN_ERR_ALIAS, "qconv2d: out overlaps x, a kernel or the bias");
+    const int64_t need = quan_qconv2d_packed_bytes(c_in, c_out, k_h, k_w, dtype);
+    if (need < 0)
+        return int(need);
+
+    void *wpack = nullptr;
+    if (int rc = workspace(stream, kWeightPack, size_t(need), &wpack))
+        return rc;
+    const quan::DType dt = to_dt(dtype);
+    const quan::PackGeom pg = quan::qconv2d_pack_geom(c_in, c_out, k_h, k_w, dt);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = quan::qconv2d_pack_weights(pg, c_in, c_out, k_h, k_w, dt, w_r, w_i, w_j, w_k,
+                                              wpack, s);
+    if (e != hipSuccess)
+        return fail_hip(e, "qconv2d weight pack launch");
+    e = quan::qconv2d_run(quan::qconv2d_plan(g, dt), pg, g, dt, x, wpack, bias, out, s);
+    if (e != hipSuccess)
+        return fail_hip(e, "qconv2d launch");
+    return QUAN_OK;
+}
+
+QUAN_API int quan_iqbn_forward(const void *x, const float *gamma, const float *beta, float eps,
+                               void *out, float *mean, float *var, int32_t n, int32_t c, int32_t h,
+                               int32_t w, int32_t dtype, void *stream)
+{
+    return iqbn_common(x, gamma, beta, eps, out, mean, var, n, c, h, w, dtype, stream, false);
+}
+
+QUAN_API int quan_iqbn_relu_forward(const void *x, const float *gamma, const float *beta, float eps,
+                                    void *out, float *mean, float *var, int32_t n, int32_t c,
+                                    int32_t h, int32_t w, int32_t dtype, void *stream)
+{
+    return iqbn_common(x, gamma, beta, eps, out, mean, var, n, c, h, w, dtype, stream, true);
+}
+
+QUAN_API const char *quan_last_error(void)
+{
+    return g_last_error.c_str();
+}
+
+QUAN_API int quan_release(void)
+{
+    std::lock_guard<std::mutex> lock(g_ws_mutex);
+    int rc = QUAN_OK;
+    int saved = -1;
+    if (hipGetDevice(&saved) != hipSuccess)
+        saved = -1;
+    for (auto &kv : g_ws) {
+        Workspace &ws = kv.second;
+        if (!ws.ptr)
+            continue;
+        hipError_t e = hipSetDevice(kv.first.first);
+        if (e == hipSuccess)
+            e = hipDeviceSynchronize();
+        if (e == hipSuccess)
+            e = hipFree(ws.ptr);
+        if (e != hipSuccess && rc == QUAN_OK)
+            rc = fail_hip(e, "quan_release");
+        ws.ptr = nullptr;
+        ws.bytes = 0;
+    }
+    g_ws.clear();
+    if (saved >= 0 && hipSetDevice(saved) != hipSuccess && rc == QUAN_OK)
+        rc = fail(QUAN_ERR_HIP, "quan_release: hipSetDevice failed");
+    return rc;
+}
+
+QUAN_API const char *quan_version(void)
+{
+    return "libquan 0.1 (gfx950)";
+}
+
+}  // extern "C"

@@ -1,0 +1,62 @@
+// Internal launch interface between the C ABI (quan_api.cpp) and the HIP
+// kernels.  Host-only declarations; every argument has been validated by the
+// caller before one of these runs.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace quan {
+
+enum class DType : int { F32 = 0, BF16 = 1 };
+
+// Geometry of one quaternion convolution (quaternion channel counts).
+struct ConvGeom {
+    int n, c_in, h, w, c_out, k_h, k_w;
+    int s_h, s_w, p_h, p_w, d_h, d_w;
+    int h_out, w_out;
+    int64_t m() const { return int64_t(n) * h_out * w_out; }
+};
+
+// Layout of the packed weights: [tap][cblk][kernel r,i,j,k][cout_pad][pk]
+// with pk input channels per block.  It depends only on (dtype, c_in, c_out,
+// k_h, k_w), never on the tile configuration, so weights packed once serve
+// every later call.
+struct PackGeom {
+    int pk;        // input channels per block (16 bf16, 8 fp32)
+    int n_cblk;    // ceil(c_in / pk)
+    int cout_pad;  // c_out rounded up to kPackCoutAlign
+    size_t bytes;
+};
+constexpr int kPackCoutAlign = 64;
+PackGeom qconv2d_pack_geom(int c_in, int c_out, int k_h, int k_w, DType dt);
+
+// Tile configuration chosen for a convolution.
+struct ConvPlan {
+    int id;              // index into the kernel table
+    int bm, bnc;         // output pixels, output channels per component
+    int m_tiles, n_tiles;
+    const char *name;
+};
+
+// Pick a tile configuration for the convolution.
+ConvPlan qconv2d_plan(const ConvGeom &g, DType dt);
+
+// Pack W_r..W_k (OIHW) into the PackGeom layout, zero padded.
+hipError_t qconv2d_pack_weights(const PackGeom &pg, int c_in, int c_out, int k_h, int k_w, DType dt,
+                                const void *w_r, const void *w_i, const void *w_j,
+                                const void *w_k, void *wpack, hipStream_t stream);
+
+// The implicit-GEMM Hamilton convolution.
+hipError_t qconv2d_run(const ConvPlan &plan, const PackGeom &pg, const ConvGeom &g, DType dt,
+                       const void *x, const void *wpack, const void *bias, void *out,
+                       hipStream_t stream);
+
+// IQBN.  `work` must hold iqbn_workspace_bytes(...) bytes.
+size_t iqbn_workspace_bytes(int64_t pixels, int c);
+hipError_t iqbn_run(const void *x, const float *gamma, const float *beta, float eps, bool relu,
+                    void *out, float *mean, float *var, int64_t pixels, int c, DType dt,
+                    void *work, hipStream_t stream);
+
+}  // namespace quan

@@ -1,0 +1,109 @@
+"""GPU parity of quan_iqbn_forward / quan_iqbn_relu_forward against the CPU
+oracle, through the C ABI: statistics and normalised output, both dtypes,
+vector and scalar column paths, in-place use and the degenerate cases."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2509_05512_amd import quan
+from parity import assert_close, f64, say
+
+pytestmark = pytest.mark.gpu
+
+DT = {"fp32": torch.float32, "bf16": torch.bfloat16}
+
+# (N, C, H, W)
+SHAPES = [
+    (2, 4, 16, 16),        # the tiny layer
+    (3, 16, 7, 9),
+    (1, 64, 13, 11),
+    (5, 3, 5, 5),          # 4C = 12: scalar column path for bf16
+    (2, 256, 3, 3),        # wide rows
+    (1, 600, 2, 3),        # more than one column group
+    (7, 2, 1, 1),
+    (1, 1, 1, 1),          # one value per column
+    (64, 8, 32, 16),       # many rows, many blocks
+]
+
+
+def _case(shape, dtype, seed, shift=0.0):
+    N, C, H, W = shape
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal((N, 4, C, H, W), dtype=np.float32) * np.float32(1.7)
+    x += np.float32(shift) + rng.standard_normal((1, 4, C, 1, 1), dtype=np.float32)
+    g = rng.uniform(0.5, 1.5, (4, C)).astype(np.float32)
+    b = (rng.standard_normal((4, C), dtype=np.float32) * np.float32(0.3))
+    return torch.from_numpy(x).to(dtype), torch.from_numpy(g), torch.from_numpy(b)
+
+
+def _run(x, g, b, eps, relu, inplace=False):
+    dev = torch.device("cuda:0")
+    xg = quan.to_device_layout(x.to(dev))
+    gg, bg = g.to(dev), b.to(dev)
+    out = xg if inplace else quan.empty_qmap(*x.shape[:1], x.shape[2], x.shape[3], x.shape[4],
+                                              x.dtype, dev).fill_(float("nan"))
+    mean = torch.full((4, x.shape[2]), float("nan"), device=dev)
+    var = torch.full((4, x.shape[2]), float("nan"), device=dev)
+    fn = quan.quan_iqbn_relu_forward if relu else quan.quan_iqbn_forward
+    fn(xg, gg, bg, eps, out=out, mean=mean, var=var)
+    torch.cuda.synchronize()
+    return out, mean, var
+
+
+@pytest.mark.parametrize("relu", [False, True])
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("shape", SHAPES, ids=[str(s) for s in SHAPES])
+def test_iqbn_matches_oracle(shape, dtype, relu):
+    say(f"iqbn parity {dtype} {shape} relu={relu}")
+    dt = DT[dtype]
+    x, g, b = _case(shape, dt, seed=sum(shape))
+    out, mean, var = _run(x, g, b, 1e-5, relu)
+    ref, rmean, rvar = oracle.iqbn(f64(x), f64(g), f64(b), 1e-5, relu)
+    assert_close(f64(mean), rmean, dt, "mean")
+    assert_close(f64(var), rvar, dt, "var")
+    assert_close(f64(out), ref, dt, "out")
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_iqbn_large_offset_does_not_cancel(dtype):
+    """|mean| >> std: the shifted accumulation keeps the variance accurate."""
+    say(f"iqbn offset {dtype}")
+    dt = DT[dtype]
+    x, g, b = _case((4, 8, 12, 12), dt, seed=3, shift=300.0)
+    out, mean, var = _run(x, g, b, 1e-5, False)
+    ref, rmean, rvar = oracle.iqbn(f64(x), f64(g), f64(b), 1e-5, False)
+    assert_close(f64(var), rvar, dt, "var")
+    assert_close(f64(out), ref, dt, "out")
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_iqbn_in_place(dtype):
+    say(f"iqbn in-place {dtype}")
+    dt = DT[dtype]
+    x, g, b = _case((3, 16, 10, 10), dt, seed=4)
+    out, mean, var = _run(x, g, b, 1e-5, True, inplace=True)
+    ref, _, _ = oracle.iqbn(f64(x), f64(g), f64(b), 1e-5, True)
+    assert_close(f64(out), ref, dt, "in-place out")
+
+
+def test_iqbn_constant_input_gives_beta():
+    say("iqbn constant input")
+    x = torch.full((2, 4, 6, 5, 5), 3.25)
+    g = torch.rand(4, 6) + 0.5
+    b = torch.randn(4, 6)
+    out, mean, var = _run(x, g, b, 1e-5, False)
+    assert torch.all(var.cpu() == 0)
+    assert torch.allclose(mean.cpu(), torch.full((4, 6), 3.25))
+    assert torch.allclose(out.cpu(), b[None, :, :, None, None].expand(2, 4, 6, 5, 5), atol=1e-6)
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_iqbn_deterministic(dtype):
+    say(f"iqbn determinism {dtype}")
+    dt = DT[dtype]
+    x, g, b = _case((16, 32, 14, 14), dt, seed=8)
+    o1, m1, v1 = _run(x, g, b, 1e-5, False)
+    o2, m2, v2 = _run(x, g, b, 1e-5, False)
+    assert torch.equal(o1.cpu(), o2.cpu()) and torch.equal(m1.cpu(), m2.cpu()) \
+        and torch.equal(v1.cpu(), v2.cpu())
