@@ -14,9 +14,11 @@
 //                     gives one (s1, s2) per column per block.
 //   2. iqbn_finalize  merges the per-block partials in fp64, in block order
 //                     (deterministic: no atomics), and writes mean, var and the
-//                     per-column affine  scale = gamma / sqrt(var + eps),
-//                     shift = beta - mean * scale.
-//   3. iqbn_affine    streams x again: out = x * scale + shift, optional ReLU.
+//                     per-column scale = gamma / sqrt(var + eps).
+//   3. iqbn_affine    streams x again: out = (x - mean) * scale + beta, optional
+//                     ReLU.  Subtracting the mean first keeps a near-constant
+//                     column exact (a folded x * scale + shift would cancel
+//                     two terms of size |mean| * scale).
 #include <hip/hip_runtime.h>
 
 #include "quan_launch.h"
@@ -25,7 +27,8 @@ namespace quan {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kMaxBlocks = 1024;
+constexpr int kMaxBlocks = 512;      // partial-statistics blocks (grid.x * grid.y)
+constexpr int kMinRowsPerThread = 24;
 constexpr int kFinalizeCols = 16;
 
 template <typename T, int VW>
@@ -56,7 +59,8 @@ Layout make_layout(int64_t pixels, int c, int vw)
     l.cg = l.chunks < kThreads ? l.chunks : kThreads;
     l.rpi = kThreads / l.cg;
     l.col_groups = (l.chunks + l.cg - 1) / l.cg;
-    int64_t want = (pixels + int64_t(l.rpi) * 16 - 1) / (int64_t(l.rpi) * 16);
+    const int64_t rows_per_iter_block = int64_t(l.rpi) * kMinRowsPerThread;
+    int64_t want = (pixels + rows_per_iter_block - 1) / rows_per_iter_block;
     int max_blocks = kMaxBlocks / l.col_groups;
     if (max_blocks < 1)
         max_blocks = 1;
@@ -169,13 +173,33 @@ __global__ __launch_bounds__(kThreads) void iqbn_finalize(const T *__restrict__ 
     const int cl = tid % kFinalizeCols;
     const int gl = tid / kFinalizeCols;
     const int col = blockIdx.x * kFinalizeCols + cl;
-    double s1 = 0.0, s2 = 0.0;
+    // Eight independent accumulators per thread so the partial loads overlap.
+    constexpr int G = kThreads / kFinalizeCols;
+    double a1[8], a2[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+        a1[u] = a2[u] = 0.0;
     if (col < l.row_len) {
-        for (int b = gl; b < l.blocks; b += kThreads / kFinalizeCols) {
-            const float *p = part + size_t(b) * 2 * l.row_len + col;
-            s1 += double(p[0]);
-            s2 += double(p[l.row_len]);
+        int b = gl;
+        for (; b + 7 * G < l.blocks; b += 8 * G) {
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const float *p = part + size_t(b + u * G) * 2 * l.row_len + col;
+                a1[u] += double(p[0]);
+                a2[u] += double(p[l.row_len]);
+            }
         }
+        for (int u = 0; b < l.blocks; b += G, ++u) {
+            const float *p = part + size_t(b) * 2 * l.row_len + col;
+            a1[u & 7] += double(p[0]);
+            a2[u & 7] += double(p[l.row_len]);
+        }
+    }
+    double s1 = 0.0, s2 = 0.0;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+        s1 += a1[u];
+        s2 += a2[u];
     }
     red[0][tid] = s1;
     red[1][tid] = s2;
@@ -195,8 +219,9 @@ __global__ __launch_bounds__(kThreads) void iqbn_finalize(const T *__restrict__ 
         const double sc = double(gamma[col]) / sqrt(v + double(eps));
         mean[col] = float(mu);
         var[col] = float(v);
-        affine[col] = float(sc);
-        affine[l.row_len + col] = float(double(beta[col]) - mu * sc);
+        affine[col] = float(mu);
+        affine[l.row_len + col] = float(sc);
+        affine[2 * l.row_len + col] = beta[col];
     }
 }
 
@@ -210,11 +235,12 @@ __global__ __launch_bounds__(kThreads) void iqbn_affine(const T *x, T *out, Layo
     const int col = blockIdx.y * l.cg + cl;
     if (rl >= l.rpi || col >= l.chunks)
         return;
-    float sc[VW], sh[VW];
+    float mu[VW], sc[VW], be[VW];
 #pragma unroll
     for (int e = 0; e < VW; ++e) {
-        sc[e] = affine[col * VW + e];
-        sh[e] = affine[l.row_len + col * VW + e];
+        mu[e] = affine[col * VW + e];
+        sc[e] = affine[l.row_len + col * VW + e];
+        be[e] = affine[2 * l.row_len + col * VW + e];
     }
     const int64_t r0 = int64_t(blockIdx.x) * l.rows_per_block;
     int64_t r1 = r0 + l.rows_per_block;
@@ -234,7 +260,7 @@ __global__ __launch_bounds__(kThreads) void iqbn_affine(const T *x, T *out, Layo
             Vec<T, VW> o;
 #pragma unroll
             for (int e = 0; e < VW; ++e) {
-                float y = fmaf(float(v[u].v[e]), sc[e], sh[e]);
+                float y = fmaf(float(v[u].v[e]) - mu[e], sc[e], be[e]);
                 if (RELU)
                     y = fmaxf(y, 0.0f);
                 o.v[e] = T(y);
@@ -247,7 +273,7 @@ __global__ __launch_bounds__(kThreads) void iqbn_affine(const T *x, T *out, Layo
         Vec<T, VW> o;
 #pragma unroll
         for (int e = 0; e < VW; ++e) {
-            float y = fmaf(float(v.v[e]), sc[e], sh[e]);
+            float y = fmaf(float(v.v[e]) - mu[e], sc[e], be[e]);
             if (RELU)
                 y = fmaxf(y, 0.0f);
             o.v[e] = T(y);
@@ -289,7 +315,7 @@ size_t iqbn_workspace_bytes(int64_t pixels, int c)
         if ((4 * c) % vw)
             continue;
         const Layout l = make_layout(pixels, c, vw);
-        const size_t b = (size_t(l.blocks) * 2 + 2) * size_t(l.row_len) * sizeof(float);
+        const size_t b = (size_t(l.blocks) * 2 + 3) * size_t(l.row_len) * sizeof(float);
         if (b > best)
             best = b;
     }
