@@ -27,9 +27,8 @@ namespace quan {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kMaxBlocks = 512;      // partial-statistics blocks (grid.x * grid.y)
+constexpr int kMaxBlocks = 512;  // partial-statistics blocks per column group (grid.x)
 constexpr int kMinRowsPerThread = 24;
-constexpr int kFinalizeCols = 16;
 
 template <typename T, int VW>
 struct alignas(sizeof(T) * VW) Vec {
@@ -61,7 +60,7 @@ Layout make_layout(int64_t pixels, int c, int vw)
     l.col_groups = (l.chunks + l.cg - 1) / l.cg;
     const int64_t rows_per_iter_block = int64_t(l.rpi) * kMinRowsPerThread;
     int64_t want = (pixels + rows_per_iter_block - 1) / rows_per_iter_block;
-    int max_blocks = kMaxBlocks / l.col_groups;
+    int max_blocks = kMaxBlocks;  // per column group
     if (max_blocks < 1)
         max_blocks = 1;
     if (want > max_blocks)
@@ -150,16 +149,21 @@ __global__ __launch_bounds__(kThreads) void iqbn_stats(const T *__restrict__ x, 
                 t2[e] += red[1][j * l.cg + cl][e];
             }
         }
-        float *p1 = part + (size_t(blockIdx.x) * 2) * l.row_len + col * VW;
-        float *p2 = p1 + l.row_len;
+        // Partials are column-major, [2][L][blocks]: the finalize pass reads
+        // one column's partials with consecutive lanes.
+        const size_t stride2 = size_t(l.row_len) * l.blocks;
 #pragma unroll
         for (int e = 0; e < VW; ++e) {
-            p1[e] = t1[e];
-            p2[e] = t2[e];
+            const size_t idx = size_t(col * VW + e) * l.blocks + blockIdx.x;
+            part[idx] = t1[e];
+            part[stride2 + idx] = t2[e];
         }
     }
 }
 
+// One wave per column: lane i adds the partials of blocks i, i+64, ... (all
+// loads issued before any is used), then a fixed butterfly across the wave
+// gives every lane the same fp64 total.  Deterministic: no atomics.
 template <typename T>
 __global__ __launch_bounds__(kThreads) void iqbn_finalize(const T *__restrict__ x, Layout l,
                                                           const float *__restrict__ part,
@@ -168,51 +172,38 @@ __global__ __launch_bounds__(kThreads) void iqbn_finalize(const T *__restrict__ 
                                                           float *__restrict__ mean, float *__restrict__ var,
                                                           float *__restrict__ affine)
 {
-    __shared__ double red[2][kThreads];
-    const int tid = threadIdx.x;
-    const int cl = tid % kFinalizeCols;
-    const int gl = tid / kFinalizeCols;
-    const int col = blockIdx.x * kFinalizeCols + cl;
-    // Eight independent accumulators per thread so the partial loads overlap.
-    constexpr int G = kThreads / kFinalizeCols;
-    double a1[8], a2[8];
+    constexpr int PER_LANE = kMaxBlocks / 64;
+    const int lane = threadIdx.x & 63;
+    const int col = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
+    if (col >= l.row_len)
+        return;
+    const float *p1 = part + size_t(col) * l.blocks;
+    const float *p2 = p1 + size_t(l.row_len) * l.blocks;
+    float v1[PER_LANE], v2[PER_LANE];
 #pragma unroll
-    for (int u = 0; u < 8; ++u)
-        a1[u] = a2[u] = 0.0;
-    if (col < l.row_len) {
-        int b = gl;
-        for (; b + 7 * G < l.blocks; b += 8 * G) {
-#pragma unroll
-            for (int u = 0; u < 8; ++u) {
-                const float *p = part + size_t(b + u * G) * 2 * l.row_len + col;
-                a1[u] += double(p[0]);
-                a2[u] += double(p[l.row_len]);
-            }
-        }
-        for (int u = 0; b < l.blocks; b += G, ++u) {
-            const float *p = part + size_t(b) * 2 * l.row_len + col;
-            a1[u & 7] += double(p[0]);
-            a2[u & 7] += double(p[l.row_len]);
-        }
+    for (int u = 0; u < PER_LANE; ++u) {
+        const int b = lane + 64 * u;
+        const int bc = b < l.blocks ? b : l.blocks - 1;
+        v1[u] = p1[bc];
+        v2[u] = p2[bc];
     }
     double s1 = 0.0, s2 = 0.0;
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-        s1 += a1[u];
-        s2 += a2[u];
-    }
-    red[0][tid] = s1;
-    red[1][tid] = s2;
-    __syncthreads();
-    if (gl == 0 && col < l.row_len) {
-        double t1 = 0.0, t2 = 0.0;
-        for (int j = 0; j < kThreads / kFinalizeCols; ++j) {
-            t1 += red[0][j * kFinalizeCols + cl];
-            t2 += red[1][j * kFinalizeCols + cl];
+    for (int u = 0; u < PER_LANE; ++u) {
+        if (lane + 64 * u < l.blocks) {
+            s1 += double(v1[u]);
+            s2 += double(v2[u]);
         }
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        s1 += __shfl_xor(s1, off);
+        s2 += __shfl_xor(s2, off);
+    }
+    if (lane == 0) {
         const double n = double(l.pixels);
-        const double d = t1 / n;          // mean - K
-        double v = t2 / n - d * d;        // biased variance
+        const double d = s1 / n;          // mean - K
+        double v = s2 / n - d * d;        // biased variance
         if (v < 0.0)
             v = 0.0;
         const double mu = double(float(x[col])) + d;
@@ -293,7 +284,7 @@ hipError_t launch_all(const void *x, const float *gamma, const float *beta, floa
     const T *xt = static_cast<const T *>(x);
     const dim3 grid(l.blocks, l.col_groups);
     hipLaunchKernelGGL((iqbn_stats<T, VW>), grid, dim3(kThreads), 0, stream, xt, l, part);
-    const int fin_blocks = (l.row_len + kFinalizeCols - 1) / kFinalizeCols;
+    const int fin_blocks = (l.row_len + kThreads / 64 - 1) / (kThreads / 64);
     hipLaunchKernelGGL((iqbn_finalize<T>), dim3(fin_blocks), dim3(kThreads), 0, stream, xt, l, part,
                        gamma, beta, eps, mean, var, affine);
     if (relu)

@@ -13,22 +13,29 @@
 // components ordered r, i, j, k = 0..3, the entry in row p, column q is the
 // kernel component p xor q, negated at (r,i) (r,j) (r,k) (i,j) (j,k) (k,i).
 //
-// Data flow of one work-group tile (BM output pixels x 4*BNC output reals):
-//   - the K loop runs over stages (tap, channel block of BKC channels); a
-//     stage holds all four input components of those channels;
-//   - activations are loaded channels-last (16-byte vectors along c) into an
-//     LDS tile [BM][4*BKC], XOR-swizzled so the MFMA fragment reads are
-//     bank-conflict free; taps outside the image load zeros;
-//   - only the four shared real kernels are staged: LDS holds
-//     W_0..W_3 [BNC][BKC] for the stage.  The signed 4x4 Hamilton block is
-//     formed on the LDS->register read: the fragment for (output component p,
-//     input component q) reads kernel p xor q and flips its sign bits with
-//     one XOR when sign(p, q) < 0;
-//   - v_mfma_f32_32x32x16_bf16 (bf16) / v_mfma_f32_32x32x2f32 (fp32) with fp32
-//     accumulators; two LDS stages, register prefetch of the next stage while
-//     the current one is multiplied;
-//   - epilogue: bias, round to the output type (RNE), channels-last stores.
+// One work-group computes a tile of BM output pixels x 4*BNC output reals
+// (all four output components of BNC channels):
+//   - K runs over stages.  A stage is QS input components x CS channels with
+//     QS*CS*sizeof(T) = 128 bytes, so each activation row of a stage is one
+//     contiguous 128-byte piece of the channels-last pixel (full cache lines);
+//   - only the four shared real kernels are staged: an LDS weight block holds
+//     W_0..W_3 [BNC][CS] for one (tap, channel block) and serves all 4/QS
+//     stages of that block.  The signed 4x4 Hamilton block is formed on the
+//     LDS->register read: the fragment for (output component p, input
+//     component q) reads kernel p xor q and flips its sign bits with one XOR;
+//   - global -> LDS direct loads (global_load_lds_dwordx4) fill a ring of three
+//     activation stages and two weight blocks two stages ahead; the layout in
+//     LDS is XOR-swizzled so the MFMA fragment reads are bank-conflict free.
+//     Taps outside the image read a zero chunk;
+//   - fragments of the next k-step are read from LDS while the current
+//     k-step's MFMAs run; the next loads are issued after the stage's last LDS
+//     read (an LDS DMA holds back later LDS reads of its wave until it lands);
+//   - v_mfma_f32_32x32x16_bf16 (bf16) / v_mfma_f32_32x32x2f32 (fp32), fp32
+//     accumulators; epilogue adds the bias, rounds to the output type (RNE)
+//     and stores channels-last.
 #include <hip/hip_runtime.h>
+
+#include <cstdlib>
 
 #include "quan_launch.h"
 
@@ -74,16 +81,24 @@ struct KArgs {
     int vec_in;  // c_in is a multiple of the 16-byte chunk
 };
 
-// XOR swizzle of the 16-byte chunk index within an LDS row of `cpr` chunks:
-// rows that a group of 8 lanes reads together land in 8 different bank
-// groups.
+// XOR swizzle of the 16-byte chunk index within an LDS row of CPR chunks.
+// A ds_read_b128 from a wave reads one chunk from each of 16 consecutive rows
+// per group of 16 lanes (256 bytes, the full bank width) and from 8
+// consecutive rows per group of 8 lanes (128 bytes); the swizzle puts every
+// such group on distinct 16-byte bank slots in both views, so the MFMA
+// fragment reads are conflict free.
 template <int CPR>
 __device__ __forceinline__ int swz(int row)
 {
-    if constexpr (CPR >= 8)
-        return row & 7;
+    static_assert(CPR == 2 || CPR == 4 || CPR == 8 || CPR == 16, "swizzle defined for 32..256-byte rows");
+    if constexpr (CPR == 16)
+        return row & 15;
+    else if constexpr (CPR == 8)
+        return (row & 7) ^ ((row >> 3) & 1);
+    else if constexpr (CPR == 4)
+        return ((row >> 1) ^ (row >> 3)) & 3;
     else
-        return (row * CPR / 8) % CPR;
+        return ((row >> 2) ^ (row >> 3)) & 1;
 }
 
 template <typename T>
@@ -408,38 +423,54 @@ __device__ __forceinline__ void dma16(const void *g, const unsigned char *lds_sl
                  : "memory");
 }
 
-template <typename T, int BM, int BNC, int WAVES_M, int WAVES_N, int BKC, int STAGES>
+// Stage geometry of the pipelined kernel: a K stage is QS input components
+// x CS channels, chosen so that one activation row of a stage is exactly one
+// contiguous 128-byte segment of the channels-last pixel.  The weight block
+// of a (tap, channel block) -- the four real kernels W_0..W_3 for BNC output
+// channels x CS input channels -- serves all 4/QS stages of that block.
+template <typename T, int QS>
+struct StageGeom {
+    static constexpr int EPC = Elem<T>::per_chunk;
+    static constexpr int CS = 128 / (QS * int(sizeof(T)));  // channels per component
+    static constexpr int CPQ = CS / EPC;                     // chunks per component
+    static constexpr int NQG = 4 / QS;                       // stages per weight block
+};
+
+template <typename T, int BM, int BNC, int WAVES_M, int WAVES_N, int QS>
 __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void qconv2d_igemm_dma(KArgs a)
 {
-    constexpr int EPC = Elem<T>::per_chunk;
+    using SG = StageGeom<T, QS>;
+    constexpr int EPC = SG::EPC;
+    constexpr int CS = SG::CS;
+    constexpr int CPQ = SG::CPQ;
+    constexpr int NQG = SG::NQG;
     constexpr int NWAVES = WAVES_M * WAVES_N;
     constexpr int BN = 4 * BNC;
-    constexpr int CPQ = BKC / EPC;
-    constexpr int CPR = 4 * CPQ;
+    constexpr int CPR = 8;  // 128-byte activation rows
     constexpr int WTM = BM / WAVES_M;
     constexpr int WTN = BN / WAVES_N;
     constexpr int MB = WTM / 32;
     constexpr int NB = WTN / 32;
-    constexpr int A_BYTES = BM * CPR * 16;
+    constexpr int A_ST = 3;                   // activation ring
+    constexpr int B_ST = NQG == 1 ? 3 : 2;    // weight-block ring
+    constexpr int A_BYTES = BM * 128;
     constexpr int B_BYTES = 4 * BNC * CPQ * 16;
-    constexpr int STAGE = A_BYTES + B_BYTES;
-    constexpr int A_INSTR = A_BYTES / 1024;  // 1 KB wave-loads per stage
-    constexpr int B_INSTR = B_BYTES / 1024;
+    constexpr int A_INSTR = A_BYTES / 1024;  // 1 KB wave loads per stage
+    constexpr int B_INSTR = B_BYTES / 1024;  // 1 KB wave loads per weight block
     constexpr int A_PER_WAVE = A_INSTR / NWAVES;
-    // Weight loads are dealt round-robin: wave w issues loads w, w+NWAVES, ...
-    constexpr int B_MAX = (B_INSTR + NWAVES - 1) / NWAVES;
-    constexpr int LPS_HI = A_PER_WAVE + B_MAX;  // loads per stage, waves with B_MAX weight loads
-    constexpr int LPS_LO = B_INSTR % NWAVES == 0 ? LPS_HI : LPS_HI - 1;
-    constexpr int A_ROWS_PER_INSTR = 64 / CPR;
+    constexpr int B_MAX = (B_INSTR + NWAVES - 1) / NWAVES;  // round-robin over waves
+    constexpr int LB_HI = B_MAX;
+    constexpr int LB_LO = B_INSTR % NWAVES == 0 ? B_MAX : B_MAX - 1;
     constexpr int B_ROWS_PER_INSTR = 64 / CPQ;
-    static_assert(A_BYTES % 1024 == 0 && A_INSTR % NWAVES == 0, "activation stage must split into wave loads");
-    static_assert(B_BYTES % 1024 == 0, "weight stage must be whole 1 KB wave loads");
-    static_assert(CPR <= 64 && CPQ % 2 == 0, "stage geometry");
+    constexpr int KSTEPS = 4;  // 32x32 MFMA k-steps per stage (two chunks each)
+    static_assert(A_INSTR % NWAVES == 0, "activation stage must split into wave loads");
+    static_assert(B_BYTES % 1024 == 0, "weight block must be whole 1 KB wave loads");
     static_assert(WTM % 32 == 0 && WTN % 32 == 0 && BNC % 4 == 0, "tile geometry");
-    static_assert(STAGES >= 2, "need at least two stages");
+    static_assert(QS * CPQ == 8, "a stage row is eight chunks");
 
-    __shared__ __attribute__((aligned(1024))) unsigned char smem[STAGES * STAGE];
-    auto ring = [&](int b) -> unsigned char * { return smem + b * STAGE; };
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[A_ST * A_BYTES + B_ST * B_BYTES];
+    unsigned char *const a_ring = smem;
+    unsigned char *const b_ring = smem + A_ST * A_BYTES;
 
     const T *__restrict__ xp = static_cast<const T *>(a.x);
     const T *__restrict__ wp = static_cast<const T *>(a.wpack);
@@ -462,16 +493,16 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void qconv2d_igemm_dma(KArg
     const int o0 = n_tile * BNC;
 
     // ---- per-lane activation load plan: A_PER_WAVE rows, one chunk each ----
+    // a_off: element offset of the chunk at tap (0, 0), channel block 0,
+    // component group 0 (only used when the tap lies inside the image).
     const int hw_out = a.h_out * a.w_out;
-    int a_img[A_PER_WAVE], a_iy0[A_PER_WAVE], a_ix0[A_PER_WAVE];
-    int a_coff[A_PER_WAVE];  // component offset + channel offset of the chunk
-    int a_cin[A_PER_WAVE];   // channel offset of the chunk inside its component
+    const int row_elems = 4 * a.c_in;
+    int a_off[A_PER_WAVE], a_iy0[A_PER_WAVE], a_ix0[A_PER_WAVE], a_cin[A_PER_WAVE];
 #pragma unroll
     for (int i = 0; i < A_PER_WAVE; ++i) {
-        const int r = (wave * A_PER_WAVE + i) * A_ROWS_PER_INSTR + lane / CPR;
-        const int lc = (lane % CPR) ^ swz<CPR>(r);  // logical chunk this slot holds
-        const int q = lc / CPQ, piece = lc % CPQ;
-        a_coff[i] = q * a.c_in + piece * EPC;  // + cblk * BKC at each stage
+        const int r = (wave * A_PER_WAVE + i) * 8 + lane / 8;
+        const int lc = (lane % 8) ^ swz<CPR>(r);  // logical chunk this slot holds
+        const int qi = lc / CPQ, piece = lc % CPQ;
         a_cin[i] = piece * EPC;
         const int m = m0 + r;
         if (m < a.m) {
@@ -479,53 +510,54 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void qconv2d_igemm_dma(KArg
             const int rr = m - img * hw_out;
             const int oy = rr / a.w_out;
             const int ox = rr - oy * a.w_out;
-            a_img[i] = img * a.h * a.w;
             a_iy0[i] = oy * a.s_h - a.p_h;
             a_ix0[i] = ox * a.s_w - a.p_w;
+            a_off[i] = ((img * a.h + a_iy0[i]) * a.w + a_ix0[i]) * row_elems + qi * a.c_in + piece * EPC;
         } else {
-            a_img[i] = 0;
-            a_iy0[i] = -0x20000000;
+            a_iy0[i] = -0x20000000;  // rows past M never load
             a_ix0[i] = 0;
+            a_off[i] = 0;
         }
     }
     // ---- per-lane weight load plan ----
     const bool b_full = B_INSTR % NWAVES == 0 || wave < B_INSTR % NWAVES;  // issues B_MAX loads
-    int b_off[B_MAX];  // element offset inside one stage's packed block
+    int b_off[B_MAX];
 #pragma unroll
     for (int j = 0; j < B_MAX; ++j) {
         const int row = (wave + j * NWAVES) * B_ROWS_PER_INSTR + lane / CPQ;  // ws * BNC + o
         const int lc = (lane % CPQ) ^ swz<CPQ>(row);
         const int ws = row / BNC, o = row - (row / BNC) * BNC;
-        b_off[j] = ws * a.cout_pad * BKC + (o0 + o) * BKC + lc * EPC;
+        b_off[j] = ws * a.cout_pad * CS + (o0 + o) * CS + lc * EPC;
     }
-    const int row_elems = 4 * a.c_in;
 
-    auto issue = [&](int s, int buf) {
-        const int tap = s / a.n_cblk;
-        const int cblk = s - tap * a.n_cblk;
+    // Loads of stage s: its weight block first when s opens a block, then the
+    // activation tile.
+    auto issue = [&](int s) {
+        const int blk = s / NQG;
+        const int qg = s - blk * NQG;
+        if (qg == 0) {
+            unsigned char *Bs = b_ring + (blk % B_ST) * B_BYTES;
+            const T *wsrc = wp + (size_t)blk * 4 * a.cout_pad * CS;
+#pragma unroll
+            for (int j = 0; j < B_MAX; ++j)
+                if (j < B_MAX - 1 || b_full)
+                    dma16(wsrc + b_off[j], Bs + (wave + j * NWAVES) * 1024);
+        }
+        const int tap = blk / a.n_cblk;
+        const int cblk = blk - tap * a.n_cblk;
         const int ky = tap / a.k_w;
         const int kx = tap - ky * a.k_w;
         const int dy = ky * a.d_h, dx = kx * a.d_w;
-        const int cbase = cblk * BKC;
-        unsigned char *As = ring(buf);
-        unsigned char *Bs = As + A_BYTES;
+        const int cbase = cblk * CS;
+        const int shift = (dy * a.w + dx) * row_elems + qg * QS * a.c_in + cbase;  // uniform
+        unsigned char *As = a_ring + (s % A_ST) * A_BYTES;
 #pragma unroll
         for (int i = 0; i < A_PER_WAVE; ++i) {
-            const int iy = a_iy0[i] + dy;
-            const int ix = a_ix0[i] + dx;
-            const int c = a_coff[i] + cbase;
-            const bool inside = (unsigned)iy < (unsigned)a.h && (unsigned)ix < (unsigned)a.w &&
-                                cbase + a_cin[i] < a.c_in;
-            const void *src = zero;
-            if (inside)
-                src = xp + ((a_img[i] + iy * a.w + ix) * row_elems + c);
+            const bool inside = (unsigned)(a_iy0[i] + dy) < (unsigned)a.h &&
+                                (unsigned)(a_ix0[i] + dx) < (unsigned)a.w && cbase + a_cin[i] < a.c_in;
+            const void *src = inside ? (const void *)(xp + (a_off[i] + shift)) : zero;
             dma16(src, As + (wave * A_PER_WAVE + i) * 1024);
         }
-        const T *wsrc = wp + (size_t)(tap * a.n_cblk + cblk) * 4 * a.cout_pad * BKC;
-#pragma unroll
-        for (int j = 0; j < B_MAX; ++j)
-            if (j < B_MAX - 1 || b_full)
-                dma16(wsrc + b_off[j], Bs + (wave + j * NWAVES) * 1024);
     };
 
     int frag_p[NB], frag_o[NB];
@@ -545,63 +577,90 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void qconv2d_igemm_dma(KArg
             for (int e = 0; e < 16; ++e)
                 acc[nb][mb][e] = 0.0f;
 
-    auto compute = [&](int buf) {
-        const unsigned char *As = ring(buf);
-        const unsigned char *Bs = As + A_BYTES;
+    // The eight chunks of a stage row form four 32x32 k-steps; k-step j uses
+    // chunks 2*(j % (CPQ/2)) + {0, 1} of local component j / (CPQ/2), i.e.
+    // input component q = qbase + j / (CPQ/2).
+    auto read_frags = [&](const unsigned char *As, const unsigned char *Bs, int qbase, int j,
+                          u32x4 (&wf)[NB], u32x4 (&pf)[MB]) {
+        const int qi = j / (CPQ / 2);
+        const int pc = 2 * (j % (CPQ / 2)) + khalf;
+        const int q = qbase + qi;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
+        for (int nb = 0; nb < NB; ++nb) {
+            const int row = (frag_p[nb] ^ q) * BNC + frag_o[nb];
+            wf[nb] = *reinterpret_cast<const u32x4 *>(Bs + (row * CPQ + (pc ^ swz<CPQ>(row))) * 16);
+        }
 #pragma unroll
-            for (int kk = 0; kk < CPQ / 2; ++kk) {
-                const int pc = kk * 2 + khalf;
-                u32x4 wf[NB], pf[MB];
-#pragma unroll
-                for (int nb = 0; nb < NB; ++nb) {
-                    const int p = frag_p[nb];
-                    const int row = (p ^ q) * BNC + frag_o[nb];
-                    u32x4 v = *reinterpret_cast<const u32x4 *>(Bs + (row * CPQ + (pc ^ swz<CPQ>(row))) * 16);
-                    const unsigned flip = ((kHamiltonNeg >> (4 * p + q)) & 1u) ? Elem<T>::sign : 0u;
-                    v ^= flip;
-                    wf[nb] = v;
-                }
-#pragma unroll
-                for (int mb = 0; mb < MB; ++mb) {
-                    const int r = wm * WTM + mb * 32 + l32;
-                    const int lc = q * CPQ + pc;
-                    pf[mb] = *reinterpret_cast<const u32x4 *>(As + (r * CPR + (lc ^ swz<CPR>(r))) * 16);
-                }
-#pragma unroll
-                for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-                    for (int mb = 0; mb < MB; ++mb)
-                        mfma_step<T>(acc[nb][mb], wf[nb], pf[mb]);
-            }
+        for (int mb = 0; mb < MB; ++mb) {
+            const int r = wm * WTM + mb * 32 + l32;
+            const int lc = qi * CPQ + pc;
+            pf[mb] = *reinterpret_cast<const u32x4 *>(As + (r * CPR + (lc ^ swz<CPR>(r))) * 16);
         }
     };
-
-    // ---- main loop: STAGES-deep ring, one barrier per stage ----
-    const int S = a.stages;
+    // Sign of block (p, q) applied to the weight fragment, then the MFMAs.
+    auto mfmas = [&](int qbase, int j, u32x4 (&wf)[NB], const u32x4 (&pf)[MB]) {
+        const int q = qbase + j / (CPQ / 2);
 #pragma unroll
-    for (int u = 0; u < STAGES - 1; ++u)
-        if (u < S)
-            issue(u, u);
-    for (int s0 = 0; s0 < S; s0 += STAGES) {
-#pragma unroll
-        for (int u = 0; u < STAGES; ++u) {
-            const int s = s0 + u;
-            if (s < S) {
-                // Loads of stages s .. s+STAGES-2 may be in flight; wait for s.
-                if (s + STAGES - 2 >= S)
-                    wait_vmcnt<0>();
-                else if (b_full)
-                    wait_vmcnt<LPS_HI * (STAGES - 2)>();
-                else
-                    wait_vmcnt<LPS_LO * (STAGES - 2)>();
-                block_barrier();
-                if (s + STAGES - 1 < S)
-                    issue(s + STAGES - 1, (u + STAGES - 1) % STAGES);
-                compute(u);
-            }
+        for (int nb = 0; nb < NB; ++nb) {
+            const unsigned flip = ((kHamiltonNeg >> (4 * frag_p[nb] + q)) & 1u) ? Elem<T>::sign : 0u;
+            wf[nb] ^= flip;
         }
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb)
+                mfma_step<T>(acc[nb][mb], wf[nb], pf[mb]);
+    };
+
+    // ---- main loop: loads run two stages ahead, one barrier per stage ----
+    // Within a stage the fragments of k-step j+1 are read before the MFMAs of
+    // k-step j (scheduling fences keep that order).  The loads of stage s+2
+    // are issued once every LDS read of stage s has been issued: an LDS DMA
+    // holds back the issuing wave's later LDS reads until it lands, so issued
+    // there it only has to land before the next stage's reads, with the
+    // remaining MFMAs of this stage in between.
+    const int S = a.stages;
+    issue(0);
+    if (S > 1)
+        issue(1);
+    for (int s = 0; s < S; ++s) {
+        // Wait for the loads of stage s; only those of stage s+1 (issued in
+        // the previous step: a weight block if s+1 opens one, then the
+        // activations) may stay in flight.
+        if (s + 1 >= S) {
+            wait_vmcnt<0>();
+        } else if ((s + 1) % NQG != 0) {
+            wait_vmcnt<A_PER_WAVE>();
+        } else if (b_full) {
+            wait_vmcnt<A_PER_WAVE + LB_HI>();
+        } else {
+            wait_vmcnt<A_PER_WAVE + LB_LO>();
+        }
+        block_barrier();
+        const int blk = s / NQG;
+        const unsigned char *As = a_ring + (s % A_ST) * A_BYTES;
+        const unsigned char *Bs = b_ring + (blk % B_ST) * B_BYTES;
+        const int qbase = (s - blk * NQG) * QS;
+        u32x4 wf0[NB], pf0[MB], wf1[NB], pf1[MB];
+        read_frags(As, Bs, qbase, 0, wf0, pf0);
+        read_frags(As, Bs, qbase, 1, wf1, pf1);
+        __builtin_amdgcn_sched_barrier(0);
+        mfmas(qbase, 0, wf0, pf0);
+        __builtin_amdgcn_sched_barrier(0);
+        read_frags(As, Bs, qbase, 2, wf0, pf0);
+        __builtin_amdgcn_sched_barrier(0);
+        mfmas(qbase, 1, wf1, pf1);
+        __builtin_amdgcn_sched_barrier(0);
+        read_frags(As, Bs, qbase, 3, wf1, pf1);
+        __builtin_amdgcn_sched_barrier(0);
+        // Stage s+2 reuses buffers every wave finished before this step's
+        // barrier.
+        if (s + 2 < S)
+            issue(s + 2);
+        __builtin_amdgcn_sched_barrier(0);
+        mfmas(qbase, 2, wf0, pf0);
+        __builtin_amdgcn_sched_barrier(0);
+        mfmas(qbase, 3, wf1, pf1);
     }
 
     // ---- epilogue: bias, round, channels-last store ----
@@ -676,7 +735,7 @@ __global__ __launch_bounds__(256) void qconv2d_pack(const T *__restrict__ w0, co
     const int ky = tap / k_w, kx = tap - (tap / k_w) * k_w;
     const T *src = ws == 0 ? w0 : ws == 1 ? w1 : ws == 2 ? w2 : w3;
     T v = T(0);
-    if (o < c_out && c < c_in)
+    if (tap < k_h * k_w && o < c_out && c < c_in)  // the zero tail past the last tap stays 0
         v = src[((o * c_in + c) * k_h + ky) * k_w + kx];
     wp[idx] = v;
 }
@@ -684,62 +743,85 @@ __global__ __launch_bounds__(256) void qconv2d_pack(const T *__restrict__ w0, co
 // ----------------------------- kernel table -------------------------------
 
 struct KernelEntry {
-    int bm, bnc, bkc, threads;
+    int bm, bnc, qs, threads;  // qs: input components per K stage (pack block = 128 B / qs)
     DType dt;
     bool dma;  // pipelined direct-to-LDS kernel (needs c_in % vector == 0)
     const void *fn;
     const char *name;
 };
 
-#define QCONV_REG(T, DT, BM, BNC, WM, WN, BKC)                                                  \
-    KernelEntry                                                                                 \
-    {                                                                                           \
-        BM, BNC, BKC, 64 * WM * WN, DT, false, (const void *)&qconv2d_igemm<T, BM, BNC, WM, WN, BKC>, \
-            "reg_" #T "_bm" #BM "_bnc" #BNC "_w" #WM "x" #WN "_bkc" #BKC                        \
+#define QCONV_REG(T, DT, BM, BNC, WM, WN, BKC)                                                 \
+    KernelEntry                                                                                \
+    {                                                                                          \
+        BM, BNC, 4, 64 * WM * WN, DT, false, (const void *)&qconv2d_igemm<T, BM, BNC, WM, WN, BKC>, \
+            "reg_" #T "_bm" #BM "_bnc" #BNC "_w" #WM "x" #WN "_bkc" #BKC                       \
     }
-#define QCONV_DMA(T, DT, BM, BNC, WM, WN, BKC, ST)                                                  \
-    KernelEntry                                                                                     \
-    {                                                                                               \
-        BM, BNC, BKC, 64 * WM * WN, DT, true,                                                       \
-            (const void *)&qconv2d_igemm_dma<T, BM, BNC, WM, WN, BKC, ST>,                          \
-            "dma_" #T "_bm" #BM "_bnc" #BNC "_w" #WM "x" #WN "_bkc" #BKC "_s" #ST                   \
+#define QCONV_DMA(T, DT, BM, BNC, WM, WN, QS)                                                     \
+    KernelEntry                                                                                   \
+    {                                                                                             \
+        BM, BNC, QS, 64 * WM * WN, DT, true, (const void *)&qconv2d_igemm_dma<T, BM, BNC, WM, WN, QS>, \
+            "dma_" #T "_bm" #BM "_bnc" #BNC "_w" #WM "x" #WN "_qs" #QS                            \
     }
+#define QCONV_DMA3(T, DT, BM, BNC, WM, WN) \
+    QCONV_DMA(T, DT, BM, BNC, WM, WN, 1), QCONV_DMA(T, DT, BM, BNC, WM, WN, 2), QCONV_DMA(T, DT, BM, BNC, WM, WN, 4)
 
-// Every entry's BKC equals the pack block (16 bf16, 8 fp32) and its BNC
-// divides kPackCoutAlign.
+// Register-staged kernels use the 4-component stage (qs 4); every entry's BNC
+// divides kPackCoutAlign.  DMA entries come in qs = 1, 2, 4 triples.
 enum KernelId {
     kRegBf16N64 = 0,
     kRegBf16N32,
     kRegBf16N16,
     kRegF32,
-    kDmaBf16M256N64,
-    kDmaBf16M128N64,
-    kDmaBf16M128N32,
-    kDmaBf16M128N16,
-    kDmaF32,
+    kDmaBf16M256N64 = 4,   // +0/+1/+2 for qs 1/2/4
+    kDmaBf16M128N64 = 7,
+    kDmaBf16M128N32 = 10,
+    kDmaBf16M128N16 = 13,
+    kDmaF32M64N16 = 16,
+    kNumKernels = 19,
 };
 const KernelEntry kKernels[] = {
     QCONV_REG(__bf16, DType::BF16, 128, 64, 2, 2, 16),
     QCONV_REG(__bf16, DType::BF16, 128, 32, 2, 2, 16),
     QCONV_REG(__bf16, DType::BF16, 128, 16, 2, 2, 16),
     QCONV_REG(float, DType::F32, 64, 16, 2, 2, 8),
-    QCONV_DMA(__bf16, DType::BF16, 256, 64, 4, 2, 16, 3),
-    QCONV_DMA(__bf16, DType::BF16, 128, 64, 2, 2, 16, 3),
-    QCONV_DMA(__bf16, DType::BF16, 128, 32, 2, 2, 16, 3),
-    QCONV_DMA(__bf16, DType::BF16, 128, 16, 2, 2, 16, 3),
-    QCONV_DMA(float, DType::F32, 64, 16, 2, 2, 8, 3),
+    QCONV_DMA3(__bf16, DType::BF16, 256, 64, 4, 2),
+    QCONV_DMA3(__bf16, DType::BF16, 128, 64, 2, 2),
+    QCONV_DMA3(__bf16, DType::BF16, 128, 32, 2, 2),
+    QCONV_DMA3(__bf16, DType::BF16, 128, 16, 2, 2),
+    QCONV_DMA3(float, DType::F32, 64, 16, 2, 2),
 };
+static_assert(sizeof(kKernels) / sizeof(kKernels[0]) == kNumKernels, "kernel table");
+
+int qs_index(int qs)
+{
+    return qs == 1 ? 0 : (qs == 2 ? 1 : 2);
+}
+
+// Input components per stage for c_in: the widest 128-byte stage whose
+// channel block divides c_in (no zero padding), else the narrowest.
+int choose_qs(int c_in, DType dt)
+{
+    const int es = dt == DType::BF16 ? 2 : 4;
+    const int epc = 16 / es;
+    if (c_in % epc != 0)
+        return 4;
+    for (int qs : {1, 2})
+        if (c_in % (128 / (qs * es)) == 0)
+            return qs;
+    return 4;
+}
 
 }  // namespace
 
 PackGeom qconv2d_pack_geom(int c_in, int c_out, int k_h, int k_w, DType dt)
 {
     PackGeom pg;
-    pg.pk = dt == DType::BF16 ? 16 : 8;
+    const int es = dt == DType::BF16 ? 2 : 4;
+    pg.pk = 128 / (choose_qs(c_in, dt) * es);
     pg.n_cblk = (c_in + pg.pk - 1) / pg.pk;
     pg.cout_pad = (c_out + kPackCoutAlign - 1) / kPackCoutAlign * kPackCoutAlign;
-    const size_t esz = dt == DType::BF16 ? 2 : 4;
-    pg.bytes = size_t(k_h) * k_w * pg.n_cblk * 4 * pg.cout_pad * pg.pk * esz;
+    pg.zero_offset = size_t(k_h) * k_w * pg.n_cblk * 4 * pg.cout_pad * pg.pk * es;
+    pg.bytes = pg.zero_offset + kPackZeroTail;
     return pg;
 }
 
@@ -747,19 +829,29 @@ ConvPlan qconv2d_plan(const ConvGeom &g, DType dt)
 {
     const int epc = dt == DType::BF16 ? 8 : 4;
     const bool vec = g.c_in % epc == 0;
+    const int qi = qs_index(choose_qs(g.c_in, dt));
     const int64_t m = g.m();
     int id;
     if (dt == DType::F32) {
-        id = vec ? kDmaF32 : kRegF32;
+        id = vec ? kDmaF32M64N16 + qi : kRegF32;
     } else if (g.c_out >= 64) {
         // 256-pixel tiles when they still give the 256 CUs two rounds of work.
         const int64_t tiles256 = (m + 255) / 256 * ((g.c_out + 63) / 64);
-        id = !vec ? kRegBf16N64 : (tiles256 >= 512 ? kDmaBf16M256N64 : kDmaBf16M128N64);
+        id = !vec ? kRegBf16N64 : (tiles256 >= 512 ? kDmaBf16M256N64 : kDmaBf16M128N64) + qi;
     } else if (g.c_out > 16) {
-        id = vec ? kDmaBf16M128N32 : kRegBf16N32;
+        id = vec ? kDmaBf16M128N32 + qi : kRegBf16N32;
     } else {
-        id = vec ? kDmaBf16M128N16 : kRegBf16N16;
+        id = vec ? kDmaBf16M128N16 + qi : kRegBf16N16;
     }
+#ifdef QUAN_TUNING
+    // Tuning builds only: force a tile family (QUAN_QCONV_KERNEL=<id of its
+    // qs-1 entry>); the qs member still follows c_in.
+    if (const char *force = getenv("QUAN_QCONV_KERNEL")) {
+        const int f = atoi(force);
+        if (f >= kDmaBf16M256N64 && f < kNumKernels && kKernels[f].dt == dt && vec)
+            id = f + qi;
+    }
+#endif
     const KernelEntry &k = kKernels[id];
     ConvPlan p;
     p.id = id;
@@ -796,7 +888,9 @@ hipError_t qconv2d_run(const ConvPlan &plan, const PackGeom &pg, const ConvGeom 
 {
     const KernelEntry &k = kKernels[plan.id];
     const int epc = dt == DType::BF16 ? 8 : 4;
-    if (k.bkc != pg.pk || kPackCoutAlign % k.bnc != 0 || k.dt != dt || (k.dma && g.c_in % epc != 0))
+    const int es = dt == DType::BF16 ? 2 : 4;
+    if (128 / (k.qs * es) != pg.pk || kPackCoutAlign % k.bnc != 0 || k.dt != dt ||
+        (k.dma && g.c_in % epc != 0))
         return hipErrorInvalidValue;
     KArgs a;
     a.x = x;
@@ -817,7 +911,7 @@ hipError_t qconv2d_run(const ConvPlan &plan, const PackGeom &pg, const ConvGeom 
     a.h_out = g.h_out;
     a.w_out = g.w_out;
     a.m = int(g.m());
-    a.stages = g.k_h * g.k_w * pg.n_cblk;
+    a.stages = g.k_h * g.k_w * pg.n_cblk * (k.dma ? 4 / k.qs : 1);
     a.n_cblk = pg.n_cblk;
     a.cout_pad = pg.cout_pad;
     a.n_tiles = plan.n_tiles;

@@ -13,7 +13,7 @@
 #include <string>
 #include <utility>
 
-#include "../../include/quan.h"
+#include "quan.h"
 #include "quan_launch.h"
 
 namespace {

@@ -20,16 +20,18 @@ struct ConvGeom {
 };
 
 // Layout of the packed weights: [tap][cblk][kernel r,i,j,k][cout_pad][pk]
-// with pk input channels per block.  It depends only on (dtype, c_in, c_out,
+// with pk input channels per block, then kPackZeroTail zero bytes.  It depends only on (dtype, c_in, c_out,
 // k_h, k_w), never on the tile configuration, so weights packed once serve
 // every later call.
 struct PackGeom {
-    int pk;        // input channels per block (16 bf16, 8 fp32)
-    int n_cblk;    // ceil(c_in / pk)
-    int cout_pad;  // c_out rounded up to kPackCoutAlign
+    int pk;              // input channels per block (128 bytes / components per stage)
+    int n_cblk;          // ceil(c_in / pk)
+    int cout_pad;        // c_out rounded up to kPackCoutAlign
+    size_t zero_offset;  // bytes of packed weights; kPackZeroTail zero bytes follow
     size_t bytes;
 };
 constexpr int kPackCoutAlign = 64;
+constexpr int kPackZeroTail = 64;
 PackGeom qconv2d_pack_geom(int c_in, int c_out, int k_h, int k_w, DType dt);
 
 // Tile configuration chosen for a convolution.

@@ -30,6 +30,10 @@ SHAPES = [
     (1, 48, 128, 11, 7, 3, 1, 1, 1),    # several output-channel tiles
     (3, 2, 1, 6, 6, 3, 1, 1, 1),        # single output channel
     (1, 1, 2, 5, 4, 1, 2, 0, 1),        # single input channel, 1x1 stride 2
+    (2, 128, 64, 9, 10, 3, 1, 1, 1),    # one component per K stage, two channel blocks
+    (1, 96, 48, 11, 9, 3, 2, 1, 1),     # two components per K stage, three channel blocks
+    (1, 64, 256, 7, 8, 3, 1, 1, 1),     # one component per stage, four output-channel tiles
+    (3, 40, 24, 6, 7, 3, 1, 1, 2),      # ragged channel block, dilation 2
 ]
 
 
