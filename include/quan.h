@@ -20,7 +20,9 @@
  * All tensor pointers are device pointers owned by the caller; the library
  * never frees or retains them.  Activation and output pointers must be 16-byte
  * aligned; every other pointer must be aligned to its element size.  No tensor
- * may hold 2^31 or more elements.
+ * may hold 2^31 or more elements, and for the convolution one input image
+ * (H*W*4*C elements) times (256 / (H_out*W_out) + 2) must stay below 2^31
+ * bytes (the kernels address a tile's activations with 32-bit offsets).
  *
  * dtype is QUAN_F32 or QUAN_BF16 and applies to activations, weights, bias and
  * outputs of the convolution and to the IQBN input/output; accumulation is
@@ -106,9 +108,10 @@ QUAN_API int quan_qconv2d_forward(const void *x,
  * quan_qconv2d_forward_packed.
  *
  * quan_qconv2d_packed_bytes returns the size in bytes of the packed weights
- * for (c_in, c_out, k_h, k_w, dtype), or a negative QUAN_ERR_* code.  The
- * packed layout is private to the library but depends only on these five
- * values: weights packed once serve every later call with the same ones.
+ * for (c_in, c_out, k_h, k_w, dtype), or a negative QUAN_ERR_* code
+ * (QUAN_ERR_UNSUPPORTED when they would reach 2^31 bytes).  The packed
+ * layout is private to the library but depends only on these five values:
+ * weights packed once serve every later call with the same ones.
  *
  * quan_qconv2d_pack_weights reads w_r..w_k (as in quan_qconv2d_forward) and
  * writes `packed`, a caller-owned, 16-byte-aligned device buffer of at least

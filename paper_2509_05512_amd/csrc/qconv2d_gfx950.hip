@@ -15,27 +15,35 @@
 //
 // One work-group computes a tile of BM output pixels x 4*BNC output reals
 // (all four output components of BNC channels):
-//   - K runs over stages.  A stage is QS input components x CS channels with
-//     QS*CS*sizeof(T) = 128 bytes, so each activation row of a stage is one
-//     contiguous 128-byte piece of the channels-last pixel (full cache lines);
-//   - only the four shared real kernels are staged: an LDS weight block holds
-//     W_0..W_3 [BNC][CS] for one (tap, channel block) and serves all 4/QS
-//     stages of that block.  The signed 4x4 Hamilton block is formed on the
-//     LDS->register read: the fragment for (output component p, input
-//     component q) reads kernel p xor q and flips its sign bits with one XOR;
-//   - global -> LDS direct loads (global_load_lds_dwordx4) fill a ring of three
-//     activation stages and two weight blocks two stages ahead; the layout in
-//     LDS is XOR-swizzled so the MFMA fragment reads are bank-conflict free.
-//     Taps outside the image read a zero chunk;
-//   - fragments of the next k-step are read from LDS while the current
-//     k-step's MFMAs run; the next loads are issued after the stage's last LDS
-//     read (an LDS DMA holds back later LDS reads of its wave until it lands);
+//   - K runs over stages.  A stage is one tap and one block of CS channels
+//     of all four input components, 4*CS*sizeof(T) = 128 bytes: each
+//     activation row of a stage is one contiguous 128-byte piece of the
+//     channels-last pixel (one cache line);
+//   - only the four shared real kernels are staged: a stage's weights are
+//     W_0..W_3 [BNC][CS] (4*BNC rows of 32 bytes).  The signed 4x4 Hamilton
+//     block is formed on the LDS->register read: the fragment for (output
+//     component p, input component q) reads kernel p xor q and flips its
+//     sign bits with one XOR;
+//   - the work-group is four compute waves and two producer waves.  The
+//     producers move stages from global memory straight into LDS
+//     (buffer_load ... lds, 1 KB per instruction; each producer moves half
+//     of every stage), three stages ahead of the compute waves, into a
+//     four-stage ring.  One wave can keep at most 63 loads in flight (its
+//     6-bit vmcnt), too few to cover the latency at this bandwidth, hence two
+//     producers.  Rows outside the image
+//     read past the buffer range and land as zeros.  Compute waves only read
+//     fragments from LDS and issue MFMAs, one fragment read between
+//     consecutive MFMAs (a burst of LDS reads stalls the matrix pipe);
+//   - one barrier per stage, in the middle of the compute waves' step: the
+//     fragments of the next stage's first k-step are read after it while the
+//     current stage's last MFMAs run;
 //   - v_mfma_f32_32x32x16_bf16 (bf16) / v_mfma_f32_32x32x2f32 (fp32), fp32
-//     accumulators; epilogue adds the bias, rounds to the output type (RNE)
-//     and stores channels-last.
+//     accumulators in AGPRs; the epilogue adds the bias, rounds to the output
+//     type (RNE) and stores channels-last.
 #include <hip/hip_runtime.h>
 
 #include <cstdlib>
+#include <type_traits>
 
 #include "quan_launch.h"
 
@@ -65,20 +73,28 @@ struct Elem<float> {
     static constexpr unsigned sign = 0x80000000u;
 };
 
+// Channels per component in one stage (4 components x CS x sizeof(T) = 128 B).
+template <typename T>
+constexpr int stage_channels()
+{
+    return 128 / (4 * int(sizeof(T)));
+}
+
 struct KArgs {
     const void *x;
     const void *wpack;
     const void *bias;
     void *out;
-    int c_in, h, w, c_out, k_w;
+    int c_in, h, w, c_out, k_h, k_w;
     int s_h, s_w, p_h, p_w, d_h, d_w;
     int h_out, w_out;
     int m;       // n * h_out * w_out output pixels
     int stages;  // taps * n_cblk
     int n_cblk;
     int cout_pad;
-    int n_tiles;
-    int vec_in;  // c_in is a multiple of the 16-byte chunk
+    int m_tiles, n_tiles;
+    unsigned w_bytes;   // bytes of packed weights
+    long long x_elems;  // elements of x (n * h * w * 4 * c_in)
 };
 
 // XOR swizzle of the 16-byte chunk index within an LDS row of CPR chunks.
@@ -86,17 +102,14 @@ struct KArgs {
 // per group of 16 lanes (256 bytes, the full bank width) and from 8
 // consecutive rows per group of 8 lanes (128 bytes); the swizzle puts every
 // such group on distinct 16-byte bank slots in both views, so the MFMA
-// fragment reads are conflict free.
+// fragment reads are conflict free.  It depends on row % 16 only, so a row
+// offset by a multiple of 16 keeps its swizzle.
 template <int CPR>
 __device__ __forceinline__ int swz(int row)
 {
-    static_assert(CPR == 2 || CPR == 4 || CPR == 8 || CPR == 16, "swizzle defined for 32..256-byte rows");
-    if constexpr (CPR == 16)
-        return row & 15;
-    else if constexpr (CPR == 8)
+    static_assert(CPR == 2 || CPR == 8, "swizzle defined for 32- and 128-byte rows");
+    if constexpr (CPR == 8)
         return (row & 7) ^ ((row >> 3) & 1);
-    else if constexpr (CPR == 4)
-        return ((row >> 1) ^ (row >> 3)) & 3;
     else
         return ((row >> 2) ^ (row >> 3)) & 1;
 }
@@ -135,607 +148,592 @@ __device__ __forceinline__ void mfma_step(f32x16 &acc, u32x4 a, u32x4 b)
     }
 }
 
-template <typename T, int BM, int BNC, int WAVES_M, int WAVES_N, int BKC>
-__global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void qconv2d_igemm(KArgs a)
+// Instruction classes of __builtin_amdgcn_sched_group_barrier.
+constexpr int kSchedValu = 0x002, kSchedMfma = 0x008, kSchedDsRead = 0x100;
+
+// Orders one k-step's scheduling region: the VALU sign flips first, then
+// every MFMA followed by up to RPM LDS reads while any remain.  A burst of
+// LDS reads between MFMA groups stalls the matrix pipe on gfx950; a few reads
+// behind each MFMA hide it, and issuing them early in the k-step gives them
+// time to land before the next k-step needs them.
+template <int NMFMA, int NFLIP, int NDSR, int RPM = 2>
+__device__ __forceinline__ void interleave_kstep()
 {
-    constexpr int EPC = Elem<T>::per_chunk;
-    constexpr int NT = 64 * WAVES_M * WAVES_N;
-    constexpr int BN = 4 * BNC;
-    constexpr int CPQ = BKC / EPC;  // chunks per component in a stage
-    constexpr int CPR = 4 * CPQ;    // chunks per activation row in a stage
-    constexpr int WTM = BM / WAVES_M;
-    constexpr int WTN = BN / WAVES_N;
-    constexpr int MB = WTM / 32;
-    constexpr int NB = WTN / 32;
-    constexpr int A_CHUNKS = BM * CPR;
-    constexpr int B_CHUNKS = 4 * BNC * CPQ;
-    constexpr int A_PER_T = A_CHUNKS / NT;
-    constexpr int B_PER_T = (B_CHUNKS + NT - 1) / NT;
-    constexpr int A_BYTES = A_CHUNKS * 16;
-    constexpr int B_BYTES = B_CHUNKS * 16;
-    constexpr int STAGE = A_BYTES + B_BYTES;
-    constexpr int ROWS_PER_PASS = NT / CPR;
-    static_assert(A_CHUNKS % NT == 0 && NT % CPR == 0, "activation tile must split evenly");
-    static_assert(CPQ % 2 == 0, "a k-step takes two chunks of one component");
-    static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile must be whole 32x32 blocks");
-    static_assert(BNC % 4 == 0, "epilogue stores groups of four channels");
-
-    __shared__ __attribute__((aligned(16))) unsigned char smem[2 * STAGE];
-
-    const T *__restrict__ xp = static_cast<const T *>(a.x);
-    const T *__restrict__ wp = static_cast<const T *>(a.wpack);
-
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = tid >> 6;
-    const int wm = wave % WAVES_M;
-    const int wn = wave / WAVES_M;
-    const int khalf = lane >> 5;
-    const int l32 = lane & 31;
-
-    // Work-groups are dealt to the 8 XCDs round-robin; give each XCD a
-    // contiguous run of tiles so neighbouring tiles share its L2.
-    const int nblk = gridDim.x;
-    const int bid = blockIdx.x;
-    const int per = nblk >> 3, rem = nblk & 7, xcd = bid & 7;
-    const int tile = (xcd < rem ? xcd * (per + 1) : rem * (per + 1) + (xcd - rem) * per) + (bid >> 3);
-    const int n_tile = tile % a.n_tiles;
-    const int m0 = (tile / a.n_tiles) * BM;
-    const int o0 = n_tile * BNC;
-
-    // ---- activation rows this thread loads (fixed for the whole K loop) ----
-    const int cc = tid % CPR;  // chunk column within the stage row
-    const int q_ld = cc / CPQ;
-    const int piece = cc % CPQ;
-    const int hw_out = a.h_out * a.w_out;
-    int row_iy0[A_PER_T], row_ix0[A_PER_T], row_img[A_PER_T];
+    if constexpr (NFLIP > 0)
+        __builtin_amdgcn_sched_group_barrier(kSchedValu, NFLIP, 0);
 #pragma unroll
-    for (int i = 0; i < A_PER_T; ++i) {
-        const int m = m0 + i * ROWS_PER_PASS + tid / CPR;
-        if (m < a.m) {
-            const int img = m / hw_out;
-            const int rr = m - img * hw_out;
-            const int oy = rr / a.w_out;
-            const int ox = rr - oy * a.w_out;
-            row_img[i] = img * a.h * a.w;
-            row_iy0[i] = oy * a.s_h - a.p_h;
-            row_ix0[i] = ox * a.s_w - a.p_w;
-        } else {
-            row_img[i] = 0;
-            row_iy0[i] = -0x20000000;  // never inside the image
-            row_ix0[i] = 0;
-        }
+    for (int i = 0; i < NMFMA; ++i) {
+        __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+#pragma unroll
+        for (int r = 0; r < RPM; ++r)
+            if (i * RPM + r < NDSR)
+                __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
     }
-    const int row_elems = 4 * a.c_in;
-
-    u32x4 ra[A_PER_T], rb[B_PER_T];
-
-    auto load_stage = [&](int s) {
-        const int tap = s / a.n_cblk;
-        const int cblk = s - tap * a.n_cblk;
-        const int ky = tap / a.k_w;
-        const int kx = tap - ky * a.k_w;
-        const int dy = ky * a.d_h, dx = kx * a.d_w;
-        const int c = cblk * BKC + piece * EPC;
-        const int cvalid = a.c_in - c;  // elements of this chunk inside c_in
-#pragma unroll
-        for (int i = 0; i < A_PER_T; ++i) {
-            const int iy = row_iy0[i] + dy;
-            const int ix = row_ix0[i] + dx;
-            const bool inside = (unsigned)iy < (unsigned)a.h && (unsigned)ix < (unsigned)a.w && cvalid > 0;
-            u32x4 v = {0u, 0u, 0u, 0u};
-            if (inside) {
-                const T *src = xp + ((row_img[i] + iy * a.w + ix) * row_elems + q_ld * a.c_in + c);
-                if (a.vec_in)
-                    v = *reinterpret_cast<const u32x4 *>(src);
-                else
-                    v = load_chunk_masked<T>(src, cvalid);
-            }
-            ra[i] = v;
-        }
-        const T *wsrc = wp + ((size_t)(tap * a.n_cblk + cblk) * 4 * a.cout_pad + o0) * BKC;
-#pragma unroll
-        for (int j = 0; j < B_PER_T; ++j) {
-            const int id = j * NT + tid;
-            if (B_CHUNKS % NT == 0 || id < B_CHUNKS) {
-                const int ws = id / (BNC * CPQ);
-                const int rest = id - ws * (BNC * CPQ);
-                rb[j] = *reinterpret_cast<const u32x4 *>(wsrc + (size_t)ws * a.cout_pad * BKC +
-                                                         rest * EPC);
-            }
-        }
-    };
-
-    auto store_stage = [&](int buf) {
-        unsigned char *As = smem + buf * STAGE;
-        unsigned char *Bs = As + A_BYTES;
-#pragma unroll
-        for (int i = 0; i < A_PER_T; ++i) {
-            const int r = i * ROWS_PER_PASS + tid / CPR;
-            *reinterpret_cast<u32x4 *>(As + (r * CPR + (cc ^ swz<CPR>(r))) * 16) = ra[i];
-        }
-#pragma unroll
-        for (int j = 0; j < B_PER_T; ++j) {
-            const int id = j * NT + tid;
-            if (B_CHUNKS % NT == 0 || id < B_CHUNKS) {
-                const int row = id / CPQ;  // kernel slice * BNC + o
-                const int pc = id - row * CPQ;
-                *reinterpret_cast<u32x4 *>(Bs + (row * CPQ + (pc ^ swz<CPQ>(row))) * 16) = rb[j];
-            }
-        }
-    };
-
-    // Per-lane output component and channel of the weight-fragment rows.
-    int frag_p[NB], frag_o[NB];
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-        const int tn = wn * WTN + nb * 32 + l32;
-        frag_p[nb] = tn / BNC;
-        frag_o[nb] = tn - frag_p[nb] * BNC;
-    }
-
-    f32x16 acc[NB][MB];
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-        for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-            for (int e = 0; e < 16; ++e)
-                acc[nb][mb][e] = 0.0f;
-
-    auto compute = [&](int buf) {
-        const unsigned char *As = smem + buf * STAGE;
-        const unsigned char *Bs = As + A_BYTES;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-#pragma unroll
-            for (int kk = 0; kk < CPQ / 2; ++kk) {
-                const int pc = kk * 2 + khalf;
-                u32x4 wf[NB], pf[MB];
-#pragma unroll
-                for (int nb = 0; nb < NB; ++nb) {
-                    const int p = frag_p[nb];
-                    const int row = (p ^ q) * BNC + frag_o[nb];
-                    u32x4 v = *reinterpret_cast<const u32x4 *>(Bs + (row * CPQ + (pc ^ swz<CPQ>(row))) * 16);
-                    const unsigned flip = ((kHamiltonNeg >> (4 * p + q)) & 1u) ? Elem<T>::sign : 0u;
-                    v ^= flip;
-                    wf[nb] = v;
-                }
-#pragma unroll
-                for (int mb = 0; mb < MB; ++mb) {
-                    const int r = wm * WTM + mb * 32 + l32;
-                    const int lc = q * CPQ + pc;
-                    pf[mb] = *reinterpret_cast<const u32x4 *>(As + (r * CPR + (lc ^ swz<CPR>(r))) * 16);
-                }
-#pragma unroll
-                for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-                    for (int mb = 0; mb < MB; ++mb)
-                        mfma_step<T>(acc[nb][mb], wf[nb], pf[mb]);
-            }
-        }
-    };
-
-    // ---- main loop: two LDS stages, next stage prefetched into registers ----
-    load_stage(0);
-    store_stage(0);
-    __syncthreads();
-    for (int s = 0; s < a.stages; ++s) {
-        const int cur = s & 1;
-        const bool more = s + 1 < a.stages;
-        if (more)
-            load_stage(s + 1);
-        compute(cur);
-        if (more)
-            store_stage(cur ^ 1);
-        __syncthreads();
-    }
-
-    // ---- epilogue: bias, round, channels-last store ----
-    // Accumulator register 4*g + e of lane l holds output channel row
-    // 8*g + 4*(l/32) + e of the 32x32 block and pixel column l%32.
-    const T *__restrict__ bias = static_cast<const T *>(a.bias);
-    T *__restrict__ out = static_cast<T *>(a.out);
-    const bool vec_out = (a.c_out & 3) == 0;
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-            const int tn = wn * WTN + nb * 32 + 8 * g + 4 * khalf;
-            const int p = tn / BNC;
-            const int o = o0 + (tn - p * BNC);
-            if (o >= a.c_out)
-                continue;
-            float bv[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-                bv[e] = (bias != nullptr && o + e < a.c_out) ? float(bias[p * a.c_out + o + e]) : 0.0f;
-#pragma unroll
-            for (int mb = 0; mb < MB; ++mb) {
-                const int m = m0 + wm * WTM + mb * 32 + l32;
-                if (m >= a.m)
-                    continue;
-                T *dst = out + ((size_t)m * 4 * a.c_out + p * a.c_out + o);
-                T v[4];
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    v[e] = T(acc[nb][mb][4 * g + e] + bv[e]);
-                if (vec_out) {
-                    if constexpr (sizeof(T) == 2) {
-                        uint2 pk;
-                        __builtin_memcpy(&pk, v, 8);
-                        *reinterpret_cast<uint2 *>(dst) = pk;
-                    } else {
-                        float4 pk;
-                        __builtin_memcpy(&pk, v, 16);
-                        *reinterpret_cast<float4 *>(dst) = pk;
-                    }
-                } else {
-#pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        if (o + e < a.c_out)
-                            dst[e] = v[e];
-                }
-            }
-        }
-    }
+    if constexpr (NDSR > NMFMA * RPM)
+        __builtin_amdgcn_sched_group_barrier(kSchedDsRead, NDSR - NMFMA * RPM, 0);
 }
 
-// ---------------------------------------------------------------------------
-// Pipelined variant: global -> LDS direct loads into a ring of STAGES LDS
-// buffers, so the loads of the next STAGES-1 stages are in flight while the
-// current stage is multiplied.  Each global_load_lds_dwordx4 of a wave writes
-// 64 consecutive 16-byte LDS slots (lane order); the swizzled layout is
-// obtained by choosing which global chunk each lane fetches.  Taps outside
-// the image, channels past c_in and rows past M fetch a zero chunk.
-// Requires c_in to be a multiple of the 16-byte vector (vec_in).
-// ---------------------------------------------------------------------------
+// Raw buffer resource over [base, base + bytes): loads past the end return
+// zero.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, unsigned bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, 0x00020000);
+}
 
-__device__ __attribute__((aligned(64))) unsigned int g_qconv_zero16[16];
+// LDS address of a __shared__ pointer, as the 32-bit value M0 takes.
+__device__ __forceinline__ unsigned lds_addr(const void *p)
+{
+    return __builtin_amdgcn_readfirstlane(
+        (unsigned)(size_t)(const __attribute__((address_space(3))) void *)p);
+}
+
+// One 16-byte chunk per lane from byte offset voff + soff of the buffer
+// [base, base + bytes) straight into LDS at m0 + 16 * lane; offsets past the
+// end land as zeros.  The compiler does not see this load: the issuing wave
+// waits for it with s_waitcnt vmcnt, and no wave that issues these reads LDS
+// (an outstanding LDS DMA holds back the issuing wave's own LDS reads).  The
+// scalar operands go through readfirstlane so they sit in SGPRs even where
+// the compiler kept a copy in a VGPR.
+__device__ __forceinline__ void dma16(const void *base, unsigned bytes, unsigned voff, unsigned soff,
+                                      unsigned m0)
+{
+    const unsigned long long b = (unsigned long long)base;
+    const unsigned lo = __builtin_amdgcn_readfirstlane(unsigned(b));
+    const unsigned hi = __builtin_amdgcn_readfirstlane(unsigned(b >> 32));
+    const __amdgpu_buffer_rsrc_t rsrc =
+        make_rsrc((const void *)(((unsigned long long)hi << 32) | lo), __builtin_amdgcn_readfirstlane(bytes));
+    asm volatile("s_mov_b32 m0, %3\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds" ::"v"(voff),
+                 "s"(rsrc), "s"(__builtin_amdgcn_readfirstlane(soff)), "s"(__builtin_amdgcn_readfirstlane(m0))
+                 : "memory");
+}
 
 template <int N>
 __device__ __forceinline__ void wait_vmcnt()
 {
-    static_assert(N >= 0 && N < 64, "vmcnt range");
-    // gfx9 s_waitcnt: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt_hi[15:14]
+    static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
+    // vmcnt[3:0] | expcnt (7) | lgkmcnt (15) | vmcnt[5:4]
     __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
 
-__device__ __forceinline__ void block_barrier()
+// One work-group: WAVES_M x WAVES_N compute waves, each MB x NB blocks of 32
+// pixels x 32 output reals, and NPROD producer waves.  Tile: BM = 32*MB*WAVES_M
+// pixels x BN = 32*NB*WAVES_N output reals (BN/4 output channels, all four
+// components).  VEC: c_in is a multiple of the 16-byte chunk, so activations
+// move by DMA; otherwise the producer loads partial chunks element-wise.
+template <typename T, int MB, int NB, int WAVES_M, int WAVES_N, bool VEC>
+__global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + 2)) void qconv2d_igemm(KArgs a)
 {
-    __atomic_signal_fence(__ATOMIC_SEQ_CST);
-    __builtin_amdgcn_s_barrier();
-    __atomic_signal_fence(__ATOMIC_SEQ_CST);
-}
+    constexpr int ES = int(sizeof(T));
+    constexpr int EPC = Elem<T>::per_chunk;
+    constexpr int CS = stage_channels<T>();
+    constexpr int CPQ = CS / EPC;  // 16-byte chunks per component (2)
+    constexpr int NCW = WAVES_M * WAVES_N;
+    constexpr int NPROD = 2;                    // producer waves
+    constexpr int WTM = 32 * MB;
+    constexpr int WTN = 32 * NB;
+    constexpr int BM = WTM * WAVES_M;
+    constexpr int BN = WTN * WAVES_N;
+    constexpr int BNC = BN / 4;
+    constexpr int NBUF = 4;                     // stages in the LDS ring
+    constexpr int A_BYTES = BM * 128;           // one stage of activations
+    constexpr int B_BYTES = 4 * BNC * CS * ES;  // one stage of weights
+    constexpr int A_INSTR = BM / 8;             // DMA instructions per stage (8 rows of 128 B each)
+    constexpr int B_INSTR = B_BYTES / 1024;
+    // DMA instructions of one producer per stage (producer pr takes the
+    // instructions with index = pr mod NPROD)
+    constexpr int PER_STAGE = (A_INSTR + NPROD - 1) / NPROD + (B_INSTR + NPROD - 1) / NPROD;
+    constexpr int LOOKAHEAD = 3;                // stages issued ahead of the one being read
+    constexpr int N_MFMA = MB * NB * (ES == 2 ? 1 : 4);  // MFMA instructions per k-step
+    constexpr bool P_UNIFORM = BNC >= 32;       // a 32-wide N block lies in one output component
+    static_assert(CPQ == 2 && CS * 4 * ES == 128, "stage row is 128 bytes");
+    static_assert(BNC % 16 == 0 && kPackCoutAlign % BNC == 0 && B_BYTES % 1024 == 0, "tile geometry");
+    static_assert(LOOKAHEAD * PER_STAGE <= 63, "the stages in flight must fit the vmcnt counter");
+    static_assert(A_INSTR % NPROD == 0 && B_INSTR % NPROD == 0, "producers split every stage evenly");
 
-// One wave-wide 16-byte-per-lane global -> LDS load: lane l's 16 bytes land at
-// LDS byte address lds_base + 16*l.  Issued as assembly so that the compiler
-// does not track it as an LDS write (it would otherwise wait for every such
-// load before each LDS read); completion is awaited explicitly with
-// wait_vmcnt before the barrier that publishes the stage.  M0 is set here and
-// is not used by any other instruction of these kernels; the s_nop is the
-// wait state the ISA requires between writing M0 and an LDS DMA reading it.
-__device__ __forceinline__ void dma16(const void *g, const unsigned char *lds_slot0)
-{
-    const unsigned base = __builtin_amdgcn_readfirstlane(
-        (unsigned)(size_t)(const __attribute__((address_space(3))) void *)lds_slot0);
-    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(base)
-                 : "memory");
-}
+    // Deferred epilogue (DEFER): when a wave holds one output component for
+    // all BM pixels, it parks each finished tile in its own LDS region and
+    // drains it with full-line 16-byte stores during the next tile's steps,
+    // instead of every work-group writing its tile at the same moment.
+    constexpr bool DEFER = WAVES_M == 1 && WTN == BNC && P_UNIFORM;
+    constexpr int OUT_ROW = BNC * ES;     // bytes of one pixel in a wave's region
+    constexpr int OUT_CPR = OUT_ROW / 16;  // 16-byte chunks per pixel
+    constexpr int OUT_WAVE = BM * OUT_ROW;
+    constexpr int N_DRAIN = OUT_WAVE / 1024;  // 1 KB stores per wave per tile
+    constexpr int OUT_BYTES = DEFER ? NCW * OUT_WAVE : 0;
+    static_assert(!DEFER || (OUT_CPR >= 2 && (64 / OUT_CPR) % OUT_CPR == 0), "drain geometry");
 
-// Stage geometry of the pipelined kernel: a K stage is QS input components
-// x CS channels, chosen so that one activation row of a stage is exactly one
-// contiguous 128-byte segment of the channels-last pixel.  The weight block
-// of a (tap, channel block) -- the four real kernels W_0..W_3 for BNC output
-// channels x CS input channels -- serves all 4/QS stages of that block.
-template <typename T, int QS>
-struct StageGeom {
-    static constexpr int EPC = Elem<T>::per_chunk;
-    static constexpr int CS = 128 / (QS * int(sizeof(T)));  // channels per component
-    static constexpr int CPQ = CS / EPC;                     // chunks per component
-    static constexpr int NQG = 4 / QS;                       // stages per weight block
-};
-
-template <typename T, int BM, int BNC, int WAVES_M, int WAVES_N, int QS>
-__global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void qconv2d_igemm_dma(KArgs a)
-{
-    using SG = StageGeom<T, QS>;
-    constexpr int EPC = SG::EPC;
-    constexpr int CS = SG::CS;
-    constexpr int CPQ = SG::CPQ;
-    constexpr int NQG = SG::NQG;
-    constexpr int NWAVES = WAVES_M * WAVES_N;
-    constexpr int BN = 4 * BNC;
-    constexpr int CPR = 8;  // 128-byte activation rows
-    constexpr int WTM = BM / WAVES_M;
-    constexpr int WTN = BN / WAVES_N;
-    constexpr int MB = WTM / 32;
-    constexpr int NB = WTN / 32;
-    constexpr int A_ST = 3;                   // activation ring
-    constexpr int B_ST = NQG == 1 ? 3 : 2;    // weight-block ring
-    constexpr int A_BYTES = BM * 128;
-    constexpr int B_BYTES = 4 * BNC * CPQ * 16;
-    constexpr int A_INSTR = A_BYTES / 1024;  // 1 KB wave loads per stage
-    constexpr int B_INSTR = B_BYTES / 1024;  // 1 KB wave loads per weight block
-    constexpr int A_PER_WAVE = A_INSTR / NWAVES;
-    constexpr int B_MAX = (B_INSTR + NWAVES - 1) / NWAVES;  // round-robin over waves
-    constexpr int LB_HI = B_MAX;
-    constexpr int LB_LO = B_INSTR % NWAVES == 0 ? B_MAX : B_MAX - 1;
-    constexpr int B_ROWS_PER_INSTR = 64 / CPQ;
-    constexpr int KSTEPS = 4;  // 32x32 MFMA k-steps per stage (two chunks each)
-    static_assert(A_INSTR % NWAVES == 0, "activation stage must split into wave loads");
-    static_assert(B_BYTES % 1024 == 0, "weight block must be whole 1 KB wave loads");
-    static_assert(WTM % 32 == 0 && WTN % 32 == 0 && BNC % 4 == 0, "tile geometry");
-    static_assert(QS * CPQ == 8, "a stage row is eight chunks");
-
-    __shared__ __attribute__((aligned(1024))) unsigned char smem[A_ST * A_BYTES + B_ST * B_BYTES];
-    unsigned char *const a_ring = smem;
-    unsigned char *const b_ring = smem + A_ST * A_BYTES;
-
-    const T *__restrict__ xp = static_cast<const T *>(a.x);
-    const T *__restrict__ wp = static_cast<const T *>(a.wpack);
-    const void *zero = g_qconv_zero16;
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[NBUF * (A_BYTES + B_BYTES) + OUT_BYTES];
+    unsigned char *const a_lds = smem;
+    unsigned char *const b_lds = smem + NBUF * A_BYTES;
+    unsigned char *const o_lds = smem + NBUF * (A_BYTES + B_BYTES);
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+    // Persistent work-groups (at most one per tile).  Work-groups are dealt
+    // to the 8 XCDs round-robin, block b to XCD b % 8; XCD x owns a
+    // contiguous range of tiles in proportion to its work-groups, so
+    // neighbouring tiles share its L2, and its work-groups take that range's
+    // tiles in turn.  The split only steers locality: every tile belongs to
+    // exactly one work-group whatever the placement.
+    const int n_wg = gridDim.x, bid = blockIdx.x;
+    const int xcd = bid & 7, xslot = bid >> 3;
+    const int cnt_x = (n_wg >> 3) + (xcd < (n_wg & 7) ? 1 : 0);
+    const int before_x = xcd * (n_wg >> 3) + (xcd < (n_wg & 7) ? xcd : (n_wg & 7));
+    const int tiles = a.m_tiles * a.n_tiles;
+    const int x_lo = int((long long)tiles * before_x / n_wg);
+    const int x_hi = int((long long)tiles * (before_x + cnt_x) / n_wg);
+    const int n_mine = x_hi - x_lo > xslot ? (x_hi - x_lo - xslot + cnt_x - 1) / cnt_x : 0;
+    if (n_mine == 0)
+        return;  // the whole work-group leaves: no barrier is pending
+    auto tile_of = [&](int k) { return x_lo + xslot + k * cnt_x; };
+    const int S = a.stages;
+    const int total = n_mine * S;  // steps of this work-group, all tiles
+
+    if (wave >= NCW) {
+        // ================= producer waves =================
+        const int pr = wave - NCW;
+        const int hw_out = a.h_out * a.w_out;
+        const int row_elems = 4 * a.c_in;
+        const long long img_elems = (long long)a.h * a.w * row_elems;
+        const unsigned a_base = lds_addr(a_lds), b_base = lds_addr(b_lds);
+        const unsigned w_stage_bytes = unsigned(4 * a.cout_pad * CS * ES);
+        constexpr int A_MINE = A_INSTR / NPROD, B_MINE = B_INSTR / NPROD;
+
+        // Issue cursor: tile k (of this work-group), stage t of that tile at
+        // tap (ky, kx) and channel block cblk, and the tile's DMA plan.
+        int k = 0, ky = 0, kx = 0, cblk = 0;
+        const T *xt = nullptr;
+        unsigned x_bytes = 0;  // bytes of x from xt on (capped at 2^31 - 1)
+        int p_off[A_MINE], p_iy[A_MINE], p_ix[A_MINE], p_cl[A_MINE];
+        unsigned p_woff[B_MINE];
+        // Activation DMA i covers rows 8i..8i+7 of the tile: lane l loads
+        // row 8i + l/8 into physical chunk l%8, i.e. logical chunk
+        // lc = (l%8) ^ swz(row): component lc/2, channels 8*(lc%2).. of the
+        // stage's channel block (bf16; 4*(lc%2).. for fp32).  Offsets are
+        // relative to the first image of the tile.  Weight DMA j covers LDS
+        // slots 64j..64j+63 of the stage's weights: slot = row * 2 +
+        // physical chunk, row = kernel * BNC + o.
+        auto plan_tile = [&](int kt) {
+            const int tile = tile_of(kt);
+            const int m0 = (tile / a.n_tiles) * BM;
+            const int o0 = (tile % a.n_tiles) * BNC;
+            const int img0 = m0 / hw_out;
+            xt = static_cast<const T *>(a.x) + img0 * img_elems;
+            const long long rest = (a.x_elems - img0 * img_elems) * ES;
+            x_bytes = rest <= 0 ? 0u : (rest < 0x7fffffffLL ? unsigned(rest) : 0x7fffffffu);
+#pragma unroll
+            for (int ii = 0; ii < A_MINE; ++ii) {
+                const int i = ii * NPROD + pr;  // instruction index within the stage
+                const int row = 8 * i + (lane >> 3);
+                const int lc = (lane & 7) ^ swz<8>(row);
+                const int comp = lc / CPQ, cin = (lc % CPQ) * EPC;
+                const int m = m0 + row;
+                p_cl[ii] = a.c_in - cin;  // channels of this chunk left before block 0
+                if (m < a.m) {
+                    const int img = m / hw_out;
+                    const int rr = m - img * hw_out;
+                    const int oy = rr / a.w_out;
+                    const int ox = rr - oy * a.w_out;
+                    p_iy[ii] = oy * a.s_h - a.p_h;
+                    p_ix[ii] = ox * a.s_w - a.p_w;
+                    const int e = (((img - img0) * a.h + p_iy[ii]) * a.w + p_ix[ii]) * row_elems +
+                                  comp * a.c_in + cin;
+                    p_off[ii] = VEC ? e * ES : e;
+                } else {
+                    p_iy[ii] = -0x20000000;  // rows past M never load
+                    p_ix[ii] = 0;
+                    p_off[ii] = 0;
+                }
+            }
+#pragma unroll
+            for (int jj = 0; jj < B_MINE; ++jj) {
+                const int j = jj * NPROD + pr;
+                const int slot = 64 * j + lane;
+                const int row = slot / CPQ;
+                const int lc = (slot % CPQ) ^ swz<CPQ>(row);
+                const int ws = row / BNC, o = row - (row / BNC) * BNC;
+                p_woff[jj] = unsigned(((ws * a.cout_pad + o0 + o) * CS + lc * EPC) * ES);
+            }
+        };
+        plan_tile(0);
+        // Issues the cursor's stage into ring slot g % NBUF and advances the
+        // cursor (to the next tile after its last stage).
+        auto issue = [&](int g) {
+            const int buf = g & (NBUF - 1);
+            const int t = (ky * a.k_w + kx) * a.n_cblk + cblk;  // stage within the tile
+#pragma unroll
+            for (int jj = 0; jj < B_MINE; ++jj)
+                dma16(a.wpack, a.w_bytes, p_woff[jj], unsigned(t) * w_stage_bytes,
+                      b_base + buf * B_BYTES + (jj * NPROD + pr) * 1024);
+            const int dy = ky * a.d_h, dx = kx * a.d_w, cbase = cblk * CS;
+            const int shift = (dy * a.w + dx) * row_elems + cbase;  // elements
+#pragma unroll
+            for (int ii = 0; ii < A_MINE; ++ii) {
+                const int i = ii * NPROD + pr;
+                const bool inside = ((unsigned)(p_iy[ii] + dy) < (unsigned)a.h) &
+                                    ((unsigned)(p_ix[ii] + dx) < (unsigned)a.w) & (cbase < p_cl[ii]);
+                if constexpr (VEC) {
+                    const unsigned off = inside ? unsigned(p_off[ii] + shift * ES) : 0x80000000u;
+                    dma16(xt, x_bytes, off, 0u, a_base + buf * A_BYTES + i * 1024);
+                } else {
+                    u32x4 v = {0u, 0u, 0u, 0u};
+                    if (inside)
+                        v = load_chunk_masked<T>(xt + (p_off[ii] + shift), p_cl[ii] - cbase);
+                    *reinterpret_cast<u32x4 *>(a_lds + buf * A_BYTES + i * 1024 + lane * 16) = v;
+                }
+            }
+            if (++cblk == a.n_cblk) {
+                cblk = 0;
+                if (++kx == a.k_w) {
+                    kx = 0;
+                    if (++ky == a.k_h && ++k < n_mine) {
+                        ky = 0;
+                        plan_tile(k);
+                    }
+                }
+            }
+        };
+        // Waits until all but this producer's DMAs of the `later` most
+        // recently issued stages have landed.
+        auto wait_landed = [&](int later) {
+            if constexpr (VEC) {
+                if (later >= 2)
+                    wait_vmcnt<2 * PER_STAGE>();
+                else if (later == 1)
+                    wait_vmcnt<PER_STAGE>();
+                else
+                    wait_vmcnt<0>();
+            } else {
+                wait_vmcnt<0>();
+            }
+        };
+        // prologue: steps 0..2; step 0 lands before the first barrier
+        for (int g = 0; g < LOOKAHEAD && g < total; ++g)
+            issue(g);
+        wait_landed(total - 1 < LOOKAHEAD - 1 ? total - 1 : LOOKAHEAD - 1);
+        __syncthreads();
+        // Iteration g: step g+3 goes into the slot step g-1 left before the
+        // barrier of step g-1; step g+1 lands before the barrier of step g,
+        // after which the compute waves first read it.  Steps run on across
+        // tiles, so the next tile's first stages arrive during this tile's
+        // last steps and epilogue.
+        for (int g = 0; g < total; ++g) {
+            if (g + LOOKAHEAD < total)
+                issue(g + LOOKAHEAD);
+            wait_landed(g + 3 < total ? 2 : (g + 2 < total ? 1 : 0));
+            __syncthreads();
+        }
+        return;
+    }
+
+    // ================= compute waves =================
     const int wm = wave % WAVES_M;
     const int wn = wave / WAVES_M;
     const int khalf = lane >> 5;
     const int l32 = lane & 31;
 
-    const int nblk = gridDim.x;
-    const int bid = blockIdx.x;
-    const int per = nblk >> 3, rem = nblk & 7, xcd = bid & 7;
-    const int tile = (xcd < rem ? xcd * (per + 1) : rem * (per + 1) + (xcd - rem) * per) + (bid >> 3);
-    const int n_tile = tile % a.n_tiles;
-    const int m0 = (tile / a.n_tiles) * BM;
-    const int o0 = n_tile * BNC;
-
-    // ---- per-lane activation load plan: A_PER_WAVE rows, one chunk each ----
-    // a_off: element offset of the chunk at tap (0, 0), channel block 0,
-    // component group 0 (only used when the tap lies inside the image).
-    const int hw_out = a.h_out * a.w_out;
-    const int row_elems = 4 * a.c_in;
-    int a_off[A_PER_WAVE], a_iy0[A_PER_WAVE], a_ix0[A_PER_WAVE], a_cin[A_PER_WAVE];
+    // K-step j of a stage is input component q = j: chunks 2j + {0, 1} of the
+    // activation row and chunks {0, 1} of weight row (p ^ j) * BNC + o.  Lane
+    // l reads chunk 2j + l/32 (activations) / chunk l/32 (weights) of row
+    // l%32 of its 32-row block.
+    int a_rd[4];
 #pragma unroll
-    for (int i = 0; i < A_PER_WAVE; ++i) {
-        const int r = (wave * A_PER_WAVE + i) * 8 + lane / 8;
-        const int lc = (lane % 8) ^ swz<CPR>(r);  // logical chunk this slot holds
-        const int qi = lc / CPQ, piece = lc % CPQ;
-        a_cin[i] = piece * EPC;
-        const int m = m0 + r;
-        if (m < a.m) {
-            const int img = m / hw_out;
-            const int rr = m - img * hw_out;
-            const int oy = rr / a.w_out;
-            const int ox = rr - oy * a.w_out;
-            a_iy0[i] = oy * a.s_h - a.p_h;
-            a_ix0[i] = ox * a.s_w - a.p_w;
-            a_off[i] = ((img * a.h + a_iy0[i]) * a.w + a_ix0[i]) * row_elems + qi * a.c_in + piece * EPC;
-        } else {
-            a_iy0[i] = -0x20000000;  // rows past M never load
-            a_ix0[i] = 0;
-            a_off[i] = 0;
-        }
-    }
-    // ---- per-lane weight load plan ----
-    const bool b_full = B_INSTR % NWAVES == 0 || wave < B_INSTR % NWAVES;  // issues B_MAX loads
-    int b_off[B_MAX];
-#pragma unroll
-    for (int j = 0; j < B_MAX; ++j) {
-        const int row = (wave + j * NWAVES) * B_ROWS_PER_INSTR + lane / CPQ;  // ws * BNC + o
-        const int lc = (lane % CPQ) ^ swz<CPQ>(row);
-        const int ws = row / BNC, o = row - (row / BNC) * BNC;
-        b_off[j] = ws * a.cout_pad * CS + (o0 + o) * CS + lc * EPC;
-    }
-
-    // Loads of stage s: its weight block first when s opens a block, then the
-    // activation tile.
-    auto issue = [&](int s) {
-        const int blk = s / NQG;
-        const int qg = s - blk * NQG;
-        if (qg == 0) {
-            unsigned char *Bs = b_ring + (blk % B_ST) * B_BYTES;
-            const T *wsrc = wp + (size_t)blk * 4 * a.cout_pad * CS;
-#pragma unroll
-            for (int j = 0; j < B_MAX; ++j)
-                if (j < B_MAX - 1 || b_full)
-                    dma16(wsrc + b_off[j], Bs + (wave + j * NWAVES) * 1024);
-        }
-        const int tap = blk / a.n_cblk;
-        const int cblk = blk - tap * a.n_cblk;
-        const int ky = tap / a.k_w;
-        const int kx = tap - ky * a.k_w;
-        const int dy = ky * a.d_h, dx = kx * a.d_w;
-        const int cbase = cblk * CS;
-        const int shift = (dy * a.w + dx) * row_elems + qg * QS * a.c_in + cbase;  // uniform
-        unsigned char *As = a_ring + (s % A_ST) * A_BYTES;
-#pragma unroll
-        for (int i = 0; i < A_PER_WAVE; ++i) {
-            const bool inside = (unsigned)(a_iy0[i] + dy) < (unsigned)a.h &&
-                                (unsigned)(a_ix0[i] + dx) < (unsigned)a.w && cbase + a_cin[i] < a.c_in;
-            const void *src = inside ? (const void *)(xp + (a_off[i] + shift)) : zero;
-            dma16(src, As + (wave * A_PER_WAVE + i) * 1024);
-        }
-    };
-
-    int frag_p[NB], frag_o[NB];
+    for (int j = 0; j < 4; ++j)
+        a_rd[j] = (wm * WTM + l32) * 128 + (((2 * j + khalf) ^ swz<8>(l32)) * 16);
+    // When all N blocks of a wave lie in one output component (SHARED_P),
+    // block nb's weight rows are block 0's plus 32*nb: an immediate offset.
+    constexpr bool SHARED_P = P_UNIFORM && WTN <= BNC;
+    constexpr int NB_RD = SHARED_P ? 1 : NB;
+    int b_rd[NB_RD][4];
+    unsigned flip[NB][4];
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
         const int tn = wn * WTN + nb * 32 + l32;
-        frag_p[nb] = tn / BNC;
-        frag_o[nb] = tn - frag_p[nb] * BNC;
+        const int p = P_UNIFORM ? __builtin_amdgcn_readfirstlane(tn / BNC) : tn / BNC;
+        const int o = tn % BNC;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int row = (p ^ j) * BNC + o;
+            if (nb < NB_RD)
+                b_rd[nb][j] = row * CPQ * 16 + ((khalf ^ swz<CPQ>(o)) * 16);
+            flip[nb][j] = ((kHamiltonNeg >> (4 * p + j)) & 1u) ? Elem<T>::sign : 0u;
+        }
     }
 
     f32x16 acc[NB][MB];
+    struct Frags {
+        u32x4 w[NB];
+        u32x4 p[MB];
+    };
+    auto read_frags = [&](int buf, int j, Frags &f) {
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
+        for (int nb = 0; nb < NB; ++nb) {
+            const int rd = SHARED_P ? b_rd[0][j] + nb * 32 * CPQ * 16 : b_rd[nb < NB_RD ? nb : 0][j];
+            f.w[nb] = *reinterpret_cast<const u32x4 *>(b_lds + buf * B_BYTES + rd);
+        }
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-            for (int e = 0; e < 16; ++e)
-                acc[nb][mb][e] = 0.0f;
-
-    // The eight chunks of a stage row form four 32x32 k-steps; k-step j uses
-    // chunks 2*(j % (CPQ/2)) + {0, 1} of local component j / (CPQ/2), i.e.
-    // input component q = qbase + j / (CPQ/2).
-    auto read_frags = [&](const unsigned char *As, const unsigned char *Bs, int qbase, int j,
-                          u32x4 (&wf)[NB], u32x4 (&pf)[MB]) {
-        const int qi = j / (CPQ / 2);
-        const int pc = 2 * (j % (CPQ / 2)) + khalf;
-        const int q = qbase + qi;
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-            const int row = (frag_p[nb] ^ q) * BNC + frag_o[nb];
-            wf[nb] = *reinterpret_cast<const u32x4 *>(Bs + (row * CPQ + (pc ^ swz<CPQ>(row))) * 16);
-        }
-#pragma unroll
-        for (int mb = 0; mb < MB; ++mb) {
-            const int r = wm * WTM + mb * 32 + l32;
-            const int lc = qi * CPQ + pc;
-            pf[mb] = *reinterpret_cast<const u32x4 *>(As + (r * CPR + (lc ^ swz<CPR>(r))) * 16);
-        }
+            f.p[mb] = *reinterpret_cast<const u32x4 *>(a_lds + buf * A_BYTES + mb * 32 * 128 + a_rd[j]);
     };
-    // Sign of block (p, q) applied to the weight fragment, then the MFMAs.
-    auto mfmas = [&](int qbase, int j, u32x4 (&wf)[NB], const u32x4 (&pf)[MB]) {
-        const int q = qbase + j / (CPQ / 2);
+    // Sign of block (p, q = j) applied to the weight fragments, then the MFMAs.
+    auto mfmas = [&](int j, Frags &f) {
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-            const unsigned flip = ((kHamiltonNeg >> (4 * frag_p[nb] + q)) & 1u) ? Elem<T>::sign : 0u;
-            wf[nb] ^= flip;
-        }
+        for (int nb = 0; nb < NB; ++nb)
+            f.w[nb] ^= flip[nb][j];
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
             for (int mb = 0; mb < MB; ++mb)
-                mfma_step<T>(acc[nb][mb], wf[nb], pf[mb]);
+                mfma_step<T>(acc[nb][mb], f.w[nb], f.p[mb]);
     };
 
-    // ---- main loop: loads run two stages ahead, one barrier per stage ----
-    // Within a stage the fragments of k-step j+1 are read before the MFMAs of
-    // k-step j (scheduling fences keep that order).  The loads of stage s+2
-    // are issued once every LDS read of stage s has been issued: an LDS DMA
-    // holds back the issuing wave's later LDS reads until it lands, so issued
-    // there it only has to land before the next stage's reads, with the
-    // remaining MFMAs of this stage in between.
-    const int S = a.stages;
-    issue(0);
-    if (S > 1)
-        issue(1);
-    for (int s = 0; s < S; ++s) {
-        // Wait for the loads of stage s; only those of stage s+1 (issued in
-        // the previous step: a weight block if s+1 opens one, then the
-        // activations) may stay in flight.
-        if (s + 1 >= S) {
-            wait_vmcnt<0>();
-        } else if ((s + 1) % NQG != 0) {
-            wait_vmcnt<A_PER_WAVE>();
-        } else if (b_full) {
-            wait_vmcnt<A_PER_WAVE + LB_HI>();
-        } else {
-            wait_vmcnt<A_PER_WAVE + LB_LO>();
-        }
-        block_barrier();
-        const int blk = s / NQG;
-        const unsigned char *As = a_ring + (s % A_ST) * A_BYTES;
-        const unsigned char *Bs = b_ring + (blk % B_ST) * B_BYTES;
-        const int qbase = (s - blk * NQG) * QS;
-        u32x4 wf0[NB], pf0[MB], wf1[NB], pf1[MB];
-        read_frags(As, Bs, qbase, 0, wf0, pf0);
-        read_frags(As, Bs, qbase, 1, wf1, pf1);
-        __builtin_amdgcn_sched_barrier(0);
-        mfmas(qbase, 0, wf0, pf0);
-        __builtin_amdgcn_sched_barrier(0);
-        read_frags(As, Bs, qbase, 2, wf0, pf0);
-        __builtin_amdgcn_sched_barrier(0);
-        mfmas(qbase, 1, wf1, pf1);
-        __builtin_amdgcn_sched_barrier(0);
-        read_frags(As, Bs, qbase, 3, wf1, pf1);
-        __builtin_amdgcn_sched_barrier(0);
-        // Stage s+2 reuses buffers every wave finished before this step's
-        // barrier.
-        if (s + 2 < S)
-            issue(s + 2);
-        __builtin_amdgcn_sched_barrier(0);
-        mfmas(qbase, 2, wf0, pf0);
-        __builtin_amdgcn_sched_barrier(0);
-        mfmas(qbase, 3, wf1, pf1);
-    }
+    // ---- deferred-epilogue drain ----
+    // Store i of a wave's region covers pixels i*(64/OUT_CPR) + l/OUT_CPR,
+    // chunk l%OUT_CPR (its physical chunk is XOR-swizzled with the pixel).
+    // Stores past N_DRAIN, pixels past M and channels past c_out get an
+    // offset outside the buffer and are dropped.
+    constexpr int CPC = 16 / ES;  // channels per 16-byte chunk
+    const bool defer = DEFER && a.c_out % CPC == 0;
+    const int d_pix = lane / OUT_CPR, d_chk = lane % OUT_CPR;
+    const unsigned char *const d_lds = o_lds + wn * OUT_WAVE + d_pix * OUT_ROW + ((d_chk ^ (d_pix % OUT_CPR)) * 16);
+    const int row_bytes = 4 * a.c_out * ES;
+    int d_next = N_DRAIN;        // next store of the pending tile
+    const T *d_base = nullptr;   // pending tile: first pixel's output row
+    unsigned d_bytes = 0;        // bytes of output from d_base on (capped)
+    unsigned d_lane = 0;         // lane's byte offset in a store, or out of range
+    auto drain_read = [&](int i) {
+        const int ic = i < N_DRAIN ? i : N_DRAIN - 1;
+        return *reinterpret_cast<const u32x4 *>(d_lds + ic * 1024);
+    };
+    auto drain_store = [&](int i, u32x4 v) {
+        const unsigned off = (i < N_DRAIN && d_lane != 0x80000000u)
+                                 ? d_lane + unsigned(i * (64 / OUT_CPR) * row_bytes)
+                                 : 0x80000000u;
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), make_rsrc(d_base, d_bytes), off, 0, 0);
+    };
 
-    // ---- epilogue: bias, round, channels-last store ----
+    // Step g (its stage in ring slot g % 4):
+    //   k-step 0 on f0, reading k-step 1 into f1;
+    //   k-step 1 on f1, reading k-step 2 into f0;
+    //   k-step 2 on f0, reading k-step 3 into f1;
+    //   barrier (step g+1's stage has landed; step g's is read no more);
+    //   k-step 3 on f1, reading step g+1's k-step 0 into f0.
+    // Past the last step that read fetches unused data from an idle slot.
+    constexpr int N_READ = MB + NB;
+    constexpr int N_FLIP = NB * 4;
+    Frags f0, f1;
+    __syncthreads();
+    read_frags(0, 0, f0);
+    auto step = [&](auto slot) {
+        constexpr int B = decltype(slot)::value;  // ring slot of this step's stage
+        // one drain store per step: read from LDS now, stored after k-step 1
+        u32x4 dv0;
+        if constexpr (DEFER)
+            dv0 = drain_read(d_next);
+        __builtin_amdgcn_sched_barrier(0);
+        read_frags(B, 1, f1);
+        mfmas(0, f0);
+        interleave_kstep<N_MFMA, N_FLIP, N_READ>();
+        __builtin_amdgcn_sched_barrier(0);
+        read_frags(B, 2, f0);
+        mfmas(1, f1);
+        interleave_kstep<N_MFMA, N_FLIP, N_READ>();
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (DEFER) {
+            drain_store(d_next, dv0);
+            d_next = d_next < N_DRAIN ? d_next + 1 : N_DRAIN;
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        read_frags(B, 3, f1);
+        mfmas(2, f0);
+        interleave_kstep<N_MFMA, N_FLIP, N_READ>();
+        __builtin_amdgcn_sched_barrier(0);
+        __syncthreads();
+        read_frags((B + 1) & (NBUF - 1), 0, f0);
+        mfmas(3, f1);
+        interleave_kstep<N_MFMA, N_FLIP, N_READ>();
+        __builtin_amdgcn_sched_barrier(0);
+    };
+    using P0 = std::integral_constant<int, 0>;
+    using P1 = std::integral_constant<int, 1>;
+    using P2 = std::integral_constant<int, 2>;
+    using P3 = std::integral_constant<int, 3>;
+    // The S steps of one tile whose first stage sits in ring slot PH.
+    const int s_main = S & ~(NBUF - 1);
+    const int tail = S - s_main;
+    auto run_tile = [&](auto ph) {
+        constexpr int PH = decltype(ph)::value;
+        using Q0 = std::integral_constant<int, PH>;
+        using Q1 = std::integral_constant<int, (PH + 1) & 3>;
+        using Q2 = std::integral_constant<int, (PH + 2) & 3>;
+        using Q3 = std::integral_constant<int, (PH + 3) & 3>;
+        for (int s = 0; s < s_main; s += NBUF) {
+            step(Q0{});
+            step(Q1{});
+            step(Q2{});
+            step(Q3{});
+        }
+        if (tail > 0)
+            step(Q0{});
+        if (tail > 1)
+            step(Q1{});
+        if (tail > 2)
+            step(Q2{});
+    };
+
     const T *__restrict__ bias = static_cast<const T *>(a.bias);
     T *__restrict__ out = static_cast<T *>(a.out);
     const bool vec_out = (a.c_out & 3) == 0;
+    int ph = 0;  // ring slot of the current tile's first stage
+    for (int kt = 0; kt < n_mine; ++kt) {
+        const int tile = tile_of(kt);
+        const int m0 = (tile / a.n_tiles) * BM;
+        const int o0 = (tile % a.n_tiles) * BNC;
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
+        for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-            const int tn = wn * WTN + nb * 32 + 8 * g + 4 * khalf;
-            const int p = tn / BNC;
-            const int o = o0 + (tn - p * BNC);
-            if (o >= a.c_out)
-                continue;
-            float bv[4];
+            for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-            for (int e = 0; e < 4; ++e)
-                bv[e] = (bias != nullptr && o + e < a.c_out) ? float(bias[p * a.c_out + o + e]) : 0.0f;
+                for (int e = 0; e < 16; ++e)
+                    acc[nb][mb][e] = 0.0f;
+        if (ph == 0)
+            run_tile(P0{});
+        else if (ph == 1)
+            run_tile(P1{});
+        else if (ph == 2)
+            run_tile(P2{});
+        else
+            run_tile(P3{});
+        ph = (ph + S) & 3;
+
+        if (defer) {
+            // finish the previous tile's stores before its region is reused
+            for (; d_next < N_DRAIN; ++d_next)
+                drain_store(d_next, drain_read(d_next));
+            // park this tile: accumulator register 4*g + e of lane l holds
+            // channel 8*g + 4*(l/32) + e of the 32-channel block nb and pixel
+            // l%32 of block mb; bias added, rounded to T
+            unsigned char *const w_lds = o_lds + wn * OUT_WAVE;
 #pragma unroll
-            for (int mb = 0; mb < MB; ++mb) {
-                const int m = m0 + wm * WTM + mb * 32 + l32;
-                if (m >= a.m)
-                    continue;
-                T *dst = out + ((size_t)m * 4 * a.c_out + p * a.c_out + o);
-                T v[4];
+            for (int nb = 0; nb < NB; ++nb) {
 #pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    v[e] = T(acc[nb][mb][4 * g + e] + bv[e]);
-                if (vec_out) {
-                    if constexpr (sizeof(T) == 2) {
-                        uint2 pk;
-                        __builtin_memcpy(&pk, v, 8);
-                        *reinterpret_cast<uint2 *>(dst) = pk;
-                    } else {
-                        float4 pk;
-                        __builtin_memcpy(&pk, v, 16);
-                        *reinterpret_cast<float4 *>(dst) = pk;
-                    }
-                } else {
+                for (int g = 0; g < 4; ++g) {
+                    const int oc = nb * 32 + 8 * g + 4 * khalf;  // channel within the tile's BNC
+                    float bv[4];
 #pragma unroll
                     for (int e = 0; e < 4; ++e)
-                        if (o + e < a.c_out)
-                            dst[e] = v[e];
+                        bv[e] = (bias != nullptr && o0 + oc + e < a.c_out) ? float(bias[wn * a.c_out + o0 + oc + e])
+                                                                          : 0.0f;
+#pragma unroll
+                    for (int mb = 0; mb < MB; ++mb) {
+                        const int m = mb * 32 + l32;
+                        T v[4];
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            v[e] = T(acc[nb][mb][4 * g + e] + bv[e]);
+                        const int c = oc * ES / 16, within = (oc * ES) % 16;
+                        unsigned char *dst = w_lds + m * OUT_ROW + ((c ^ (m % OUT_CPR)) * 16) + within;
+                        if constexpr (ES == 2) {
+                            uint2 pk;
+                            __builtin_memcpy(&pk, v, 8);
+                            *reinterpret_cast<uint2 *>(dst) = pk;
+                        } else {
+                            u32x4 pk;
+                            __builtin_memcpy(&pk, v, 16);
+                            *reinterpret_cast<u32x4 *>(dst) = pk;
+                        }
+                    }
+                }
+            }
+            const long long rows_left = (long long)(a.m - m0) * row_bytes;
+            d_base = out + (size_t)m0 * 4 * a.c_out;
+            d_bytes = rows_left < 0x7fffffffLL ? unsigned(rows_left) : 0x7fffffffu;
+            const int ch = o0 + d_chk * CPC;  // first channel of the lane's chunk
+            d_lane = ch < a.c_out ? unsigned(d_pix * row_bytes + (wn * a.c_out + ch) * ES) : 0x80000000u;
+            d_next = 0;
+            continue;
+        }
+
+        // ---- epilogue: bias, round, channels-last store ----
+        // Accumulator register 4*g + e of lane l holds output channel row
+        // 8*g + 4*(l/32) + e of the 32x32 block and pixel column l%32.
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const int tn = wn * WTN + nb * 32 + 8 * g + 4 * khalf;
+                const int p = tn / BNC;
+                const int o = o0 + (tn - p * BNC);
+                if (o >= a.c_out)
+                    continue;
+                float bv[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    bv[e] = (bias != nullptr && o + e < a.c_out) ? float(bias[p * a.c_out + o + e]) : 0.0f;
+#pragma unroll
+                for (int mb = 0; mb < MB; ++mb) {
+                    const int m = m0 + wm * WTM + mb * 32 + l32;
+                    if (m >= a.m)
+                        continue;
+                    T *dst = out + ((size_t)m * 4 * a.c_out + p * a.c_out + o);
+                    T v[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        v[e] = T(acc[nb][mb][4 * g + e] + bv[e]);
+                    if (vec_out) {
+                        if constexpr (sizeof(T) == 2) {
+                            uint2 pk;
+                            __builtin_memcpy(&pk, v, 8);
+                            *reinterpret_cast<uint2 *>(dst) = pk;
+                        } else {
+                            float4 pk;
+                            __builtin_memcpy(&pk, v, 16);
+                            *reinterpret_cast<float4 *>(dst) = pk;
+                        }
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            if (o + e < a.c_out)
+                                dst[e] = v[e];
+                    }
                 }
             }
         }
     }
+    if constexpr (DEFER) {
+        for (; d_next < N_DRAIN; ++d_next)
+            drain_store(d_next, drain_read(d_next));
+    }
 }
 
-// Packs W_r, W_i, W_j, W_k (each OIHW) into [tap][cblk][kernel][cout_pad][bkc]
+// Packs W_r, W_i, W_j, W_k (each OIHW) into [tap][cblk][kernel][cout_pad][CS]
 // so that one stage of one N-tile is four contiguous runs; padding is zero.
 template <typename T>
 __global__ __launch_bounds__(256) void qconv2d_pack(const T *__restrict__ w0, const T *__restrict__ w1,
                                                     const T *__restrict__ w2, const T *__restrict__ w3,
                                                     T *__restrict__ wp, int c_in, int c_out, int k_h,
-                                                    int k_w, int n_cblk, int bkc, int cout_pad, int total)
+                                                    int k_w, int n_cblk, int cout_pad, int total)
 {
+    constexpr int CS = stage_channels<T>();
     const int idx = blockIdx.x * blockDim.x + threadIdx.x;
     if (idx >= total)
         return;
     int t = idx;
-    const int cc = t % bkc;
-    t /= bkc;
+    const int cc = t % CS;
+    t /= CS;
     const int o = t % cout_pad;
     t /= cout_pad;
     const int ws = t & 3;
     t >>= 2;
     const int cblk = t % n_cblk;
     const int tap = t / n_cblk;
-    const int c = cblk * bkc + cc;
+    const int c = cblk * CS + cc;
     const int ky = tap / k_w, kx = tap - (tap / k_w) * k_w;
     const T *src = ws == 0 ? w0 : ws == 1 ? w1 : ws == 2 ? w2 : w3;
     T v = T(0);
-    if (tap < k_h * k_w && o < c_out && c < c_in)  // the zero tail past the last tap stays 0
+    if (o < c_out && c < c_in)
         v = src[((o * c_in + c) * k_h + ky) * k_w + kx];
     wp[idx] = v;
 }
@@ -743,72 +741,78 @@ __global__ __launch_bounds__(256) void qconv2d_pack(const T *__restrict__ w0, co
 // ----------------------------- kernel table -------------------------------
 
 struct KernelEntry {
-    int bm, bnc, qs, threads;  // qs: input components per K stage (pack block = 128 B / qs)
+    int bm, bnc, mb, nb, threads;
     DType dt;
-    bool dma;  // pipelined direct-to-LDS kernel (needs c_in % vector == 0)
-    const void *fn;
+    const void *fn;         // c_in a multiple of the 16-byte vector: activations move by DMA
+    const void *fn_masked;  // any c_in: element loads with channel masking
     const char *name;
 };
 
-#define QCONV_REG(T, DT, BM, BNC, WM, WN, BKC)                                                 \
-    KernelEntry                                                                                \
-    {                                                                                          \
-        BM, BNC, 4, 64 * WM * WN, DT, false, (const void *)&qconv2d_igemm<T, BM, BNC, WM, WN, BKC>, \
-            "reg_" #T "_bm" #BM "_bnc" #BNC "_w" #WM "x" #WN "_bkc" #BKC                       \
+#define QCONV_K(T, DT, MB, NB, WM, WN)                                                                 \
+    KernelEntry                                                                                        \
+    {                                                                                                  \
+        32 * (MB) * (WM), 8 * (NB) * (WN), MB, NB, 64 * ((WM) * (WN) + 2), DT,                         \
+            (const void *)&qconv2d_igemm<T, MB, NB, WM, WN, true>,                                     \
+            (const void *)&qconv2d_igemm<T, MB, NB, WM, WN, false>,                                    \
+            #T "_mb" #MB "x" #WM "_nb" #NB "x" #WN                                                     \
     }
-#define QCONV_DMA(T, DT, BM, BNC, WM, WN, QS)                                                     \
-    KernelEntry                                                                                   \
-    {                                                                                             \
-        BM, BNC, QS, 64 * WM * WN, DT, true, (const void *)&qconv2d_igemm_dma<T, BM, BNC, WM, WN, QS>, \
-            "dma_" #T "_bm" #BM "_bnc" #BNC "_w" #WM "x" #WN "_qs" #QS                            \
-    }
-#define QCONV_DMA3(T, DT, BM, BNC, WM, WN) \
-    QCONV_DMA(T, DT, BM, BNC, WM, WN, 1), QCONV_DMA(T, DT, BM, BNC, WM, WN, 2), QCONV_DMA(T, DT, BM, BNC, WM, WN, 4)
 
-// Register-staged kernels use the 4-component stage (qs 4); every entry's BNC
-// divides kPackCoutAlign.  DMA entries come in qs = 1, 2, 4 triples.
-enum KernelId {
-    kRegBf16N64 = 0,
-    kRegBf16N32,
-    kRegBf16N16,
-    kRegF32,
-    kDmaBf16M256N64 = 4,   // +0/+1/+2 for qs 1/2/4
-    kDmaBf16M128N64 = 7,
-    kDmaBf16M128N32 = 10,
-    kDmaBf16M128N16 = 13,
-    kDmaF32M64N16 = 16,
-    kNumKernels = 19,
-};
 const KernelEntry kKernels[] = {
-    QCONV_REG(__bf16, DType::BF16, 128, 64, 2, 2, 16),
-    QCONV_REG(__bf16, DType::BF16, 128, 32, 2, 2, 16),
-    QCONV_REG(__bf16, DType::BF16, 128, 16, 2, 2, 16),
-    QCONV_REG(float, DType::F32, 64, 16, 2, 2, 8),
-    QCONV_DMA3(__bf16, DType::BF16, 256, 64, 4, 2),
-    QCONV_DMA3(__bf16, DType::BF16, 128, 64, 2, 2),
-    QCONV_DMA3(__bf16, DType::BF16, 128, 32, 2, 2),
-    QCONV_DMA3(__bf16, DType::BF16, 128, 16, 2, 2),
-    QCONV_DMA3(float, DType::F32, 64, 16, 2, 2),
+    QCONV_K(__bf16, DType::BF16, 4, 2, 1, 4),  // 128 px x 64 channels
+    QCONV_K(__bf16, DType::BF16, 4, 1, 1, 4),  // 128 px x 32 channels
+    QCONV_K(__bf16, DType::BF16, 2, 1, 2, 2),  // 128 px x 16 channels
+    QCONV_K(float, DType::F32, 1, 1, 2, 2),    // 64 px x 16 channels
 };
-static_assert(sizeof(kKernels) / sizeof(kKernels[0]) == kNumKernels, "kernel table");
+constexpr int kNumKernels = int(sizeof(kKernels) / sizeof(kKernels[0]));
 
-int qs_index(int qs)
+// Compute units of the current device (cached per device).
+int device_cus()
 {
-    return qs == 1 ? 0 : (qs == 2 ? 1 : 2);
+    static int cached[64] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64)
+        return 256;
+    if (cached[dev] == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+            n = 256;
+        cached[dev] = n;
+    }
+    return cached[dev];
 }
 
-// Input components per stage for c_in: the widest 128-byte stage whose
-// channel block divides c_in (no zero padding), else the narrowest.
-int choose_qs(int c_in, DType dt)
+// Work-groups of `fn` one compute unit holds at once (cached per kernel;
+// at least 1).
+int resident_wgs(const void *fn, int threads)
 {
-    const int es = dt == DType::BF16 ? 2 : 4;
-    const int epc = 16 / es;
-    if (c_in % epc != 0)
-        return 4;
-    for (int qs : {1, 2})
-        if (c_in % (128 / (qs * es)) == 0)
-            return qs;
-    return 4;
+    static const void *fns[2 * kNumKernels] = {};
+    static int counts[2 * kNumKernels] = {};
+    for (int i = 0; i < 2 * kNumKernels; ++i) {
+        if (fns[i] == fn)
+            return counts[i];
+        if (fns[i] == nullptr) {
+            int n = 0;
+            if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fn, threads, 0) != hipSuccess || n < 1)
+                n = 1;
+            counts[i] = n;
+            fns[i] = fn;
+            return n;
+        }
+    }
+    return 1;
+}
+
+// Estimated cycles of a launch: rounds of one tile per CU times the tile's
+// K loop (MFMA cycles per wave with an allowance for fragment reads), its
+// fill latency and its epilogue stores.
+double plan_cost(const KernelEntry &k, int64_t m, int c_out, int stages, int cus)
+{
+    const int64_t tiles = (m + k.bm - 1) / k.bm * ((c_out + k.bnc - 1) / k.bnc);
+    const int64_t rounds = (tiles + cus - 1) / cus;
+    const double mfma_cycles = k.dt == DType::BF16 ? 32.0 : 4 * 64.0;
+    const double stage = 4.0 * k.mb * k.nb * mfma_cycles * 1.15 + 150.0;
+    const double tile = stages * stage + 6000.0 + 0.3 * k.bm * 4.0 * k.bnc;
+    return double(rounds) * tile;
 }
 
 }  // namespace
@@ -817,39 +821,40 @@ PackGeom qconv2d_pack_geom(int c_in, int c_out, int k_h, int k_w, DType dt)
 {
     PackGeom pg;
     const int es = dt == DType::BF16 ? 2 : 4;
-    pg.pk = 128 / (choose_qs(c_in, dt) * es);
+    pg.pk = 128 / (4 * es);
     pg.n_cblk = (c_in + pg.pk - 1) / pg.pk;
     pg.cout_pad = (c_out + kPackCoutAlign - 1) / kPackCoutAlign * kPackCoutAlign;
-    pg.zero_offset = size_t(k_h) * k_w * pg.n_cblk * 4 * pg.cout_pad * pg.pk * es;
-    pg.bytes = pg.zero_offset + kPackZeroTail;
+    pg.bytes = size_t(k_h) * k_w * pg.n_cblk * 4 * pg.cout_pad * pg.pk * es;
     return pg;
 }
 
 ConvPlan qconv2d_plan(const ConvGeom &g, DType dt)
 {
-    const int epc = dt == DType::BF16 ? 8 : 4;
-    const bool vec = g.c_in % epc == 0;
-    const int qi = qs_index(choose_qs(g.c_in, dt));
     const int64_t m = g.m();
-    int id;
-    if (dt == DType::F32) {
-        id = vec ? kDmaF32M64N16 + qi : kRegF32;
-    } else if (g.c_out >= 64) {
-        // 256-pixel tiles when they still give the 256 CUs two rounds of work.
-        const int64_t tiles256 = (m + 255) / 256 * ((g.c_out + 63) / 64);
-        id = !vec ? kRegBf16N64 : (tiles256 >= 512 ? kDmaBf16M256N64 : kDmaBf16M128N64) + qi;
-    } else if (g.c_out > 16) {
-        id = vec ? kDmaBf16M128N32 + qi : kRegBf16N32;
-    } else {
-        id = vec ? kDmaBf16M128N16 + qi : kRegBf16N16;
+    const int pk = dt == DType::BF16 ? 16 : 8;
+    const int stages = g.k_h * g.k_w * ((g.c_in + pk - 1) / pk);
+    int id = -1;
+    double best = 0.0;
+    const int cus = device_cus();
+    for (int i = 0; i < kNumKernels; ++i) {
+        const KernelEntry &k = kKernels[i];
+        if (k.dt != dt)
+            continue;
+        // narrow tiles only where the output channels leave a wide one idle
+        if (dt == DType::BF16 && ((k.bnc == 16 && g.c_out > 16) || (k.bnc == 64 && g.c_out <= 32)))
+            continue;
+        const double cost = plan_cost(k, m, g.c_out, stages, cus);
+        if (id < 0 || cost < best) {
+            best = cost;
+            id = i;
+        }
     }
 #ifdef QUAN_TUNING
-    // Tuning builds only: force a tile family (QUAN_QCONV_KERNEL=<id of its
-    // qs-1 entry>); the qs member still follows c_in.
+    // Tuning builds only: force a kernel (QUAN_QCONV_KERNEL=<table index>).
     if (const char *force = getenv("QUAN_QCONV_KERNEL")) {
         const int f = atoi(force);
-        if (f >= kDmaBf16M256N64 && f < kNumKernels && kKernels[f].dt == dt && vec)
-            id = f + qi;
+        if (f >= 0 && f < kNumKernels && kKernels[f].dt == dt)
+            id = f;
     }
 #endif
     const KernelEntry &k = kKernels[id];
@@ -873,12 +878,12 @@ hipError_t qconv2d_pack_weights(const PackGeom &pg, int c_in, int c_out, int k_h
         hipLaunchKernelGGL(qconv2d_pack<__bf16>, dim3(blocks), dim3(256), 0, stream,
                            (const __bf16 *)w_r, (const __bf16 *)w_i, (const __bf16 *)w_j,
                            (const __bf16 *)w_k, (__bf16 *)wpack, c_in, c_out, k_h, k_w, pg.n_cblk,
-                           pg.pk, pg.cout_pad, total);
+                           pg.cout_pad, total);
     else
         hipLaunchKernelGGL(qconv2d_pack<float>, dim3(blocks), dim3(256), 0, stream,
                            (const float *)w_r, (const float *)w_i, (const float *)w_j,
                            (const float *)w_k, (float *)wpack, c_in, c_out, k_h, k_w, pg.n_cblk,
-                           pg.pk, pg.cout_pad, total);
+                           pg.cout_pad, total);
     return hipGetLastError();
 }
 
@@ -886,11 +891,12 @@ hipError_t qconv2d_run(const ConvPlan &plan, const PackGeom &pg, const ConvGeom 
                        const void *x, const void *wpack, const void *bias, void *out,
                        hipStream_t stream)
 {
+    if (plan.id < 0 || plan.id >= kNumKernels)
+        return hipErrorInvalidValue;
     const KernelEntry &k = kKernels[plan.id];
     const int epc = dt == DType::BF16 ? 8 : 4;
     const int es = dt == DType::BF16 ? 2 : 4;
-    if (128 / (k.qs * es) != pg.pk || kPackCoutAlign % k.bnc != 0 || k.dt != dt ||
-        (k.dma && g.c_in % epc != 0))
+    if (128 / (4 * es) != pg.pk || kPackCoutAlign % k.bnc != 0 || k.dt != dt || pg.bytes > 0x7fffffffu)
         return hipErrorInvalidValue;
     KArgs a;
     a.x = x;
@@ -901,6 +907,7 @@ hipError_t qconv2d_run(const ConvPlan &plan, const PackGeom &pg, const ConvGeom 
     a.h = g.h;
     a.w = g.w;
     a.c_out = g.c_out;
+    a.k_h = g.k_h;
     a.k_w = g.k_w;
     a.s_h = g.s_h;
     a.s_w = g.s_w;
@@ -911,14 +918,21 @@ hipError_t qconv2d_run(const ConvPlan &plan, const PackGeom &pg, const ConvGeom 
     a.h_out = g.h_out;
     a.w_out = g.w_out;
     a.m = int(g.m());
-    a.stages = g.k_h * g.k_w * pg.n_cblk * (k.dma ? 4 / k.qs : 1);
+    a.stages = g.k_h * g.k_w * pg.n_cblk;
     a.n_cblk = pg.n_cblk;
     a.cout_pad = pg.cout_pad;
+    a.m_tiles = plan.m_tiles;
     a.n_tiles = plan.n_tiles;
-    a.vec_in = (g.c_in % epc) == 0;
+    a.w_bytes = unsigned(pg.bytes);
+    a.x_elems = (long long)g.n * g.h * g.w * 4 * g.c_in;
     void *args[] = {&a};
-    const unsigned blocks = unsigned(plan.m_tiles) * unsigned(plan.n_tiles);
-    return hipLaunchKernel(k.fn, dim3(blocks), dim3(k.threads), args, 0, stream);
+    const void *fn = (g.c_in % epc) == 0 ? k.fn : k.fn_masked;
+    // Persistent grid: as many work-groups as fit on the device at once, at
+    // most one per tile.
+    const long long tiles = (long long)plan.m_tiles * plan.n_tiles;
+    const long long slots = (long long)device_cus() * resident_wgs(fn, k.threads);
+    const unsigned blocks = unsigned(tiles < slots ? tiles : slots);
+    return hipLaunchKernel(fn, dim3(blocks), dim3(k.threads), args, 0, stream);
 }
 
 }  // namespace quan

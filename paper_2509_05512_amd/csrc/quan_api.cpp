@@ -139,6 +139,12 @@ int check_conv(const void *x, const void *bias, int32_t stride_h, int32_t stride
     if (x_elems > kMaxElems || o_elems > kMaxElems || w_elems * 4 * 4 > kMaxElems)
         return fail(QUAN_ERR_UNSUPPORTED, "qconv2d: a tensor exceeds 2^31-1 elements");
     const size_t es = elem_size(dtype);
+    // A work-group addresses its activations with 32-bit byte offsets from
+    // the first image of its tile (at most 256 output pixels, so at most
+    // 256 / (ho * wo) + 2 images).
+    const int64_t img_bytes = int64_t(h) * w * 4 * c_in * int64_t(es);
+    if (img_bytes * (256 / (ho * wo) + 2) > kMaxElems)
+        return fail(QUAN_ERR_UNSUPPORTED, "qconv2d: images of x too large for 32-bit tile offsets");
     if (misaligned(x, 16) || misaligned(out, 16))
         return fail(QUAN_ERR_ALIGN, "qconv2d: x and out must be 16-byte aligned");
     if (bias && misaligned(bias, es))
@@ -220,8 +226,8 @@ QUAN_API int64_t quan_qconv2d_packed_bytes(int32_t c_in, int32_t c_out, int32_t 
     if (c_in < 1 || c_out < 1 || k_h < 1 || k_w < 1)
         return fail(QUAN_ERR_SHAPE, "qconv2d_packed_bytes: sizes must be >= 1");
     const quan::PackGeom pg = quan::qconv2d_pack_geom(c_in, c_out, k_h, k_w, to_dt(dtype));
-    if (pg.bytes / elem_size(dtype) > size_t(kMaxElems))
-        return fail(QUAN_ERR_UNSUPPORTED, "qconv2d: packed weights exceed 2^31-1 elements");
+    if (pg.bytes > size_t(kMaxElems))
+        return fail(QUAN_ERR_UNSUPPORTED, "qconv2d: packed weights exceed 2^31-1 bytes");
     return int64_t(pg.bytes);
 }
 

@@ -20,18 +20,17 @@ struct ConvGeom {
 };
 
 // Layout of the packed weights: [tap][cblk][kernel r,i,j,k][cout_pad][pk]
-// with pk input channels per block, then kPackZeroTail zero bytes.  It depends only on (dtype, c_in, c_out,
-// k_h, k_w), never on the tile configuration, so weights packed once serve
-// every later call.
+// with pk input channels per block (one 128-byte stage row holds pk channels
+// of all four components).  It depends only on (dtype, c_in, c_out, k_h,
+// k_w), never on the tile configuration, so weights packed once serve every
+// later call.
 struct PackGeom {
-    int pk;              // input channels per block (128 bytes / components per stage)
-    int n_cblk;          // ceil(c_in / pk)
-    int cout_pad;        // c_out rounded up to kPackCoutAlign
-    size_t zero_offset;  // bytes of packed weights; kPackZeroTail zero bytes follow
-    size_t bytes;
+    int pk;        // input channels per block: 128 bytes / (4 components x element size)
+    int n_cblk;    // ceil(c_in / pk)
+    int cout_pad;  // c_out rounded up to kPackCoutAlign
+    size_t bytes;  // bytes of packed weights
 };
 constexpr int kPackCoutAlign = 64;
-constexpr int kPackZeroTail = 64;
 PackGeom qconv2d_pack_geom(int c_in, int c_out, int k_h, int k_w, DType dt);
 
 // Tile configuration chosen for a convolution.

@@ -92,6 +92,7 @@ CONV_ERRORS = [
     ("out overlaps weight", dict(out=WK - 256), E_ALIAS),
     ("out overlaps bias", dict(out=B), E_ALIAS),
     ("input too large", dict(n=1 << 16, h=256, w=256, cin=64), E_UNSUP),
+    ("image beyond 32-bit tile offsets", dict(n=1, h=4096, w=4096, cin=16, dtype=0), E_UNSUP),
 ]
 
 
