@@ -38,7 +38,7 @@ DEFAULT_WORKLOAD = "imagenet_stage"
 # summarised in profiles/qconv2d_<workload>_hbm.md.  A figure is reported only
 # while the kernel source is the one it was measured on (sha256 prefix).
 CONV_TRAFFIC = {
-    "imagenet_stage": {"bytes": 358389698, "kernel_sha256": "d6d5cb3df7e691db"},
+    "imagenet_stage": {"bytes": 221673209, "kernel_sha256": "793983191ed25e75"},
 }
 CONV_SOURCE = os.path.join(ROOT, "paper_2509_05512_amd", "csrc", "qconv2d_gfx950.hip")
 
