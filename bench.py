@@ -2,18 +2,23 @@
 """Benchmark of the QUAN hot path on one MI355X.
 
 One step = one pass of the whole hot path over one batch of a workload: for
-every layer, pack the four real kernels, run the quaternion (Hamilton)
-convolution, then IQBN (+ReLU where the layer has it), each through libquan's
-C ABI on torch's current stream.  Inputs are seeded synthetic tensors already
-resident in HBM when the timed region starts.
+every layer, pack the four real kernels, then the quaternion (Hamilton)
+convolution with IQBN (+ReLU where the layer has it) behind it
+(quan_qconv2d_iqbn_forward with the library's default statistics mode: per
+output tile in the convolution's epilogue), through libquan's C ABI on
+torch's current stream.  Inputs are seeded synthetic tensors already resident
+in HBM when the timed region starts.  The same steps are then timed with a
+separate statistics pass, and run with every kernel on its own (pack,
+convolution, the three IQBN passes) for per-kernel times.
 
 Prints ONE JSON line:
   value        useful convolution TFLOP/s over whole steps (pack + conv + IQBN);
                useful FLOPs = 2 * N*Ho*Wo * 4Cout * 4Cin * k^2 per layer
   qconv2d      the convolution kernel alone: TFLOP/s and fraction of the bf16
                dense MFMA peak (2516.6 TFLOP/s)
-  iqbn         IQBN (stats + finalize + affine): GB/s of algorithmic traffic
-               (two reads + one write of the tensor) and fraction of 8 TB/s
+  iqbn         the stand-alone IQBN (stats + finalize + affine): GB/s of
+               algorithmic traffic (two reads + one write of the tensor) and
+               fraction of 8 TB/s
   roofline     the dominant kernel (the convolution) against its roofline,
                timed with HIP events on the stream it runs on
   cpu_baseline the CPU oracle timed on a bounded sample of the same workload
@@ -107,7 +112,21 @@ def build_layers(wl, tens, dev, quan, torch):
     return layers
 
 
+def run_step_fused(layers, quan, eps=1e-5, stats="auto"):
+    """One step of the hot path as a caller runs it: per layer, pack the
+    kernels, then the convolution with IQBN (+ ReLU) behind it."""
+    for ly in layers:
+        L = ly["spec"]
+        quan.quan_qconv2d_pack_weights(*ly["w"], packed=ly["packed"])
+        quan.quan_qconv2d_iqbn_forward(ly["x"], ly["packed"], (L.c_out, L.c_in, L.k, L.k),
+                                       ly["gamma"], ly["beta"], bias=ly["bias"], stride=L.stride,
+                                       pad=L.pad, dilation=L.dilation, eps=eps, relu=L.relu,
+                                       out=ly["z"], mean=ly["mean"], var=ly["var"], stats=stats)
+
+
 def run_step(layers, quan, events=None, eps=1e-5):
+    """The same step with every kernel on its own (pack, convolution, the
+    three IQBN passes), events between them: per-kernel times."""
     for li, ly in enumerate(layers):
         L = ly["spec"]
         if events is not None:
@@ -198,23 +217,43 @@ def main():
     iqbn_bytes = [3 * wl.n * d["ho"] * d["wo"] * 4 * L.c_out * esz for d, L in zip(dims, wl.layers)]
 
     for _ in range(args.warmup):
-        run_step(layers, quan, eps=wl.eps)
+        run_step_fused(layers, quan, eps=wl.eps)
     torch.cuda.synchronize()
     log(f"[bench] warmup {args.warmup} done; timing {args.steps} steps")
 
-    events = [[[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in layers]
-              for _ in range(args.steps)]
+    # the timed region: K whole steps (pack + convolution + IQBN)
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t_wall0 = time.perf_counter()
     start.record()
     for s in range(args.steps):
-        run_step(layers, quan, events=events[s], eps=wl.eps)
+        run_step_fused(layers, quan, eps=wl.eps)
     end.record()
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall0
     total_ms = start.elapsed_time(end)
     ms_per_step = total_ms / args.steps
+
+    # the same steps with a separate statistics pass
+    for _ in range(2):
+        run_step_fused(layers, quan, eps=wl.eps, stats="pass")
+    torch.cuda.synchronize()
+    start.record()
+    for s in range(args.steps):
+        run_step_fused(layers, quan, eps=wl.eps, stats="pass")
+    end.record()
+    torch.cuda.synchronize()
+    pass_ms = start.elapsed_time(end) / args.steps
+
+    # per-kernel times: the same steps with every kernel on its own
+    for _ in range(2):
+        run_step(layers, quan, eps=wl.eps)
+    events = [[[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in layers]
+              for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    for s in range(args.steps):
+        run_step(layers, quan, events=events[s], eps=wl.eps)
+    torch.cuda.synchronize()
 
     pack_ms = [sum(events[s][li][0].elapsed_time(events[s][li][1]) for s in range(args.steps)) / args.steps
                for li in range(len(layers))]
@@ -264,6 +303,10 @@ def main():
                         "pad": L.pad, "iqbn_relu": L.relu} for L in wl.layers],
             "useful_gflop_per_step": round(step_flops / 1e9, 3),
         },
+        "step": "per layer: pack the four kernels, then quan_qconv2d_iqbn_forward "
+                "(convolution with IQBN statistics in its epilogue, normalization)",
+        "stats_pass_us_per_step": round(pass_ms * 1e3, 3),
+        "separate_kernels_us_per_step": round((sum(pack_ms) + sum(conv_ms) + sum(iqbn_ms)) * 1e3, 3),
         "qconv2d": {
             "tflops": round(conv_tflops, 2),
             "frac_mfma_peak": round(conv_tflops / peak, 4),

@@ -169,6 +169,44 @@ QUAN_API int quan_iqbn_relu_forward(const void *x, const float *gamma, const flo
                                     int32_t n, int32_t c, int32_t h, int32_t w,
                                     int32_t dtype, void *stream);
 
+/* Where quan_qconv2d_iqbn_forward gathers the batch statistics. */
+enum quan_stats_mode {
+    QUAN_STATS_AUTO = 0,     /* the library's choice: the epilogue where the tiles allow */
+    QUAN_STATS_EPILOGUE = 1, /* per-tile statistics in the convolution's epilogue */
+    QUAN_STATS_PASS = 2      /* a separate statistics pass over out */
+};
+
+/*
+ * The convolution followed by IQBN (+ ReLU when relu = 1) of its output, in
+ * place: out receives IQBN(quan_qconv2d_forward_packed(x, packed, bias, ...)),
+ * and mean, var ([4, c_out] fp32) the batch statistics of the convolution's
+ * output (eqs. 11 and 12), as quan_iqbn_forward / quan_iqbn_relu_forward
+ * would give up to rounding.  Every argument is as in
+ * quan_qconv2d_forward_packed and quan_iqbn_forward; gamma, beta, mean and
+ * var may not overlap each other, x or out.
+ *
+ *   stats   a quan_stats_mode.  QUAN_STATS_EPILOGUE has every output tile's
+ *           mean and squared deviations computed in the convolution's
+ *           epilogue and merged exactly in fp64 afterwards (normalising then
+ *           costs one read and one write of out); tiles that cannot gather
+ *           them (fewer than 32 output channels, or c_out not a multiple of
+ *           8 for bf16 / 4 for fp32) use the separate pass instead.
+ *           QUAN_STATS_PASS reads out once more for the statistics.  The
+ *           epilogue's vector arithmetic pauses the matrix cores for about
+ *           as long as the extra read takes; measured alternately on MI355X
+ *           the epilogue is 1-3% faster per layer, so QUAN_STATS_AUTO picks
+ *           it.  Both are deterministic.
+ */
+QUAN_API int quan_qconv2d_iqbn_forward(const void *x, const void *packed, const void *bias,
+                                       int32_t stride_h, int32_t stride_w,
+                                       int32_t pad_h, int32_t pad_w,
+                                       int32_t dilation_h, int32_t dilation_w,
+                                       const float *gamma, const float *beta, float eps,
+                                       int32_t relu, int32_t stats, void *out, float *mean,
+                                       float *var, int32_t n, int32_t c_in, int32_t h, int32_t w,
+                                       int32_t c_out, int32_t k_h, int32_t k_w,
+                                       int32_t dtype, void *stream);
+
 /* Message describing the last failure of a quan_* call on this thread
  * ("" if none).  The pointer stays valid until the next call on the thread. */
 QUAN_API const char *quan_last_error(void);

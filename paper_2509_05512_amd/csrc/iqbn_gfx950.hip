@@ -19,6 +19,10 @@
 //                     ReLU.  Subtracting the mean first keeps a near-constant
 //                     column exact (a folded x * scale + shift would cancel
 //                     two terms of size |mean| * scale).
+//
+// After a convolution that wrote per-tile statistics of its output (fused
+// into its epilogue), iqbn_finalize_tiles replaces passes 1 and 2: the
+// normalization then costs one read and one write of the tensor.
 #include <hip/hip_runtime.h>
 
 #include "quan_launch.h"
@@ -216,6 +220,97 @@ __global__ __launch_bounds__(kThreads) void iqbn_finalize(const T *__restrict__ 
     }
 }
 
+// Statistics from per-tile partials (the convolution's epilogue): tile t of
+// a column holds the mean and the sum of squared deviations of its
+// n_t = min(tile_rows, pixels - t * tile_rows) rows.  One work-group per
+// column, in fp64 and two passes over the partials: the column mean is the
+// count-weighted mean of the tile means, and the sum of squared deviations
+// is the tiles' own plus n_t (mean_t - mean)^2 each (the parallel-axis
+// identity, exact; no division per tile).  Thread i takes tiles i, i+256,
+// ... with eight loads in flight; a fixed butterfly per wave and a fixed
+// order over the waves add the threads, so the result does not depend on
+// timing.
+__global__ __launch_bounds__(kThreads) void iqbn_finalize_tiles(const float *__restrict__ part, int m_tiles,
+                                                                int tile_rows, int64_t pixels, int row_len,
+                                                                const float *__restrict__ gamma,
+                                                                const float *__restrict__ beta, float eps,
+                                                                float *__restrict__ mean, float *__restrict__ var,
+                                                                float *__restrict__ affine)
+{
+    constexpr int U = 8;  // loads in flight per thread
+    constexpr int NW = kThreads / 64;
+    __shared__ double red[NW];
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int col = blockIdx.x;
+    const float *pm = part + size_t(col) * m_tiles;
+    const float *pq = part + (size_t(row_len) + col) * m_tiles;
+    const int last = m_tiles - 1;
+    const double n_last = double(pixels - int64_t(last) * tile_rows);
+    auto rows = [&](int t) { return t == last ? n_last : double(tile_rows); };
+    // loads past the last tile read the last tile again (unconditional, so
+    // all U are in flight at once) and are not added
+    auto clamp_tile = [&](int t) { return t < last ? t : last; };
+    auto block_sum = [&](double v) {
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1)
+            v += __shfl_xor(v, off);
+        if (lane == 0)
+            red[wv] = v;
+        __syncthreads();
+        double total = 0.0;
+#pragma unroll
+        for (int w = 0; w < NW; ++w)
+            total += red[w];
+        __syncthreads();  // red is reused by the next sum
+        return total;
+    };
+    // pass 1: sum of n_t * mean_t
+    double s = 0.0;
+    for (int t0 = tid; t0 < m_tiles; t0 += kThreads * U) {
+        float mt[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            mt[u] = pm[clamp_tile(t0 + kThreads * u)];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int t = t0 + kThreads * u;
+            if (t < m_tiles)
+                s += rows(t) * double(mt[u]);
+        }
+    }
+    const double mu = block_sum(s) / double(pixels);
+    // pass 2: sum of M2_t + n_t * (mean_t - mean)^2
+    double q = 0.0;
+    for (int t0 = tid; t0 < m_tiles; t0 += kThreads * U) {
+        float mt[U], qt[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            mt[u] = pm[clamp_tile(t0 + kThreads * u)];
+            qt[u] = pq[clamp_tile(t0 + kThreads * u)];
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int t = t0 + kThreads * u;
+            if (t < m_tiles) {
+                const double d = double(mt[u]) - mu;
+                q += double(qt[u]) + rows(t) * d * d;
+            }
+        }
+    }
+    const double m2 = block_sum(q);
+    if (tid == 0) {
+        double v = m2 / double(pixels);  // biased variance
+        if (v < 0.0)
+            v = 0.0;
+        const double sc = double(gamma[col]) / sqrt(v + double(eps));
+        mean[col] = float(mu);
+        var[col] = float(v);
+        affine[col] = float(mu);
+        affine[row_len + col] = float(sc);
+        affine[2 * row_len + col] = beta[col];
+    }
+}
+
 template <typename T, int VW, bool RELU>
 __global__ __launch_bounds__(kThreads) void iqbn_affine(const T *x, T *out, Layout l,
                                                         const float *__restrict__ affine)
@@ -296,7 +391,51 @@ hipError_t launch_all(const void *x, const float *gamma, const float *beta, floa
     return hipGetLastError();
 }
 
+template <typename T, int VW>
+hipError_t launch_from_tiles(const float *part, int m_tiles, int tile_rows, const float *gamma,
+                             const float *beta, float eps, bool relu, void *io, float *mean, float *var,
+                             int64_t pixels, int c, float *affine, hipStream_t stream)
+{
+    const Layout l = make_layout(pixels, c, VW);
+    hipLaunchKernelGGL(iqbn_finalize_tiles, dim3(l.row_len), dim3(kThreads), 0, stream, part, m_tiles,
+                       tile_rows, pixels, l.row_len, gamma, beta, eps, mean, var, affine);
+    T *t = static_cast<T *>(io);
+    const dim3 grid(l.blocks, l.col_groups);
+    if (relu)
+        hipLaunchKernelGGL((iqbn_affine<T, VW, true>), grid, dim3(kThreads), 0, stream, t, t, l,
+                           (const float *)affine);
+    else
+        hipLaunchKernelGGL((iqbn_affine<T, VW, false>), grid, dim3(kThreads), 0, stream, t, t, l,
+                           (const float *)affine);
+    return hipGetLastError();
+}
+
 }  // namespace
+
+size_t iqbn_tile_stats_bytes(int m_tiles, int c)
+{
+    return (size_t(2) * m_tiles + 3) * 4 * c * sizeof(float);
+}
+
+hipError_t iqbn_from_tiles_run(const float *part, int m_tiles, int tile_rows, const float *gamma,
+                               const float *beta, float eps, bool relu, void *io, float *mean, float *var,
+                               int64_t pixels, int c, DType dt, hipStream_t stream)
+{
+    float *affine = const_cast<float *>(part) + size_t(2) * m_tiles * 4 * c;
+    const int vw = vec_width(c, dt);
+    if (dt == DType::BF16) {
+        if (vw == 8)
+            return launch_from_tiles<__bf16, 8>(part, m_tiles, tile_rows, gamma, beta, eps, relu, io, mean,
+                                                var, pixels, c, affine, stream);
+        return launch_from_tiles<__bf16, 1>(part, m_tiles, tile_rows, gamma, beta, eps, relu, io, mean, var,
+                                            pixels, c, affine, stream);
+    }
+    if (vw == 4)
+        return launch_from_tiles<float, 4>(part, m_tiles, tile_rows, gamma, beta, eps, relu, io, mean, var,
+                                           pixels, c, affine, stream);
+    return launch_from_tiles<float, 1>(part, m_tiles, tile_rows, gamma, beta, eps, relu, io, mean, var,
+                                       pixels, c, affine, stream);
+}
 
 size_t iqbn_workspace_bytes(int64_t pixels, int c)
 {

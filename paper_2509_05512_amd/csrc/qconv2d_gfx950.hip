@@ -95,6 +95,11 @@ struct KArgs {
     int m_tiles, n_tiles;
     unsigned w_bytes;   // bytes of packed weights
     long long x_elems;  // elements of x (n * h * w * 4 * c_in)
+    // Optional IQBN statistics of the output, per M-tile: stats[0][col][mt]
+    // = mean and stats[1][col][mt] = sum of squared deviations of column col
+    // = p * c_out + o over the tile's pixels (after rounding to T).  Written
+    // only by kernels with the deferred epilogue; NULL: none.
+    float *stats;
 };
 
 // XOR swizzle of the 16-byte chunk index within an LDS row of CPR chunks.
@@ -583,6 +588,87 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + 2)) void qconv2d_igemm(KA
             step(Q2{});
     };
 
+    // IQBN statistics of a parked tile, read back from the wave's own LDS
+    // region into registers once: lane l holds chunk l % OUT_CPR of pixels
+    // l / OUT_CPR + PPI * i.  Two passes over those registers give the exact
+    // tile mean per column (a fixed butterfly over the lanes sharing a
+    // chunk), then the squared deviations from it, so nothing cancels.
+    // Rows past M are left out.
+    auto tile_stats = [&](const unsigned char *w_lds, int m0, int o0) {
+        constexpr int PPI = 64 / OUT_CPR;  // pixels per read
+        constexpr int NR = BM / PPI;       // reads per lane
+        const int cl = lane % OUT_CPR, pl = lane / OUT_CPR;
+        const int n_valid = a.m - m0 < BM ? a.m - m0 : BM;
+        const unsigned char *src = w_lds + pl * OUT_ROW + ((cl ^ (pl % OUT_CPR)) * 16);
+        u32x4 raw[NR];
+#pragma unroll
+        for (int i = 0; i < NR; ++i)
+            raw[i] = *reinterpret_cast<const u32x4 *>(src + i * PPI * OUT_ROW);
+        auto val = [&](int i, int k) {
+            T v[CPC];
+            __builtin_memcpy(v, &raw[i], 16);
+            return float(v[k]);
+        };
+        float mean[CPC], m2[CPC];
+#pragma unroll
+        for (int k = 0; k < CPC; ++k) { mean[k] = 0.0f; m2[k] = 0.0f; }
+        if (n_valid == BM) {  // whole tile: no row masks
+#pragma unroll
+            for (int i = 0; i < NR; ++i)
+#pragma unroll
+                for (int k = 0; k < CPC; ++k)
+                    mean[k] += val(i, k);
+        } else {
+#pragma unroll
+            for (int i = 0; i < NR; ++i)
+#pragma unroll
+                for (int k = 0; k < CPC; ++k)
+                    mean[k] += i * PPI + pl < n_valid ? val(i, k) : 0.0f;
+        }
+#pragma unroll
+        for (int off = OUT_CPR; off < 64; off <<= 1)
+#pragma unroll
+            for (int k = 0; k < CPC; ++k)
+                mean[k] += __shfl_xor(mean[k], off);
+        const float inv = 1.0f / float(n_valid);
+#pragma unroll
+        for (int k = 0; k < CPC; ++k)
+            mean[k] *= inv;
+        if (n_valid == BM) {
+#pragma unroll
+            for (int i = 0; i < NR; ++i)
+#pragma unroll
+                for (int k = 0; k < CPC; ++k) {
+                    const float d = val(i, k) - mean[k];
+                    m2[k] = fmaf(d, d, m2[k]);
+                }
+        } else {
+#pragma unroll
+            for (int i = 0; i < NR; ++i)
+#pragma unroll
+                for (int k = 0; k < CPC; ++k) {
+                    const float d = i * PPI + pl < n_valid ? val(i, k) - mean[k] : 0.0f;
+                    m2[k] = fmaf(d, d, m2[k]);
+                }
+        }
+#pragma unroll
+        for (int off = OUT_CPR; off < 64; off <<= 1)
+#pragma unroll
+            for (int k = 0; k < CPC; ++k)
+                m2[k] += __shfl_xor(m2[k], off);
+        const int ch = o0 + cl * CPC;  // first channel of the lane's chunk
+        if (pl == 0 && ch < a.c_out) {
+            const int mt = m0 / BM;
+            const size_t cols = size_t(4) * a.c_out;
+#pragma unroll
+            for (int k = 0; k < CPC; ++k) {
+                const size_t col = size_t(wn) * a.c_out + ch + k;
+                a.stats[col * a.m_tiles + mt] = mean[k];
+                a.stats[(cols + col) * a.m_tiles + mt] = m2[k];
+            }
+        }
+    };
+
     const T *__restrict__ bias = static_cast<const T *>(a.bias);
     T *__restrict__ out = static_cast<T *>(a.out);
     const bool vec_out = (a.c_out & 3) == 0;
@@ -647,6 +733,8 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + 2)) void qconv2d_igemm(KA
                     }
                 }
             }
+            if (a.stats != nullptr)
+                tile_stats(w_lds, m0, o0);
             const long long rows_left = (long long)(a.m - m0) * row_bytes;
             d_base = out + (size_t)m0 * 4 * a.c_out;
             d_bytes = rows_left < 0x7fffffffLL ? unsigned(rows_left) : 0x7fffffffu;
@@ -742,6 +830,7 @@ __global__ __launch_bounds__(256) void qconv2d_pack(const T *__restrict__ w0, co
 
 struct KernelEntry {
     int bm, bnc, mb, nb, threads;
+    bool defer;  // deferred epilogue (one output component per wave); writes IQBN statistics
     DType dt;
     const void *fn;         // c_in a multiple of the 16-byte vector: activations move by DMA
     const void *fn_masked;  // any c_in: element loads with channel masking
@@ -751,7 +840,8 @@ struct KernelEntry {
 #define QCONV_K(T, DT, MB, NB, WM, WN)                                                                 \
     KernelEntry                                                                                        \
     {                                                                                                  \
-        32 * (MB) * (WM), 8 * (NB) * (WN), MB, NB, 64 * ((WM) * (WN) + 2), DT,                         \
+        32 * (MB) * (WM), 8 * (NB) * (WN), MB, NB, 64 * ((WM) * (WN) + 2),                             \
+            (WM) == 1 && (WN) == 4 && 8 * (NB) * (WN) >= 32, DT,                                       \
             (const void *)&qconv2d_igemm<T, MB, NB, WM, WN, true>,                                     \
             (const void *)&qconv2d_igemm<T, MB, NB, WM, WN, false>,                                    \
             #T "_mb" #MB "x" #WM "_nb" #NB "x" #WN                                                     \
@@ -887,9 +977,18 @@ hipError_t qconv2d_pack_weights(const PackGeom &pg, int c_in, int c_out, int k_h
     return hipGetLastError();
 }
 
+bool qconv2d_writes_stats(const ConvPlan &plan, const ConvGeom &g, DType dt)
+{
+    if (plan.id < 0 || plan.id >= kNumKernels)
+        return false;
+    const KernelEntry &k = kKernels[plan.id];
+    // deferred epilogue and whole 16-byte output chunks
+    return k.defer && g.c_out % (dt == DType::BF16 ? 8 : 4) == 0;
+}
+
 hipError_t qconv2d_run(const ConvPlan &plan, const PackGeom &pg, const ConvGeom &g, DType dt,
                        const void *x, const void *wpack, const void *bias, void *out,
-                       hipStream_t stream)
+                       float *stats, hipStream_t stream)
 {
     if (plan.id < 0 || plan.id >= kNumKernels)
         return hipErrorInvalidValue;
@@ -925,6 +1024,9 @@ hipError_t qconv2d_run(const ConvPlan &plan, const PackGeom &pg, const ConvGeom 
     a.n_tiles = plan.n_tiles;
     a.w_bytes = unsigned(pg.bytes);
     a.x_elems = (long long)g.n * g.h * g.w * 4 * g.c_in;
+    a.stats = stats;
+    if (stats != nullptr && !qconv2d_writes_stats(plan, g, dt))
+        return hipErrorInvalidValue;
     void *args[] = {&a};
     const void *fn = (g.c_in % epc) == 0 ? k.fn : k.fn_masked;
     // Persistent grid: as many work-groups as fit on the device at once, at

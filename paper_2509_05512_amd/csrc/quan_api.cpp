@@ -287,7 +287,7 @@ QUAN_API int quan_qconv2d_forward_packed(const void *x, const void *packed, cons
     const quan::DType dt = to_dt(dtype);
     const quan::PackGeom pg = quan::qconv2d_pack_geom(c_in, c_out, k_h, k_w, dt);
     const quan::ConvPlan plan = quan::qconv2d_plan(g, dt);
-    hipError_t e = quan::qconv2d_run(plan, pg, g, dt, x, packed, bias, out,
+    hipError_t e = quan::qconv2d_run(plan, pg, g, dt, x, packed, bias, out, nullptr,
                                      static_cast<hipStream_t>(stream));
     if (e != hipSuccess)
         return fail_hip(e, "qconv2d launch");
@@ -330,9 +330,76 @@ QUAN_API int quan_qconv2d_forward(const void *x, const void *w_r, const void *w_
                                               wpack, s);
     if (e != hipSuccess)
         return fail_hip(e, "qconv2d weight pack launch");
-    e = quan::qconv2d_run(quan::qconv2d_plan(g, dt), pg, g, dt, x, wpack, bias, out, s);
+    e = quan::qconv2d_run(quan::qconv2d_plan(g, dt), pg, g, dt, x, wpack, bias, out, nullptr, s);
     if (e != hipSuccess)
         return fail_hip(e, "qconv2d launch");
+    return QUAN_OK;
+}
+
+QUAN_API int quan_qconv2d_iqbn_forward(const void *x, const void *packed, const void *bias,
+                                       int32_t stride_h, int32_t stride_w, int32_t pad_h, int32_t pad_w,
+                                       int32_t dilation_h, int32_t dilation_w, const float *gamma,
+                                       const float *beta, float eps, int32_t relu, int32_t stats,
+                                       void *out, float *mean, float *var, int32_t n, int32_t c_in,
+                                       int32_t h, int32_t w,
+                                       int32_t c_out, int32_t k_h, int32_t k_w, int32_t dtype, void *stream)
+{
+    g_last_error.clear();
+    if (!x || !packed || !out || !gamma || !beta || !mean || !var)
+        return fail(QUAN_ERR_NULL,
+                    "qconv2d_iqbn: x, packed, gamma, beta, out, mean and var must be non-NULL");
+    quan::ConvGeom g;
+    size_t xb = 0, ob = 0;
+    if (int rc = check_conv(x, bias, stride_h, stride_w, pad_h, pad_w, dilation_h, dilation_w, out,
+                            n, c_in, h, w, c_out, k_h, k_w, dtype, &g, &xb, &ob))
+        return rc;
+    if (!(eps > 0.0f) || eps != eps)
+        return fail(QUAN_ERR_SHAPE, "qconv2d_iqbn: eps must be > 0 (got %g)", double(eps));
+    if (relu != 0 && relu != 1)
+        return fail(QUAN_ERR_SHAPE, "qconv2d_iqbn: relu must be 0 or 1");
+    if (stats != QUAN_STATS_AUTO && stats != QUAN_STATS_EPILOGUE && stats != QUAN_STATS_PASS)
+        return fail(QUAN_ERR_SHAPE, "qconv2d_iqbn: stats must be QUAN_STATS_AUTO, _EPILOGUE or _PASS (got %d)",
+                    int(stats));
+    const int64_t need = quan_qconv2d_packed_bytes(c_in, c_out, k_h, k_w, dtype);
+    if (need < 0)
+        return int(need);
+    if (misaligned(packed, 16))
+        return fail(QUAN_ERR_ALIGN, "qconv2d_iqbn: packed must be 16-byte aligned");
+    if (misaligned(gamma, 4) || misaligned(beta, 4) || misaligned(mean, 4) || misaligned(var, 4))
+        return fail(QUAN_ERR_ALIGN, "qconv2d_iqbn: gamma, beta, mean and var must be 4-byte aligned");
+    const size_t sbytes = size_t(4) * c_out * sizeof(float);
+    if (overlaps(out, ob, packed, size_t(need)))
+        return fail(QUAN_ERR_ALIAS, "qconv2d_iqbn: out overlaps the packed weights");
+    if (overlaps(mean, sbytes, var, sbytes) || overlaps(mean, sbytes, out, ob) ||
+        overlaps(var, sbytes, out, ob) || overlaps(mean, sbytes, x, xb) || overlaps(var, sbytes, x, xb))
+        return fail(QUAN_ERR_ALIAS, "qconv2d_iqbn: mean/var overlap each other or a tensor");
+
+    const quan::DType dt = to_dt(dtype);
+    const quan::PackGeom pg = quan::qconv2d_pack_geom(c_in, c_out, k_h, k_w, dt);
+    const quan::ConvPlan plan = quan::qconv2d_plan(g, dt);
+    const int64_t pixels = g.m();
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    void *work = nullptr;
+    hipError_t e;
+    if (stats != QUAN_STATS_PASS && quan::qconv2d_writes_stats(plan, g, dt)) {
+        // statistics gathered in the convolution's epilogue
+        if (int rc = workspace(stream, kIqbnPartials, quan::iqbn_tile_stats_bytes(plan.m_tiles, c_out), &work))
+            return rc;
+        e = quan::qconv2d_run(plan, pg, g, dt, x, packed, bias, out, static_cast<float *>(work), s);
+        if (e != hipSuccess)
+            return fail_hip(e, "qconv2d launch");
+        e = quan::iqbn_from_tiles_run(static_cast<const float *>(work), plan.m_tiles, plan.bm, gamma, beta,
+                                      eps, relu != 0, out, mean, var, pixels, c_out, dt, s);
+    } else {
+        if (int rc = workspace(stream, kIqbnPartials, quan::iqbn_workspace_bytes(pixels, c_out), &work))
+            return rc;
+        e = quan::qconv2d_run(plan, pg, g, dt, x, packed, bias, out, nullptr, s);
+        if (e != hipSuccess)
+            return fail_hip(e, "qconv2d launch");
+        e = quan::iqbn_run(out, gamma, beta, eps, relu != 0, out, mean, var, pixels, c_out, dt, work, s);
+    }
+    if (e != hipSuccess)
+        return fail_hip(e, "iqbn launch");
     return QUAN_OK;
 }
 

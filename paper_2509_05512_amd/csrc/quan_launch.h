@@ -49,15 +49,28 @@ hipError_t qconv2d_pack_weights(const PackGeom &pg, int c_in, int c_out, int k_h
                                 const void *w_r, const void *w_i, const void *w_j,
                                 const void *w_k, void *wpack, hipStream_t stream);
 
-// The implicit-GEMM Hamilton convolution.
+// The implicit-GEMM Hamilton convolution.  With `stats` non-NULL (only where
+// qconv2d_writes_stats holds) it also writes per-M-tile IQBN statistics of
+// its output: stats[0][col][mt] = tile mean, stats[1][col][mt] = sum of
+// squared deviations from it, col = p * c_out + o, mt < plan.m_tiles; tile mt
+// covers pixels [mt * plan.bm, min((mt + 1) * plan.bm, m)).
+bool qconv2d_writes_stats(const ConvPlan &plan, const ConvGeom &g, DType dt);
 hipError_t qconv2d_run(const ConvPlan &plan, const PackGeom &pg, const ConvGeom &g, DType dt,
                        const void *x, const void *wpack, const void *bias, void *out,
-                       hipStream_t stream);
+                       float *stats, hipStream_t stream);
 
 // IQBN.  `work` must hold iqbn_workspace_bytes(...) bytes.
 size_t iqbn_workspace_bytes(int64_t pixels, int c);
 hipError_t iqbn_run(const void *x, const float *gamma, const float *beta, float eps, bool relu,
                     void *out, float *mean, float *var, int64_t pixels, int c, DType dt,
                     void *work, hipStream_t stream);
+
+// IQBN of a convolution output whose per-tile statistics the convolution
+// wrote (qconv2d_run with stats): `part` holds iqbn_tile_stats_bytes(m_tiles,
+// c) bytes, the statistics first; the normalization runs in place on `io`.
+size_t iqbn_tile_stats_bytes(int m_tiles, int c);
+hipError_t iqbn_from_tiles_run(const float *part, int m_tiles, int tile_rows, const float *gamma,
+                               const float *beta, float eps, bool relu, void *io, float *mean, float *var,
+                               int64_t pixels, int c, DType dt, hipStream_t stream);
 
 }  // namespace quan

@@ -32,6 +32,8 @@ SIGNATURES = {
     "quan_qconv2d_packed_bytes": (ctypes.c_int64, [_i32] * 5),
     "quan_qconv2d_pack_weights": (ctypes.c_int, [_vp] * 4 + [_i32] * 5 + [_vp, ctypes.c_int64, _vp]),
     "quan_qconv2d_forward_packed": (ctypes.c_int, [_vp] * 3 + [_i32] * 6 + [_vp] + [_i32] * 8 + [_vp]),
+    "quan_qconv2d_iqbn_forward": (ctypes.c_int, [_vp] * 3 + [_i32] * 6 + [_vp, _vp, _f32, _i32, _i32]
+                                  + [_vp] * 3 + [_i32] * 8 + [_vp]),
     "quan_iqbn_forward": (ctypes.c_int, [_vp, _vp, _vp, _f32, _vp, _vp, _vp] + [_i32] * 5 + [_vp]),
     "quan_iqbn_relu_forward": (ctypes.c_int, [_vp, _vp, _vp, _f32, _vp, _vp, _vp] + [_i32] * 5 + [_vp]),
     "quan_last_error": (ctypes.c_char_p, []),
@@ -218,6 +220,53 @@ def quan_qconv2d_forward_packed(x, packed, weight_shape, bias=None, stride=1, pa
                                              _dtype_code(x), _stream(x.device))
     _check(rc)
     return out
+
+
+STATS_MODES = {"auto": 0, "epilogue": 1, "pass": 2}
+
+
+def quan_qconv2d_iqbn_forward(x, packed, weight_shape, gamma, beta, bias=None, stride=1, pad=0,
+                              dilation=1, eps=1e-5, relu=False, out=None, mean=None, var=None,
+                              stats="auto"):
+    """The convolution on packed weights followed by IQBN (+ ReLU) of its
+    output.  stats: "epilogue" (per-tile statistics in the convolution's
+    epilogue), "pass" (a separate statistics pass) or "auto" (the library's
+    choice).  Returns (out, mean, var)."""
+    lib = load_library()
+    if stats not in STATS_MODES:
+        raise ValueError(f"stats must be one of {sorted(STATS_MODES)}")
+    if not is_device_layout(x):
+        raise ValueError("x must be [N, 4, Cin, H, W] stored channels-last by component")
+    n, _, c_in, h, w = x.shape
+    c_out, c_in_w, k_h, k_w = (int(v) for v in weight_shape)
+    if c_in_w != c_in:
+        raise ValueError("weight_shape does not match x's channels")
+    if bias is not None and (tuple(bias.shape) != (4, c_out) or not bias.is_contiguous()
+                             or bias.dtype != x.dtype or bias.device != x.device):
+        raise ValueError("bias must be a contiguous [4, Cout] tensor like x")
+    for name, t in (("gamma", gamma), ("beta", beta)):
+        if tuple(t.shape) != (4, c_out) or t.dtype != torch.float32 or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous float32 [4, Cout] tensor")
+    sh, sw = _pair(stride)
+    ph, pw = _pair(pad)
+    dh, dw = _pair(dilation)
+    ho, wo = conv_out_size(h, k_h, sh, ph, dh), conv_out_size(w, k_w, sw, pw, dw)
+    if out is None:
+        out = empty_qmap(n, c_out, max(ho, 1), max(wo, 1), x.dtype, x.device)
+    elif not is_device_layout(out) or tuple(out.shape) != (n, 4, c_out, ho, wo) or out.dtype != x.dtype:
+        raise ValueError("out must be [N, 4, Cout, Ho, Wo] in device layout with x's dtype")
+    if mean is None:
+        mean = torch.empty(4, c_out, dtype=torch.float32, device=x.device)
+    if var is None:
+        var = torch.empty(4, c_out, dtype=torch.float32, device=x.device)
+    with torch.cuda.device(x.device):
+        rc = lib.quan_qconv2d_iqbn_forward(_ptr(x), _ptr(packed), _ptr(bias), sh, sw, ph, pw, dh, dw,
+                                           _ptr(gamma), _ptr(beta), float(eps), int(bool(relu)),
+                                           STATS_MODES[stats], _ptr(out), _ptr(mean), _ptr(var), n,
+                                           c_in, h, w, c_out,
+                                           k_h, k_w, _dtype_code(x), _stream(x.device))
+    _check(rc)
+    return out, mean, var
 
 
 def _iqbn(fn_name, x, gamma, beta, eps, out, mean, var):

@@ -103,6 +103,43 @@ def test_qconv2d_rejects(lib, name, kw, code):
     assert msg, "an error must leave a message"
 
 
+def fused(lib, **kw):
+    a = dict(x=X, packed=WR, bias=B, sh=1, sw=1, ph=1, pw=1, dh=1, dw=1, g=G, b=BE, eps=1e-5, relu=0,
+             stats=0, out=OUT, mean=MEAN, var=VAR, n=2, cin=4, h=16, w=16, cout=4, kh=3, kw=3, dtype=1)
+    a.update(kw)
+    rc = lib.quan_qconv2d_iqbn_forward(a["x"], a["packed"], a["bias"], a["sh"], a["sw"], a["ph"], a["pw"],
+                                       a["dh"], a["dw"], a["g"], a["b"], a["eps"], a["relu"], a["stats"],
+                                       a["out"],
+                                       a["mean"], a["var"], a["n"], a["cin"], a["h"], a["w"], a["cout"],
+                                       a["kh"], a["kw"], a["dtype"], None)
+    return rc, lib.quan_last_error().decode()
+
+
+FUSED_ERRORS = [
+    ("null packed", dict(packed=None), E_NULL),
+    ("null gamma", dict(g=None), E_NULL),
+    ("null var", dict(var=None), E_NULL),
+    ("bad dtype", dict(dtype=5), E_DTYPE),
+    ("c_out = 0", dict(cout=0), E_SHAPE),
+    ("eps = 0", dict(eps=0.0), E_SHAPE),
+    ("relu = 2", dict(relu=2), E_SHAPE),
+    ("stats mode 3", dict(stats=3), E_SHAPE),
+    ("stats mode -1", dict(stats=-1), E_SHAPE),
+    ("packed misaligned", dict(packed=WR + 8), E_ALIGN),
+    ("mean misaligned", dict(mean=MEAN + 2), E_ALIGN),
+    ("out overlaps packed", dict(out=WR), E_ALIAS),
+    ("mean overlaps var", dict(var=MEAN + 4), E_ALIAS),
+    ("mean inside out", dict(mean=OUT + 64), E_ALIAS),
+]
+
+
+@pytest.mark.parametrize("name,kw,code", FUSED_ERRORS, ids=[c[0] for c in FUSED_ERRORS])
+def test_fused_conv_iqbn_rejects(lib, name, kw, code):
+    rc, msg = fused(lib, **kw)
+    assert rc == code, (name, rc, msg)
+    assert msg
+
+
 IQBN_ERRORS = [
     ("null gamma", dict(g=None), E_NULL),
     ("null var", dict(var=None), E_NULL),
