@@ -4,13 +4,15 @@ Each ``pin_*`` function takes an ``oracle.Oracle`` and raises AssertionError if
 the oracle disagrees with an independent source of truth:
 
   * the paper's printed relations and tables (``tests/golden``): the unit
-    relations of eq. 2, the expansion of eq. 5 and the Hamilton matrix of eq. 6;
+    relations of eq. 2, the expansion of eq. 5, the Hamilton matrix of eq. 6,
+    the separable form of eq. 7 and the mixing matrix printed with eq. 9;
   * an independent construction of the quaternion algebra (2x2 complex
     matrices, themselves checked against eq. 2);
   * closed forms and invariants (identity kernel, multiplicative norm,
-    conjugate = transpose, associativity, linearity, IQBN moments);
-  * special cases that reduce to library routines (torch's fp64 conv2d and
-    batch_norm, numpy's complex arithmetic, numpy mean/var).
+    conjugate = transpose, associativity, linearity, IQBN moments, adjoint
+    identities of the gradients, unit norm and inverse of the Poincare map);
+  * special cases that reduce to library routines (torch's fp64 conv2d,
+    batch_norm and autograd, numpy's complex arithmetic, numpy mean/var).
 
 The same checks run against deliberately broken builds of the oracle in
 test_oracle_mutants.py, to show that each plausible mistake fails one of them.
@@ -422,10 +424,246 @@ def pin_iqbn_degenerate(orc):
     _close(out, np.broadcast_to(b[None, :, :, None, None], out.shape), 1e-15, "const out")
 
 
+# ---------------------------- separable convolution ---------------------------
+
+def eq7_signs():
+    """S[p, q] of the eq. 7 fixture; raises if a term convolves W_a with x_b
+    for a != b (eq. 7 has none)."""
+    S = np.zeros((4, 4))
+    for ln in _lines("separable_eq7.txt"):
+        head, terms = ln.split(":")
+        p = COMP[head.strip()]
+        for t in terms.split():
+            sign = -1.0 if t[0] == "-" else 1.0
+            wpart, xpart = t[1:].split("*")
+            a, b = COMP[wpart.split("_")[1]], COMP[xpart.split("_")[1]]
+            assert a == b, "eq. 7 fixture: cross term"
+            S[p, a] += sign
+    return S
+
+
+def eq9_mixing():
+    """The mixing matrix M printed for the backward pass (eq. 9 fixture)."""
+    return np.array([[float(v) for v in ln.split()] for ln in _lines("mixing_matrix_eq9.txt")])
+
+
+def _sep_unit(orc, a, b):
+    x = np.eye(4)[b].reshape(1, 4, 1, 1, 1)
+    w = np.eye(4)[a].reshape(4, 1, 1, 1, 1)
+    return orc.qconv2d_separable(x, w).reshape(4)
+
+
+def pin_separable_eq7_terms(orc):
+    """W = e_a, X = e_b gives S[:, a] of eq. 7 when a == b and zero otherwise
+    (no cross-component terms)."""
+    S = eq7_signs()
+    for a in range(4):
+        for b in range(4):
+            ref = S[:, a] if a == b else np.zeros(4)
+            _close(_sep_unit(orc, a, b), ref, 0, f"eq. 7 W_{a} x_{b}")
+
+
+def pin_separable_mixing_transpose(orc):
+    """The sign matrix the oracle applies is the transpose of the printed
+    backward mixing matrix M (eq. 9), and S S^T = 4 I."""
+    S = np.stack([_sep_unit(orc, q, q) for q in range(4)], axis=1)
+    _close(S, eq9_mixing().T, 0, "S = M^T")
+    _close(S @ S.T, 4.0 * np.eye(4), 0, "S S^T = 4 I")
+
+
+def pin_separable_real_row(orc):
+    """Row r of eq. 7 is exactly row r of the Hamilton product (eq. 5): the
+    separable and the full convolution agree on the real component."""
+    rng = _rng(30)
+    for (N, Cin, Cout, H, W, k, s, p, d) in CONV_SWEEP[:4]:
+        x = rng.standard_normal((N, 4, Cin, H, W))
+        w = rng.standard_normal((4, Cout, Cin, k, k))
+        b = rng.standard_normal((4, Cout))
+        _close(orc.qconv2d_separable(x, w, b, s, p, d)[:, 0], orc.qconv2d(x, w, b, s, p, d)[:, 0],
+               1e-12, "separable row r")
+
+
+def pin_separable_block_matrix(orc):
+    """Agreement with torch's fp64 conv2d of the real 4Cin -> 4Cout weight
+    whose block (p, q) is S[p, q] * W_q (eq. 7 fixture), with bias."""
+    S = eq7_signs()
+    rng = _rng(31)
+    for (N, Cin, Cout, H, W, k, s, p, d) in CONV_SWEEP:
+        x = rng.standard_normal((N, 4, Cin, H, W))
+        w = rng.standard_normal((4, Cout, Cin, k, k))
+        b = rng.standard_normal((4, Cout))
+        wb = np.concatenate([np.concatenate([S[pp, q] * w[q] for q in range(4)], axis=1)
+                             for pp in range(4)], axis=0)
+        ref = F.conv2d(torch.from_numpy(np.ascontiguousarray(x.reshape(N, 4 * Cin, H, W))),
+                       torch.from_numpy(wb), torch.from_numpy(b.reshape(-1)),
+                       stride=s, padding=p, dilation=d).numpy()
+        y = orc.qconv2d_separable(x, w, b, s, p, d)
+        _close(y, ref.reshape(y.shape), 1e-12, f"separable block {(N, Cin, Cout, H, W, k, s, p, d)}")
+
+
+# ------------------------------- conv gradients -------------------------------
+
+def pin_backward_adjoint(orc):
+    """The forward pass is linear in X and in W, so <conv(X; W), G> equals
+    <X, dX> and <W, dW> for the oracle's gradients at dL/dY = G; and dbias is
+    G summed over batch and pixels."""
+    rng = _rng(32)
+    for (N, Cin, Cout, H, W, k, s, p, d) in CONV_SWEEP:
+        x = rng.standard_normal((N, 4, Cin, H, W))
+        w = rng.standard_normal((4, Cout, Cin, k, k))
+        y = orc.qconv2d(x, w, None, s, p, d)
+        g = rng.standard_normal(y.shape)
+        dx, dw, db = orc.qconv2d_backward(x, w, g, s, p, d)
+        lhs = float(np.sum(y * g))
+        tag = str((N, Cin, Cout, H, W, k, s, p, d))
+        _close(np.sum(x * dx), lhs, 1e-12, f"<X, dX> {tag}")
+        _close(np.sum(w * dw), lhs, 1e-12, f"<W, dW> {tag}")
+        _close(db, g.sum(axis=(0, 3, 4)), 1e-13, f"dbias {tag}")
+
+
+def pin_backward_autograd(orc):
+    """Gradients equal torch autograd (fp64) through conv2d of the eq. 6 block
+    weight assembled from W_r..W_k."""
+    sign, comp = eq6_matrix_pattern()
+    rng = _rng(33)
+    for (N, Cin, Cout, H, W, k, s, p, d) in CONV_SWEEP:
+        x = rng.standard_normal((N, 4, Cin, H, W))
+        w = rng.standard_normal((4, Cout, Cin, k, k))
+        b = rng.standard_normal((4, Cout))
+        xt = torch.from_numpy(x.reshape(N, 4 * Cin, H, W).copy()).requires_grad_(True)
+        wt = torch.from_numpy(w.copy()).requires_grad_(True)
+        bt = torch.from_numpy(b.copy()).requires_grad_(True)
+        wb = torch.cat([torch.cat([float(sign[pp, q]) * wt[comp[pp, q]] for q in range(4)], dim=1)
+                        for pp in range(4)], dim=0)
+        y = F.conv2d(xt, wb, bt.reshape(-1), stride=s, padding=p, dilation=d)
+        g = rng.standard_normal(tuple(y.shape))
+        y.backward(torch.from_numpy(g))
+        dx, dw, db = orc.qconv2d_backward(x, w, g.reshape(N, 4, Cout, y.shape[2], y.shape[3]), s, p, d)
+        tag = str((N, Cin, Cout, H, W, k, s, p, d))
+        _close(dx, xt.grad.numpy().reshape(x.shape), 1e-12, f"autograd dX {tag}")
+        _close(dw, wt.grad.numpy(), 1e-12, f"autograd dW {tag}")
+        _close(db, bt.grad.numpy(), 1e-12, f"autograd dbias {tag}")
+
+
+def pin_backward_conjugate_kernel(orc):
+    """For stride 1, dX is the forward convolution of dY with the kernel
+    transposed (Cin <-> Cout), flipped in space and conjugated
+    (w_r, -w_i, -w_j, -w_k), padded by d(k-1) - p: L(w)^T = L(conj w)."""
+    rng = _rng(34)
+    for (N, Cin, Cout, H, W, k, p, d) in [(2, 3, 2, 7, 6, 3, 1, 1), (1, 2, 3, 8, 9, 5, 2, 1),
+                                          (1, 2, 2, 9, 8, 3, 2, 2), (2, 3, 4, 5, 5, 1, 0, 1)]:
+        x = rng.standard_normal((N, 4, Cin, H, W))
+        w = rng.standard_normal((4, Cout, Cin, k, k))
+        g = rng.standard_normal(orc.qconv2d(x, w, None, 1, p, d).shape)
+        dx, _, _ = orc.qconv2d_backward(x, w, g, 1, p, d)
+        wt = np.transpose(w, (0, 2, 1, 3, 4))[:, :, :, ::-1, ::-1] * np.array([1, -1, -1, -1])[:, None, None, None, None]
+        _close(dx, orc.qconv2d(g, wt, None, 1, d * (k - 1) - p, d), 1e-12, f"conjugate kernel {(k, p, d)}")
+
+
+# --------------------------------- IQBN extras ---------------------------------
+
+def pin_iqbn_inference_batch_norm(orc):
+    """Inference IQBN equals torch's fp64 batch_norm with running statistics
+    (training=False), with and without ReLU."""
+    rng = _rng(35)
+    N, C, H, W = 3, 4, 5, 6
+    x = rng.standard_normal((N, 4, C, H, W)) * 2.0 + 1.0
+    m = rng.standard_normal((4, C))
+    v = rng.uniform(0.2, 3.0, (4, C))
+    g = rng.uniform(0.5, 1.5, (4, C))
+    b = rng.standard_normal((4, C))
+    for relu in (False, True):
+        out = orc.iqbn_inference(x, m, v, g, b, 1e-3, relu)
+        ref = F.batch_norm(torch.from_numpy(x.reshape(N, 4 * C, H, W)), torch.from_numpy(m.reshape(-1)),
+                           torch.from_numpy(v.reshape(-1)), torch.from_numpy(g.reshape(-1)),
+                           torch.from_numpy(b.reshape(-1)), training=False, eps=1e-3).numpy()
+        if relu:
+            ref = np.maximum(ref, 0.0)
+        _close(out, ref.reshape(x.shape), 1e-12, f"inference batch_norm relu={relu}")
+
+
+def pin_iqbn_inference_batch_stats(orc):
+    """With the batch's own mean and biased variance as the stored
+    statistics, inference IQBN reproduces training-mode IQBN."""
+    rng = _rng(36)
+    x = rng.standard_normal((2, 4, 3, 4, 5)) * 1.5 - 0.5
+    g = rng.uniform(0.5, 1.5, (4, 3))
+    b = rng.standard_normal((4, 3))
+    out, mean, var = orc.iqbn(x, g, b, 1e-5, True)
+    _close(orc.iqbn_inference(x, mean, var, g, b, 1e-5, True), out, 1e-13, "inference = training")
+
+
+def pin_iqbn_backward_autograd(orc):
+    """IQBN gradients equal torch autograd (fp64) through training-mode
+    batch_norm over the 4C real channels, with and without ReLU."""
+    rng = _rng(37)
+    for (N, C, H, W) in [(3, 2, 4, 5), (2, 3, 3, 3), (1, 1, 1, 6)]:
+        x = rng.standard_normal((N, 4, C, H, W)) * 2.0 + rng.standard_normal((1, 4, C, 1, 1))
+        g = rng.uniform(0.5, 1.5, (4, C))
+        b = rng.standard_normal((4, C))
+        dout = rng.standard_normal(x.shape)
+        for relu in (False, True):
+            xt = torch.from_numpy(x.reshape(N, 4 * C, H, W).copy()).requires_grad_(True)
+            gt = torch.from_numpy(g.reshape(-1).copy()).requires_grad_(True)
+            bt = torch.from_numpy(b.reshape(-1).copy()).requires_grad_(True)
+            y = F.batch_norm(xt, None, None, gt, bt, training=True, eps=1e-5)
+            if relu:
+                y = torch.relu(y)
+            y.backward(torch.from_numpy(dout.reshape(N, 4 * C, H, W)))
+            dx, dg, db = orc.iqbn_backward(x, g, b, dout, 1e-5, relu)
+            tag = f"{(N, C, H, W)} relu={relu}"
+            _close(dx, xt.grad.numpy().reshape(x.shape), 1e-11, f"iqbn dX {tag}")
+            _close(dg, gt.grad.numpy().reshape(4, C), 1e-11, f"iqbn dgamma {tag}")
+            _close(db, bt.grad.numpy().reshape(4, C), 1e-11, f"iqbn dbeta {tag}")
+
+
+def pin_iqbn_backward_zero_sum(orc):
+    """Without ReLU the input gradient of each (component, channel) sums to
+    zero: shifting a channel's inputs by a constant leaves the output alone."""
+    rng = _rng(38)
+    x = rng.standard_normal((3, 4, 2, 4, 4)) + 3.0
+    dx, _, _ = orc.iqbn_backward(x, rng.uniform(0.5, 1.5, (4, 2)), rng.standard_normal((4, 2)),
+                                 rng.standard_normal(x.shape), 1e-5, False)
+    _close(dx.sum(axis=(0, 3, 4)), np.zeros((4, 2)), 1e-12, "sum dX")
+
+
+# ----------------------------- Poincare mapping -----------------------------
+
+def pin_poincare_unit_norm(orc):
+    """Eq. 4 lands on the unit sphere: ((1-n^2)^2 + 4n^2) = (1+n^2)^2."""
+    rng = _rng(39)
+    rgb = np.concatenate([rng.uniform(0, 1, (2, 3, 5, 4)), rng.standard_normal((1, 3, 5, 4)) * 10], axis=0)
+    q = orc.poincare(rgb)
+    _close(np.linalg.norm(q[:, :, 0], axis=1), np.ones((3, 5, 4)), 1e-14, "unit norm")
+
+
+def pin_poincare_inverse(orc):
+    """The inverse stereographic projection (q_i, q_j, q_k) / (1 + q_r)
+    recovers (r, g, b) in order."""
+    rng = _rng(40)
+    rgb = rng.uniform(0, 1, (2, 3, 6, 5))
+    q = orc.poincare(rgb)[:, :, 0]
+    _close(q[:, 1:] / (1.0 + q[:, :1]), rgb, 1e-14, "inverse")
+
+
+def pin_poincare_special_points(orc):
+    """Black maps to 1; the unit colour axes map to i, j and k."""
+    rgb = np.zeros((1, 3, 1, 4))
+    rgb[0, 0, 0, 1] = rgb[0, 1, 0, 2] = rgb[0, 2, 0, 3] = 1.0
+    q = orc.poincare(rgb)[0, :, 0, 0, :].T
+    _close(q, np.array([UNIT["1"], UNIT["i"], UNIT["j"], UNIT["k"]]), 0, "special points")
+
+
 ALL_PINS = [
     pin_eq2_unit_relations, pin_unit_table_derived, pin_complex_model, pin_eq6_matrix,
     pin_eq5_expansion, pin_orientation, pin_identity_kernel, pin_norm, pin_conjugate_adjoint,
     pin_real_reduction, pin_complex_reduction, pin_block_matrix, pin_brute_force_complex_model,
     pin_associativity, pin_linearity, pin_bias,
     pin_iqbn_batch_norm, pin_iqbn_moments, pin_iqbn_degenerate,
+    pin_separable_eq7_terms, pin_separable_mixing_transpose, pin_separable_real_row,
+    pin_separable_block_matrix,
+    pin_backward_adjoint, pin_backward_autograd, pin_backward_conjugate_kernel,
+    pin_iqbn_inference_batch_norm, pin_iqbn_inference_batch_stats,
+    pin_iqbn_backward_autograd, pin_iqbn_backward_zero_sum,
+    pin_poincare_unit_norm, pin_poincare_inverse, pin_poincare_special_points,
 ]
