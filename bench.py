@@ -8,8 +8,10 @@ convolution with IQBN (+ReLU where the layer has it) behind it
 output tile in the convolution's epilogue), through libquan's C ABI on
 torch's current stream.  Inputs are seeded synthetic tensors already resident
 in HBM when the timed region starts.  The same steps are then timed with a
-separate statistics pass, and run with every kernel on its own (pack,
-convolution, the three IQBN passes) for per-kernel times.
+separate statistics pass and in inference form (stored statistics folded into
+the convolution's epilogue), and run with every kernel on its own (pack,
+convolution, the three IQBN passes) for per-kernel times; the Poincare input
+mapping is timed on an ImageNet-sized batch.
 
 Prints ONE JSON line:
   value        useful convolution TFLOP/s over whole steps (pack + conv + IQBN);
@@ -122,6 +124,43 @@ def run_step_fused(layers, quan, eps=1e-5, stats="auto"):
                                        ly["gamma"], ly["beta"], bias=ly["bias"], stride=L.stride,
                                        pad=L.pad, dilation=L.dilation, eps=eps, relu=L.relu,
                                        out=ly["z"], mean=ly["mean"], var=ly["var"], stats=stats)
+
+
+def run_step_inference(layers, quan, eps=1e-5):
+    """The step in inference form: per layer, pack the kernels, then the
+    convolution with IQBN (+ ReLU) folded into its epilogue, using the
+    statistics the last training-form step produced as stored statistics."""
+    for ly in layers:
+        L = ly["spec"]
+        quan.quan_qconv2d_pack_weights(*ly["w"], packed=ly["packed"])
+        quan.quan_qconv2d_iqbn_inference(ly["x"], ly["packed"], (L.c_out, L.c_in, L.k, L.k), ly["mean"],
+                                         ly["var"], ly["gamma"], ly["beta"], bias=ly["bias"],
+                                         stride=L.stride, pad=L.pad, dilation=L.dilation, eps=eps,
+                                         relu=L.relu, out=ly["z"])
+
+
+def time_poincare(quan, steps, dev):
+    """The Poincare input mapping of one ImageNet-sized bf16 batch
+    (64 x 3 x 224 x 224): microseconds per launch and algorithmic GB/s
+    (3 reads + 4 writes of a 2-byte element per pixel)."""
+    import torch
+    n, h, w = 64, 224, 224
+    g = torch.Generator(device="cpu").manual_seed(5)
+    rgb = torch.rand((n, 3, h, w), generator=g).to(torch.bfloat16).to(dev)
+    q = quan.quan_poincare_map(rgb)
+    for _ in range(3):
+        quan.quan_poincare_map(rgb, out=q)
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(steps):
+        quan.quan_poincare_map(rgb, out=q)
+    end.record()
+    torch.cuda.synchronize()
+    us = start.elapsed_time(end) * 1e3 / steps
+    gbps = n * h * w * 7 * 2 / (us * 1e-6) / 1e9
+    return {"workload": "64x3x224x224 bf16", "us": round(us, 3), "gbps": round(gbps, 1),
+            "frac_hbm_peak": round(gbps / HBM_PEAK_GBPS, 4)}
 
 
 def run_step(layers, quan, events=None, eps=1e-5):
@@ -245,6 +284,18 @@ def main():
     torch.cuda.synchronize()
     pass_ms = start.elapsed_time(end) / args.steps
 
+    # the step in inference form (stored statistics folded into the conv)
+    for _ in range(2):
+        run_step_inference(layers, quan, eps=wl.eps)
+    torch.cuda.synchronize()
+    start.record()
+    for s in range(args.steps):
+        run_step_inference(layers, quan, eps=wl.eps)
+    end.record()
+    torch.cuda.synchronize()
+    inference_ms = start.elapsed_time(end) / args.steps
+    poincare = time_poincare(quan, args.steps, dev)
+
     # per-kernel times: the same steps with every kernel on its own
     for _ in range(2):
         run_step(layers, quan, eps=wl.eps)
@@ -306,6 +357,9 @@ def main():
         "step": "per layer: pack the four kernels, then quan_qconv2d_iqbn_forward "
                 "(convolution with IQBN statistics in its epilogue, normalization)",
         "stats_pass_us_per_step": round(pass_ms * 1e3, 3),
+        "inference_us_per_step": round(inference_ms * 1e3, 3),
+        "inference_tflops": round(step_flops / (inference_ms * 1e-3) / 1e12, 2),
+        "poincare": poincare,
         "separate_kernels_us_per_step": round((sum(pack_ms) + sum(conv_ms) + sum(iqbn_ms)) * 1e3, 3),
         "qconv2d": {
             "tflops": round(conv_tflops, 2),

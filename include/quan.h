@@ -207,6 +207,48 @@ QUAN_API int quan_qconv2d_iqbn_forward(const void *x, const void *packed, const 
                                        int32_t c_out, int32_t k_h, int32_t k_w,
                                        int32_t dtype, void *stream);
 
+/*
+ * Inference-mode convolution + IQBN (+ ReLU when relu = 1): eq. 12 with
+ * stored statistics in place of the batch statistics, folded into the
+ * convolution's epilogue (no pass over out after the convolution):
+ *
+ *   out = (conv(x) + bias - running_mean) / sqrt(running_var + eps)
+ *         * gamma + beta
+ *
+ * per output component and channel, computed as conv(x) * scale + shift in
+ * fp32 before the single rounding to dtype, with scale = gamma / sqrt(var +
+ * eps) and shift = (bias - mean) * scale + beta formed in fp64 on the
+ * device.  running_mean, running_var, gamma, beta are [4, c_out] fp32 device
+ * arrays (4-byte aligned) that out may not overlap; every other argument is
+ * as in quan_qconv2d_forward_packed.  Uses a small library workspace per
+ * (device, stream) for scale and shift.
+ */
+QUAN_API int quan_qconv2d_iqbn_inference(const void *x, const void *packed, const void *bias,
+                                         int32_t stride_h, int32_t stride_w,
+                                         int32_t pad_h, int32_t pad_w,
+                                         int32_t dilation_h, int32_t dilation_w,
+                                         const float *running_mean, const float *running_var,
+                                         const float *gamma, const float *beta, float eps,
+                                         int32_t relu, void *out,
+                                         int32_t n, int32_t c_in, int32_t h, int32_t w,
+                                         int32_t c_out, int32_t k_h, int32_t k_w,
+                                         int32_t dtype, void *stream);
+
+/*
+ * Poincare mapping of RGB images into quaternions (Section III-A, eq. 4):
+ * per pixel, with n2 = r^2 + g^2 + b^2,
+ *
+ *   q = ((1 - n2), 2r, 2g, 2b) / (1 + n2),
+ *
+ * a unit quaternion.  rgb: [n, 3, h, w] colour planes (dtype, aligned to
+ * its element); out: the one-channel quaternion map [n, 4, 1, h, w] in the
+ * activation layout of quan_qconv2d_forward, i.e. [n][h][w][4] (aligned to
+ * four elements), which may not overlap rgb.  Computed in fp32 and rounded
+ * once to dtype.
+ */
+QUAN_API int quan_poincare_map(const void *rgb, void *out, int32_t n, int32_t h, int32_t w,
+                               int32_t dtype, void *stream);
+
 /* Message describing the last failure of a quan_* call on this thread
  * ("" if none).  The pointer stays valid until the next call on the thread. */
 QUAN_API const char *quan_last_error(void);

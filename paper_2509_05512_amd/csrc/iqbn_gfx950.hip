@@ -410,7 +410,41 @@ hipError_t launch_from_tiles(const float *part, int m_tiles, int tile_rows, cons
     return hipGetLastError();
 }
 
+// Inference IQBN folded into a convolution's epilogue: one thread per
+// column, fp64, scale = gamma / sqrt(var + eps), shift = (bias - mean) *
+// scale + beta.
+template <typename T>
+__global__ __launch_bounds__(kThreads) void iqbn_fold(const float *__restrict__ mean, const float *__restrict__ var,
+                                                      const float *__restrict__ gamma,
+                                                      const float *__restrict__ beta, const T *__restrict__ bias,
+                                                      float eps, int cols, float *__restrict__ scale,
+                                                      float *__restrict__ shift)
+{
+    const int col = blockIdx.x * kThreads + threadIdx.x;
+    if (col >= cols)
+        return;
+    const double sc = double(gamma[col]) / sqrt(double(var[col]) + double(eps));
+    const double b = bias != nullptr ? double(float(bias[col])) : 0.0;
+    scale[col] = float(sc);
+    shift[col] = float((b - double(mean[col])) * sc + double(beta[col]));
+}
+
 }  // namespace
+
+hipError_t iqbn_fold_run(const float *mean, const float *var, const float *gamma, const float *beta,
+                         const void *bias, float eps, int c, DType dt, float *scale, float *shift,
+                         hipStream_t stream)
+{
+    const int cols = 4 * c;
+    const int blocks = (cols + kThreads - 1) / kThreads;
+    if (dt == DType::BF16)
+        hipLaunchKernelGGL(iqbn_fold<__bf16>, dim3(blocks), dim3(kThreads), 0, stream, mean, var, gamma, beta,
+                           static_cast<const __bf16 *>(bias), eps, cols, scale, shift);
+    else
+        hipLaunchKernelGGL(iqbn_fold<float>, dim3(blocks), dim3(kThreads), 0, stream, mean, var, gamma, beta,
+                           static_cast<const float *>(bias), eps, cols, scale, shift);
+    return hipGetLastError();
+}
 
 size_t iqbn_tile_stats_bytes(int m_tiles, int c)
 {

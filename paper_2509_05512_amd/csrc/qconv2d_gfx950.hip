@@ -100,6 +100,12 @@ struct KArgs {
     // = p * c_out + o over the tile's pixels (after rounding to T).  Written
     // only by kernels with the deferred epilogue; NULL: none.
     float *stats;
+    // Optional per-column affine map applied in the epilogue instead of the
+    // bias (inference IQBN folded in): out = scale[col] * acc + shift[col],
+    // then max(0, .) when relu is non-zero.  NULL scale: out = acc + bias.
+    const float *scale;
+    const float *shift;
+    int relu;
 };
 
 // XOR swizzle of the 16-byte chunk index within an LDS row of CPR chunks.
@@ -225,7 +231,11 @@ __device__ __forceinline__ void wait_vmcnt()
 // pixels x BN = 32*NB*WAVES_N output reals (BN/4 output channels, all four
 // components).  VEC: c_in is a multiple of the 16-byte chunk, so activations
 // move by DMA; otherwise the producer loads partial chunks element-wise.
-template <typename T, int MB, int NB, int WAVES_M, int WAVES_N, bool VEC>
+// EPI: what the epilogue applies (kEpiBias, kEpiStats, kEpiFold); fixed at
+// compile time so the common bias-only kernel carries none of the others'
+// state through its main loop.
+enum : int { kEpiBias = 0, kEpiStats = 1, kEpiFold = 2 };
+template <typename T, int MB, int NB, int WAVES_M, int WAVES_N, bool VEC, int EPI>
 __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + 2)) void qconv2d_igemm(KArgs a)
 {
     constexpr int ES = int(sizeof(T));
@@ -671,6 +681,23 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + 2)) void qconv2d_igemm(KA
 
     const T *__restrict__ bias = static_cast<const T *>(a.bias);
     T *__restrict__ out = static_cast<T *>(a.out);
+    // Per-column epilogue map: (1, bias) or the folded (scale, shift).  With
+    // scale 1 the fma is exactly acc + bias.
+    auto col_affine = [&](int col, bool inside, float &sc, float &sh) {
+        if constexpr (EPI == kEpiFold) {
+            sc = inside ? a.scale[col] : 0.0f;
+            sh = inside ? a.shift[col] : 0.0f;
+        } else {
+            sc = 1.0f;
+            sh = (bias != nullptr && inside) ? float(bias[col]) : 0.0f;
+        }
+    };
+    auto epi = [&](float v, float sc, float sh) {
+        const float y = fmaf(v, sc, sh);
+        if constexpr (EPI == kEpiFold)
+            return a.relu ? fmaxf(y, 0.0f) : y;
+        return y;
+    };
     const bool vec_out = (a.c_out & 3) == 0;
     int ph = 0;  // ring slot of the current tile's first stage
     for (int kt = 0; kt < n_mine; ++kt) {
@@ -700,25 +727,25 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + 2)) void qconv2d_igemm(KA
                 drain_store(d_next, drain_read(d_next));
             // park this tile: accumulator register 4*g + e of lane l holds
             // channel 8*g + 4*(l/32) + e of the 32-channel block nb and pixel
-            // l%32 of block mb; bias added, rounded to T
+            // l%32 of block mb; bias added (or the folded affine map and
+            // ReLU applied), rounded to T
             unsigned char *const w_lds = o_lds + wn * OUT_WAVE;
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb) {
 #pragma unroll
                 for (int g = 0; g < 4; ++g) {
                     const int oc = nb * 32 + 8 * g + 4 * khalf;  // channel within the tile's BNC
-                    float bv[4];
+                    float sc[4], sh[4];
 #pragma unroll
                     for (int e = 0; e < 4; ++e)
-                        bv[e] = (bias != nullptr && o0 + oc + e < a.c_out) ? float(bias[wn * a.c_out + o0 + oc + e])
-                                                                          : 0.0f;
+                        col_affine(wn * a.c_out + o0 + oc + e, o0 + oc + e < a.c_out, sc[e], sh[e]);
 #pragma unroll
                     for (int mb = 0; mb < MB; ++mb) {
                         const int m = mb * 32 + l32;
                         T v[4];
 #pragma unroll
                         for (int e = 0; e < 4; ++e)
-                            v[e] = T(acc[nb][mb][4 * g + e] + bv[e]);
+                            v[e] = T(epi(acc[nb][mb][4 * g + e], sc[e], sh[e]));
                         const int c = oc * ES / 16, within = (oc * ES) % 16;
                         unsigned char *dst = w_lds + m * OUT_ROW + ((c ^ (m % OUT_CPR)) * 16) + within;
                         if constexpr (ES == 2) {
@@ -733,7 +760,7 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + 2)) void qconv2d_igemm(KA
                     }
                 }
             }
-            if (a.stats != nullptr)
+            if constexpr (EPI == kEpiStats)
                 tile_stats(w_lds, m0, o0);
             const long long rows_left = (long long)(a.m - m0) * row_bytes;
             d_base = out + (size_t)m0 * 4 * a.c_out;
@@ -756,10 +783,10 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + 2)) void qconv2d_igemm(KA
                 const int o = o0 + (tn - p * BNC);
                 if (o >= a.c_out)
                     continue;
-                float bv[4];
+                float sc[4], sh[4];
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
-                    bv[e] = (bias != nullptr && o + e < a.c_out) ? float(bias[p * a.c_out + o + e]) : 0.0f;
+                    col_affine(p * a.c_out + o + e, o + e < a.c_out, sc[e], sh[e]);
 #pragma unroll
                 for (int mb = 0; mb < MB; ++mb) {
                     const int m = m0 + wm * WTM + mb * 32 + l32;
@@ -769,7 +796,7 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + 2)) void qconv2d_igemm(KA
                     T v[4];
 #pragma unroll
                     for (int e = 0; e < 4; ++e)
-                        v[e] = T(acc[nb][mb][4 * g + e] + bv[e]);
+                        v[e] = T(epi(acc[nb][mb][4 * g + e], sc[e], sh[e]));
                     if (vec_out) {
                         if constexpr (sizeof(T) == 2) {
                             uint2 pk;
@@ -832,18 +859,35 @@ struct KernelEntry {
     int bm, bnc, mb, nb, threads;
     bool defer;  // deferred epilogue (one output component per wave); writes IQBN statistics
     DType dt;
-    const void *fn;         // c_in a multiple of the 16-byte vector: activations move by DMA
-    const void *fn_masked;  // any c_in: element loads with channel masking
+    // [epilogue kind][masked]: masked = 0 when c_in is a multiple of the
+    // 16-byte vector (activations move by DMA), 1 for element loads with
+    // channel masking; NULL where the kind does not apply (statistics need
+    // the deferred epilogue).
+    const void *fn[3][2];
     const char *name;
 };
 
+#define QCONV_DEFER(NB, WM, WN) ((WM) == 1 && (WN) == 4 && 8 * (NB) * (WN) >= 32)
+// the statistics variant exists only for tiles with the deferred epilogue
+template <typename T, int MB, int NB, int WM, int WN, bool VEC>
+constexpr const void *stats_fn()
+{
+    if constexpr (QCONV_DEFER(NB, WM, WN))
+        return (const void *)&qconv2d_igemm<T, MB, NB, WM, WN, VEC, kEpiStats>;
+    else
+        return nullptr;
+}
+#define QCONV_STATS_FN(T, MB, NB, WM, WN, VEC) stats_fn<T, MB, NB, WM, WN, VEC>()
 #define QCONV_K(T, DT, MB, NB, WM, WN)                                                                 \
     KernelEntry                                                                                        \
     {                                                                                                  \
         32 * (MB) * (WM), 8 * (NB) * (WN), MB, NB, 64 * ((WM) * (WN) + 2),                             \
-            (WM) == 1 && (WN) == 4 && 8 * (NB) * (WN) >= 32, DT,                                       \
-            (const void *)&qconv2d_igemm<T, MB, NB, WM, WN, true>,                                     \
-            (const void *)&qconv2d_igemm<T, MB, NB, WM, WN, false>,                                    \
+            QCONV_DEFER(NB, WM, WN), DT,                                                               \
+            {{(const void *)&qconv2d_igemm<T, MB, NB, WM, WN, true, kEpiBias>,                         \
+              (const void *)&qconv2d_igemm<T, MB, NB, WM, WN, false, kEpiBias>},                       \
+             {QCONV_STATS_FN(T, MB, NB, WM, WN, true), QCONV_STATS_FN(T, MB, NB, WM, WN, false)},      \
+             {(const void *)&qconv2d_igemm<T, MB, NB, WM, WN, true, kEpiFold>,                         \
+              (const void *)&qconv2d_igemm<T, MB, NB, WM, WN, false, kEpiFold>}},                      \
             #T "_mb" #MB "x" #WM "_nb" #NB "x" #WN                                                     \
     }
 
@@ -875,9 +919,9 @@ int device_cus()
 // at least 1).
 int resident_wgs(const void *fn, int threads)
 {
-    static const void *fns[2 * kNumKernels] = {};
-    static int counts[2 * kNumKernels] = {};
-    for (int i = 0; i < 2 * kNumKernels; ++i) {
+    static const void *fns[6 * kNumKernels] = {};
+    static int counts[6 * kNumKernels] = {};
+    for (int i = 0; i < 6 * kNumKernels; ++i) {
         if (fns[i] == fn)
             return counts[i];
         if (fns[i] == nullptr) {
@@ -988,7 +1032,7 @@ bool qconv2d_writes_stats(const ConvPlan &plan, const ConvGeom &g, DType dt)
 
 hipError_t qconv2d_run(const ConvPlan &plan, const PackGeom &pg, const ConvGeom &g, DType dt,
                        const void *x, const void *wpack, const void *bias, void *out,
-                       float *stats, hipStream_t stream)
+                       float *stats, const ConvFold *fold, hipStream_t stream)
 {
     if (plan.id < 0 || plan.id >= kNumKernels)
         return hipErrorInvalidValue;
@@ -1025,10 +1069,18 @@ hipError_t qconv2d_run(const ConvPlan &plan, const PackGeom &pg, const ConvGeom 
     a.w_bytes = unsigned(pg.bytes);
     a.x_elems = (long long)g.n * g.h * g.w * 4 * g.c_in;
     a.stats = stats;
+    a.scale = fold != nullptr ? fold->scale : nullptr;
+    a.shift = fold != nullptr ? fold->shift : nullptr;
+    a.relu = fold != nullptr && fold->relu ? 1 : 0;
     if (stats != nullptr && !qconv2d_writes_stats(plan, g, dt))
         return hipErrorInvalidValue;
+    if (fold != nullptr && (fold->scale == nullptr || fold->shift == nullptr))
+        return hipErrorInvalidValue;
     void *args[] = {&a};
-    const void *fn = (g.c_in % epc) == 0 ? k.fn : k.fn_masked;
+    const int epi = stats != nullptr ? kEpiStats : fold != nullptr ? kEpiFold : kEpiBias;
+    const void *fn = k.fn[epi][(g.c_in % epc) == 0 ? 0 : 1];
+    if (fn == nullptr)
+        return hipErrorInvalidValue;
     // Persistent grid: as many work-groups as fit on the device at once, at
     // most one per tile.
     const long long tiles = (long long)plan.m_tiles * plan.n_tiles;

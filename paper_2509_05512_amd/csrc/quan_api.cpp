@@ -46,7 +46,7 @@ struct Workspace {
 std::mutex g_ws_mutex;
 std::map<std::pair<int, std::pair<void *, int>>, Workspace> g_ws;
 
-enum Purpose { kWeightPack = 0, kIqbnPartials = 1 };
+enum Purpose { kWeightPack = 0, kIqbnPartials = 1, kIqbnFold = 2 };
 
 // Returns a device buffer of at least `bytes` for (current device, stream,
 // purpose).  Growing it first waits for the device to finish with the old one.
@@ -287,7 +287,7 @@ QUAN_API int quan_qconv2d_forward_packed(const void *x, const void *packed, cons
     const quan::DType dt = to_dt(dtype);
     const quan::PackGeom pg = quan::qconv2d_pack_geom(c_in, c_out, k_h, k_w, dt);
     const quan::ConvPlan plan = quan::qconv2d_plan(g, dt);
-    hipError_t e = quan::qconv2d_run(plan, pg, g, dt, x, packed, bias, out, nullptr,
+    hipError_t e = quan::qconv2d_run(plan, pg, g, dt, x, packed, bias, out, nullptr, nullptr,
                                      static_cast<hipStream_t>(stream));
     if (e != hipSuccess)
         return fail_hip(e, "qconv2d launch");
@@ -330,7 +330,7 @@ QUAN_API int quan_qconv2d_forward(const void *x, const void *w_r, const void *w_
                                               wpack, s);
     if (e != hipSuccess)
         return fail_hip(e, "qconv2d weight pack launch");
-    e = quan::qconv2d_run(quan::qconv2d_plan(g, dt), pg, g, dt, x, wpack, bias, out, nullptr, s);
+    e = quan::qconv2d_run(quan::qconv2d_plan(g, dt), pg, g, dt, x, wpack, bias, out, nullptr, nullptr, s);
     if (e != hipSuccess)
         return fail_hip(e, "qconv2d launch");
     return QUAN_OK;
@@ -385,7 +385,7 @@ QUAN_API int quan_qconv2d_iqbn_forward(const void *x, const void *packed, const 
         // statistics gathered in the convolution's epilogue
         if (int rc = workspace(stream, kIqbnPartials, quan::iqbn_tile_stats_bytes(plan.m_tiles, c_out), &work))
             return rc;
-        e = quan::qconv2d_run(plan, pg, g, dt, x, packed, bias, out, static_cast<float *>(work), s);
+        e = quan::qconv2d_run(plan, pg, g, dt, x, packed, bias, out, static_cast<float *>(work), nullptr, s);
         if (e != hipSuccess)
             return fail_hip(e, "qconv2d launch");
         e = quan::iqbn_from_tiles_run(static_cast<const float *>(work), plan.m_tiles, plan.bm, gamma, beta,
@@ -393,13 +393,91 @@ QUAN_API int quan_qconv2d_iqbn_forward(const void *x, const void *packed, const 
     } else {
         if (int rc = workspace(stream, kIqbnPartials, quan::iqbn_workspace_bytes(pixels, c_out), &work))
             return rc;
-        e = quan::qconv2d_run(plan, pg, g, dt, x, packed, bias, out, nullptr, s);
+        e = quan::qconv2d_run(plan, pg, g, dt, x, packed, bias, out, nullptr, nullptr, s);
         if (e != hipSuccess)
             return fail_hip(e, "qconv2d launch");
         e = quan::iqbn_run(out, gamma, beta, eps, relu != 0, out, mean, var, pixels, c_out, dt, work, s);
     }
     if (e != hipSuccess)
         return fail_hip(e, "iqbn launch");
+    return QUAN_OK;
+}
+
+QUAN_API int quan_qconv2d_iqbn_inference(const void *x, const void *packed, const void *bias,
+                                         int32_t stride_h, int32_t stride_w, int32_t pad_h, int32_t pad_w,
+                                         int32_t dilation_h, int32_t dilation_w, const float *running_mean,
+                                         const float *running_var, const float *gamma, const float *beta,
+                                         float eps, int32_t relu, void *out, int32_t n, int32_t c_in,
+                                         int32_t h, int32_t w, int32_t c_out, int32_t k_h, int32_t k_w,
+                                         int32_t dtype, void *stream)
+{
+    g_last_error.clear();
+    if (!x || !packed || !out || !running_mean || !running_var || !gamma || !beta)
+        return fail(QUAN_ERR_NULL, "qconv2d_iqbn_inference: x, packed, running_mean, running_var, gamma, "
+                                   "beta and out must be non-NULL");
+    quan::ConvGeom g;
+    size_t xb = 0, ob = 0;
+    if (int rc = check_conv(x, bias, stride_h, stride_w, pad_h, pad_w, dilation_h, dilation_w, out,
+                            n, c_in, h, w, c_out, k_h, k_w, dtype, &g, &xb, &ob))
+        return rc;
+    if (!(eps > 0.0f) || eps != eps)
+        return fail(QUAN_ERR_SHAPE, "qconv2d_iqbn_inference: eps must be > 0 (got %g)", double(eps));
+    if (relu != 0 && relu != 1)
+        return fail(QUAN_ERR_SHAPE, "qconv2d_iqbn_inference: relu must be 0 or 1");
+    const int64_t need = quan_qconv2d_packed_bytes(c_in, c_out, k_h, k_w, dtype);
+    if (need < 0)
+        return int(need);
+    if (misaligned(packed, 16))
+        return fail(QUAN_ERR_ALIGN, "qconv2d_iqbn_inference: packed must be 16-byte aligned");
+    if (misaligned(running_mean, 4) || misaligned(running_var, 4) || misaligned(gamma, 4) ||
+        misaligned(beta, 4))
+        return fail(QUAN_ERR_ALIGN, "qconv2d_iqbn_inference: statistics, gamma and beta must be 4-byte aligned");
+    const size_t sbytes = size_t(4) * c_out * sizeof(float);
+    if (overlaps(out, ob, packed, size_t(need)) || overlaps(out, ob, running_mean, sbytes) ||
+        overlaps(out, ob, running_var, sbytes) || overlaps(out, ob, gamma, sbytes) ||
+        overlaps(out, ob, beta, sbytes))
+        return fail(QUAN_ERR_ALIAS, "qconv2d_iqbn_inference: out overlaps the weights, statistics or parameters");
+
+    const quan::DType dt = to_dt(dtype);
+    const quan::PackGeom pg = quan::qconv2d_pack_geom(c_in, c_out, k_h, k_w, dt);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    void *work = nullptr;
+    if (int rc = workspace(stream, kIqbnFold, 2 * sbytes, &work))
+        return rc;
+    float *scale = static_cast<float *>(work), *shift = scale + size_t(4) * c_out;
+    hipError_t e = quan::iqbn_fold_run(running_mean, running_var, gamma, beta, bias, eps, c_out, dt, scale,
+                                       shift, s);
+    if (e != hipSuccess)
+        return fail_hip(e, "iqbn fold launch");
+    const quan::ConvFold fold{scale, shift, relu != 0};
+    e = quan::qconv2d_run(quan::qconv2d_plan(g, dt), pg, g, dt, x, packed, bias, out, nullptr, &fold, s);
+    if (e != hipSuccess)
+        return fail_hip(e, "qconv2d launch");
+    return QUAN_OK;
+}
+
+QUAN_API int quan_poincare_map(const void *rgb, void *out, int32_t n, int32_t h, int32_t w, int32_t dtype,
+                               void *stream)
+{
+    g_last_error.clear();
+    if (!rgb || !out)
+        return fail(QUAN_ERR_NULL, "poincare_map: rgb and out must be non-NULL");
+    if (int rc = check_dtype(dtype))
+        return rc;
+    if (n < 1 || h < 1 || w < 1)
+        return fail(QUAN_ERR_SHAPE, "poincare_map: sizes must be >= 1 (n=%d h=%d w=%d)", n, h, w);
+    const int64_t pixels = int64_t(n) * h * w;
+    if (pixels * 4 > kMaxElems)
+        return fail(QUAN_ERR_UNSUPPORTED, "poincare_map: output of %lld elements exceeds 2^31-1",
+                    (long long)(pixels * 4));
+    const size_t es = elem_size(dtype);
+    if (misaligned(rgb, es) || misaligned(out, 4 * es))
+        return fail(QUAN_ERR_ALIGN, "poincare_map: rgb must be aligned to its element, out to four");
+    if (overlaps(rgb, size_t(pixels) * 3 * es, out, size_t(pixels) * 4 * es))
+        return fail(QUAN_ERR_ALIAS, "poincare_map: out overlaps rgb");
+    const hipError_t e = quan::poincare_run(rgb, out, n, h, w, to_dt(dtype), static_cast<hipStream_t>(stream));
+    if (e != hipSuccess)
+        return fail_hip(e, "poincare launch");
     return QUAN_OK;
 }
 

@@ -54,10 +54,19 @@ hipError_t qconv2d_pack_weights(const PackGeom &pg, int c_in, int c_out, int k_h
 // its output: stats[0][col][mt] = tile mean, stats[1][col][mt] = sum of
 // squared deviations from it, col = p * c_out + o, mt < plan.m_tiles; tile mt
 // covers pixels [mt * plan.bm, min((mt + 1) * plan.bm, m)).
+//
+// With `fold` non-NULL the epilogue applies out = scale[col] * acc +
+// shift[col] (fp32, [4][c_out] each, col = p * c_out + o) and max(0, .) when
+// relu is set, instead of adding the bias (inference IQBN folded in).
+struct ConvFold {
+    const float *scale;
+    const float *shift;
+    bool relu;
+};
 bool qconv2d_writes_stats(const ConvPlan &plan, const ConvGeom &g, DType dt);
 hipError_t qconv2d_run(const ConvPlan &plan, const PackGeom &pg, const ConvGeom &g, DType dt,
                        const void *x, const void *wpack, const void *bias, void *out,
-                       float *stats, hipStream_t stream);
+                       float *stats, const ConvFold *fold, hipStream_t stream);
 
 // IQBN.  `work` must hold iqbn_workspace_bytes(...) bytes.
 size_t iqbn_workspace_bytes(int64_t pixels, int c);
@@ -72,5 +81,16 @@ size_t iqbn_tile_stats_bytes(int m_tiles, int c);
 hipError_t iqbn_from_tiles_run(const float *part, int m_tiles, int tile_rows, const float *gamma,
                                const float *beta, float eps, bool relu, void *io, float *mean, float *var,
                                int64_t pixels, int c, DType dt, hipStream_t stream);
+
+// Inference IQBN folded into a convolution: per column col of [4][c],
+// scale = gamma / sqrt(var + eps) and shift = (bias - mean) * scale + beta
+// (computed in fp64, stored fp32); bias (dtype dt) may be NULL.
+hipError_t iqbn_fold_run(const float *mean, const float *var, const float *gamma, const float *beta,
+                         const void *bias, float eps, int c, DType dt, float *scale, float *shift,
+                         hipStream_t stream);
+
+// Poincare mapping (eq. 4): rgb [n][3][h][w] -> out [n][h][w][4].
+hipError_t poincare_run(const void *rgb, void *out, int64_t n, int64_t h, int64_t w, DType dt,
+                        hipStream_t stream);
 
 }  // namespace quan

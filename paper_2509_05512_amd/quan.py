@@ -34,6 +34,9 @@ SIGNATURES = {
     "quan_qconv2d_forward_packed": (ctypes.c_int, [_vp] * 3 + [_i32] * 6 + [_vp] + [_i32] * 8 + [_vp]),
     "quan_qconv2d_iqbn_forward": (ctypes.c_int, [_vp] * 3 + [_i32] * 6 + [_vp, _vp, _f32, _i32, _i32]
                                   + [_vp] * 3 + [_i32] * 8 + [_vp]),
+    "quan_qconv2d_iqbn_inference": (ctypes.c_int, [_vp] * 3 + [_i32] * 6 + [_vp] * 4 + [_f32, _i32, _vp]
+                                    + [_i32] * 8 + [_vp]),
+    "quan_poincare_map": (ctypes.c_int, [_vp, _vp] + [_i32] * 4 + [_vp]),
     "quan_iqbn_forward": (ctypes.c_int, [_vp, _vp, _vp, _f32, _vp, _vp, _vp] + [_i32] * 5 + [_vp]),
     "quan_iqbn_relu_forward": (ctypes.c_int, [_vp, _vp, _vp, _f32, _vp, _vp, _vp] + [_i32] * 5 + [_vp]),
     "quan_last_error": (ctypes.c_char_p, []),
@@ -267,6 +270,58 @@ def quan_qconv2d_iqbn_forward(x, packed, weight_shape, gamma, beta, bias=None, s
                                            k_h, k_w, _dtype_code(x), _stream(x.device))
     _check(rc)
     return out, mean, var
+
+
+def quan_qconv2d_iqbn_inference(x, packed, weight_shape, running_mean, running_var, gamma, beta,
+                                bias=None, stride=1, pad=0, dilation=1, eps=1e-5, relu=False, out=None):
+    """Inference-mode convolution + IQBN (+ ReLU) with stored statistics,
+    folded into the convolution's epilogue.  Returns out."""
+    lib = load_library()
+    if not is_device_layout(x):
+        raise ValueError("x must be [N, 4, Cin, H, W] stored channels-last by component")
+    n, _, c_in, h, w = x.shape
+    c_out, c_in_w, k_h, k_w = (int(v) for v in weight_shape)
+    if c_in_w != c_in:
+        raise ValueError("weight_shape does not match x's channels")
+    if bias is not None and (tuple(bias.shape) != (4, c_out) or not bias.is_contiguous()
+                             or bias.dtype != x.dtype or bias.device != x.device):
+        raise ValueError("bias must be a contiguous [4, Cout] tensor like x")
+    for name, t in (("running_mean", running_mean), ("running_var", running_var), ("gamma", gamma),
+                    ("beta", beta)):
+        if tuple(t.shape) != (4, c_out) or t.dtype != torch.float32 or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous float32 [4, Cout] tensor")
+    sh, sw = _pair(stride)
+    ph, pw = _pair(pad)
+    dh, dw = _pair(dilation)
+    ho, wo = conv_out_size(h, k_h, sh, ph, dh), conv_out_size(w, k_w, sw, pw, dw)
+    if out is None:
+        out = empty_qmap(n, c_out, max(ho, 1), max(wo, 1), x.dtype, x.device)
+    elif not is_device_layout(out) or tuple(out.shape) != (n, 4, c_out, ho, wo) or out.dtype != x.dtype:
+        raise ValueError("out must be [N, 4, Cout, Ho, Wo] in device layout with x's dtype")
+    with torch.cuda.device(x.device):
+        rc = lib.quan_qconv2d_iqbn_inference(_ptr(x), _ptr(packed), _ptr(bias), sh, sw, ph, pw, dh, dw,
+                                             _ptr(running_mean), _ptr(running_var), _ptr(gamma),
+                                             _ptr(beta), float(eps), int(bool(relu)), _ptr(out), n, c_in,
+                                             h, w, c_out, k_h, k_w, _dtype_code(x), _stream(x.device))
+    _check(rc)
+    return out
+
+
+def quan_poincare_map(rgb, out=None):
+    """Poincare mapping (eq. 4) of RGB images [N, 3, H, W] (contiguous) into a
+    one-channel quaternion map [N, 4, 1, H, W] in device layout."""
+    lib = load_library()
+    if rgb.dim() != 4 or rgb.shape[1] != 3 or not rgb.is_contiguous():
+        raise ValueError("rgb must be a contiguous [N, 3, H, W] tensor")
+    n, _, h, w = rgb.shape
+    if out is None:
+        out = empty_qmap(n, 1, h, w, rgb.dtype, rgb.device)
+    elif not is_device_layout(out) or tuple(out.shape) != (n, 4, 1, h, w) or out.dtype != rgb.dtype:
+        raise ValueError("out must be [N, 4, 1, H, W] in device layout with rgb's dtype")
+    with torch.cuda.device(rgb.device):
+        rc = lib.quan_poincare_map(_ptr(rgb), _ptr(out), n, h, w, _dtype_code(rgb), _stream(rgb.device))
+    _check(rc)
+    return out
 
 
 def _iqbn(fn_name, x, gamma, beta, eps, out, mean, var):

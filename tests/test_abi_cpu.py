@@ -140,6 +140,64 @@ def test_fused_conv_iqbn_rejects(lib, name, kw, code):
     assert msg
 
 
+def infer(lib, **kw):
+    a = dict(x=X, packed=WR, bias=B, sh=1, sw=1, ph=1, pw=1, dh=1, dw=1, m=MEAN, v=VAR, g=G, b=BE,
+             eps=1e-5, relu=0, out=OUT, n=2, cin=4, h=16, w=16, cout=4, kh=3, kw=3, dtype=1)
+    a.update(kw)
+    rc = lib.quan_qconv2d_iqbn_inference(a["x"], a["packed"], a["bias"], a["sh"], a["sw"], a["ph"],
+                                         a["pw"], a["dh"], a["dw"], a["m"], a["v"], a["g"], a["b"],
+                                         a["eps"], a["relu"], a["out"], a["n"], a["cin"], a["h"], a["w"],
+                                         a["cout"], a["kh"], a["kw"], a["dtype"], None)
+    return rc, lib.quan_last_error().decode()
+
+
+INFER_ERRORS = [
+    ("null packed", dict(packed=None), E_NULL),
+    ("null running mean", dict(m=None), E_NULL),
+    ("null running var", dict(v=None), E_NULL),
+    ("null beta", dict(b=None), E_NULL),
+    ("bad dtype", dict(dtype=7), E_DTYPE),
+    ("k = 0", dict(kh=0), E_SHAPE),
+    ("eps = 0", dict(eps=0.0), E_SHAPE),
+    ("eps nan", dict(eps=float("nan")), E_SHAPE),
+    ("relu = -1", dict(relu=-1), E_SHAPE),
+    ("packed misaligned", dict(packed=WR + 4), E_ALIGN),
+    ("var misaligned", dict(v=VAR + 1), E_ALIGN),
+    ("out overlaps packed", dict(out=WR), E_ALIAS),
+    ("mean inside out", dict(m=OUT + 128), E_ALIAS),
+    ("gamma inside out", dict(g=OUT + 4), E_ALIAS),
+]
+
+
+@pytest.mark.parametrize("name,kw,code", INFER_ERRORS, ids=[c[0] for c in INFER_ERRORS])
+def test_inference_conv_iqbn_rejects(lib, name, kw, code):
+    rc, msg = infer(lib, **kw)
+    assert rc == code, (name, rc, msg)
+    assert msg
+
+
+POINCARE_ERRORS = [
+    ("null rgb", dict(rgb=None), E_NULL),
+    ("null out", dict(out=None), E_NULL),
+    ("bad dtype", dict(dtype=2), E_DTYPE),
+    ("h = 0", dict(h=0), E_SHAPE),
+    ("n < 0", dict(n=-1), E_SHAPE),
+    ("too large", dict(n=1 << 12, h=1024, w=1024), E_UNSUP),
+    ("rgb misaligned", dict(rgb=X + 1), E_ALIGN),
+    ("out misaligned", dict(out=OUT + 2), E_ALIGN),
+    ("out overlaps rgb", dict(out=X + 64), E_ALIAS),
+]
+
+
+@pytest.mark.parametrize("name,kw,code", POINCARE_ERRORS, ids=[c[0] for c in POINCARE_ERRORS])
+def test_poincare_rejects(lib, name, kw, code):
+    a = dict(rgb=X, out=OUT, n=2, h=16, w=16, dtype=1)
+    a.update(kw)
+    rc = lib.quan_poincare_map(a["rgb"], a["out"], a["n"], a["h"], a["w"], a["dtype"], None)
+    assert rc == code, (name, rc, lib.quan_last_error())
+    assert lib.quan_last_error()
+
+
 IQBN_ERRORS = [
     ("null gamma", dict(g=None), E_NULL),
     ("null var", dict(var=None), E_NULL),

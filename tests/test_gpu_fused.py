@@ -167,3 +167,55 @@ def test_fused_statistics_many_tiles_per_work_group(case):
     xg = quan.to_device_layout(x.to(dev))
     wg = [w[q].contiguous().to(dev) for q in range(4)]
     _check_layer_statistics(xg, wg, g.to(dev), be.to(dev), 1, k // 2, str(case))
+
+
+# ------------------------- inference IQBN folded in -------------------------
+
+def _running_stats(case, seed):
+    Cout = case[2]
+    rng = np.random.default_rng(seed)
+    rm = torch.from_numpy((rng.standard_normal((4, Cout)) * 0.5).astype(np.float32))
+    rv = torch.from_numpy(rng.uniform(0.5, 2.0, (4, Cout)).astype(np.float32))
+    return rm, rv
+
+
+@pytest.mark.parametrize("relu", [False, True])
+@pytest.mark.parametrize("case", CASES, ids=[str(c) for c in CASES])
+def test_inference_conv_iqbn_matches_oracle(case, relu):
+    """quan_qconv2d_iqbn_inference against the oracle's conv followed by its
+    inference IQBN (fp64), with random stored statistics."""
+    say(f"inference conv+iqbn {case} relu={relu}")
+    N, Cin, Cout, H, W, k, s, p, _, dtype = case
+    dt = DT[dtype]
+    seed = sum(map(ord, str(case))) % 997
+    x, w, b, g, be = _case(case, seed=seed)
+    rm, rv = _running_stats(case, seed + 1)
+    dev = torch.device("cuda:0")
+    xg = quan.to_device_layout(x.to(dev))
+    wg = [w[q].contiguous().to(dev) for q in range(4)]
+    packed = quan.quan_qconv2d_pack_weights(*wg)
+    out = quan.quan_qconv2d_iqbn_inference(xg, packed, tuple(wg[0].shape), rm.to(dev), rv.to(dev), g.to(dev),
+                                           be.to(dev), bias=b.to(dev), stride=s, pad=p, relu=relu)
+    torch.cuda.synchronize()
+    ref = oracle.iqbn_inference(oracle.qconv2d(f64(x), f64(w), f64(b), s, p, 1), f64(rm), f64(rv),
+                                f64(g), f64(be), 1e-5, relu)
+    assert_close(f64(out.cpu()), ref, dt, f"inference {case} relu={relu}")
+
+
+def test_inference_with_batch_statistics_equals_training():
+    """Stored statistics equal to the batch's own give the training-mode
+    result (same conv output, same normalization up to rounding)."""
+    say("inference vs training")
+    case = (2, 32, 64, 14, 14, 3, 1, 1, True, "bf16")
+    x, w, b, g, be = _case(case, seed=5)
+    dev = torch.device("cuda:0")
+    conv, out, mean, var = _gpu(x, w, b, g, be, 1, 1, True, "pass")
+    xg = quan.to_device_layout(x.to(dev))
+    wg = [w[q].contiguous().to(dev) for q in range(4)]
+    packed = quan.quan_qconv2d_pack_weights(*wg)
+    inf = quan.quan_qconv2d_iqbn_inference(xg, packed, tuple(wg[0].shape), mean.to(dev), var.to(dev),
+                                           g.to(dev), be.to(dev), bias=b.to(dev), stride=1, pad=1, relu=True)
+    torch.cuda.synchronize()
+    # training normalizes the rounded conv output, inference the fp32
+    # accumulator: one bf16 rounding apart
+    assert_close(f64(inf.cpu()), f64(out), torch.bfloat16, "inference vs training")
