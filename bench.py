@@ -139,6 +139,28 @@ def run_step_inference(layers, quan, eps=1e-5):
                                          relu=L.relu, out=ly["z"])
 
 
+def time_separable(layers, quan, steps):
+    """The separable convolution (eq. 7) on every layer's packed weights:
+    microseconds per step (all layers) of the convolution alone."""
+    import torch
+    def once():
+        for ly in layers:
+            L = ly["spec"]
+            quan.quan_qconv2d_separable_forward_packed(ly["x"], ly["packed"], (L.c_out, L.c_in, L.k, L.k),
+                                                       bias=ly["bias"], stride=L.stride, pad=L.pad,
+                                                       dilation=L.dilation, out=ly["y"])
+    for _ in range(2):
+        once()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(steps):
+        once()
+    end.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) * 1e3 / steps
+
+
 def time_poincare(quan, steps, dev):
     """The Poincare input mapping of one ImageNet-sized bf16 batch
     (64 x 3 x 224 x 224): microseconds per launch and algorithmic GB/s
@@ -295,6 +317,7 @@ def main():
     torch.cuda.synchronize()
     inference_ms = start.elapsed_time(end) / args.steps
     poincare = time_poincare(quan, args.steps, dev)
+    separable_us = time_separable(layers, quan, args.steps)
 
     # per-kernel times: the same steps with every kernel on its own
     for _ in range(2):
@@ -360,6 +383,12 @@ def main():
         "inference_us_per_step": round(inference_ms * 1e3, 3),
         "inference_tflops": round(step_flops / (inference_ms * 1e-3) / 1e12, 2),
         "poincare": poincare,
+        "separable": {
+            "us_per_step": round(separable_us, 3),
+            # eq. 7 does a quarter of the Hamilton product's multiply-adds
+            "tflops": round(step_flops / 4 / (separable_us * 1e-6) / 1e12, 2),
+            "frac_mfma_peak": round(step_flops / 4 / (separable_us * 1e-6) / 1e12 / peak, 4),
+        },
         "separate_kernels_us_per_step": round((sum(pack_ms) + sum(conv_ms) + sum(iqbn_ms)) * 1e3, 3),
         "qconv2d": {
             "tflops": round(conv_tflops, 2),

@@ -141,6 +141,39 @@ QUAN_API int quan_qconv2d_forward_packed(const void *x, const void *packed, cons
                                          int32_t dtype, void *stream);
 
 /*
+ * The separable QUAN convolution of Section III-B, eq. 7, with the same
+ * arguments, layouts, packed weights and limits as quan_qconv2d_forward and
+ * quan_qconv2d_forward_packed: each output component is a signed sum of the
+ * four real convolutions W_q (*) x_q only,
+ *
+ *   y_r = W_r*x_r - W_i*x_i - W_j*x_j - W_k*x_k
+ *   y_i = W_r*x_r + W_i*x_i + W_j*x_j - W_k*x_k
+ *   y_j = W_r*x_r - W_i*x_i + W_j*x_j + W_k*x_k
+ *   y_k = W_r*x_r + W_i*x_i - W_j*x_j + W_k*x_k      (+ bias per component)
+ *
+ * a quarter of the Hamilton product's multiply-adds.  It is not a Hamilton
+ * product (the identity kernel maps x to (x_r, x_r, x_r, x_r)); its sign
+ * matrix is the transpose of the mixing matrix printed for the backward
+ * pass (eq. 9).  The four sums are formed in fp32 and rounded once.
+ */
+QUAN_API int quan_qconv2d_separable_forward(const void *x, const void *w_r, const void *w_i,
+                                            const void *w_j, const void *w_k, const void *bias,
+                                            int32_t stride_h, int32_t stride_w,
+                                            int32_t pad_h, int32_t pad_w,
+                                            int32_t dilation_h, int32_t dilation_w,
+                                            void *out, int32_t n, int32_t c_in, int32_t h,
+                                            int32_t w, int32_t c_out, int32_t k_h, int32_t k_w,
+                                            int32_t dtype, void *stream);
+
+QUAN_API int quan_qconv2d_separable_forward_packed(const void *x, const void *packed,
+                                                   const void *bias, int32_t stride_h,
+                                                   int32_t stride_w, int32_t pad_h, int32_t pad_w,
+                                                   int32_t dilation_h, int32_t dilation_w,
+                                                   void *out, int32_t n, int32_t c_in, int32_t h,
+                                                   int32_t w, int32_t c_out, int32_t k_h,
+                                                   int32_t k_w, int32_t dtype, void *stream);
+
+/*
  * Independent Quaternion Batch Normalization (Section III-C, eqs. 11, 12).
  *
  * For every component q and channel ch separately, over the P = n*h*w values

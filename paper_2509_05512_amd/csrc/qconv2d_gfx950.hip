@@ -60,6 +60,12 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 constexpr unsigned kHamiltonNeg =
     (1u << 1) | (1u << 2) | (1u << 3) | (1u << 6) | (1u << 11) | (1u << 13);
 
+// Bit 4*p + q is set when the separable form (eq. 7) subtracts W_q (*) x_q
+// from output component p.  Row r: + - - -, row i: + + + -, row j: + - + +,
+// row k: + + - +.
+constexpr unsigned kSeparableNeg =
+    (1u << 1) | (1u << 2) | (1u << 3) | (1u << 7) | (1u << 9) | (1u << 14);
+
 template <typename T>
 struct Elem;
 template <>
@@ -234,8 +240,16 @@ __device__ __forceinline__ void wait_vmcnt()
 // EPI: what the epilogue applies (kEpiBias, kEpiStats, kEpiFold); fixed at
 // compile time so the common bias-only kernel carries none of the others'
 // state through its main loop.
+//
+// SEP: the separable convolution of eq. 7 instead of the Hamilton product.
+// Each wave then keeps the four real convolutions c_q = W_q (*) x_q of its
+// MB x NB blocks (32 pixels x 32 output channels each) in separate
+// accumulators: k-step q multiplies only x_q by W_q (a quarter of the
+// Hamilton MFMAs), and the epilogue mixes y_p = sum_q S[p][q] c_q in fp32.
+// The tile is BM pixels x BN/4 = 32*NB*WAVES_N output channels, all four
+// output components.
 enum : int { kEpiBias = 0, kEpiStats = 1, kEpiFold = 2 };
-template <typename T, int MB, int NB, int WAVES_M, int WAVES_N, bool VEC, int EPI>
+template <typename T, int MB, int NB, int WAVES_M, int WAVES_N, bool VEC, int EPI, bool SEP>
 __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + 2)) void qconv2d_igemm(KArgs a)
 {
     constexpr int ES = int(sizeof(T));
@@ -247,8 +261,9 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + 2)) void qconv2d_igemm(KA
     constexpr int WTM = 32 * MB;
     constexpr int WTN = 32 * NB;
     constexpr int BM = WTM * WAVES_M;
-    constexpr int BN = WTN * WAVES_N;
+    constexpr int BN = (SEP ? 4 : 1) * WTN * WAVES_N;  // output reals per tile
     constexpr int BNC = BN / 4;
+    constexpr int QS = SEP ? 4 : 1;  // accumulator sets per block
     constexpr int NBUF = 4;                     // stages in the LDS ring
     constexpr int A_BYTES = BM * 128;           // one stage of activations
     constexpr int B_BYTES = 4 * BNC * CS * ES;  // one stage of weights
@@ -269,7 +284,7 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + 2)) void qconv2d_igemm(KA
     // all BM pixels, it parks each finished tile in its own LDS region and
     // drains it with full-line 16-byte stores during the next tile's steps,
     // instead of every work-group writing its tile at the same moment.
-    constexpr bool DEFER = WAVES_M == 1 && WTN == BNC && P_UNIFORM;
+    constexpr bool DEFER = WAVES_M == 1 && WTN == BNC && P_UNIFORM && !SEP;
     constexpr int OUT_ROW = BNC * ES;     // bytes of one pixel in a wave's region
     constexpr int OUT_CPR = OUT_ROW / 16;  // 16-byte chunks per pixel
     constexpr int OUT_WAVE = BM * OUT_ROW;
@@ -450,34 +465,45 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + 2)) void qconv2d_igemm(KA
     const int l32 = lane & 31;
 
     // K-step j of a stage is input component q = j: chunks 2j + {0, 1} of the
-    // activation row and chunks {0, 1} of weight row (p ^ j) * BNC + o.  Lane
-    // l reads chunk 2j + l/32 (activations) / chunk l/32 (weights) of row
-    // l%32 of its 32-row block.
+    // activation row and chunks {0, 1} of weight row (p ^ j) * BNC + o (the
+    // Hamilton block), or j * BNC + o (separable: W_j only).  Lane l reads
+    // chunk 2j + l/32 (activations) / chunk l/32 (weights) of row l%32 of
+    // its 32-row block.
     int a_rd[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j)
         a_rd[j] = (wm * WTM + l32) * 128 + (((2 * j + khalf) ^ swz<8>(l32)) * 16);
     // When all N blocks of a wave lie in one output component (SHARED_P),
     // block nb's weight rows are block 0's plus 32*nb: an immediate offset.
-    constexpr bool SHARED_P = P_UNIFORM && WTN <= BNC;
+    constexpr bool SHARED_P = SEP || (P_UNIFORM && WTN <= BNC);
     constexpr int NB_RD = SHARED_P ? 1 : NB;
     int b_rd[NB_RD][4];
     unsigned flip[NB][4];
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
-        const int tn = wn * WTN + nb * 32 + l32;
-        const int p = P_UNIFORM ? __builtin_amdgcn_readfirstlane(tn / BNC) : tn / BNC;
-        const int o = tn % BNC;
+        if constexpr (SEP) {
+            const int o = wn * WTN + nb * 32 + l32;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int row = (p ^ j) * BNC + o;
-            if (nb < NB_RD)
-                b_rd[nb][j] = row * CPQ * 16 + ((khalf ^ swz<CPQ>(o)) * 16);
-            flip[nb][j] = ((kHamiltonNeg >> (4 * p + j)) & 1u) ? Elem<T>::sign : 0u;
+            for (int j = 0; j < 4; ++j) {
+                if (nb < NB_RD)
+                    b_rd[nb][j] = (j * BNC + o) * CPQ * 16 + ((khalf ^ swz<CPQ>(o)) * 16);
+                flip[nb][j] = 0u;
+            }
+        } else {
+            const int tn = wn * WTN + nb * 32 + l32;
+            const int p = P_UNIFORM ? __builtin_amdgcn_readfirstlane(tn / BNC) : tn / BNC;
+            const int o = tn % BNC;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int row = (p ^ j) * BNC + o;
+                if (nb < NB_RD)
+                    b_rd[nb][j] = row * CPQ * 16 + ((khalf ^ swz<CPQ>(o)) * 16);
+                flip[nb][j] = ((kHamiltonNeg >> (4 * p + j)) & 1u) ? Elem<T>::sign : 0u;
+            }
         }
     }
 
-    f32x16 acc[NB][MB];
+    f32x16 acc[QS][NB][MB];
     struct Frags {
         u32x4 w[NB];
         u32x4 p[MB];
@@ -492,16 +518,25 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + 2)) void qconv2d_igemm(KA
         for (int mb = 0; mb < MB; ++mb)
             f.p[mb] = *reinterpret_cast<const u32x4 *>(a_lds + buf * A_BYTES + mb * 32 * 128 + a_rd[j]);
     };
-    // Sign of block (p, q = j) applied to the weight fragments, then the MFMAs.
+    // Sign of block (p, q = j) applied to the weight fragments, then the
+    // MFMAs (separable: into the accumulators of c_j, no signs).
     auto mfmas = [&](int j, Frags &f) {
+        if constexpr (SEP) {
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
-            f.w[nb] ^= flip[nb][j];
+            for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
+                for (int mb = 0; mb < MB; ++mb)
+                    mfma_step<T>(acc[j][nb][mb], f.w[nb], f.p[mb]);
+        } else {
 #pragma unroll
-            for (int mb = 0; mb < MB; ++mb)
-                mfma_step<T>(acc[nb][mb], f.w[nb], f.p[mb]);
+            for (int nb = 0; nb < NB; ++nb)
+                f.w[nb] ^= flip[nb][j];
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                for (int mb = 0; mb < MB; ++mb)
+                    mfma_step<T>(acc[0][nb][mb], f.w[nb], f.p[mb]);
+        }
     };
 
     // ---- deferred-epilogue drain ----
@@ -536,12 +571,49 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + 2)) void qconv2d_igemm(KA
     //   barrier (step g+1's stage has landed; step g's is read no more);
     //   k-step 3 on f1, reading step g+1's k-step 0 into f0.
     // Past the last step that read fetches unused data from an idle slot.
+    //
+    // Separable form: a k-step has only MB x NB MFMAs, too few to cover one
+    // fragment read, so each read is issued two k-steps ahead into one of
+    // four fragment sets (fa..fd hold k-steps 0..3):
+    //   k-step 0 on fa, reading k-step 2 into fc;
+    //   k-step 1 on fb, reading k-step 3 into fd;
+    //   barrier;
+    //   k-step 2 on fc, reading step g+1's k-step 0 into fa;
+    //   k-step 3 on fd, reading step g+1's k-step 1 into fb.
     constexpr int N_READ = MB + NB;
-    constexpr int N_FLIP = NB * 4;
+    constexpr int N_FLIP = SEP ? 0 : NB * 4;
     Frags f0, f1;
+    Frags fc, fd;  // separable form only
     __syncthreads();
     read_frags(0, 0, f0);
+    if constexpr (SEP)
+        read_frags(0, 1, f1);
+    auto step_sep = [&](auto slot) {
+        constexpr int B = decltype(slot)::value;
+        __builtin_amdgcn_sched_barrier(0);
+        read_frags(B, 2, fc);
+        mfmas(0, f0);
+        interleave_kstep<N_MFMA, 0, N_READ, 1>();
+        __builtin_amdgcn_sched_barrier(0);
+        read_frags(B, 3, fd);
+        mfmas(1, f1);
+        interleave_kstep<N_MFMA, 0, N_READ, 1>();
+        __builtin_amdgcn_sched_barrier(0);
+        __syncthreads();
+        read_frags((B + 1) & (NBUF - 1), 0, f0);
+        mfmas(2, fc);
+        interleave_kstep<N_MFMA, 0, N_READ, 1>();
+        __builtin_amdgcn_sched_barrier(0);
+        read_frags((B + 1) & (NBUF - 1), 1, f1);
+        mfmas(3, fd);
+        interleave_kstep<N_MFMA, 0, N_READ, 1>();
+        __builtin_amdgcn_sched_barrier(0);
+    };
     auto step = [&](auto slot) {
+        if constexpr (SEP) {
+            step_sep(slot);
+            return;
+        }
         constexpr int B = decltype(slot)::value;  // ring slot of this step's stage
         // one drain store per step: read from LDS now, stored after k-step 1
         u32x4 dv0;
@@ -705,12 +777,14 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + 2)) void qconv2d_igemm(KA
         const int m0 = (tile / a.n_tiles) * BM;
         const int o0 = (tile % a.n_tiles) * BNC;
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
+        for (int qs = 0; qs < QS; ++qs)
 #pragma unroll
-            for (int mb = 0; mb < MB; ++mb)
+            for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-                for (int e = 0; e < 16; ++e)
-                    acc[nb][mb][e] = 0.0f;
+                for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e)
+                        acc[qs][nb][mb][e] = 0.0f;
         if (ph == 0)
             run_tile(P0{});
         else if (ph == 1)
@@ -745,7 +819,7 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + 2)) void qconv2d_igemm(KA
                         T v[4];
 #pragma unroll
                         for (int e = 0; e < 4; ++e)
-                            v[e] = T(epi(acc[nb][mb][4 * g + e], sc[e], sh[e]));
+                            v[e] = T(epi(acc[0][nb][mb][4 * g + e], sc[e], sh[e]));
                         const int c = oc * ES / 16, within = (oc * ES) % 16;
                         unsigned char *dst = w_lds + m * OUT_ROW + ((c ^ (m % OUT_CPR)) * 16) + within;
                         if constexpr (ES == 2) {
@@ -774,44 +848,80 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + 2)) void qconv2d_igemm(KA
         // ---- epilogue: bias, round, channels-last store ----
         // Accumulator register 4*g + e of lane l holds output channel row
         // 8*g + 4*(l/32) + e of the 32x32 block and pixel column l%32.
+        // Writes the four channels o..o+3 of component p at pixel m.
+        auto store4 = [&](int m, int p, int o, const float *y) {
+            float sc[4], sh[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                col_affine(p * a.c_out + o + e, o + e < a.c_out, sc[e], sh[e]);
+            T *dst = out + ((size_t)m * 4 * a.c_out + p * a.c_out + o);
+            T v[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                v[e] = T(epi(y[e], sc[e], sh[e]));
+            if (vec_out) {
+                if constexpr (sizeof(T) == 2) {
+                    uint2 pk;
+                    __builtin_memcpy(&pk, v, 8);
+                    *reinterpret_cast<uint2 *>(dst) = pk;
+                } else {
+                    float4 pk;
+                    __builtin_memcpy(&pk, v, 16);
+                    *reinterpret_cast<float4 *>(dst) = pk;
+                }
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (o + e < a.c_out)
+                        dst[e] = v[e];
+            }
+        };
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
-                const int tn = wn * WTN + nb * 32 + 8 * g + 4 * khalf;
-                const int p = tn / BNC;
-                const int o = o0 + (tn - p * BNC);
-                if (o >= a.c_out)
-                    continue;
-                float sc[4], sh[4];
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    col_affine(p * a.c_out + o + e, o + e < a.c_out, sc[e], sh[e]);
-#pragma unroll
-                for (int mb = 0; mb < MB; ++mb) {
-                    const int m = m0 + wm * WTM + mb * 32 + l32;
-                    if (m >= a.m)
+                if constexpr (SEP) {
+                    const int o = o0 + wn * WTN + nb * 32 + 8 * g + 4 * khalf;
+                    if (o >= a.c_out)
                         continue;
-                    T *dst = out + ((size_t)m * 4 * a.c_out + p * a.c_out + o);
-                    T v[4];
 #pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        v[e] = T(epi(acc[nb][mb][4 * g + e], sc[e], sh[e]));
-                    if (vec_out) {
-                        if constexpr (sizeof(T) == 2) {
-                            uint2 pk;
-                            __builtin_memcpy(&pk, v, 8);
-                            *reinterpret_cast<uint2 *>(dst) = pk;
-                        } else {
-                            float4 pk;
-                            __builtin_memcpy(&pk, v, 16);
-                            *reinterpret_cast<float4 *>(dst) = pk;
+                    for (int mb = 0; mb < MB; ++mb) {
+                        const int m = m0 + wm * WTM + mb * 32 + l32;
+                        if (m >= a.m)
+                            continue;
+                        // eq. 7: y_p = sum_q S[p][q] c_q, in fp32
+#pragma unroll
+                        for (int p = 0; p < 4; ++p) {
+                            float y[4];
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) {
+                                float t = 0.0f;
+#pragma unroll
+                                for (int q = 0; q < 4; ++q) {
+                                    const float c = acc[q][nb][mb][4 * g + e];
+                                    t = ((kSeparableNeg >> (4 * p + q)) & 1u) ? t - c : t + c;
+                                }
+                                y[e] = t;
+                            }
+                            store4(m, p, o, y);
                         }
-                    } else {
+                    }
+                } else {
+                    const int tn = wn * WTN + nb * 32 + 8 * g + 4 * khalf;
+                    const int p = tn / BNC;
+                    const int o = o0 + (tn - p * BNC);
+                    if (o >= a.c_out)
+                        continue;
+#pragma unroll
+                    for (int mb = 0; mb < MB; ++mb) {
+                        const int m = m0 + wm * WTM + mb * 32 + l32;
+                        if (m >= a.m)
+                            continue;
+                        float y[4];
 #pragma unroll
                         for (int e = 0; e < 4; ++e)
-                            if (o + e < a.c_out)
-                                dst[e] = v[e];
+                            y[e] = acc[0][nb][mb][4 * g + e];
+                        store4(m, p, o, y);
                     }
                 }
             }
@@ -857,6 +967,7 @@ __global__ __launch_bounds__(256) void qconv2d_pack(const T *__restrict__ w0, co
 
 struct KernelEntry {
     int bm, bnc, mb, nb, threads;
+    bool sep;    // separable convolution (eq. 7) instead of the Hamilton product
     bool defer;  // deferred epilogue (one output component per wave); writes IQBN statistics
     DType dt;
     // [epilogue kind][masked]: masked = 0 when c_in is a multiple of the
@@ -867,35 +978,40 @@ struct KernelEntry {
     const char *name;
 };
 
-#define QCONV_DEFER(NB, WM, WN) ((WM) == 1 && (WN) == 4 && 8 * (NB) * (WN) >= 32)
+#define QCONV_DEFER(NB, WM, WN, SEP) (!(SEP) && (WM) == 1 && (WN) == 4 && 8 * (NB) * (WN) >= 32)
 // the statistics variant exists only for tiles with the deferred epilogue
-template <typename T, int MB, int NB, int WM, int WN, bool VEC>
+template <typename T, int MB, int NB, int WM, int WN, bool VEC, bool SEP>
 constexpr const void *stats_fn()
 {
-    if constexpr (QCONV_DEFER(NB, WM, WN))
-        return (const void *)&qconv2d_igemm<T, MB, NB, WM, WN, VEC, kEpiStats>;
+    if constexpr (QCONV_DEFER(NB, WM, WN, SEP))
+        return (const void *)&qconv2d_igemm<T, MB, NB, WM, WN, VEC, kEpiStats, SEP>;
     else
         return nullptr;
 }
-#define QCONV_STATS_FN(T, MB, NB, WM, WN, VEC) stats_fn<T, MB, NB, WM, WN, VEC>()
-#define QCONV_K(T, DT, MB, NB, WM, WN)                                                                 \
+#define QCONV_STATS_FN(T, MB, NB, WM, WN, VEC, SEP) stats_fn<T, MB, NB, WM, WN, VEC, SEP>()
+#define QCONV_K(T, DT, MB, NB, WM, WN, SEP)                                                            \
     KernelEntry                                                                                        \
     {                                                                                                  \
-        32 * (MB) * (WM), 8 * (NB) * (WN), MB, NB, 64 * ((WM) * (WN) + 2),                             \
-            QCONV_DEFER(NB, WM, WN), DT,                                                               \
-            {{(const void *)&qconv2d_igemm<T, MB, NB, WM, WN, true, kEpiBias>,                         \
-              (const void *)&qconv2d_igemm<T, MB, NB, WM, WN, false, kEpiBias>},                       \
-             {QCONV_STATS_FN(T, MB, NB, WM, WN, true), QCONV_STATS_FN(T, MB, NB, WM, WN, false)},      \
-             {(const void *)&qconv2d_igemm<T, MB, NB, WM, WN, true, kEpiFold>,                         \
-              (const void *)&qconv2d_igemm<T, MB, NB, WM, WN, false, kEpiFold>}},                      \
-            #T "_mb" #MB "x" #WM "_nb" #NB "x" #WN                                                     \
+        32 * (MB) * (WM), ((SEP) ? 32 : 8) * (NB) * (WN), MB, NB, 64 * ((WM) * (WN) + 2), SEP,         \
+            QCONV_DEFER(NB, WM, WN, SEP), DT,                                                          \
+            {{(const void *)&qconv2d_igemm<T, MB, NB, WM, WN, true, kEpiBias, SEP>,                    \
+              (const void *)&qconv2d_igemm<T, MB, NB, WM, WN, false, kEpiBias, SEP>},                  \
+             {QCONV_STATS_FN(T, MB, NB, WM, WN, true, SEP), QCONV_STATS_FN(T, MB, NB, WM, WN, false, SEP)}, \
+             {(const void *)&qconv2d_igemm<T, MB, NB, WM, WN, true, kEpiFold, SEP>,                    \
+              (const void *)&qconv2d_igemm<T, MB, NB, WM, WN, false, kEpiFold, SEP>}},                 \
+            #T "_mb" #MB "x" #WM "_nb" #NB "x" #WN #SEP                                                \
     }
 
 const KernelEntry kKernels[] = {
-    QCONV_K(__bf16, DType::BF16, 4, 2, 1, 4),  // 128 px x 64 channels
-    QCONV_K(__bf16, DType::BF16, 4, 1, 1, 4),  // 128 px x 32 channels
-    QCONV_K(__bf16, DType::BF16, 2, 1, 2, 2),  // 128 px x 16 channels
-    QCONV_K(float, DType::F32, 1, 1, 2, 2),    // 64 px x 16 channels
+    // Hamilton product (eq. 5)
+    QCONV_K(__bf16, DType::BF16, 4, 2, 1, 4, false),  // 128 px x 64 channels
+    QCONV_K(__bf16, DType::BF16, 4, 1, 1, 4, false),  // 128 px x 32 channels
+    QCONV_K(__bf16, DType::BF16, 2, 1, 2, 2, false),  // 128 px x 16 channels
+    QCONV_K(float, DType::F32, 1, 1, 2, 2, false),    // 64 px x 16 channels
+    // separable form (eq. 7): each wave all four c_q of 32 px x 32*NB channels
+    QCONV_K(__bf16, DType::BF16, 1, 2, 4, 1, true),   // 128 px x 64 channels
+    QCONV_K(__bf16, DType::BF16, 1, 1, 4, 1, true),   // 128 px x 32 channels
+    QCONV_K(float, DType::F32, 1, 1, 4, 1, true),     // 128 px x 32 channels
 };
 constexpr int kNumKernels = int(sizeof(kKernels) / sizeof(kKernels[0]));
 
@@ -962,7 +1078,7 @@ PackGeom qconv2d_pack_geom(int c_in, int c_out, int k_h, int k_w, DType dt)
     return pg;
 }
 
-ConvPlan qconv2d_plan(const ConvGeom &g, DType dt)
+ConvPlan qconv2d_plan(const ConvGeom &g, DType dt, bool sep)
 {
     const int64_t m = g.m();
     const int pk = dt == DType::BF16 ? 16 : 8;
@@ -972,10 +1088,12 @@ ConvPlan qconv2d_plan(const ConvGeom &g, DType dt)
     const int cus = device_cus();
     for (int i = 0; i < kNumKernels; ++i) {
         const KernelEntry &k = kKernels[i];
-        if (k.dt != dt)
+        if (k.dt != dt || k.sep != sep)
             continue;
         // narrow tiles only where the output channels leave a wide one idle
         if (dt == DType::BF16 && ((k.bnc == 16 && g.c_out > 16) || (k.bnc == 64 && g.c_out <= 32)))
+            continue;
+        if (sep && k.bnc == 64 && g.c_out <= 32)
             continue;
         const double cost = plan_cost(k, m, g.c_out, stages, cus);
         if (id < 0 || cost < best) {
@@ -987,7 +1105,7 @@ ConvPlan qconv2d_plan(const ConvGeom &g, DType dt)
     // Tuning builds only: force a kernel (QUAN_QCONV_KERNEL=<table index>).
     if (const char *force = getenv("QUAN_QCONV_KERNEL")) {
         const int f = atoi(force);
-        if (f >= 0 && f < kNumKernels && kKernels[f].dt == dt)
+        if (f >= 0 && f < kNumKernels && kKernels[f].dt == dt && kKernels[f].sep == sep)
             id = f;
     }
 #endif

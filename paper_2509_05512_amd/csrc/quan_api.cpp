@@ -217,6 +217,84 @@ int iqbn_common(const void *x, const float *gamma, const float *beta, float eps,
 
 extern "C" {
 
+namespace {
+
+// The convolution on packed weights (Hamilton, eq. 5, or separable, eq. 7).
+int conv_packed(const char *name, bool sep, const void *x, const void *packed, const void *bias,
+                int32_t stride_h, int32_t stride_w, int32_t pad_h, int32_t pad_w, int32_t dilation_h,
+                int32_t dilation_w, void *out, int32_t n, int32_t c_in, int32_t h, int32_t w, int32_t c_out,
+                int32_t k_h, int32_t k_w, int32_t dtype, void *stream)
+{
+    g_last_error.clear();
+    if (!x || !packed || !out)
+        return fail(QUAN_ERR_NULL, "%s: x, packed and out must be non-NULL", name);
+    quan::ConvGeom g;
+    size_t xb = 0, ob = 0;
+    if (int rc = check_conv(x, bias, stride_h, stride_w, pad_h, pad_w, dilation_h, dilation_w, out,
+                            n, c_in, h, w, c_out, k_h, k_w, dtype, &g, &xb, &ob))
+        return rc;
+    const int64_t need = quan_qconv2d_packed_bytes(c_in, c_out, k_h, k_w, dtype);
+    if (need < 0)
+        return int(need);
+    if (misaligned(packed, 16))
+        return fail(QUAN_ERR_ALIGN, "%s: packed must be 16-byte aligned", name);
+    if (overlaps(out, ob, packed, size_t(need)))
+        return fail(QUAN_ERR_ALIAS, "%s: out overlaps the packed weights", name);
+    const quan::DType dt = to_dt(dtype);
+    const quan::PackGeom pg = quan::qconv2d_pack_geom(c_in, c_out, k_h, k_w, dt);
+    const quan::ConvPlan plan = quan::qconv2d_plan(g, dt, sep);
+    hipError_t e = quan::qconv2d_run(plan, pg, g, dt, x, packed, bias, out, nullptr, nullptr,
+                                     static_cast<hipStream_t>(stream));
+    if (e != hipSuccess)
+        return fail_hip(e, "qconv2d launch");
+    return QUAN_OK;
+}
+
+// The convolution on the four real kernels, packed into a library workspace
+// first.
+int conv_unpacked(const char *name, bool sep, const void *x, const void *w_r, const void *w_i,
+                  const void *w_j, const void *w_k, const void *bias, int32_t stride_h, int32_t stride_w,
+                  int32_t pad_h, int32_t pad_w, int32_t dilation_h, int32_t dilation_w, void *out, int32_t n,
+                  int32_t c_in, int32_t h, int32_t w, int32_t c_out, int32_t k_h, int32_t k_w, int32_t dtype,
+                  void *stream)
+{
+    g_last_error.clear();
+    if (!x || !w_r || !w_i || !w_j || !w_k || !out)
+        return fail(QUAN_ERR_NULL, "%s: x, w_r, w_i, w_j, w_k and out must be non-NULL", name);
+    quan::ConvGeom g;
+    size_t xb = 0, ob = 0;
+    if (int rc = check_conv(x, bias, stride_h, stride_w, pad_h, pad_w, dilation_h, dilation_w, out,
+                            n, c_in, h, w, c_out, k_h, k_w, dtype, &g, &xb, &ob))
+        return rc;
+    const size_t es = elem_size(dtype);
+    if (misaligned(w_r, es) || misaligned(w_i, es) || misaligned(w_j, es) || misaligned(w_k, es))
+        return fail(QUAN_ERR_ALIGN, "%s: weights and bias must be aligned to their element size", name);
+    const size_t wb = size_t(c_out) * c_in * k_h * k_w * es;
+    if (overlaps(out, ob, w_r, wb) || overlaps(out, ob, w_i, wb) || overlaps(out, ob, w_j, wb) ||
+        overlaps(out, ob, w_k, wb))
+        return fail(QUAN_ERR_ALIAS, "%s: out overlaps x, a kernel or the bias", name);
+    const int64_t need = quan_qconv2d_packed_bytes(c_in, c_out, k_h, k_w, dtype);
+    if (need < 0)
+        return int(need);
+
+    void *wpack = nullptr;
+    if (int rc = workspace(stream, kWeightPack, size_t(need), &wpack))
+        return rc;
+    const quan::DType dt = to_dt(dtype);
+    const quan::PackGeom pg = quan::qconv2d_pack_geom(c_in, c_out, k_h, k_w, dt);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = quan::qconv2d_pack_weights(pg, c_in, c_out, k_h, k_w, dt, w_r, w_i, w_j, w_k,
+                                              wpack, s);
+    if (e != hipSuccess)
+        return fail_hip(e, "qconv2d weight pack launch");
+    e = quan::qconv2d_run(quan::qconv2d_plan(g, dt, sep), pg, g, dt, x, wpack, bias, out, nullptr, nullptr, s);
+    if (e != hipSuccess)
+        return fail_hip(e, "qconv2d launch");
+    return QUAN_OK;
+}
+
+}  // namespace
+
 QUAN_API int64_t quan_qconv2d_packed_bytes(int32_t c_in, int32_t c_out, int32_t k_h, int32_t k_w,
                                            int32_t dtype)
 {
@@ -269,29 +347,19 @@ QUAN_API int quan_qconv2d_forward_packed(const void *x, const void *packed, cons
                                          int32_t c_out, int32_t k_h, int32_t k_w, int32_t dtype,
                                          void *stream)
 {
-    g_last_error.clear();
-    if (!x || !packed || !out)
-        return fail(QUAN_ERR_NULL, "qconv2d_forward_packed: x, packed and out must be non-NULL");
-    quan::ConvGeom g;
-    size_t xb = 0, ob = 0;
-    if (int rc = check_conv(x, bias, stride_h, stride_w, pad_h, pad_w, dilation_h, dilation_w, out,
-                            n, c_in, h, w, c_out, k_h, k_w, dtype, &g, &xb, &ob))
-        return rc;
-    const int64_t need = quan_qconv2d_packed_bytes(c_in, c_out, k_h, k_w, dtype);
-    if (need < 0)
-        return int(need);
-    if (misaligned(packed, 16))
-        return fail(QUAN_ERR_ALIGN, "qconv2d_forward_packed: packed must be 16-byte aligned");
-    if (overlaps(out, ob, packed, size_t(need)))
-        return fail(QUAN_ERR_ALIAS, "qconv2d_forward_packed: out overlaps the packed weights");
-    const quan::DType dt = to_dt(dtype);
-    const quan::PackGeom pg = quan::qconv2d_pack_geom(c_in, c_out, k_h, k_w, dt);
-    const quan::ConvPlan plan = quan::qconv2d_plan(g, dt);
-    hipError_t e = quan::qconv2d_run(plan, pg, g, dt, x, packed, bias, out, nullptr, nullptr,
-                                     static_cast<hipStream_t>(stream));
-    if (e != hipSuccess)
-        return fail_hip(e, "qconv2d launch");
-    return QUAN_OK;
+    return conv_packed("qconv2d_forward_packed", false, x, packed, bias, stride_h, stride_w, pad_h, pad_w,
+                       dilation_h, dilation_w, out, n, c_in, h, w, c_out, k_h, k_w, dtype, stream);
+}
+
+QUAN_API int quan_qconv2d_separable_forward_packed(const void *x, const void *packed, const void *bias,
+                                                   int32_t stride_h, int32_t stride_w, int32_t pad_h,
+                                                   int32_t pad_w, int32_t dilation_h, int32_t dilation_w,
+                                                   void *out, int32_t n, int32_t c_in, int32_t h, int32_t w,
+                                                   int32_t c_out, int32_t k_h, int32_t k_w, int32_t dtype,
+                                                   void *stream)
+{
+    return conv_packed("qconv2d_separable_forward_packed", true, x, packed, bias, stride_h, stride_w, pad_h,
+                       pad_w, dilation_h, dilation_w, out, n, c_in, h, w, c_out, k_h, k_w, dtype, stream);
 }
 
 QUAN_API int quan_qconv2d_forward(const void *x, const void *w_r, const void *w_i, const void *w_j,
@@ -301,39 +369,19 @@ QUAN_API int quan_qconv2d_forward(const void *x, const void *w_r, const void *w_
                                   int32_t w, int32_t c_out, int32_t k_h, int32_t k_w, int32_t dtype,
                                   void *stream)
 {
-    g_last_error.clear();
-    if (!x || !w_r || !w_i || !w_j || !w_k || !out)
-        return fail(QUAN_ERR_NULL, "qconv2d: x, w_r, w_i, w_j, w_k and out must be non-NULL");
-    quan::ConvGeom g;
-    size_t xb = 0, ob = 0;
-    if (int rc = check_conv(x, bias, stride_h, stride_w, pad_h, pad_w, dilation_h, dilation_w, out,
-                            n, c_in, h, w, c_out, k_h, k_w, dtype, &g, &xb, &ob))
-        return rc;
-    const size_t es = elem_size(dtype);
-    if (misaligned(w_r, es) || misaligned(w_i, es) || misaligned(w_j, es) || misaligned(w_k, es))
-        return fail(QUAN_ERR_ALIGN, "qconv2d: weights and bias must be aligned to their element size");
-    const size_t wb = size_t(c_out) * c_in * k_h * k_w * es;
-    if (overlaps(out, ob, w_r, wb) || overlaps(out, ob, w_i, wb) || overlaps(out, ob, w_j, wb) ||
-        overlaps(out, ob, w_k, wb))
-        return fail(QUAN_ERR_ALIAS, "qconv2d: out overlaps x, a kernel or the bias");
-    const int64_t need = quan_qconv2d_packed_bytes(c_in, c_out, k_h, k_w, dtype);
-    if (need < 0)
-        return int(need);
+    return conv_unpacked("qconv2d", false, x, w_r, w_i, w_j, w_k, bias, stride_h, stride_w, pad_h, pad_w,
+                         dilation_h, dilation_w, out, n, c_in, h, w, c_out, k_h, k_w, dtype, stream);
+}
 
-    void *wpack = nullptr;
-    if (int rc = workspace(stream, kWeightPack, size_t(need), &wpack))
-        return rc;
-    const quan::DType dt = to_dt(dtype);
-    const quan::PackGeom pg = quan::qconv2d_pack_geom(c_in, c_out, k_h, k_w, dt);
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    hipError_t e = quan::qconv2d_pack_weights(pg, c_in, c_out, k_h, k_w, dt, w_r, w_i, w_j, w_k,
-                                              wpack, s);
-    if (e != hipSuccess)
-        return fail_hip(e, "qconv2d weight pack launch");
-    e = quan::qconv2d_run(quan::qconv2d_plan(g, dt), pg, g, dt, x, wpack, bias, out, nullptr, nullptr, s);
-    if (e != hipSuccess)
-        return fail_hip(e, "qconv2d launch");
-    return QUAN_OK;
+QUAN_API int quan_qconv2d_separable_forward(const void *x, const void *w_r, const void *w_i, const void *w_j,
+                                            const void *w_k, const void *bias, int32_t stride_h,
+                                            int32_t stride_w, int32_t pad_h, int32_t pad_w, int32_t dilation_h,
+                                            int32_t dilation_w, void *out, int32_t n, int32_t c_in, int32_t h,
+                                            int32_t w, int32_t c_out, int32_t k_h, int32_t k_w, int32_t dtype,
+                                            void *stream)
+{
+    return conv_unpacked("qconv2d_separable", true, x, w_r, w_i, w_j, w_k, bias, stride_h, stride_w, pad_h,
+                         pad_w, dilation_h, dilation_w, out, n, c_in, h, w, c_out, k_h, k_w, dtype, stream);
 }
 
 QUAN_API int quan_qconv2d_iqbn_forward(const void *x, const void *packed, const void *bias,
@@ -376,7 +424,7 @@ QUAN_API int quan_qconv2d_iqbn_forward(const void *x, const void *packed, const 
 
     const quan::DType dt = to_dt(dtype);
     const quan::PackGeom pg = quan::qconv2d_pack_geom(c_in, c_out, k_h, k_w, dt);
-    const quan::ConvPlan plan = quan::qconv2d_plan(g, dt);
+    const quan::ConvPlan plan = quan::qconv2d_plan(g, dt, false);
     const int64_t pixels = g.m();
     hipStream_t s = static_cast<hipStream_t>(stream);
     void *work = nullptr;
@@ -450,7 +498,7 @@ QUAN_API int quan_qconv2d_iqbn_inference(const void *x, const void *packed, cons
     if (e != hipSuccess)
         return fail_hip(e, "iqbn fold launch");
     const quan::ConvFold fold{scale, shift, relu != 0};
-    e = quan::qconv2d_run(quan::qconv2d_plan(g, dt), pg, g, dt, x, packed, bias, out, nullptr, &fold, s);
+    e = quan::qconv2d_run(quan::qconv2d_plan(g, dt, false), pg, g, dt, x, packed, bias, out, nullptr, &fold, s);
     if (e != hipSuccess)
         return fail_hip(e, "qconv2d launch");
     return QUAN_OK;

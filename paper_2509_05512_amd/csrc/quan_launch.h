@@ -41,8 +41,9 @@ struct ConvPlan {
     const char *name;
 };
 
-// Pick a tile configuration for the convolution.
-ConvPlan qconv2d_plan(const ConvGeom &g, DType dt);
+// Pick a tile configuration for the convolution: the Hamilton product
+// (eq. 5) or, with sep, the separable form (eq. 7).
+ConvPlan qconv2d_plan(const ConvGeom &g, DType dt, bool sep);
 
 // Pack W_r..W_k (OIHW) into the PackGeom layout, zero padded.
 hipError_t qconv2d_pack_weights(const PackGeom &pg, int c_in, int c_out, int k_h, int k_w, DType dt,

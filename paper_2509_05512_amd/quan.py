@@ -32,6 +32,9 @@ SIGNATURES = {
     "quan_qconv2d_packed_bytes": (ctypes.c_int64, [_i32] * 5),
     "quan_qconv2d_pack_weights": (ctypes.c_int, [_vp] * 4 + [_i32] * 5 + [_vp, ctypes.c_int64, _vp]),
     "quan_qconv2d_forward_packed": (ctypes.c_int, [_vp] * 3 + [_i32] * 6 + [_vp] + [_i32] * 8 + [_vp]),
+    "quan_qconv2d_separable_forward": (ctypes.c_int, [_vp] * 6 + [_i32] * 6 + [_vp] + [_i32] * 8 + [_vp]),
+    "quan_qconv2d_separable_forward_packed": (ctypes.c_int, [_vp] * 3 + [_i32] * 6 + [_vp] + [_i32] * 8
+                                              + [_vp]),
     "quan_qconv2d_iqbn_forward": (ctypes.c_int, [_vp] * 3 + [_i32] * 6 + [_vp, _vp, _f32, _i32, _i32]
                                   + [_vp] * 3 + [_i32] * 8 + [_vp]),
     "quan_qconv2d_iqbn_inference": (ctypes.c_int, [_vp] * 3 + [_i32] * 6 + [_vp] * 4 + [_f32, _i32, _vp]
@@ -125,6 +128,18 @@ def quan_qconv2d_forward(x, w_r, w_i, w_j, w_k, bias=None, stride=1, pad=0, dila
 
     x: [N, 4, Cin, H, W] in device layout; w_*: [Cout, Cin, kh, kw] contiguous;
     bias: [4, Cout] or None.  Returns out [N, 4, Cout, Ho, Wo] (device layout)."""
+    return _conv("quan_qconv2d_forward", x, w_r, w_i, w_j, w_k, bias, stride, pad, dilation, out)
+
+
+def quan_qconv2d_separable_forward(x, w_r, w_i, w_j, w_k, bias=None, stride=1, pad=0, dilation=1,
+                                   out=None):
+    """Separable QUAN convolution (Section III-B, eq. 7): y_p = sum_q
+    S[p, q] (W_q (*) x_q) + b_p.  Arguments as in quan_qconv2d_forward."""
+    return _conv("quan_qconv2d_separable_forward", x, w_r, w_i, w_j, w_k, bias, stride, pad, dilation,
+                 out)
+
+
+def _conv(fn_name, x, w_r, w_i, w_j, w_k, bias, stride, pad, dilation, out):
     lib = load_library()
     if not is_device_layout(x):
         raise ValueError("x must be [N, 4, Cin, H, W] stored channels-last by component")
@@ -147,10 +162,10 @@ def quan_qconv2d_forward(x, w_r, w_i, w_j, w_k, bias=None, stride=1, pad=0, dila
     elif not is_device_layout(out) or tuple(out.shape) != (n, 4, c_out, ho, wo) or out.dtype != x.dtype:
         raise ValueError("out must be [N, 4, Cout, Ho, Wo] in device layout with x's dtype")
     with torch.cuda.device(x.device):
-        rc = lib.quan_qconv2d_forward(_ptr(x), _ptr(w_r), _ptr(w_i), _ptr(w_j), _ptr(w_k),
-                                      _ptr(bias), sh, sw, ph, pw, dh, dw, _ptr(out),
-                                      n, c_in, h, w, c_out, k_h, k_w, _dtype_code(x),
-                                      _stream(x.device))
+        rc = getattr(lib, fn_name)(_ptr(x), _ptr(w_r), _ptr(w_i), _ptr(w_j), _ptr(w_k),
+                                   _ptr(bias), sh, sw, ph, pw, dh, dw, _ptr(out),
+                                   n, c_in, h, w, c_out, k_h, k_w, _dtype_code(x),
+                                   _stream(x.device))
     _check(rc)
     return out
 
@@ -199,6 +214,19 @@ def quan_qconv2d_forward_packed(x, packed, weight_shape, bias=None, stride=1, pa
     """quan_qconv2d_forward on weights packed by quan_qconv2d_pack_weights.
 
     weight_shape: (Cout, Cin, kh, kw) of the kernels that were packed."""
+    return _conv_packed("quan_qconv2d_forward_packed", x, packed, weight_shape, bias, stride, pad,
+                        dilation, out)
+
+
+def quan_qconv2d_separable_forward_packed(x, packed, weight_shape, bias=None, stride=1, pad=0,
+                                          dilation=1, out=None):
+    """quan_qconv2d_separable_forward on weights packed by
+    quan_qconv2d_pack_weights (the same packed layout as the Hamilton conv)."""
+    return _conv_packed("quan_qconv2d_separable_forward_packed", x, packed, weight_shape, bias, stride,
+                        pad, dilation, out)
+
+
+def _conv_packed(fn_name, x, packed, weight_shape, bias, stride, pad, dilation, out):
     lib = load_library()
     if not is_device_layout(x):
         raise ValueError("x must be [N, 4, Cin, H, W] stored channels-last by component")
@@ -218,9 +246,9 @@ def quan_qconv2d_forward_packed(x, packed, weight_shape, bias=None, stride=1, pa
     elif not is_device_layout(out) or tuple(out.shape) != (n, 4, c_out, ho, wo) or out.dtype != x.dtype:
         raise ValueError("out must be [N, 4, Cout, Ho, Wo] in device layout with x's dtype")
     with torch.cuda.device(x.device):
-        rc = lib.quan_qconv2d_forward_packed(_ptr(x), _ptr(packed), _ptr(bias), sh, sw, ph, pw,
-                                             dh, dw, _ptr(out), n, c_in, h, w, c_out, k_h, k_w,
-                                             _dtype_code(x), _stream(x.device))
+        rc = getattr(lib, fn_name)(_ptr(x), _ptr(packed), _ptr(bias), sh, sw, ph, pw,
+                                   dh, dw, _ptr(out), n, c_in, h, w, c_out, k_h, k_w,
+                                   _dtype_code(x), _stream(x.device))
     _check(rc)
     return out
 

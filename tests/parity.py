@@ -43,15 +43,17 @@ def assert_close(got, ref, dtype, what=""):
     return float((err / (BF16_ATOL + BF16_RTOL * np.abs(ref))).max()) if err.size else 0.0
 
 
-def conv_reference_sampled(x64, w64, b64, stride, pad, dil, k, samples):
+def conv_reference_sampled(x64, w64, b64, stride, pad, dil, k, samples, conv=None):
     """Oracle values at the sampled output pixels [(n, oy, ox), ...], all
-    channels: each pixel is the oracle run on its own receptive field."""
+    channels: each pixel is the oracle run on its own receptive field
+    (conv: the oracle convolution to use, the Hamilton one by default)."""
+    conv = conv or oracle.qconv2d
     N, _, Cin, H, W = x64.shape
     span = dil * (k - 1) + 1
     xp = np.pad(x64, ((0, 0), (0, 0), (0, 0), (pad, pad), (pad, pad)))
     patches = np.stack([xp[n, :, :, oy * stride:oy * stride + span, ox * stride:ox * stride + span]
                         for (n, oy, ox) in samples])
-    y = oracle.qconv2d(patches, w64, b64, stride=1, pad=0, dilation=dil)
+    y = conv(patches, w64, b64, stride=1, pad=0, dilation=dil)
     return y[:, :, :, 0, 0]                      # [S, 4, Cout]
 
 

@@ -50,14 +50,14 @@ X, WR, WI, WJ, WK, B, OUT = (0x10000000 * (i + 1) for i in range(7))
 G, BE, MEAN, VAR = (0x90000000 + 0x100000 * i for i in range(4))
 
 
-def conv(lib, **kw):
+def conv(lib, fn="quan_qconv2d_forward", **kw):
     a = dict(x=X, wr=WR, wi=WI, wj=WJ, wk=WK, bias=B, sh=1, sw=1, ph=1, pw=1, dh=1, dw=1,
              out=OUT, n=2, cin=4, h=16, w=16, cout=4, kh=3, kw=3, dtype=1)
     a.update(kw)
-    rc = lib.quan_qconv2d_forward(a["x"], a["wr"], a["wi"], a["wj"], a["wk"], a["bias"],
-                                  a["sh"], a["sw"], a["ph"], a["pw"], a["dh"], a["dw"], a["out"],
-                                  a["n"], a["cin"], a["h"], a["w"], a["cout"], a["kh"], a["kw"],
-                                  a["dtype"], None)
+    rc = getattr(lib, fn)(a["x"], a["wr"], a["wi"], a["wj"], a["wk"], a["bias"],
+                          a["sh"], a["sw"], a["ph"], a["pw"], a["dh"], a["dw"], a["out"],
+                          a["n"], a["cin"], a["h"], a["w"], a["cout"], a["kh"], a["kw"],
+                          a["dtype"], None)
     return rc, lib.quan_last_error().decode()
 
 
@@ -96,9 +96,10 @@ CONV_ERRORS = [
 ]
 
 
+@pytest.mark.parametrize("fn", ["quan_qconv2d_forward", "quan_qconv2d_separable_forward"])
 @pytest.mark.parametrize("name,kw,code", CONV_ERRORS, ids=[c[0] for c in CONV_ERRORS])
-def test_qconv2d_rejects(lib, name, kw, code):
-    rc, msg = conv(lib, **kw)
+def test_qconv2d_rejects(lib, name, kw, code, fn):
+    rc, msg = conv(lib, fn, **kw)
     assert rc == code, (name, rc, msg)
     assert msg, "an error must leave a message"
 
