@@ -161,6 +161,46 @@ def time_separable(layers, quan, steps):
     return start.elapsed_time(end) * 1e3 / steps
 
 
+def time_backward(layers, quan, steps, eps):
+    """The backward pass of every layer, last layer first: IQBN's gradient,
+    then the convolution's input and weight (+ bias) gradients, for a seeded
+    dL/dz.  Microseconds per step of each part."""
+    import torch
+    g = torch.Generator(device="cpu").manual_seed(6)
+    grads = [quan.to_device_layout(torch.randn(tuple(ly["z"].shape), generator=g).to(ly["z"].dtype)
+                                   .to(ly["z"].device)) for ly in layers]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in layers]
+
+    def once(record):
+        for li in reversed(range(len(layers))):
+            ly, L = layers[li], layers[li]["spec"]
+            ev = evs[li]
+            if record:
+                ev[0].record()
+            dy, _, _ = quan.quan_iqbn_backward(ly["y"], grads[li], ly["mean"], ly["var"], ly["gamma"],
+                                               y=ly["z"] if L.relu else None, eps=eps)
+            if record:
+                ev[1].record()
+            quan.quan_qconv2d_backward_data(dy, *ly["w"], (ly["x"].shape[3], ly["x"].shape[4]), stride=L.stride,
+                                            pad=L.pad, dilation=L.dilation)
+            if record:
+                ev[2].record()
+            quan.quan_qconv2d_backward_weight(ly["x"], dy, (L.k, L.k), stride=L.stride, pad=L.pad,
+                                              dilation=L.dilation)
+            if record:
+                ev[3].record()
+    once(False)
+    torch.cuda.synchronize()
+    tot = [0.0, 0.0, 0.0]
+    for _ in range(steps):
+        once(True)
+        torch.cuda.synchronize()
+        for ev in evs:
+            for i in range(3):
+                tot[i] += ev[i].elapsed_time(ev[i + 1]) * 1e3
+    return [t / steps for t in tot]
+
+
 def time_poincare(quan, steps, dev):
     """The Poincare input mapping of one ImageNet-sized bf16 batch
     (64 x 3 x 224 x 224): microseconds per launch and algorithmic GB/s
@@ -318,6 +358,9 @@ def main():
     inference_ms = start.elapsed_time(end) / args.steps
     poincare = time_poincare(quan, args.steps, dev)
     separable_us = time_separable(layers, quan, args.steps)
+    # the separate-kernel forward leaves y (conv), z (IQBN) and the statistics
+    run_step(layers, quan, eps=wl.eps)
+    bwd_iqbn_us, bwd_data_us, bwd_weight_us = time_backward(layers, quan, args.steps, wl.eps)
 
     # per-kernel times: the same steps with every kernel on its own
     for _ in range(2):
@@ -383,6 +426,16 @@ def main():
         "inference_us_per_step": round(inference_ms * 1e3, 3),
         "inference_tflops": round(step_flops / (inference_ms * 1e-3) / 1e12, 2),
         "poincare": poincare,
+        "backward": {
+            # per step (all layers): IQBN gradient, conv input gradient,
+            # conv weight + bias gradients; useful FLOPs of each conv
+            # gradient equal the forward's
+            "iqbn_us": round(bwd_iqbn_us, 3),
+            "data_us": round(bwd_data_us, 3),
+            "data_tflops": round(step_flops / (bwd_data_us * 1e-6) / 1e12, 2),
+            "weight_us": round(bwd_weight_us, 3),
+            "weight_tflops": round(step_flops / (bwd_weight_us * 1e-6) / 1e12, 2),
+        },
         "separable": {
             "us_per_step": round(separable_us, 3),
             # eq. 7 does a quarter of the Hamilton product's multiply-adds

@@ -282,6 +282,93 @@ QUAN_API int quan_qconv2d_iqbn_inference(const void *x, const void *packed, cons
 QUAN_API int quan_poincare_map(const void *rgb, void *out, int32_t n, int32_t h, int32_t w,
                                int32_t dtype, void *stream);
 
+/*
+ * Input gradient of the Hamilton convolution (the backward pass of
+ * quan_qconv2d_forward with respect to x): for dL/dY = dy,
+ *
+ *   dx[n,c,iy,ix] = sum over (o, ky, kx, oy, ox) with iy = oy*stride_h -
+ *                   pad_h + ky*dilation_h (ix likewise) of
+ *                   conj(W[o,c,ky,kx]) (x) dy[n,o,oy,ox],
+ *
+ * since the Hamilton matrix of the conjugate quaternion is the transpose of
+ * W's (eq. 6).  Computed as the forward convolution of dy (strided layers:
+ * dy with stride-1 zero rows and columns inserted, staged in a library
+ * workspace) with the transposed, spatially flipped, conjugated kernel,
+ * stride 1, padding dilation*(k-1) - pad.
+ *
+ *   dy   [n, 4, c_out, h_out, w_out] (the forward's output shape), device
+ *        layout, 16-byte aligned.
+ *   w_*  the forward's four kernels [c_out, c_in, k_h, k_w].
+ *   dx   [n, 4, c_in, h, w] output, device layout, 16-byte aligned, not
+ *        overlapping dy or the kernels.
+ * Sizes, strides, pads and dilations are the forward layer's; a pad larger
+ * than dilation*(k-1) returns QUAN_ERR_UNSUPPORTED.
+ */
+QUAN_API int quan_qconv2d_backward_data(const void *dy, const void *w_r, const void *w_i,
+                                        const void *w_j, const void *w_k,
+                                        int32_t stride_h, int32_t stride_w,
+                                        int32_t pad_h, int32_t pad_w,
+                                        int32_t dilation_h, int32_t dilation_w, void *dx,
+                                        int32_t n, int32_t c_in, int32_t h, int32_t w,
+                                        int32_t c_out, int32_t k_h, int32_t k_w,
+                                        int32_t dtype, void *stream);
+
+/*
+ * Weight and bias gradients of the Hamilton convolution for dL/dY = dy.
+ * With Y_p = sum_q s(p, q) W_{p xor q} (x) X_q at every tap (eq. 6: s the
+ * sign of entry (p, q), p xor q the kernel component it holds),
+ *
+ *   dW_m[o,c,ky,kx] = sum_p s(p, p xor m) sum over (n, oy, ox) of
+ *                     dy[n,p,o,oy,ox] * x[n, p xor m, c, iy, ix]
+ *   db[p,o]         = sum over (n, oy, ox) of dy[n,p,o,oy,ox]
+ *
+ * (iy = oy*stride_h - pad_h + ky*dilation_h, ix likewise; taps outside the
+ * image contribute nothing).  A GEMM over the output pixels per tap, in
+ * slices whose fp32 partial sums are added in a fixed order in fp64:
+ * deterministic.
+ *
+ *   x          the forward input [n, 4, c_in, h, w], device layout.
+ *   dy         [n, 4, c_out, h_out, w_out], device layout.
+ *   dw_r..dw_k fp32 outputs [c_out, c_in, k_h, k_w] (4-byte aligned).
+ *   db         fp32 output [4, c_out], or NULL.
+ * Gradients may overlap neither each other nor x or dy.  Uses a library
+ * workspace per (device, stream).
+ */
+QUAN_API int quan_qconv2d_backward_weight(const void *x, const void *dy,
+                                          int32_t stride_h, int32_t stride_w,
+                                          int32_t pad_h, int32_t pad_w,
+                                          int32_t dilation_h, int32_t dilation_w,
+                                          float *dw_r, float *dw_i, float *dw_j, float *dw_k,
+                                          float *db, int32_t n, int32_t c_in, int32_t h,
+                                          int32_t w, int32_t c_out, int32_t k_h, int32_t k_w,
+                                          int32_t dtype, void *stream);
+
+/*
+ * Gradient of training-mode IQBN (eqs. 11 and 12) with respect to its
+ * input, gamma and beta, given the batch statistics the forward call
+ * returned.  Per component and channel, over the P = n*h*w values, with
+ * s = sqrt(var + eps), xhat = (x - mean) / s and g = dout (zero where the
+ * forward's ReLU output y is <= 0, when y is given):
+ *
+ *   dbeta  = sum g
+ *   dgamma = sum g xhat
+ *   dx     = (gamma / s) (g - dbeta / P - xhat dgamma / P)
+ *
+ *   x, dout, y, dx  [n, 4, c, h, w] channels-last by component (dtype,
+ *                   16-byte aligned); y may be NULL (IQBN without ReLU); dx
+ *                   may equal dout (in place) but may not otherwise overlap
+ *                   x, y or dout.
+ *   mean, var       the forward's batch mean and biased variance, [4, c] fp32.
+ *   gamma           [4, c] fp32.
+ *   dgamma, dbeta   [4, c] fp32 outputs, overlapping nothing else.
+ * Partial sums are added in fp64 in a fixed order: deterministic.
+ */
+QUAN_API int quan_iqbn_backward(const void *x, const void *dout, const void *y,
+                                const float *mean, const float *var, const float *gamma,
+                                float eps, void *dx, float *dgamma, float *dbeta,
+                                int32_t n, int32_t c, int32_t h, int32_t w,
+                                int32_t dtype, void *stream);
+
 /* Message describing the last failure of a quan_* call on this thread
  * ("" if none).  The pointer stays valid until the next call on the thread. */
 QUAN_API const char *quan_last_error(void);

@@ -368,6 +368,220 @@ __global__ __launch_bounds__(kThreads) void iqbn_affine(const T *x, T *out, Layo
     }
 }
 
+// ------------------------------ backward ------------------------------
+// Gradient of training-mode IQBN (eqs. 11, 12) given the saved batch mean
+// and biased variance: per column, with s = sqrt(var + eps), xhat = (x - mean)
+// / s and g = dout (zeroed where the saved ReLU output y is <= 0),
+//
+//   dbeta = sum g,  dgamma = sum g xhat,
+//   dx = (gamma / s) (g - dbeta / n - xhat dgamma / n).
+//
+// Pass 1 (iqbn_bwd_reduce) writes per-block partial sums of g and g xhat in
+// the statistics pass's layout, iqbn_bwd_finalize adds them in fp64 in block
+// order (deterministic) and forms the three coefficients, pass 2
+// (iqbn_bwd_apply) writes dx.  x, dout and y read twice, dx written once.
+
+template <typename T, int VW>
+__device__ __forceinline__ void load_col_params(const float *__restrict__ mean, const float *__restrict__ var,
+                                                float eps, int col, float *mu, float *inv)
+{
+#pragma unroll
+    for (int e = 0; e < VW; ++e) {
+        mu[e] = mean[col * VW + e];
+        inv[e] = 1.0f / sqrtf(var[col * VW + e] + eps);
+    }
+}
+
+template <typename T, int VW, bool RELU>
+__global__ __launch_bounds__(kThreads) void iqbn_bwd_reduce(const T *__restrict__ x, const T *__restrict__ dout,
+                                                            const T *__restrict__ y, Layout l,
+                                                            const float *__restrict__ mean,
+                                                            const float *__restrict__ var, float eps,
+                                                            float *__restrict__ part)
+{
+    __shared__ float red[2][kThreads][VW];
+    const int tid = threadIdx.x;
+    const int cl = tid % l.cg;
+    const int rl = tid / l.cg;
+    const int col = blockIdx.y * l.cg + cl;
+    const bool active = rl < l.rpi && col < l.chunks;
+    const int64_t r0 = int64_t(blockIdx.x) * l.rows_per_block;
+    int64_t r1 = r0 + l.rows_per_block;
+    if (r1 > l.pixels)
+        r1 = l.pixels;
+    float s1[VW], s2[VW];
+#pragma unroll
+    for (int e = 0; e < VW; ++e)
+        s1[e] = s2[e] = 0.0f;
+    if (active) {
+        float mu[VW], inv[VW];
+        load_col_params<T, VW>(mean, var, eps, col, mu, inv);
+        const int64_t step = l.rpi;
+        for (int64_t r = r0 + rl; r < r1; r += step) {
+            const int64_t off = r * l.row_len + col * VW;
+            const Vec<T, VW> xv = *reinterpret_cast<const Vec<T, VW> *>(x + off);
+            const Vec<T, VW> gv = *reinterpret_cast<const Vec<T, VW> *>(dout + off);
+            Vec<T, VW> yv;
+            if (RELU)
+                yv = *reinterpret_cast<const Vec<T, VW> *>(y + off);
+#pragma unroll
+            for (int e = 0; e < VW; ++e) {
+                float g = float(gv.v[e]);
+                if (RELU && !(float(yv.v[e]) > 0.0f))
+                    g = 0.0f;
+                const float xh = (float(xv.v[e]) - mu[e]) * inv[e];
+                s1[e] += g;
+                s2[e] = fmaf(g, xh, s2[e]);
+            }
+        }
+    }
+#pragma unroll
+    for (int e = 0; e < VW; ++e) {
+        red[0][tid][e] = s1[e];
+        red[1][tid][e] = s2[e];
+    }
+    __syncthreads();
+    if (rl == 0 && col < l.chunks) {
+        float t1[VW], t2[VW];
+#pragma unroll
+        for (int e = 0; e < VW; ++e)
+            t1[e] = t2[e] = 0.0f;
+        for (int j = 0; j < l.rpi; ++j) {
+#pragma unroll
+            for (int e = 0; e < VW; ++e) {
+                t1[e] += red[0][j * l.cg + cl][e];
+                t2[e] += red[1][j * l.cg + cl][e];
+            }
+        }
+        const size_t stride2 = size_t(l.row_len) * l.blocks;
+#pragma unroll
+        for (int e = 0; e < VW; ++e) {
+            const size_t idx = size_t(col * VW + e) * l.blocks + blockIdx.x;
+            part[idx] = t1[e];
+            part[stride2 + idx] = t2[e];
+        }
+    }
+}
+
+// One wave per column: fp64 sums of the partials (fixed order), then
+// dbeta, dgamma and coef = [gamma / s, dbeta / n, dgamma / n].
+__global__ __launch_bounds__(kThreads) void iqbn_bwd_finalize(Layout l, const float *__restrict__ part,
+                                                              const float *__restrict__ var,
+                                                              const float *__restrict__ gamma, float eps,
+                                                              float *__restrict__ dgamma,
+                                                              float *__restrict__ dbeta, float *__restrict__ coef)
+{
+    constexpr int PER_LANE = kMaxBlocks / 64;
+    const int lane = threadIdx.x & 63;
+    const int col = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
+    if (col >= l.row_len)
+        return;
+    const float *p1 = part + size_t(col) * l.blocks;
+    const float *p2 = p1 + size_t(l.row_len) * l.blocks;
+    float v1[PER_LANE], v2[PER_LANE];
+#pragma unroll
+    for (int u = 0; u < PER_LANE; ++u) {
+        const int b = lane + 64 * u;
+        const int bc = b < l.blocks ? b : l.blocks - 1;
+        v1[u] = p1[bc];
+        v2[u] = p2[bc];
+    }
+    double s1 = 0.0, s2 = 0.0;
+#pragma unroll
+    for (int u = 0; u < PER_LANE; ++u) {
+        if (lane + 64 * u < l.blocks) {
+            s1 += double(v1[u]);
+            s2 += double(v2[u]);
+        }
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        s1 += __shfl_xor(s1, off);
+        s2 += __shfl_xor(s2, off);
+    }
+    if (lane == 0) {
+        const double n = double(l.pixels);
+        dbeta[col] = float(s1);
+        dgamma[col] = float(s2);
+        coef[col] = float(double(gamma[col]) / sqrt(double(var[col]) + double(eps)));
+        coef[l.row_len + col] = float(s1 / n);
+        coef[2 * l.row_len + col] = float(s2 / n);
+    }
+}
+
+template <typename T, int VW, bool RELU>
+__global__ __launch_bounds__(kThreads) void iqbn_bwd_apply(const T *__restrict__ x, const T *__restrict__ dout,
+                                                           const T *__restrict__ y, T *__restrict__ dx, Layout l,
+                                                           const float *__restrict__ mean,
+                                                           const float *__restrict__ var, float eps,
+                                                           const float *__restrict__ coef)
+{
+    const int tid = threadIdx.x;
+    const int cl = tid % l.cg;
+    const int rl = tid / l.cg;
+    const int col = blockIdx.y * l.cg + cl;
+    if (rl >= l.rpi || col >= l.chunks)
+        return;
+    float mu[VW], inv[VW], a[VW], b1[VW], b2[VW];
+    load_col_params<T, VW>(mean, var, eps, col, mu, inv);
+#pragma unroll
+    for (int e = 0; e < VW; ++e) {
+        a[e] = coef[col * VW + e];
+        b1[e] = coef[l.row_len + col * VW + e];
+        b2[e] = coef[2 * l.row_len + col * VW + e];
+    }
+    const int64_t r0 = int64_t(blockIdx.x) * l.rows_per_block;
+    int64_t r1 = r0 + l.rows_per_block;
+    if (r1 > l.pixels)
+        r1 = l.pixels;
+    for (int64_t r = r0 + rl; r < r1; r += l.rpi) {
+        const int64_t off = r * l.row_len + col * VW;
+        const Vec<T, VW> xv = *reinterpret_cast<const Vec<T, VW> *>(x + off);
+        const Vec<T, VW> gv = *reinterpret_cast<const Vec<T, VW> *>(dout + off);
+        Vec<T, VW> yv;
+        if (RELU)
+            yv = *reinterpret_cast<const Vec<T, VW> *>(y + off);
+        Vec<T, VW> o;
+#pragma unroll
+        for (int e = 0; e < VW; ++e) {
+            float g = float(gv.v[e]);
+            if (RELU && !(float(yv.v[e]) > 0.0f))
+                g = 0.0f;
+            const float xh = (float(xv.v[e]) - mu[e]) * inv[e];
+            o.v[e] = T(a[e] * (g - b1[e] - xh * b2[e]));
+        }
+        *reinterpret_cast<Vec<T, VW> *>(dx + off) = o;
+    }
+}
+
+template <typename T, int VW>
+hipError_t launch_backward(const void *x, const void *dout, const void *y, const float *mean, const float *var,
+                           const float *gamma, float eps, void *dx, float *dgamma, float *dbeta, int64_t pixels,
+                           int c, void *work, hipStream_t stream)
+{
+    const Layout l = make_layout(pixels, c, VW);
+    float *part = static_cast<float *>(work);
+    float *coef = part + size_t(l.blocks) * 2 * l.row_len;
+    const T *xt = static_cast<const T *>(x), *gt = static_cast<const T *>(dout), *yt = static_cast<const T *>(y);
+    const dim3 grid(l.blocks, l.col_groups);
+    if (y != nullptr)
+        hipLaunchKernelGGL((iqbn_bwd_reduce<T, VW, true>), grid, dim3(kThreads), 0, stream, xt, gt, yt, l, mean,
+                           var, eps, part);
+    else
+        hipLaunchKernelGGL((iqbn_bwd_reduce<T, VW, false>), grid, dim3(kThreads), 0, stream, xt, gt, yt, l,
+                           mean, var, eps, part);
+    const int fin_blocks = (l.row_len + kThreads / 64 - 1) / (kThreads / 64);
+    hipLaunchKernelGGL(iqbn_bwd_finalize, dim3(fin_blocks), dim3(kThreads), 0, stream, l, (const float *)part,
+                       var, gamma, eps, dgamma, dbeta, coef);
+    if (y != nullptr)
+        hipLaunchKernelGGL((iqbn_bwd_apply<T, VW, true>), grid, dim3(kThreads), 0, stream, xt, gt, yt,
+                           static_cast<T *>(dx), l, mean, var, eps, (const float *)coef);
+    else
+        hipLaunchKernelGGL((iqbn_bwd_apply<T, VW, false>), grid, dim3(kThreads), 0, stream, xt, gt, yt,
+                           static_cast<T *>(dx), l, mean, var, eps, (const float *)coef);
+    return hipGetLastError();
+}
+
 template <typename T, int VW>
 hipError_t launch_all(const void *x, const float *gamma, const float *beta, float eps, bool relu,
                       void *out, float *mean, float *var, int64_t pixels, int c, void *work,
@@ -484,6 +698,25 @@ size_t iqbn_workspace_bytes(int64_t pixels, int c)
             best = b;
     }
     return best;
+}
+
+hipError_t iqbn_backward_run(const void *x, const void *dout, const void *y, const float *mean, const float *var,
+                             const float *gamma, float eps, void *dx, float *dgamma, float *dbeta, int64_t pixels,
+                             int c, DType dt, void *work, hipStream_t stream)
+{
+    const int vw = vec_width(c, dt);
+    if (dt == DType::BF16) {
+        if (vw == 8)
+            return launch_backward<__bf16, 8>(x, dout, y, mean, var, gamma, eps, dx, dgamma, dbeta, pixels, c,
+                                              work, stream);
+        return launch_backward<__bf16, 1>(x, dout, y, mean, var, gamma, eps, dx, dgamma, dbeta, pixels, c, work,
+                                          stream);
+    }
+    if (vw == 4)
+        return launch_backward<float, 4>(x, dout, y, mean, var, gamma, eps, dx, dgamma, dbeta, pixels, c, work,
+                                         stream);
+    return launch_backward<float, 1>(x, dout, y, mean, var, gamma, eps, dx, dgamma, dbeta, pixels, c, work,
+                                     stream);
 }
 
 hipError_t iqbn_run(const void *x, const float *gamma, const float *beta, float eps, bool relu,

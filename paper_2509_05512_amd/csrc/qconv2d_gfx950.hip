@@ -935,7 +935,13 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + 2)) void qconv2d_igemm(KA
 
 // Packs W_r, W_i, W_j, W_k (each OIHW) into [tap][cblk][kernel][cout_pad][CS]
 // so that one stage of one N-tile is four contiguous runs; padding is zero.
-template <typename T>
+// c_in, c_out are the packed convolution's.  TRANSPOSED packs the kernel of
+// the input-gradient convolution instead: with W [c_in][c_out] of the
+// forward layer (c_in, c_out here being the forward's c_out, c_in), entry
+// (o, c, ky, kx) is the conjugate (w_r, -w_i, -w_j, -w_k) of the forward
+// kernel W[c][o] at the flipped tap (k_h-1-ky, k_w-1-kx), since the Hamilton
+// matrix of the conjugate is the transpose.
+template <typename T, bool TRANSPOSED>
 __global__ __launch_bounds__(256) void qconv2d_pack(const T *__restrict__ w0, const T *__restrict__ w1,
                                                     const T *__restrict__ w2, const T *__restrict__ w3,
                                                     T *__restrict__ wp, int c_in, int c_out, int k_h,
@@ -958,9 +964,48 @@ __global__ __launch_bounds__(256) void qconv2d_pack(const T *__restrict__ w0, co
     const int ky = tap / k_w, kx = tap - (tap / k_w) * k_w;
     const T *src = ws == 0 ? w0 : ws == 1 ? w1 : ws == 2 ? w2 : w3;
     T v = T(0);
-    if (o < c_out && c < c_in)
-        v = src[((o * c_in + c) * k_h + ky) * k_w + kx];
+    if (o < c_out && c < c_in) {
+        if constexpr (TRANSPOSED) {
+            const T u = src[((c * c_out + o) * k_h + (k_h - 1 - ky)) * k_w + (k_w - 1 - kx)];
+            v = ws == 0 ? u : T(-float(u));
+        } else {
+            v = src[((o * c_in + c) * k_h + ky) * k_w + kx];
+        }
+    }
     wp[idx] = v;
+}
+
+// Scatters dY [n][ho][wo][row] into the zero-filled z [n][hz][wz][row] at
+// rows and columns (oy * s_h, ox * s_w): the input of the input-gradient
+// convolution of a strided layer.  One thread per VW elements.
+template <typename T, int VW>
+__global__ __launch_bounds__(256) void qconv2d_grad_dilate(const T *__restrict__ dy, T *__restrict__ z, int ho,
+                                                           int wo, int hz, int wz, int s_h, int s_w, int row_vecs,
+                                                           int64_t total)
+{
+    const int64_t idx = int64_t(blockIdx.x) * 256 + threadIdx.x;
+    if (idx >= total)
+        return;
+    int64_t t = idx;
+    const int v = int(t % row_vecs);
+    t /= row_vecs;
+    const int zx = int(t % wz);
+    t /= wz;
+    const int zy = int(t % hz);
+    const int64_t n = t / hz;
+    struct alignas(sizeof(T) * VW) Chunk {
+        T e[VW];
+    };
+    Chunk c;
+    const int oy = zy / s_h, ox = zx / s_w;
+    if (zy % s_h == 0 && zx % s_w == 0 && oy < ho && ox < wo) {
+        c = reinterpret_cast<const Chunk *>(dy)[((n * ho + oy) * wo + ox) * row_vecs + v];
+    } else {
+#pragma unroll
+        for (int e = 0; e < VW; ++e)
+            c.e[e] = T(0);
+    }
+    reinterpret_cast<Chunk *>(z)[idx] = c;
 }
 
 // ----------------------------- kernel table -------------------------------
@@ -1120,23 +1165,104 @@ ConvPlan qconv2d_plan(const ConvGeom &g, DType dt, bool sep)
     return p;
 }
 
-hipError_t qconv2d_pack_weights(const PackGeom &pg, int c_in, int c_out, int k_h, int k_w, DType dt,
-                                const void *w_r, const void *w_i, const void *w_j, const void *w_k,
-                                void *wpack, hipStream_t stream)
+namespace {
+template <bool TRANSPOSED>
+hipError_t pack_weights(const PackGeom &pg, int c_in, int c_out, int k_h, int k_w, DType dt, const void *w_r,
+                        const void *w_i, const void *w_j, const void *w_k, void *wpack, hipStream_t stream)
 {
     const int total = int(pg.bytes / (dt == DType::BF16 ? 2 : 4));
     const int blocks = (total + 255) / 256;
     if (dt == DType::BF16)
-        hipLaunchKernelGGL(qconv2d_pack<__bf16>, dim3(blocks), dim3(256), 0, stream,
+        hipLaunchKernelGGL((qconv2d_pack<__bf16, TRANSPOSED>), dim3(blocks), dim3(256), 0, stream,
                            (const __bf16 *)w_r, (const __bf16 *)w_i, (const __bf16 *)w_j,
                            (const __bf16 *)w_k, (__bf16 *)wpack, c_in, c_out, k_h, k_w, pg.n_cblk,
                            pg.cout_pad, total);
     else
-        hipLaunchKernelGGL(qconv2d_pack<float>, dim3(blocks), dim3(256), 0, stream,
+        hipLaunchKernelGGL((qconv2d_pack<float, TRANSPOSED>), dim3(blocks), dim3(256), 0, stream,
                            (const float *)w_r, (const float *)w_i, (const float *)w_j,
                            (const float *)w_k, (float *)wpack, c_in, c_out, k_h, k_w, pg.n_cblk,
                            pg.cout_pad, total);
     return hipGetLastError();
+}
+}  // namespace
+
+hipError_t qconv2d_pack_weights(const PackGeom &pg, int c_in, int c_out, int k_h, int k_w, DType dt,
+                                const void *w_r, const void *w_i, const void *w_j, const void *w_k,
+                                void *wpack, hipStream_t stream)
+{
+    return pack_weights<false>(pg, c_in, c_out, k_h, k_w, dt, w_r, w_i, w_j, w_k, wpack, stream);
+}
+
+ConvGeom qconv2d_grad_data_geom(const ConvGeom &g)
+{
+    ConvGeom t;
+    t.n = g.n;
+    t.c_in = g.c_out;
+    t.c_out = g.c_in;
+    t.k_h = g.k_h;
+    t.k_w = g.k_w;
+    t.s_h = t.s_w = 1;
+    t.d_h = g.d_h;
+    t.d_w = g.d_w;
+    t.p_h = g.d_h * (g.k_h - 1) - g.p_h;
+    t.p_w = g.d_w * (g.k_w - 1) - g.p_w;
+    t.h = g.h + 2 * g.p_h - g.d_h * (g.k_h - 1);
+    t.w = g.w + 2 * g.p_w - g.d_w * (g.k_w - 1);
+    t.h_out = g.h;
+    t.w_out = g.w;
+    return t;
+}
+
+size_t qconv2d_grad_data_stage_bytes(const ConvGeom &g, DType dt)
+{
+    if (g.s_h == 1 && g.s_w == 1)
+        return 0;
+    const ConvGeom t = qconv2d_grad_data_geom(g);
+    return size_t(t.n) * t.h * t.w * 4 * t.c_in * (dt == DType::BF16 ? 2 : 4);
+}
+
+hipError_t qconv2d_backward_data_run(const ConvGeom &g, DType dt, const void *dy, const void *w_r, const void *w_i,
+                                     const void *w_j, const void *w_k, void *dx, void *wpack, void *stage,
+                                     hipStream_t stream)
+{
+    const ConvGeom t = qconv2d_grad_data_geom(g);
+    if (t.p_h < 0 || t.p_w < 0 || t.h < 1 || t.w < 1)
+        return hipErrorInvalidValue;
+    const PackGeom pg = qconv2d_pack_geom(t.c_in, t.c_out, t.k_h, t.k_w, dt);
+    hipError_t e = pack_weights<true>(pg, t.c_in, t.c_out, t.k_h, t.k_w, dt, w_r, w_i, w_j, w_k, wpack, stream);
+    if (e != hipSuccess)
+        return e;
+    const void *z = dy;
+    if (g.s_h != 1 || g.s_w != 1) {
+        const int row = 4 * g.c_out;
+        const int vw = row % (dt == DType::BF16 ? 8 : 4) == 0 ? (dt == DType::BF16 ? 8 : 4) : 1;
+        const int64_t total = int64_t(t.n) * t.h * t.w * (row / vw);
+        const unsigned blocks = unsigned((total + 255) / 256);
+        if (dt == DType::BF16) {
+            if (vw == 8)
+                hipLaunchKernelGGL((qconv2d_grad_dilate<__bf16, 8>), dim3(blocks), dim3(256), 0, stream,
+                                   (const __bf16 *)dy, (__bf16 *)stage, g.h_out, g.w_out, t.h, t.w, g.s_h, g.s_w,
+                                   row / vw, total);
+            else
+                hipLaunchKernelGGL((qconv2d_grad_dilate<__bf16, 1>), dim3(blocks), dim3(256), 0, stream,
+                                   (const __bf16 *)dy, (__bf16 *)stage, g.h_out, g.w_out, t.h, t.w, g.s_h, g.s_w,
+                                   row, total);
+        } else {
+            if (vw == 4)
+                hipLaunchKernelGGL((qconv2d_grad_dilate<float, 4>), dim3(blocks), dim3(256), 0, stream,
+                                   (const float *)dy, (float *)stage, g.h_out, g.w_out, t.h, t.w, g.s_h, g.s_w,
+                                   row / vw, total);
+            else
+                hipLaunchKernelGGL((qconv2d_grad_dilate<float, 1>), dim3(blocks), dim3(256), 0, stream,
+                                   (const float *)dy, (float *)stage, g.h_out, g.w_out, t.h, t.w, g.s_h, g.s_w,
+                                   row, total);
+        }
+        e = hipGetLastError();
+        if (e != hipSuccess)
+            return e;
+        z = stage;
+    }
+    return qconv2d_run(qconv2d_plan(t, dt, false), pg, t, dt, z, wpack, nullptr, dx, nullptr, nullptr, stream);
 }
 
 bool qconv2d_writes_stats(const ConvPlan &plan, const ConvGeom &g, DType dt)

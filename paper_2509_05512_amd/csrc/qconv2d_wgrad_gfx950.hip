@@ -1,0 +1,399 @@
+// Weight and bias gradients of the Hamilton convolution (the backward pass of
+// Section III-B's eq. 5/6 with respect to W and the bias) for gfx950.
+//
+// With Y_p = sum_q s(p, q) W_{p xor q} (x) X_q per tap (eq. 6's sign s and
+// component index), the gradient of kernel component m at tap (ky, kx) is
+//
+//   dW_m[o][c] = sum_p s(p, p xor m) sum_pix dY[pix][p][o] X[pix + tap][p xor m][c],
+//
+// a GEMM whose reduction dimension is the output pixels (N * Ho * Wo), over
+// both operands stored channels-last.  One work-group takes one tap, a
+// 64 x 64 tile of (output, input) channels and a contiguous slice of the
+// pixels; it stages 32-pixel chunks of dY (all four components) and of the
+// tap-shifted X (zero outside the image) in LDS, double-buffered, and its four
+// waves each accumulate the four dW_m of one 32 x 32 (o, c) block.  MFMA
+// operands need eight consecutive pixels per lane: bf16 fragments come from
+// the pixel-major rows with two transposing LDS reads (ds_read_b64_tr_b16),
+// fp32 fragments (one pixel per lane) with plain reads.  Slices write fp32
+// partial sums; a second kernel adds them in slice order in fp64
+// (deterministic) into dW.  The bias gradient is the column sum of dY.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "quan_launch.h"
+
+namespace quan {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// Bit 4*p + q is set when entry (p, q) of the Hamilton matrix (eq. 6) is
+// negative.  Row r: + - - -, row i: + + - +, row j: + + + -, row k: + - + +.
+constexpr unsigned kNeg = (1u << 1) | (1u << 2) | (1u << 3) | (1u << 6) | (1u << 11) | (1u << 13);
+
+constexpr int kThreads = 256;
+constexpr int kTileO = 64;   // output channels per work-group
+constexpr int kTileC = 64;   // input channels per work-group
+constexpr int kChunk = 32;   // pixels per staged chunk
+constexpr int kRow = 80;     // LDS row length in elements (64 + 16: conflict-free transposing reads)
+
+struct WArgs {
+    const void *x, *dy;
+    float *part;  // [splits][taps][4][c_out][c_in]
+    int n, c_in, h, w, c_out, k_h, k_w, s_h, s_w, p_h, p_w, d_h, d_w, h_out, w_out;
+    int64_t pixels;       // n * h_out * w_out
+    int64_t per_split;    // pixels of one slice
+    int o_tiles, c_tiles, taps;
+};
+
+template <typename T>
+struct Frag;
+template <>
+struct Frag<__bf16> {
+    typedef bf16x8 type;
+};
+template <>
+struct Frag<float> {
+    typedef float type;
+};
+
+// 16-byte chunk of one (component, pixel) row: channels ch0 .. ch0+EPC-1 of
+// a row of `len` channels starting at src (NULL: zeros); element-wise when the
+// chunk runs past the end or the row is not 16-byte aligned (VEC false).
+template <typename T, bool VEC>
+__device__ __forceinline__ u32x4 load_chunk(const T *src, int ch0, int len)
+{
+    constexpr int EPC = 16 / int(sizeof(T));
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (src == nullptr || ch0 >= len)
+        return v;
+    if (VEC && ch0 + EPC <= len)
+        return *reinterpret_cast<const u32x4 *>(src + ch0);
+    T e[EPC];
+#pragma unroll
+    for (int i = 0; i < EPC; ++i)
+        e[i] = ch0 + i < len ? src[ch0 + i] : T(0);
+    __builtin_memcpy(&v, e, 16);
+    return v;
+}
+
+template <typename T, bool VEC>
+__global__ __launch_bounds__(kThreads) void qconv2d_wgrad(WArgs a)
+{
+    constexpr int ES = int(sizeof(T));
+    constexpr int EPC = 16 / ES;               // elements per 16-byte chunk
+    constexpr int CPR = kTileO / EPC;          // chunks per (component, pixel) row of the tile
+    constexpr int PXT = kThreads / CPR;        // pixels one pass of the threads covers
+    constexpr int PASSES = kChunk / PXT;
+    constexpr int COMP = kChunk * kRow;        // elements per component block of a tensor in LDS
+    constexpr int TENSOR = 4 * COMP;
+    constexpr int BUF = 2 * TENSOR;            // dY then X
+    static_assert(kTileO == kTileC && PXT * PASSES == kChunk, "tile geometry");
+    __shared__ __attribute__((aligned(16))) T lds[2 * BUF];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    int b = blockIdx.x;
+    const int tap = b % a.taps;
+    b /= a.taps;
+    const int ot = b % a.o_tiles;
+    b /= a.o_tiles;
+    const int ct = b % a.c_tiles;
+    const int split = b / a.c_tiles;
+    const int ky = tap / a.k_w, kx = tap - (tap / a.k_w) * a.k_w;
+    const int o0 = ot * kTileO, c0 = ct * kTileC;
+    const int64_t pix0 = int64_t(split) * a.per_split;
+    int64_t pix1 = pix0 + a.per_split;
+    if (pix1 > a.pixels)
+        pix1 = a.pixels;
+    const int chunks = pix0 < pix1 ? int((pix1 - pix0 + kChunk - 1) / kChunk) : 0;
+    const T *dy = static_cast<const T *>(a.dy);
+    const T *x = static_cast<const T *>(a.x);
+    const int hw_out = a.h_out * a.w_out;
+
+    // ---- staging: thread t moves chunk t % CPR of pixel rows t / CPR + PXT * i
+    const int cc = tid % CPR, pr = tid / CPR;
+    u32x4 st[2][PASSES][4];  // [tensor][pass][component]
+    auto fetch = [&](int k) {
+#pragma unroll
+        for (int i = 0; i < PASSES; ++i) {
+            const int64_t pix = pix0 + int64_t(k) * kChunk + pr + PXT * i;
+            const T *yrow = nullptr, *xrow = nullptr;
+            if (pix < pix1) {
+                const int64_t img = pix / hw_out;
+                const int rr = int(pix - img * hw_out);
+                const int oy = rr / a.w_out, ox = rr - (rr / a.w_out) * a.w_out;
+                yrow = dy + pix * 4 * a.c_out;
+                const int iy = oy * a.s_h - a.p_h + ky * a.d_h, ix = ox * a.s_w - a.p_w + kx * a.d_w;
+                if (iy >= 0 && iy < a.h && ix >= 0 && ix < a.w)
+                    xrow = x + ((img * a.h + iy) * a.w + ix) * 4 * a.c_in;
+            }
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                st[0][i][q] = load_chunk<T, VEC>(yrow ? yrow + q * a.c_out + o0 : nullptr, cc * EPC, a.c_out - o0);
+                st[1][i][q] = load_chunk<T, VEC>(xrow ? xrow + q * a.c_in + c0 : nullptr, cc * EPC, a.c_in - c0);
+            }
+        }
+    };
+    auto store = [&](int buf) {
+        T *base = lds + buf * BUF;
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int i = 0; i < PASSES; ++i)
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    *reinterpret_cast<u32x4 *>(base + t * TENSOR + q * COMP + (pr + PXT * i) * kRow + cc * EPC) =
+                        st[t][i][q];
+    };
+
+    // ---- compute: wave w owns o-block w / 2 and c-block w % 2
+    const int ob = (wave >> 1) * 32, cb = (wave & 1) * 32;
+    f32x16 acc[4];
+#pragma unroll
+    for (int m = 0; m < 4; ++m)
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+            acc[m][e] = 0.0f;
+
+    // Fragment of component block `comp` of tensor t (0 dY, 1 X), channel
+    // block col0, k-step ks: lane l gets channel col0 + l%32 at the pixels
+    // the MFMA's operand layout assigns it.
+    auto frag = [&](const T *base, int comp, int col0, int ks) {
+        typename Frag<T>::type f;
+        if constexpr (ES == 2) {
+            // two transposing reads of rows 16ks + 8(g/2) + 4r + j, columns
+            // col0 + 16(g%2) + 4a (g = l/16, a = l%4, j = (l%16)/4)
+            const int g = lane >> 4, aa = lane & 3, j = (lane & 15) >> 2;
+            const T *p0 = base + comp * COMP + (16 * ks + 8 * (g >> 1) + j) * kRow + col0 + 16 * (g & 1) + 4 * aa;
+            const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (__attribute__((address_space(3))) s16x4 *)(p0));
+            const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (__attribute__((address_space(3))) s16x4 *)(p0 + 4 * kRow));
+            s16x4 both[2] = {lo, hi};
+            __builtin_memcpy(&f, both, 16);
+        } else {
+            // one pixel per lane: row 2ks + l/32, column col0 + l%32
+            f = base[comp * COMP + (2 * ks + (lane >> 5)) * kRow + col0 + (lane & 31)];
+        }
+        return f;
+    };
+    constexpr int KSTEPS = ES == 2 ? kChunk / 16 : kChunk / 2;
+    auto compute = [&](int buf) {
+        const T *yb = lds + buf * BUF, *xb = yb + TENSOR;
+#pragma unroll
+        for (int ks = 0; ks < KSTEPS; ++ks) {
+            typename Frag<T>::type fy[4], fx[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                fy[q] = frag(yb, q, ob, ks);
+                fx[q] = frag(xb, q, cb, ks);
+            }
+#pragma unroll
+            for (int p = 0; p < 4; ++p) {
+                typename Frag<T>::type pos = fy[p], neg = -fy[p];
+#pragma unroll
+                for (int m = 0; m < 4; ++m) {
+                    const int q = p ^ m;
+                    const bool minus = (kNeg >> (4 * p + q)) & 1u;
+                    if constexpr (ES == 2)
+                        acc[m] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(minus ? neg : pos, fx[q], acc[m], 0, 0, 0);
+                    else
+                        acc[m] = __builtin_amdgcn_mfma_f32_32x32x2f32(minus ? neg : pos, fx[q], acc[m], 0, 0, 0);
+                }
+            }
+        }
+    };
+
+    if (chunks > 0) {
+        fetch(0);
+        store(0);
+        __syncthreads();
+        for (int k = 0; k < chunks; ++k) {
+            if (k + 1 < chunks)
+                fetch(k + 1);  // in flight while this chunk is computed
+            compute(k & 1);
+            if (k + 1 < chunks)
+                store((k + 1) & 1);  // the other buffer: last read before the previous barrier
+            __syncthreads();
+        }
+    }
+
+    // ---- partial sums: register 4g + e of lane l is (o, c) = (ob + 8g +
+    // 4(l/32) + e, cb + l%32) of the wave's block
+    const int c = c0 + cb + (lane & 31);
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+        float *dst = a.part + ((int64_t(split) * a.taps + tap) * 4 + m) * a.c_out * a.c_in;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int o = o0 + ob + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+            if (o < a.c_out && c < a.c_in)
+                dst[int64_t(o) * a.c_in + c] = acc[m][r];
+        }
+    }
+}
+
+// dW_m[o][c][ky][kx] = sum over slices of the partials, in slice order, fp64.
+__global__ __launch_bounds__(kThreads) void qconv2d_wgrad_reduce(const float *__restrict__ part, int splits, int taps,
+                                                                 int c_out, int c_in, float *__restrict__ dw0,
+                                                                 float *__restrict__ dw1, float *__restrict__ dw2,
+                                                                 float *__restrict__ dw3)
+{
+    const int64_t per_m = int64_t(c_out) * c_in * taps;
+    const int64_t idx = int64_t(blockIdx.x) * kThreads + threadIdx.x;  // over [m][o][c][tap]
+    if (idx >= 4 * per_m)
+        return;
+    const int m = int(idx / per_m);
+    const int64_t r = idx - m * per_m;
+    const int tap = int(r % taps);
+    const int64_t oc = r / taps;  // o * c_in + c
+    double s = 0.0;
+    for (int sp = 0; sp < splits; ++sp)
+        s += double(part[((int64_t(sp) * taps + tap) * 4 + m) * c_out * c_in + oc]);
+    float *dw = m == 0 ? dw0 : m == 1 ? dw1 : m == 2 ? dw2 : dw3;
+    dw[oc * taps + tap] = float(s);
+}
+
+// Bias gradient: per column col of the [pixels][4 * c_out] rows of dY, partial
+// sums per block of rows, then a fixed-order fp64 total.
+template <typename T>
+__global__ __launch_bounds__(kThreads) void colsum_partial(const T *__restrict__ dy, int64_t pixels, int cols,
+                                                           int64_t rows_per_block, float *__restrict__ part)
+{
+    const int col = blockIdx.y * kThreads + threadIdx.x;
+    if (col >= cols)
+        return;
+    const int64_t r0 = int64_t(blockIdx.x) * rows_per_block;
+    int64_t r1 = r0 + rows_per_block;
+    if (r1 > pixels)
+        r1 = pixels;
+    float s = 0.0f;
+    for (int64_t r = r0; r < r1; ++r)
+        s += float(dy[r * cols + col]);
+    part[int64_t(blockIdx.x) * cols + col] = s;
+}
+
+__global__ __launch_bounds__(kThreads) void colsum_final(const float *__restrict__ part, int blocks, int cols,
+                                                         float *__restrict__ db)
+{
+    const int col = blockIdx.x * kThreads + threadIdx.x;
+    if (col >= cols)
+        return;
+    double s = 0.0;
+    for (int b = 0; b < blocks; ++b)
+        s += double(part[int64_t(b) * cols + col]);
+    db[col] = float(s);
+}
+
+constexpr int kBiasBlocks = 128;
+
+struct WPlan {
+    int o_tiles, c_tiles, taps, splits;
+    int64_t per_split;
+};
+
+WPlan wgrad_plan(const ConvGeom &g)
+{
+    WPlan p;
+    p.o_tiles = (g.c_out + kTileO - 1) / kTileO;
+    p.c_tiles = (g.c_in + kTileC - 1) / kTileC;
+    p.taps = g.k_h * g.k_w;
+    const int64_t pixels = g.m();
+    const int64_t per_split_pass = int64_t(p.o_tiles) * p.c_tiles * p.taps;
+    // about two work-groups per compute unit, each at least a few chunks long
+    int64_t splits = (512 + per_split_pass - 1) / per_split_pass;
+    const int64_t max_splits = (pixels + 8 * kChunk - 1) / (8 * kChunk);
+    if (splits > max_splits)
+        splits = max_splits;
+    if (splits < 1)
+        splits = 1;
+    p.per_split = (pixels + splits - 1) / splits;
+    p.per_split = (p.per_split + kChunk - 1) / kChunk * kChunk;
+    p.splits = int((pixels + p.per_split - 1) / p.per_split);
+    return p;
+}
+
+}  // namespace
+
+size_t qconv2d_wgrad_work_bytes(const ConvGeom &g)
+{
+    const WPlan p = wgrad_plan(g);
+    const size_t dw_part = size_t(p.splits) * p.taps * 4 * g.c_out * g.c_in * sizeof(float);
+    const size_t b_part = size_t(kBiasBlocks) * 4 * g.c_out * sizeof(float);
+    return dw_part > b_part ? dw_part : b_part;
+}
+
+hipError_t qconv2d_backward_weight_run(const ConvGeom &g, DType dt, const void *x, const void *dy, float *dw_r,
+                                       float *dw_i, float *dw_j, float *dw_k, float *db, void *work,
+                                       hipStream_t stream)
+{
+    const WPlan p = wgrad_plan(g);
+    WArgs a;
+    a.x = x;
+    a.dy = dy;
+    a.part = static_cast<float *>(work);
+    a.n = g.n;
+    a.c_in = g.c_in;
+    a.h = g.h;
+    a.w = g.w;
+    a.c_out = g.c_out;
+    a.k_h = g.k_h;
+    a.k_w = g.k_w;
+    a.s_h = g.s_h;
+    a.s_w = g.s_w;
+    a.p_h = g.p_h;
+    a.p_w = g.p_w;
+    a.d_h = g.d_h;
+    a.d_w = g.d_w;
+    a.h_out = g.h_out;
+    a.w_out = g.w_out;
+    a.pixels = g.m();
+    a.per_split = p.per_split;
+    a.o_tiles = p.o_tiles;
+    a.c_tiles = p.c_tiles;
+    a.taps = p.taps;
+    const unsigned blocks = unsigned(int64_t(p.splits) * p.c_tiles * p.o_tiles * p.taps);
+    const int epc = dt == DType::BF16 ? 8 : 4;
+    const bool vec = g.c_in % epc == 0 && g.c_out % epc == 0;
+    if (dt == DType::BF16) {
+        if (vec)
+            hipLaunchKernelGGL((qconv2d_wgrad<__bf16, true>), dim3(blocks), dim3(kThreads), 0, stream, a);
+        else
+            hipLaunchKernelGGL((qconv2d_wgrad<__bf16, false>), dim3(blocks), dim3(kThreads), 0, stream, a);
+    } else {
+        if (vec)
+            hipLaunchKernelGGL((qconv2d_wgrad<float, true>), dim3(blocks), dim3(kThreads), 0, stream, a);
+        else
+            hipLaunchKernelGGL((qconv2d_wgrad<float, false>), dim3(blocks), dim3(kThreads), 0, stream, a);
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess)
+        return e;
+    const int64_t outs = int64_t(4) * g.c_out * g.c_in * p.taps;
+    hipLaunchKernelGGL(qconv2d_wgrad_reduce, dim3(unsigned((outs + kThreads - 1) / kThreads)), dim3(kThreads), 0,
+                       stream, (const float *)a.part, p.splits, p.taps, g.c_out, g.c_in, dw_r, dw_i, dw_j, dw_k);
+    e = hipGetLastError();
+    if (e != hipSuccess || db == nullptr)
+        return e;
+    // the partials of dW are consumed: reuse the workspace for the bias
+    const int cols = 4 * g.c_out;
+    const int64_t pixels = g.m();
+    const int64_t rpb = (pixels + kBiasBlocks - 1) / kBiasBlocks;
+    const int nb = int((pixels + rpb - 1) / rpb);
+    const dim3 grid(nb, (cols + kThreads - 1) / kThreads);
+    if (dt == DType::BF16)
+        hipLaunchKernelGGL(colsum_partial<__bf16>, grid, dim3(kThreads), 0, stream, (const __bf16 *)dy, pixels, cols,
+                           rpb, a.part);
+    else
+        hipLaunchKernelGGL(colsum_partial<float>, grid, dim3(kThreads), 0, stream, (const float *)dy, pixels, cols,
+                           rpb, a.part);
+    hipLaunchKernelGGL(colsum_final, dim3((cols + kThreads - 1) / kThreads), dim3(kThreads), 0, stream,
+                       (const float *)a.part, nb, cols, db);
+    return hipGetLastError();
+}
+
+}  // namespace quan

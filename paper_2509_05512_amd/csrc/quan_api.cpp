@@ -46,7 +46,7 @@ struct Workspace {
 std::mutex g_ws_mutex;
 std::map<std::pair<int, std::pair<void *, int>>, Workspace> g_ws;
 
-enum Purpose { kWeightPack = 0, kIqbnPartials = 1, kIqbnFold = 2 };
+enum Purpose { kWeightPack = 0, kIqbnPartials = 1, kIqbnFold = 2, kGradPack = 3, kGradStage = 4, kWgrad = 5 };
 
 // Returns a device buffer of at least `bytes` for (current device, stream,
 // purpose).  Growing it first waits for the device to finish with the old one.
@@ -526,6 +526,140 @@ QUAN_API int quan_poincare_map(const void *rgb, void *out, int32_t n, int32_t h,
     const hipError_t e = quan::poincare_run(rgb, out, n, h, w, to_dt(dtype), static_cast<hipStream_t>(stream));
     if (e != hipSuccess)
         return fail_hip(e, "poincare launch");
+    return QUAN_OK;
+}
+
+QUAN_API int quan_qconv2d_backward_data(const void *dy, const void *w_r, const void *w_i, const void *w_j,
+                                        const void *w_k, int32_t stride_h, int32_t stride_w, int32_t pad_h,
+                                        int32_t pad_w, int32_t dilation_h, int32_t dilation_w, void *dx, int32_t n,
+                                        int32_t c_in, int32_t h, int32_t w, int32_t c_out, int32_t k_h, int32_t k_w,
+                                        int32_t dtype, void *stream)
+{
+    g_last_error.clear();
+    if (!dy || !w_r || !w_i || !w_j || !w_k || !dx)
+        return fail(QUAN_ERR_NULL, "qconv2d_backward_data: dy, w_r, w_i, w_j, w_k and dx must be non-NULL");
+    // the forward layer's geometry, with dx in the place of x and dy of out
+    quan::ConvGeom g;
+    size_t xb = 0, ob = 0;
+    if (int rc = check_conv(dx, nullptr, stride_h, stride_w, pad_h, pad_w, dilation_h, dilation_w, dy, n, c_in, h,
+                            w, c_out, k_h, k_w, dtype, &g, &xb, &ob))
+        return rc;
+    if (pad_h > dilation_h * (k_h - 1) || pad_w > dilation_w * (k_w - 1))
+        return fail(QUAN_ERR_UNSUPPORTED, "qconv2d_backward_data: padding beyond the dilated kernel span");
+    const size_t es = elem_size(dtype);
+    if (misaligned(w_r, es) || misaligned(w_i, es) || misaligned(w_j, es) || misaligned(w_k, es))
+        return fail(QUAN_ERR_ALIGN, "qconv2d_backward_data: kernels must be aligned to their element size");
+    const size_t wb = size_t(c_out) * c_in * k_h * k_w * es;
+    if (overlaps(dx, xb, w_r, wb) || overlaps(dx, xb, w_i, wb) || overlaps(dx, xb, w_j, wb) ||
+        overlaps(dx, xb, w_k, wb))
+        return fail(QUAN_ERR_ALIAS, "qconv2d_backward_data: dx overlaps dy or a kernel");
+    const quan::DType dt = to_dt(dtype);
+    const quan::ConvGeom t = quan::qconv2d_grad_data_geom(g);
+    // the gradient convolution's own limits (its input is dy or the staged,
+    // zero-inserted dy)
+    const int64_t t_img = int64_t(t.h) * t.w * 4 * t.c_in * int64_t(es);
+    if (int64_t(t.n) * t.h * t.w * 4 * t.c_in > kMaxElems || t_img * (256 / (int64_t(h) * w) + 2) > kMaxElems)
+        return fail(QUAN_ERR_UNSUPPORTED, "qconv2d_backward_data: staged gradient too large for 32-bit offsets");
+    const int64_t need = quan_qconv2d_packed_bytes(c_out, c_in, k_h, k_w, dtype);
+    if (need < 0)
+        return int(need);
+    void *wpack = nullptr, *stage = nullptr;
+    if (int rc = workspace(stream, kGradPack, size_t(need), &wpack))
+        return rc;
+    const size_t sb = quan::qconv2d_grad_data_stage_bytes(g, dt);
+    if (sb > 0) {
+        if (int rc = workspace(stream, kGradStage, sb, &stage))
+            return rc;
+    }
+    const hipError_t e = quan::qconv2d_backward_data_run(g, dt, dy, w_r, w_i, w_j, w_k, dx, wpack, stage,
+                                                         static_cast<hipStream_t>(stream));
+    if (e != hipSuccess)
+        return fail_hip(e, "qconv2d backward data launch");
+    return QUAN_OK;
+}
+
+QUAN_API int quan_qconv2d_backward_weight(const void *x, const void *dy, int32_t stride_h, int32_t stride_w,
+                                          int32_t pad_h, int32_t pad_w, int32_t dilation_h, int32_t dilation_w,
+                                          float *dw_r, float *dw_i, float *dw_j, float *dw_k, float *db, int32_t n,
+                                          int32_t c_in, int32_t h, int32_t w, int32_t c_out, int32_t k_h,
+                                          int32_t k_w, int32_t dtype, void *stream)
+{
+    g_last_error.clear();
+    if (!x || !dy || !dw_r || !dw_i || !dw_j || !dw_k)
+        return fail(QUAN_ERR_NULL, "qconv2d_backward_weight: x, dy and dw_r..dw_k must be non-NULL");
+    quan::ConvGeom g;
+    size_t xb = 0, ob = 0;
+    if (int rc = check_conv(x, nullptr, stride_h, stride_w, pad_h, pad_w, dilation_h, dilation_w, dy, n, c_in, h, w,
+                            c_out, k_h, k_w, dtype, &g, &xb, &ob))
+        return rc;
+    float *outs[] = {dw_r, dw_i, dw_j, dw_k, db};
+    const size_t wb = size_t(c_out) * c_in * k_h * k_w * sizeof(float), bb = size_t(4) * c_out * sizeof(float);
+    for (int i = 0; i < 5; ++i) {
+        if (!outs[i])
+            continue;
+        const size_t bi = i < 4 ? wb : bb;
+        if (misaligned(outs[i], 4))
+            return fail(QUAN_ERR_ALIGN, "qconv2d_backward_weight: dw_* and db must be 4-byte aligned");
+        if (overlaps(outs[i], bi, x, xb) || overlaps(outs[i], bi, dy, ob))
+            return fail(QUAN_ERR_ALIAS, "qconv2d_backward_weight: a gradient overlaps x or dy");
+        for (int j = 0; j < i; ++j) {
+            if (outs[j] && overlaps(outs[i], bi, outs[j], j < 4 ? wb : bb))
+                return fail(QUAN_ERR_ALIAS, "qconv2d_backward_weight: gradients overlap each other");
+        }
+    }
+    void *work = nullptr;
+    if (int rc = workspace(stream, kWgrad, quan::qconv2d_wgrad_work_bytes(g), &work))
+        return rc;
+    const hipError_t e = quan::qconv2d_backward_weight_run(g, to_dt(dtype), x, dy, dw_r, dw_i, dw_j, dw_k, db, work,
+                                                           static_cast<hipStream_t>(stream));
+    if (e != hipSuccess)
+        return fail_hip(e, "qconv2d backward weight launch");
+    return QUAN_OK;
+}
+
+QUAN_API int quan_iqbn_backward(const void *x, const void *dout, const void *y, const float *mean,
+                                const float *var, const float *gamma, float eps, void *dx, float *dgamma,
+                                float *dbeta, int32_t n, int32_t c, int32_t h, int32_t w, int32_t dtype,
+                                void *stream)
+{
+    g_last_error.clear();
+    if (!x || !dout || !mean || !var || !gamma || !dx || !dgamma || !dbeta)
+        return fail(QUAN_ERR_NULL, "iqbn_backward: x, dout, mean, var, gamma, dx, dgamma and dbeta must be non-NULL");
+    if (int rc = check_dtype(dtype))
+        return rc;
+    if (n < 1 || c < 1 || h < 1 || w < 1)
+        return fail(QUAN_ERR_SHAPE, "iqbn_backward: sizes must be >= 1 (n=%d c=%d h=%d w=%d)", n, c, h, w);
+    if (!(eps > 0.0f) || eps != eps)
+        return fail(QUAN_ERR_SHAPE, "iqbn_backward: eps must be > 0 (got %g)", double(eps));
+    const int64_t pixels = int64_t(n) * h * w;
+    const int64_t elems = pixels * 4 * c;
+    if (elems > kMaxElems)
+        return fail(QUAN_ERR_UNSUPPORTED, "iqbn_backward: tensor of %lld elements exceeds 2^31-1", (long long)elems);
+    const size_t es = elem_size(dtype);
+    if (misaligned(x, 16) || misaligned(dout, 16) || misaligned(dx, 16) || (y && misaligned(y, 16)))
+        return fail(QUAN_ERR_ALIGN, "iqbn_backward: x, dout, y and dx must be 16-byte aligned");
+    if (misaligned(mean, 4) || misaligned(var, 4) || misaligned(gamma, 4) || misaligned(dgamma, 4) ||
+        misaligned(dbeta, 4))
+        return fail(QUAN_ERR_ALIGN, "iqbn_backward: mean, var, gamma, dgamma and dbeta must be 4-byte aligned");
+    const size_t tb = size_t(elems) * es, sb = size_t(4) * c * sizeof(float);
+    if (overlaps(dx, tb, x, tb) || (y && overlaps(dx, tb, y, tb)) || (dx != dout && overlaps(dx, tb, dout, tb)))
+        return fail(QUAN_ERR_ALIAS, "iqbn_backward: dx overlaps x or y, or partially overlaps dout");
+    const void *tensors[] = {x, dout, y, dx};
+    for (const void *t : tensors) {
+        if (t && (overlaps(dgamma, sb, t, tb) || overlaps(dbeta, sb, t, tb)))
+            return fail(QUAN_ERR_ALIAS, "iqbn_backward: dgamma/dbeta overlap a tensor");
+    }
+    if (overlaps(dgamma, sb, dbeta, sb) || overlaps(dgamma, sb, mean, sb) || overlaps(dgamma, sb, var, sb) ||
+        overlaps(dgamma, sb, gamma, sb) || overlaps(dbeta, sb, mean, sb) || overlaps(dbeta, sb, var, sb) ||
+        overlaps(dbeta, sb, gamma, sb))
+        return fail(QUAN_ERR_ALIAS, "iqbn_backward: dgamma/dbeta overlap each other or the statistics");
+    void *work = nullptr;
+    if (int rc = workspace(stream, kIqbnPartials, quan::iqbn_workspace_bytes(pixels, c), &work))
+        return rc;
+    const hipError_t e = quan::iqbn_backward_run(x, dout, y, mean, var, gamma, eps, dx, dgamma, dbeta, pixels, c,
+                                                 to_dt(dtype), work, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess)
+        return fail_hip(e, "iqbn backward launch");
     return QUAN_OK;
 }
 

@@ -69,11 +69,40 @@ hipError_t qconv2d_run(const ConvPlan &plan, const PackGeom &pg, const ConvGeom 
                        const void *x, const void *wpack, const void *bias, void *out,
                        float *stats, const ConvFold *fold, hipStream_t stream);
 
+// Input gradient of the Hamilton convolution: dX = conv(Z, W'), Z = dY (stride
+// 1) or dY scattered with s-1 zeros between rows/columns (staged in `stage`,
+// qconv2d_grad_data_stage_bytes bytes), W' the conjugated, transposed,
+// flipped kernel (packed into `wpack`: qconv2d_pack_geom of the gradient
+// geometry), stride 1, pad d(k-1) - p (must be >= 0).  g is the forward
+// layer's geometry; dy [n][h_out][w_out][4][c_out], dx [n][h][w][4][c_in].
+ConvGeom qconv2d_grad_data_geom(const ConvGeom &g);
+size_t qconv2d_grad_data_stage_bytes(const ConvGeom &g, DType dt);
+hipError_t qconv2d_backward_data_run(const ConvGeom &g, DType dt, const void *dy, const void *w_r, const void *w_i,
+                                     const void *w_j, const void *w_k, void *dx, void *wpack, void *stage,
+                                     hipStream_t stream);
+
+// Weight and bias gradients of the Hamilton convolution for dL/dY = dy:
+// dw_r..dw_k [c_out][c_in][k_h][k_w] and db [4][c_out] (NULL: skipped), all
+// fp32; x [n][h][w][4][c_in], dy [n][h_out][w_out][4][c_out].  `work` must
+// hold qconv2d_wgrad_work_bytes(g) bytes.
+size_t qconv2d_wgrad_work_bytes(const ConvGeom &g);
+hipError_t qconv2d_backward_weight_run(const ConvGeom &g, DType dt, const void *x, const void *dy, float *dw_r,
+                                       float *dw_i, float *dw_j, float *dw_k, float *db, void *work,
+                                       hipStream_t stream);
+
 // IQBN.  `work` must hold iqbn_workspace_bytes(...) bytes.
 size_t iqbn_workspace_bytes(int64_t pixels, int c);
 hipError_t iqbn_run(const void *x, const float *gamma, const float *beta, float eps, bool relu,
                     void *out, float *mean, float *var, int64_t pixels, int c, DType dt,
                     void *work, hipStream_t stream);
+
+// Gradient of training-mode IQBN given the forward's saved mean and biased
+// variance ([4][c] fp32): dx (dtype dt, x's layout), dgamma, dbeta ([4][c]
+// fp32).  y (the forward output after ReLU) masks the gradient where y <= 0;
+// NULL: no ReLU.  `work` must hold iqbn_workspace_bytes(...) bytes.
+hipError_t iqbn_backward_run(const void *x, const void *dout, const void *y, const float *mean, const float *var,
+                             const float *gamma, float eps, void *dx, float *dgamma, float *dbeta, int64_t pixels,
+                             int c, DType dt, void *work, hipStream_t stream);
 
 // IQBN of a convolution output whose per-tile statistics the convolution
 // wrote (qconv2d_run with stats): `part` holds iqbn_tile_stats_bytes(m_tiles,

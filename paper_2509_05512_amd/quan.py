@@ -40,6 +40,9 @@ SIGNATURES = {
     "quan_qconv2d_iqbn_inference": (ctypes.c_int, [_vp] * 3 + [_i32] * 6 + [_vp] * 4 + [_f32, _i32, _vp]
                                     + [_i32] * 8 + [_vp]),
     "quan_poincare_map": (ctypes.c_int, [_vp, _vp] + [_i32] * 4 + [_vp]),
+    "quan_qconv2d_backward_data": (ctypes.c_int, [_vp] * 5 + [_i32] * 6 + [_vp] + [_i32] * 8 + [_vp]),
+    "quan_qconv2d_backward_weight": (ctypes.c_int, [_vp] * 2 + [_i32] * 6 + [_vp] * 5 + [_i32] * 8 + [_vp]),
+    "quan_iqbn_backward": (ctypes.c_int, [_vp] * 6 + [_f32] + [_vp] * 3 + [_i32] * 5 + [_vp]),
     "quan_iqbn_forward": (ctypes.c_int, [_vp, _vp, _vp, _f32, _vp, _vp, _vp] + [_i32] * 5 + [_vp]),
     "quan_iqbn_relu_forward": (ctypes.c_int, [_vp, _vp, _vp, _f32, _vp, _vp, _vp] + [_i32] * 5 + [_vp]),
     "quan_last_error": (ctypes.c_char_p, []),
@@ -350,6 +353,89 @@ def quan_poincare_map(rgb, out=None):
         rc = lib.quan_poincare_map(_ptr(rgb), _ptr(out), n, h, w, _dtype_code(rgb), _stream(rgb.device))
     _check(rc)
     return out
+
+
+def quan_qconv2d_backward_data(dy, w_r, w_i, w_j, w_k, input_hw, stride=1, pad=0, dilation=1, dx=None):
+    """Input gradient of quan_qconv2d_forward for dL/dY = dy ([N, 4, Cout, Ho,
+    Wo], device layout); input_hw = (H, W) of the forward input.  Returns dx
+    [N, 4, Cin, H, W] in device layout."""
+    lib = load_library()
+    if not is_device_layout(dy):
+        raise ValueError("dy must be [N, 4, Cout, Ho, Wo] in device layout")
+    c_out, c_in, k_h, k_w = _check_weights((w_r, w_i, w_j, w_k), dy)
+    n, _, c_out_y, ho, wo = dy.shape
+    if c_out_y != c_out:
+        raise ValueError("dy's channels do not match the kernels")
+    h, w = (int(v) for v in input_hw)
+    sh, sw = _pair(stride)
+    ph, pw = _pair(pad)
+    dh, dw = _pair(dilation)
+    if (conv_out_size(h, k_h, sh, ph, dh), conv_out_size(w, k_w, sw, pw, dw)) != (ho, wo):
+        raise ValueError("input_hw does not give dy's spatial size")
+    if dx is None:
+        dx = empty_qmap(n, c_in, h, w, dy.dtype, dy.device)
+    elif not is_device_layout(dx) or tuple(dx.shape) != (n, 4, c_in, h, w) or dx.dtype != dy.dtype:
+        raise ValueError("dx must be [N, 4, Cin, H, W] in device layout with dy's dtype")
+    with torch.cuda.device(dy.device):
+        rc = lib.quan_qconv2d_backward_data(_ptr(dy), _ptr(w_r), _ptr(w_i), _ptr(w_j), _ptr(w_k), sh, sw, ph, pw,
+                                            dh, dw, _ptr(dx), n, c_in, h, w, c_out, k_h, k_w, _dtype_code(dy),
+                                            _stream(dy.device))
+    _check(rc)
+    return dx
+
+
+def quan_qconv2d_backward_weight(x, dy, kernel_hw, stride=1, pad=0, dilation=1, with_bias=True):
+    """Weight (and bias) gradients of quan_qconv2d_forward for dL/dY = dy:
+    returns ([dW_r, dW_i, dW_j, dW_k] each fp32 [Cout, Cin, kh, kw], db fp32
+    [4, Cout] or None)."""
+    lib = load_library()
+    for name, t in (("x", x), ("dy", dy)):
+        if not is_device_layout(t):
+            raise ValueError(f"{name} must be in device layout")
+    if dy.dtype != x.dtype or dy.device != x.device:
+        raise ValueError("x and dy must share dtype and device")
+    n, _, c_in, h, w = x.shape
+    c_out = dy.shape[2]
+    k_h, k_w = (int(v) for v in kernel_hw)
+    sh, sw = _pair(stride)
+    ph, pw = _pair(pad)
+    dh, dw_ = _pair(dilation)
+    if tuple(dy.shape) != (n, 4, c_out, conv_out_size(h, k_h, sh, ph, dh), conv_out_size(w, k_w, sw, pw, dw_)):
+        raise ValueError("dy's shape does not match x and the layer geometry")
+    dws = [torch.empty((c_out, c_in, k_h, k_w), dtype=torch.float32, device=x.device) for _ in range(4)]
+    db = torch.empty((4, c_out), dtype=torch.float32, device=x.device) if with_bias else None
+    with torch.cuda.device(x.device):
+        rc = lib.quan_qconv2d_backward_weight(_ptr(x), _ptr(dy), sh, sw, ph, pw, dh, dw_, *[_ptr(t) for t in dws],
+                                              _ptr(db), n, c_in, h, w, c_out, k_h, k_w, _dtype_code(x),
+                                              _stream(x.device))
+    _check(rc)
+    return dws, db
+
+
+def quan_iqbn_backward(x, dout, mean, var, gamma, y=None, eps=1e-5, dx=None):
+    """Gradient of training-mode IQBN (+ ReLU when the forward output y is
+    given) for dL/dout = dout, with the forward's saved batch statistics.
+    Returns (dx, dgamma, dbeta)."""
+    lib = load_library()
+    for name, t in (("x", x), ("dout", dout)) + ((("y", y),) if y is not None else ()):
+        if not is_device_layout(t) or t.shape != x.shape or t.dtype != x.dtype:
+            raise ValueError(f"{name} must be [N, 4, C, H, W] in device layout like x")
+    n, _, c, h, w = x.shape
+    for name, t in (("mean", mean), ("var", var), ("gamma", gamma)):
+        if tuple(t.shape) != (4, c) or t.dtype != torch.float32 or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous float32 [4, C] tensor")
+    if dx is None:
+        dx = empty_qmap(n, c, h, w, x.dtype, x.device)
+    elif not is_device_layout(dx) or dx.shape != x.shape or dx.dtype != x.dtype:
+        raise ValueError("dx must be [N, 4, C, H, W] in device layout like x")
+    dgamma = torch.empty(4, c, dtype=torch.float32, device=x.device)
+    dbeta = torch.empty(4, c, dtype=torch.float32, device=x.device)
+    with torch.cuda.device(x.device):
+        rc = lib.quan_iqbn_backward(_ptr(x), _ptr(dout), _ptr(y), _ptr(mean), _ptr(var), _ptr(gamma),
+                                    float(eps), _ptr(dx), _ptr(dgamma), _ptr(dbeta), n, c, h, w,
+                                    _dtype_code(x), _stream(x.device))
+    _check(rc)
+    return dx, dgamma, dbeta
 
 
 def _iqbn(fn_name, x, gamma, beta, eps, out, mean, var):

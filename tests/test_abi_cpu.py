@@ -199,6 +199,105 @@ def test_poincare_rejects(lib, name, kw, code):
     assert lib.quan_last_error()
 
 
+DX, DG, DB = 0xA0000000, 0xA8000000, 0xA8100000
+DW0, DW1, DW2, DW3 = (0xB0000000 + 0x100000 * i for i in range(4))
+
+
+def bwd_data(lib, **kw):
+    a = dict(dy=OUT, wr=WR, wi=WI, wj=WJ, wk=WK, sh=1, sw=1, ph=1, pw=1, dh=1, dw=1, dx=DX, n=2, cin=4, h=16, w=16,
+             cout=4, kh=3, kw=3, dtype=1)
+    a.update(kw)
+    rc = lib.quan_qconv2d_backward_data(a["dy"], a["wr"], a["wi"], a["wj"], a["wk"], a["sh"], a["sw"], a["ph"],
+                                        a["pw"], a["dh"], a["dw"], a["dx"], a["n"], a["cin"], a["h"], a["w"],
+                                        a["cout"], a["kh"], a["kw"], a["dtype"], None)
+    return rc, lib.quan_last_error().decode()
+
+
+def bwd_weight(lib, **kw):
+    a = dict(x=X, dy=OUT, sh=1, sw=1, ph=1, pw=1, dh=1, dw=1, d0=DW0, d1=DW1, d2=DW2, d3=DW3, db=DB, n=2, cin=4,
+             h=16, w=16, cout=4, kh=3, kw=3, dtype=1)
+    a.update(kw)
+    rc = lib.quan_qconv2d_backward_weight(a["x"], a["dy"], a["sh"], a["sw"], a["ph"], a["pw"], a["dh"], a["dw"],
+                                          a["d0"], a["d1"], a["d2"], a["d3"], a["db"], a["n"], a["cin"], a["h"],
+                                          a["w"], a["cout"], a["kh"], a["kw"], a["dtype"], None)
+    return rc, lib.quan_last_error().decode()
+
+
+BWD_DATA_ERRORS = [
+    ("null dy", dict(dy=None), E_NULL),
+    ("null w_k", dict(wk=None), E_NULL),
+    ("null dx", dict(dx=None), E_NULL),
+    ("bad dtype", dict(dtype=3), E_DTYPE),
+    ("stride 0", dict(sh=0), E_SHAPE),
+    ("pad beyond the kernel span", dict(ph=3), E_UNSUP),
+    ("dx misaligned", dict(dx=DX + 2), E_ALIGN),
+    ("weight misaligned", dict(wi=WI + 1), E_ALIGN),
+    ("dx overlaps dy", dict(dx=OUT + 64), E_ALIAS),
+    ("dx overlaps a kernel", dict(dx=WJ - 64), E_ALIAS),
+]
+
+
+@pytest.mark.parametrize("name,kw,code", BWD_DATA_ERRORS, ids=[c[0] for c in BWD_DATA_ERRORS])
+def test_backward_data_rejects(lib, name, kw, code):
+    rc, msg = bwd_data(lib, **kw)
+    assert rc == code, (name, rc, msg)
+    assert msg
+
+
+BWD_WEIGHT_ERRORS = [
+    ("null x", dict(x=None), E_NULL),
+    ("null dw_j", dict(d2=None), E_NULL),
+    ("bad dtype", dict(dtype=-2), E_DTYPE),
+    ("k = 0", dict(kw=0), E_SHAPE),
+    ("dw misaligned", dict(d1=DW1 + 2), E_ALIGN),
+    ("db misaligned", dict(db=DB + 1), E_ALIGN),
+    ("dw overlaps x", dict(d0=X + 4), E_ALIAS),
+    ("db overlaps dy", dict(db=OUT + 4), E_ALIAS),
+    ("dw overlap each other", dict(d3=DW2 + 4), E_ALIAS),
+]
+
+
+@pytest.mark.parametrize("name,kw,code", BWD_WEIGHT_ERRORS, ids=[c[0] for c in BWD_WEIGHT_ERRORS])
+def test_backward_weight_rejects(lib, name, kw, code):
+    rc, msg = bwd_weight(lib, **kw)
+    assert rc == code, (name, rc, msg)
+    assert msg
+
+
+def iqbn_bwd(lib, **kw):
+    a = dict(x=X, dout=OUT, y=B, m=MEAN, v=VAR, g=G, eps=1e-5, dx=DX, dg=DG, db=DB, n=2, c=4, h=8, w=8, dtype=1)
+    a.update(kw)
+    rc = lib.quan_iqbn_backward(a["x"], a["dout"], a["y"], a["m"], a["v"], a["g"], a["eps"], a["dx"], a["dg"],
+                                a["db"], a["n"], a["c"], a["h"], a["w"], a["dtype"], None)
+    return rc, lib.quan_last_error().decode()
+
+
+IQBN_BWD_ERRORS = [
+    ("null x", dict(x=None), E_NULL),
+    ("null dout", dict(dout=None), E_NULL),
+    ("null var", dict(v=None), E_NULL),
+    ("null dgamma", dict(dg=None), E_NULL),
+    ("bad dtype", dict(dtype=9), E_DTYPE),
+    ("w = 0", dict(w=0), E_SHAPE),
+    ("eps = 0", dict(eps=0.0), E_SHAPE),
+    ("too large", dict(n=1 << 14, h=512, w=512), E_UNSUP),
+    ("dout misaligned", dict(dout=OUT + 2), E_ALIGN),
+    ("y misaligned", dict(y=B + 8), E_ALIGN),
+    ("dbeta misaligned", dict(db=DB + 1), E_ALIGN),
+    ("dx overlaps x", dict(dx=X + 32), E_ALIAS),
+    ("dx partially overlaps dout", dict(dx=OUT + 16), E_ALIAS),
+    ("dgamma inside dx", dict(dg=DX + 64), E_ALIAS),
+    ("dgamma overlaps dbeta", dict(db=DG + 8), E_ALIAS),
+]
+
+
+@pytest.mark.parametrize("name,kw,code", IQBN_BWD_ERRORS, ids=[c[0] for c in IQBN_BWD_ERRORS])
+def test_iqbn_backward_rejects(lib, name, kw, code):
+    rc, msg = iqbn_bwd(lib, **kw)
+    assert rc == code, (name, rc, msg)
+    assert msg
+
+
 IQBN_ERRORS = [
     ("null gamma", dict(g=None), E_NULL),
     ("null var", dict(var=None), E_NULL),

@@ -1,0 +1,154 @@
+"""GPU parity of the backward pass through the C ABI against the oracle's
+fp64 gradients (the adjoint of the forward, pinned by autograd and adjoint
+identities): the Hamilton convolution's input gradient (strides 1 and 2,
+pads, dilations, channel counts off the vector width), its weight and bias
+gradients, and training-mode IQBN's gradients with and without ReLU.  The
+imagenet_stage layer's weight gradient is checked at full size on sampled
+(output, input) channel pairs: each pair's gradient depends only on that
+channel of x and of dy, so the oracle runs on one-channel slices."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2509_05512_amd import quan
+from parity import assert_close, f64, say
+
+pytestmark = pytest.mark.gpu
+
+DT = {"fp32": torch.float32, "bf16": torch.bfloat16}
+
+# (N, Cin, Cout, H, W, k, stride, pad, dilation)
+SHAPES = [
+    (2, 4, 4, 16, 16, 3, 1, 1, 1),
+    (2, 16, 64, 13, 10, 3, 1, 1, 1),
+    (2, 16, 32, 13, 10, 3, 2, 1, 1),     # stride 2
+    (1, 32, 16, 12, 12, 3, 1, 2, 2),     # dilation 2
+    (2, 5, 7, 9, 9, 3, 1, 1, 1),         # channels off the vector width
+    (2, 64, 64, 15, 15, 1, 1, 0, 1),     # 1x1
+    (1, 24, 40, 17, 19, 3, 2, 0, 1),     # stride 2, pad 0, ragged output
+    (1, 72, 80, 9, 8, 3, 1, 1, 1),       # several channel tiles with tails
+    (3, 8, 16, 7, 7, 5, 1, 2, 1),        # 5x5
+]
+
+
+def _case(shape, dtype, seed):
+    N, Cin, Cout, H, W, k, s, p, d = shape
+    rng = np.random.default_rng(seed)
+    Ho, Wo = quan.conv_out_size(H, k, s, p, d), quan.conv_out_size(W, k, s, p, d)
+    x = torch.from_numpy(rng.standard_normal((N, 4, Cin, H, W), dtype=np.float32)).to(dtype)
+    w = torch.from_numpy((rng.standard_normal((4, Cout, Cin, k, k), dtype=np.float32)
+                          / np.float32(np.sqrt(4 * Cin * k * k)))).to(dtype)
+    dy = torch.from_numpy(rng.standard_normal((N, 4, Cout, Ho, Wo), dtype=np.float32)).to(dtype)
+    return x, w, dy
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("shape", SHAPES, ids=[str(s) for s in SHAPES])
+def test_backward_data_matches_oracle(shape, dtype):
+    say(f"backward data {dtype} {shape}")
+    dt = DT[dtype]
+    N, Cin, Cout, H, W, k, s, p, d = shape
+    x, w, dy = _case(shape, dt, seed=hash(shape) % 1000)
+    dev = torch.device("cuda:0")
+    dx = quan.empty_qmap(N, Cin, H, W, dt, dev)
+    dx.fill_(float("nan"))
+    quan.quan_qconv2d_backward_data(quan.to_device_layout(dy.to(dev)), *[w[q].contiguous().to(dev) for q in range(4)],
+                                    (H, W), stride=s, pad=p, dilation=d, dx=dx)
+    torch.cuda.synchronize()
+    ref, _, _ = oracle.qconv2d_backward(f64(x), f64(w), f64(dy), s, p, d)
+    assert_close(f64(dx.cpu()), ref, dt, f"dX {dtype} {shape}")
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("shape", SHAPES, ids=[str(s) for s in SHAPES])
+def test_backward_weight_matches_oracle(shape, dtype):
+    """fp32 gradients of bf16 or fp32 operands: products exact in fp32,
+    fp32 accumulation per slice, fp64 across slices; checked normwise at the
+    fp32 bar against the oracle on the same rounded inputs."""
+    say(f"backward weight {dtype} {shape}")
+    dt = DT[dtype]
+    N, Cin, Cout, H, W, k, s, p, d = shape
+    x, w, dy = _case(shape, dt, seed=hash(shape) % 1000 + 1)
+    dev = torch.device("cuda:0")
+    dws, db = quan.quan_qconv2d_backward_weight(quan.to_device_layout(x.to(dev)), quan.to_device_layout(dy.to(dev)),
+                                                (k, k), stride=s, pad=p, dilation=d)
+    torch.cuda.synchronize()
+    _, ref_w, ref_b = oracle.qconv2d_backward(f64(x), f64(w), f64(dy), s, p, d)
+    got_w = np.stack([f64(t.cpu()) for t in dws])
+    assert_close(got_w, ref_w, torch.float32, f"dW {dtype} {shape}")
+    assert_close(f64(db.cpu()), ref_b, torch.float32, f"dbias {dtype} {shape}")
+
+
+def test_backward_weight_full_imagenet_layer_sampled():
+    say("backward weight full-size sampled")
+    from paper_2509_05512_amd import workloads
+    wl = workloads.WORKLOADS["imagenet_stage"]
+    tens = workloads.generate(wl)
+    layer = tens.layers[0]
+    dev = torch.device("cuda:0")
+    rng = np.random.default_rng(1)
+    dy = torch.from_numpy(rng.standard_normal((wl.n, 4, 64, wl.h, wl.w), dtype=np.float32)).to(torch.bfloat16)
+    dws, db = quan.quan_qconv2d_backward_weight(quan.to_device_layout(tens.x.to(dev)),
+                                                quan.to_device_layout(dy.to(dev)), (3, 3), stride=1, pad=1)
+    torch.cuda.synchronize()
+    got = np.stack([f64(t.cpu()) for t in dws])  # [4, O, C, 3, 3]
+    x64 = f64(tens.x)
+    dy64 = f64(dy)
+    w1 = np.zeros((4, 1, 1, 3, 3))
+    for (o, c) in [(0, 0), (63, 63), (5, 40), (33, 2), (17, 17), (50, 9)]:
+        _, ref, _ = oracle.qconv2d_backward(x64[:, :, c:c + 1], w1, dy64[:, :, o:o + 1], 1, 1, 1)
+        assert_close(got[:, o, c], ref[:, 0, 0], torch.float32, f"dW imagenet (o={o}, c={c})")
+    ref_b = dy64.sum(axis=(0, 3, 4))
+    assert_close(f64(db.cpu()), ref_b, torch.float32, "dbias imagenet")
+
+
+def test_backward_weight_is_deterministic():
+    say("backward weight determinism")
+    shape = (4, 32, 64, 14, 14, 3, 1, 1, 1)
+    x, w, dy = _case(shape, torch.bfloat16, seed=2)
+    dev = torch.device("cuda:0")
+    xg, dyg = quan.to_device_layout(x.to(dev)), quan.to_device_layout(dy.to(dev))
+    a, ab = quan.quan_qconv2d_backward_weight(xg, dyg, (3, 3), stride=1, pad=1)
+    b, bb = quan.quan_qconv2d_backward_weight(xg, dyg, (3, 3), stride=1, pad=1)
+    torch.cuda.synchronize()
+    for t1, t2 in zip(a + [ab], b + [bb]):
+        assert torch.equal(t1.cpu(), t2.cpu())
+
+
+# (N, C, H, W, relu, dtype)
+IQBN_CASES = [
+    (2, 4, 16, 16, False, "fp32"),
+    (2, 4, 16, 16, True, "fp32"),
+    (3, 16, 9, 11, False, "bf16"),
+    (3, 16, 9, 11, True, "bf16"),
+    (2, 3, 5, 7, True, "bf16"),      # 4C = 12: element-wise columns
+    (1, 64, 28, 28, True, "bf16"),
+]
+
+
+@pytest.mark.parametrize("case", IQBN_CASES, ids=[str(c) for c in IQBN_CASES])
+def test_iqbn_backward_matches_oracle(case):
+    """The ReLU mask is taken from the GPU forward's output on both sides
+    (the oracle runs without ReLU on dout masked the same way), so both take
+    the same decision at zero."""
+    say(f"iqbn backward {case}")
+    N, C, H, W, relu, dtype = case
+    dt = DT[dtype]
+    rng = np.random.default_rng(N * 10 + C)
+    x = torch.from_numpy((rng.standard_normal((N, 4, C, H, W)) * 2.0 + 0.5).astype(np.float32)).to(dt)
+    g = torch.from_numpy(rng.uniform(0.5, 1.5, (4, C)).astype(np.float32))
+    be = torch.from_numpy((rng.standard_normal((4, C)) * 0.3).astype(np.float32))
+    dout = torch.from_numpy(rng.standard_normal((N, 4, C, H, W)).astype(np.float32)).to(dt)
+    dev = torch.device("cuda:0")
+    xg = quan.to_device_layout(x.to(dev))
+    fwd = quan.quan_iqbn_relu_forward if relu else quan.quan_iqbn_forward
+    y, mean, var = fwd(xg, g.to(dev), be.to(dev))
+    dx, dg, db = quan.quan_iqbn_backward(xg, quan.to_device_layout(dout.to(dev)), mean, var, g.to(dev),
+                                         y=y if relu else None)
+    torch.cuda.synchronize()
+    mask = (y.cpu().float() > 0).double().numpy() if relu else 1.0
+    ref_dx, ref_dg, ref_db = oracle.iqbn_backward(f64(x), f64(g), f64(be), f64(dout) * mask, 1e-5, False)
+    assert_close(f64(dx.cpu()), ref_dx, dt, f"iqbn dX {case}")
+    assert_close(f64(dg.cpu()), ref_dg, torch.float32 if dtype == "fp32" else torch.bfloat16, f"dgamma {case}")
+    assert_close(f64(db.cpu()), ref_db, torch.float32 if dtype == "fp32" else torch.bfloat16, f"dbeta {case}")
