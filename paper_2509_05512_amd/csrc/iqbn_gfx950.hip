@@ -417,13 +417,7 @@ __global__ __launch_bounds__(kThreads) void iqbn_bwd_reduce(const T *__restrict_
         float mu[VW], inv[VW];
         load_col_params<T, VW>(mean, var, eps, col, mu, inv);
         const int64_t step = l.rpi;
-        for (int64_t r = r0 + rl; r < r1; r += step) {
-            const int64_t off = r * l.row_len + col * VW;
-            const Vec<T, VW> xv = *reinterpret_cast<const Vec<T, VW> *>(x + off);
-            const Vec<T, VW> gv = *reinterpret_cast<const Vec<T, VW> *>(dout + off);
-            Vec<T, VW> yv;
-            if (RELU)
-                yv = *reinterpret_cast<const Vec<T, VW> *>(y + off);
+        auto add = [&](const Vec<T, VW> &xv, const Vec<T, VW> &gv, const Vec<T, VW> &yv) {
 #pragma unroll
             for (int e = 0; e < VW; ++e) {
                 float g = float(gv.v[e]);
@@ -433,6 +427,30 @@ __global__ __launch_bounds__(kThreads) void iqbn_bwd_reduce(const T *__restrict_
                 s1[e] += g;
                 s2[e] = fmaf(g, xh, s2[e]);
             }
+        };
+        int64_t r = r0 + rl;
+        // four rows in flight per thread
+        for (; r + 3 * step < r1; r += 4 * step) {
+            Vec<T, VW> xv[4], gv[4], yv[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int64_t off = (r + u * step) * l.row_len + col * VW;
+                xv[u] = *reinterpret_cast<const Vec<T, VW> *>(x + off);
+                gv[u] = *reinterpret_cast<const Vec<T, VW> *>(dout + off);
+                if (RELU)
+                    yv[u] = *reinterpret_cast<const Vec<T, VW> *>(y + off);
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                add(xv[u], gv[u], yv[u]);
+        }
+        for (; r < r1; r += step) {
+            const int64_t off = r * l.row_len + col * VW;
+            Vec<T, VW> yv;
+            if (RELU)
+                yv = *reinterpret_cast<const Vec<T, VW> *>(y + off);
+            add(*reinterpret_cast<const Vec<T, VW> *>(x + off), *reinterpret_cast<const Vec<T, VW> *>(dout + off),
+                yv);
         }
     }
 #pragma unroll
@@ -534,13 +552,7 @@ __global__ __launch_bounds__(kThreads) void iqbn_bwd_apply(const T *__restrict__
     int64_t r1 = r0 + l.rows_per_block;
     if (r1 > l.pixels)
         r1 = l.pixels;
-    for (int64_t r = r0 + rl; r < r1; r += l.rpi) {
-        const int64_t off = r * l.row_len + col * VW;
-        const Vec<T, VW> xv = *reinterpret_cast<const Vec<T, VW> *>(x + off);
-        const Vec<T, VW> gv = *reinterpret_cast<const Vec<T, VW> *>(dout + off);
-        Vec<T, VW> yv;
-        if (RELU)
-            yv = *reinterpret_cast<const Vec<T, VW> *>(y + off);
+    auto grad = [&](const Vec<T, VW> &xv, const Vec<T, VW> &gv, const Vec<T, VW> &yv) {
         Vec<T, VW> o;
 #pragma unroll
         for (int e = 0; e < VW; ++e) {
@@ -550,7 +562,33 @@ __global__ __launch_bounds__(kThreads) void iqbn_bwd_apply(const T *__restrict__
             const float xh = (float(xv.v[e]) - mu[e]) * inv[e];
             o.v[e] = T(a[e] * (g - b1[e] - xh * b2[e]));
         }
-        *reinterpret_cast<Vec<T, VW> *>(dx + off) = o;
+        return o;
+    };
+    const int64_t step = l.rpi;
+    int64_t r = r0 + rl;
+    // four rows in flight per thread; each row's dx is written after its own
+    // loads (dx may be dout)
+    for (; r + 3 * step < r1; r += 4 * step) {
+        Vec<T, VW> xv[4], gv[4], yv[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int64_t off = (r + u * step) * l.row_len + col * VW;
+            xv[u] = *reinterpret_cast<const Vec<T, VW> *>(x + off);
+            gv[u] = *reinterpret_cast<const Vec<T, VW> *>(dout + off);
+            if (RELU)
+                yv[u] = *reinterpret_cast<const Vec<T, VW> *>(y + off);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            *reinterpret_cast<Vec<T, VW> *>(dx + (r + u * step) * l.row_len + col * VW) = grad(xv[u], gv[u], yv[u]);
+    }
+    for (; r < r1; r += step) {
+        const int64_t off = r * l.row_len + col * VW;
+        Vec<T, VW> yv;
+        if (RELU)
+            yv = *reinterpret_cast<const Vec<T, VW> *>(y + off);
+        *reinterpret_cast<Vec<T, VW> *>(dx + off) =
+            grad(*reinterpret_cast<const Vec<T, VW> *>(x + off), *reinterpret_cast<const Vec<T, VW> *>(dout + off), yv);
     }
 }
 

@@ -10,8 +10,11 @@
 // both operands stored channels-last.  One work-group takes one tap, a
 // 64 x 64 tile of (output, input) channels and a contiguous slice of the
 // pixels; it stages 32-pixel chunks of dY (all four components) and of the
-// tap-shifted X (zero outside the image) in LDS, double-buffered, and its four
-// waves each accumulate the four dW_m of one 32 x 32 (o, c) block.  MFMA
+// tap-shifted X (zero outside the image) in LDS, double-buffered, with the
+// global loads issued two chunks ahead, and its four waves each accumulate
+// the four dW_m of one 32 x 32 (o, c) block.  The taps of one (slice, tile)
+// are placed on one XCD (work-group b runs on XCD b % 8), so the nine reads
+// of a slice of dY and its shifted copies of X share that XCD's L2.  MFMA
 // operands need eight consecutive pixels per lane: bf16 fragments come from
 // the pixel-major rows with two transposing LDS reads (ds_read_b64_tr_b16),
 // fp32 fragments (one pixel per lane) with plain reads.  Slices write fp32
@@ -48,6 +51,7 @@ struct WArgs {
     int64_t pixels;       // n * h_out * w_out
     int64_t per_split;    // pixels of one slice
     int o_tiles, c_tiles, taps;
+    int groups;  // slices x tiles
 };
 
 template <typename T>
@@ -62,23 +66,32 @@ struct Frag<float> {
 };
 
 // 16-byte chunk of one (component, pixel) row: channels ch0 .. ch0+EPC-1 of
-// a row of `len` channels starting at src (NULL: zeros); element-wise when the
-// chunk runs past the end or the row is not 16-byte aligned (VEC false).
+// a row of `len` channels starting at src, zeros where `valid` is false or
+// past len.  Branch-free: an invalid lane loads from `safe` (the tensor's
+// first element) and selects zero, so every load of a chunk stays in flight
+// together.  VEC: rows 16-byte aligned and len a multiple of EPC, so a chunk
+// is wholly inside or outside; otherwise element by element.
 template <typename T, bool VEC>
-__device__ __forceinline__ u32x4 load_chunk(const T *src, int ch0, int len)
+__device__ __forceinline__ u32x4 load_chunk(const T *src, bool valid, int ch0, int len, const T *safe)
 {
     constexpr int EPC = 16 / int(sizeof(T));
-    u32x4 v = {0u, 0u, 0u, 0u};
-    if (src == nullptr || ch0 >= len)
-        return v;
-    if (VEC && ch0 + EPC <= len)
-        return *reinterpret_cast<const u32x4 *>(src + ch0);
-    T e[EPC];
+    if constexpr (VEC) {
+        const bool ok = valid && ch0 < len;
+        const u32x4 v = *reinterpret_cast<const u32x4 *>(ok ? src + ch0 : safe);
+        const unsigned keep = ok ? 0xffffffffu : 0u;
+        return u32x4{v[0] & keep, v[1] & keep, v[2] & keep, v[3] & keep};
+    } else {
+        T e[EPC];
 #pragma unroll
-    for (int i = 0; i < EPC; ++i)
-        e[i] = ch0 + i < len ? src[ch0 + i] : T(0);
-    __builtin_memcpy(&v, e, 16);
-    return v;
+        for (int i = 0; i < EPC; ++i) {
+            const bool ok = valid && ch0 + i < len;
+            const T u = *(ok ? src + ch0 + i : safe);
+            e[i] = ok ? u : T(0);
+        }
+        u32x4 v;
+        __builtin_memcpy(&v, e, 16);
+        return v;
+    }
 }
 
 template <typename T, bool VEC>
@@ -96,9 +109,13 @@ __global__ __launch_bounds__(kThreads) void qconv2d_wgrad(WArgs a)
     __shared__ __attribute__((aligned(16))) T lds[2 * BUF];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    int b = blockIdx.x;
-    const int tap = b % a.taps;
-    b /= a.taps;
+    // work-group b on XCD b % 8 takes tap (b / 8) % taps of group
+    // b % 8 + 8 * (b / 8 / taps)
+    const int xs = int(blockIdx.x) >> 3;
+    const int tap = xs % a.taps;
+    int b = (int(blockIdx.x) & 7) + 8 * (xs / a.taps);
+    if (b >= a.groups)
+        return;  // padding of the last round of groups: nothing to do
     const int ot = b % a.o_tiles;
     b /= a.o_tiles;
     const int ct = b % a.c_tiles;
@@ -116,29 +133,30 @@ __global__ __launch_bounds__(kThreads) void qconv2d_wgrad(WArgs a)
 
     // ---- staging: thread t moves chunk t % CPR of pixel rows t / CPR + PXT * i
     const int cc = tid % CPR, pr = tid / CPR;
-    u32x4 st[2][PASSES][4];  // [tensor][pass][component]
-    auto fetch = [&](int k) {
+    struct Staged {
+        u32x4 v[2][PASSES][4];  // [tensor][pass][component]
+    };
+    auto fetch = [&](int k, Staged &st) {
 #pragma unroll
         for (int i = 0; i < PASSES; ++i) {
-            const int64_t pix = pix0 + int64_t(k) * kChunk + pr + PXT * i;
-            const T *yrow = nullptr, *xrow = nullptr;
-            if (pix < pix1) {
-                const int64_t img = pix / hw_out;
-                const int rr = int(pix - img * hw_out);
-                const int oy = rr / a.w_out, ox = rr - (rr / a.w_out) * a.w_out;
-                yrow = dy + pix * 4 * a.c_out;
-                const int iy = oy * a.s_h - a.p_h + ky * a.d_h, ix = ox * a.s_w - a.p_w + kx * a.d_w;
-                if (iy >= 0 && iy < a.h && ix >= 0 && ix < a.w)
-                    xrow = x + ((img * a.h + iy) * a.w + ix) * 4 * a.c_in;
-            }
+            int64_t pix = pix0 + int64_t(k) * kChunk + pr + PXT * i;
+            const bool yok = pix < pix1;
+            pix = yok ? pix : pix0;  // keep the address arithmetic in range
+            const int64_t img = pix / hw_out;
+            const int rr = int(pix - img * hw_out);
+            const int oy = rr / a.w_out, ox = rr - (rr / a.w_out) * a.w_out;
+            const int iy = oy * a.s_h - a.p_h + ky * a.d_h, ix = ox * a.s_w - a.p_w + kx * a.d_w;
+            const bool xok = yok && iy >= 0 && iy < a.h && ix >= 0 && ix < a.w;
+            const T *yrow = dy + pix * 4 * a.c_out;
+            const T *xrow = x + ((img * a.h + (xok ? iy : 0)) * a.w + (xok ? ix : 0)) * 4 * a.c_in;
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-                st[0][i][q] = load_chunk<T, VEC>(yrow ? yrow + q * a.c_out + o0 : nullptr, cc * EPC, a.c_out - o0);
-                st[1][i][q] = load_chunk<T, VEC>(xrow ? xrow + q * a.c_in + c0 : nullptr, cc * EPC, a.c_in - c0);
+                st.v[0][i][q] = load_chunk<T, VEC>(yrow + q * a.c_out + o0, yok, cc * EPC, a.c_out - o0, dy);
+                st.v[1][i][q] = load_chunk<T, VEC>(xrow + q * a.c_in + c0, xok, cc * EPC, a.c_in - c0, x);
             }
         }
     };
-    auto store = [&](int buf) {
+    auto store = [&](int buf, const Staged &st) {
         T *base = lds + buf * BUF;
 #pragma unroll
         for (int t = 0; t < 2; ++t)
@@ -147,7 +165,7 @@ __global__ __launch_bounds__(kThreads) void qconv2d_wgrad(WArgs a)
 #pragma unroll
                 for (int q = 0; q < 4; ++q)
                     *reinterpret_cast<u32x4 *>(base + t * TENSOR + q * COMP + (pr + PXT * i) * kRow + cc * EPC) =
-                        st[t][i][q];
+                        st.v[t][i][q];
     };
 
     // ---- compute: wave w owns o-block w / 2 and c-block w % 2
@@ -208,18 +226,33 @@ __global__ __launch_bounds__(kThreads) void qconv2d_wgrad(WArgs a)
         }
     };
 
-    if (chunks > 0) {
-        fetch(0);
-        store(0);
+    // Chunk k is computed from LDS buffer k % 2 while chunk k + 1 waits in
+    // registers (loaded an iteration earlier) and chunk k + 2 is loaded; after
+    // the computation chunk k + 1 goes to the other buffer, which the previous
+    // barrier freed.  Two register sets alternate, so the loop is unrolled by
+    // two.
+    Staged sa, sb;
+    auto iteration = [&](int k, Staged &next, Staged &after) {
+        if (k + 2 < chunks)
+            fetch(k + 2, after);
+        compute(k & 1);
+        if (k + 1 < chunks)
+            store((k + 1) & 1, next);
         __syncthreads();
-        for (int k = 0; k < chunks; ++k) {
-            if (k + 1 < chunks)
-                fetch(k + 1);  // in flight while this chunk is computed
-            compute(k & 1);
-            if (k + 1 < chunks)
-                store((k + 1) & 1);  // the other buffer: last read before the previous barrier
-            __syncthreads();
+    };
+    if (chunks > 0) {
+        fetch(0, sa);
+        if (chunks > 1)
+            fetch(1, sb);
+        store(0, sa);
+        __syncthreads();
+        int k = 0;
+        for (; k + 1 < chunks; k += 2) {
+            iteration(k, sb, sa);
+            iteration(k + 1, sa, sb);
         }
+        if (k < chunks)
+            iteration(k, sb, sa);
     }
 
     // ---- partial sums: register 4g + e of lane l is (o, c) = (ob + 8g +
@@ -238,19 +271,20 @@ __global__ __launch_bounds__(kThreads) void qconv2d_wgrad(WArgs a)
 }
 
 // dW_m[o][c][ky][kx] = sum over slices of the partials, in slice order, fp64.
+// Consecutive threads take consecutive (o, c) of one (m, tap), so every
+// slice's partials are read contiguously.
 __global__ __launch_bounds__(kThreads) void qconv2d_wgrad_reduce(const float *__restrict__ part, int splits, int taps,
                                                                  int c_out, int c_in, float *__restrict__ dw0,
                                                                  float *__restrict__ dw1, float *__restrict__ dw2,
                                                                  float *__restrict__ dw3)
 {
-    const int64_t per_m = int64_t(c_out) * c_in * taps;
-    const int64_t idx = int64_t(blockIdx.x) * kThreads + threadIdx.x;  // over [m][o][c][tap]
-    if (idx >= 4 * per_m)
+    const int64_t oc_n = int64_t(c_out) * c_in;
+    const int64_t idx = int64_t(blockIdx.x) * kThreads + threadIdx.x;  // over [m][tap][o][c]
+    if (idx >= 4 * taps * oc_n)
         return;
-    const int m = int(idx / per_m);
-    const int64_t r = idx - m * per_m;
-    const int tap = int(r % taps);
-    const int64_t oc = r / taps;  // o * c_in + c
+    const int64_t oc = idx % oc_n;  // o * c_in + c
+    const int mt = int(idx / oc_n);
+    const int m = mt / taps, tap = mt - (mt / taps) * taps;
     double s = 0.0;
     for (int sp = 0; sp < splits; ++sp)
         s += double(part[((int64_t(sp) * taps + tap) * 4 + m) * c_out * c_in + oc]);
@@ -258,38 +292,105 @@ __global__ __launch_bounds__(kThreads) void qconv2d_wgrad_reduce(const float *__
     dw[oc * taps + tap] = float(s);
 }
 
-// Bias gradient: per column col of the [pixels][4 * c_out] rows of dY, partial
-// sums per block of rows, then a fixed-order fp64 total.
-template <typename T>
+// Bias gradient: column sums of the [pixels][cols = 4 * c_out] rows of dY.
+// Thread t of a block sums the VW-element column chunk t % CG over rows
+// t / CG + RPI * i of the block's row range (four rows in flight), the
+// threads sharing a chunk add in a fixed order through LDS, and each block
+// writes one partial per column; colsum_final adds the blocks in order in
+// fp64.
+template <typename T, int VW>
 __global__ __launch_bounds__(kThreads) void colsum_partial(const T *__restrict__ dy, int64_t pixels, int cols,
                                                            int64_t rows_per_block, float *__restrict__ part)
 {
-    const int col = blockIdx.y * kThreads + threadIdx.x;
-    if (col >= cols)
-        return;
+    __shared__ float red[kThreads][VW];
+    const int chunks = cols / VW;
+    const int cg = chunks < kThreads ? chunks : kThreads;
+    const int rpi = kThreads / cg;
+    const int tid = threadIdx.x, cl = tid % cg, rl = tid / cg;
+    const int chunk = blockIdx.y * cg + cl;
+    const bool active = rl < rpi && chunk < chunks;
     const int64_t r0 = int64_t(blockIdx.x) * rows_per_block;
     int64_t r1 = r0 + rows_per_block;
     if (r1 > pixels)
         r1 = pixels;
-    float s = 0.0f;
-    for (int64_t r = r0; r < r1; ++r)
-        s += float(dy[r * cols + col]);
-    part[int64_t(blockIdx.x) * cols + col] = s;
+    struct alignas(sizeof(T) * VW) V {
+        T e[VW];
+    };
+    float acc[VW];
+#pragma unroll
+    for (int e = 0; e < VW; ++e)
+        acc[e] = 0.0f;
+    if (active) {
+        const T *base = dy + chunk * VW;
+        int64_t r = r0 + rl;
+        for (; r + 3 * rpi < r1; r += 4 * rpi) {
+            V v[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                v[u] = *reinterpret_cast<const V *>(base + (r + u * rpi) * cols);
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+#pragma unroll
+                for (int e = 0; e < VW; ++e)
+                    acc[e] += float(v[u].e[e]);
+        }
+        for (; r < r1; r += rpi) {
+            const V v = *reinterpret_cast<const V *>(base + r * cols);
+#pragma unroll
+            for (int e = 0; e < VW; ++e)
+                acc[e] += float(v.e[e]);
+        }
+    }
+#pragma unroll
+    for (int e = 0; e < VW; ++e)
+        red[tid][e] = acc[e];
+    __syncthreads();
+    if (rl == 0 && chunk < chunks) {
+        float t[VW];
+#pragma unroll
+        for (int e = 0; e < VW; ++e)
+            t[e] = 0.0f;
+        for (int j = 0; j < rpi; ++j)
+#pragma unroll
+            for (int e = 0; e < VW; ++e)
+                t[e] += red[j * cg + cl][e];
+#pragma unroll
+        for (int e = 0; e < VW; ++e)
+            part[int64_t(blockIdx.x) * cols + chunk * VW + e] = t[e];
+    }
 }
 
+// One wave per column: lane i adds blocks i, i+64, ... (eight loads in
+// flight), then a fixed butterfly adds the lanes in fp64.
 __global__ __launch_bounds__(kThreads) void colsum_final(const float *__restrict__ part, int blocks, int cols,
                                                          float *__restrict__ db)
 {
-    const int col = blockIdx.x * kThreads + threadIdx.x;
+    constexpr int U = 8;
+    const int lane = threadIdx.x & 63;
+    const int col = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
     if (col >= cols)
         return;
     double s = 0.0;
-    for (int b = 0; b < blocks; ++b)
-        s += double(part[int64_t(b) * cols + col]);
-    db[col] = float(s);
+    for (int b0 = lane; b0 < blocks; b0 += 64 * U) {
+        float v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int b = b0 + 64 * u;
+            v[u] = part[int64_t(b < blocks ? b : blocks - 1) * cols + col];
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (b0 + 64 * u < blocks)
+                s += double(v[u]);
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1)
+        s += __shfl_xor(s, off);
+    if (lane == 0)
+        db[col] = float(s);
 }
 
-constexpr int kBiasBlocks = 128;
+constexpr int kBiasBlocks = 512;
 
 struct WPlan {
     int o_tiles, c_tiles, taps, splits;
@@ -356,7 +457,8 @@ hipError_t qconv2d_backward_weight_run(const ConvGeom &g, DType dt, const void *
     a.o_tiles = p.o_tiles;
     a.c_tiles = p.c_tiles;
     a.taps = p.taps;
-    const unsigned blocks = unsigned(int64_t(p.splits) * p.c_tiles * p.o_tiles * p.taps);
+    a.groups = p.splits * p.c_tiles * p.o_tiles;
+    const unsigned blocks = unsigned(int64_t(8) * p.taps * ((a.groups + 7) / 8));
     const int epc = dt == DType::BF16 ? 8 : 4;
     const bool vec = g.c_in % epc == 0 && g.c_out % epc == 0;
     if (dt == DType::BF16) {
@@ -384,14 +486,26 @@ hipError_t qconv2d_backward_weight_run(const ConvGeom &g, DType dt, const void *
     const int64_t pixels = g.m();
     const int64_t rpb = (pixels + kBiasBlocks - 1) / kBiasBlocks;
     const int nb = int((pixels + rpb - 1) / rpb);
-    const dim3 grid(nb, (cols + kThreads - 1) / kThreads);
-    if (dt == DType::BF16)
-        hipLaunchKernelGGL(colsum_partial<__bf16>, grid, dim3(kThreads), 0, stream, (const __bf16 *)dy, pixels, cols,
-                           rpb, a.part);
-    else
-        hipLaunchKernelGGL(colsum_partial<float>, grid, dim3(kThreads), 0, stream, (const float *)dy, pixels, cols,
-                           rpb, a.part);
-    hipLaunchKernelGGL(colsum_final, dim3((cols + kThreads - 1) / kThreads), dim3(kThreads), 0, stream,
+    const int vw = cols % (dt == DType::BF16 ? 8 : 4) == 0 ? (dt == DType::BF16 ? 8 : 4) : 1;
+    const int chunks = cols / vw;
+    const int cg = chunks < kThreads ? chunks : kThreads;
+    const dim3 grid(nb, (chunks + cg - 1) / cg);
+    if (dt == DType::BF16) {
+        if (vw == 8)
+            hipLaunchKernelGGL((colsum_partial<__bf16, 8>), grid, dim3(kThreads), 0, stream, (const __bf16 *)dy,
+                               pixels, cols, rpb, a.part);
+        else
+            hipLaunchKernelGGL((colsum_partial<__bf16, 1>), grid, dim3(kThreads), 0, stream, (const __bf16 *)dy,
+                               pixels, cols, rpb, a.part);
+    } else {
+        if (vw == 4)
+            hipLaunchKernelGGL((colsum_partial<float, 4>), grid, dim3(kThreads), 0, stream, (const float *)dy,
+                               pixels, cols, rpb, a.part);
+        else
+            hipLaunchKernelGGL((colsum_partial<float, 1>), grid, dim3(kThreads), 0, stream, (const float *)dy,
+                               pixels, cols, rpb, a.part);
+    }
+    hipLaunchKernelGGL(colsum_final, dim3((cols + kThreads / 64 - 1) / (kThreads / 64)), dim3(kThreads), 0, stream,
                        (const float *)a.part, nb, cols, db);
     return hipGetLastError();
 }
