@@ -671,83 +671,83 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + 2)) void qconv2d_igemm(KA
     };
 
     // IQBN statistics of a parked tile, read back from the wave's own LDS
-    // region into registers once: lane l holds chunk l % OUT_CPR of pixels
-    // l / OUT_CPR + PPI * i.  Two passes over those registers give the exact
-    // tile mean per column (a fixed butterfly over the lanes sharing a
-    // chunk), then the squared deviations from it, so nothing cancels.
-    // Rows past M are left out.
-    auto tile_stats = [&](const unsigned char *w_lds, int m0, int o0) {
-        constexpr int PPI = 64 / OUT_CPR;  // pixels per read
-        constexpr int NR = BM / PPI;       // reads per lane
-        const int cl = lane % OUT_CPR, pl = lane / OUT_CPR;
-        const int n_valid = a.m - m0 < BM ? a.m - m0 : BM;
-        const unsigned char *src = w_lds + pl * OUT_ROW + ((cl ^ (pl % OUT_CPR)) * 16);
-        u32x4 raw[NR];
-#pragma unroll
-        for (int i = 0; i < NR; ++i)
-            raw[i] = *reinterpret_cast<const u32x4 *>(src + i * PPI * OUT_ROW);
-        auto val = [&](int i, int k) {
-            T v[CPC];
-            __builtin_memcpy(v, &raw[i], 16);
-            return float(v[k]);
+    // region with transposing reads (ds_read_b64_tr_b16): in each 16-lane
+    // group, lane 4a+b receives element b of the 8-byte pieces addressed by
+    // lanes a, a+4, a+8, a+12.  With those four lanes pointing at one
+    // 4-channel group of four consecutive pixels, every lane ends up with
+    // one channel (lane % BNC) of four pixels per read, two per dword, and
+    // reduces over pixels without talking to other lanes.  Two passes: the
+    // exact tile mean per column (pairs summed by v_dot2 with ones), then
+    // the squared deviations from it, so nothing cancels.  Rows past M of a
+    // partial tile hold one and the same parked value (their activations
+    // load as zeros); it is read back once and its share taken out of both
+    // sums.
+    auto tile_stats = [&](const auto *w_lds, int m0, int o0) {  // generic: instantiated where called
+        static_assert(ES == 2 && (BNC == 64 || BNC == 32), "statistics read-back geometry");
+        typedef short s16x4 __attribute__((ext_vector_type(4)));
+        typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+        constexpr int NCG = BNC / 4;     // 4-channel groups per pixel
+        constexpr int LPS = 4 * NCG;     // lanes per pixel set: one per channel
+        constexpr int SETS = 64 / LPS;   // pixel sets read side by side
+        constexpr int PPR = 4 * SETS;    // pixels per read
+        constexpr int NR = BM / PPR;     // reads per lane
+        const int q = 4 * (lane >> 4) + (lane & 3);
+        const int cg = q % NCG, set = q / NCG, r = (lane & 15) >> 2;
+        const int p_lane = 4 * set + r;  // pixel of the piece this lane addresses, within a read
+        // physical chunk = logical chunk ^ (pixel % OUT_CPR); the read's own
+        // share of the pixel index, (PPR * i) % OUT_CPR, is 0 or 4 and shares
+        // no bit with p_lane % OUT_CPR
+        auto piece = [&](int xr) {
+            return w_lds + p_lane * OUT_ROW + ((((cg >> 1) ^ (p_lane % OUT_CPR)) ^ xr) * 16) + (cg & 1) * 8;
         };
-        float mean[CPC], m2[CPC];
+        const unsigned char *const src0 = piece(0);
+        const unsigned char *const src4 = piece(4 % OUT_CPR);
+        unsigned dw[2 * NR];
 #pragma unroll
-        for (int k = 0; k < CPC; ++k) { mean[k] = 0.0f; m2[k] = 0.0f; }
-        if (n_valid == BM) {  // whole tile: no row masks
-#pragma unroll
-            for (int i = 0; i < NR; ++i)
-#pragma unroll
-                for (int k = 0; k < CPC; ++k)
-                    mean[k] += val(i, k);
-        } else {
-#pragma unroll
-            for (int i = 0; i < NR; ++i)
-#pragma unroll
-                for (int k = 0; k < CPC; ++k)
-                    mean[k] += i * PPI + pl < n_valid ? val(i, k) : 0.0f;
+        for (int i = 0; i < NR; ++i) {
+            const int xr = (PPR * i) % OUT_CPR;
+            const unsigned char *p = (xr == 0 ? src0 : src4) + i * PPR * OUT_ROW;
+            const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4 *)(p));
+            __builtin_memcpy(&dw[2 * i], &v, 8);
         }
-#pragma unroll
-        for (int off = OUT_CPR; off < 64; off <<= 1)
-#pragma unroll
-            for (int k = 0; k < CPC; ++k)
-                mean[k] += __shfl_xor(mean[k], off);
-        const float inv = 1.0f / float(n_valid);
-#pragma unroll
-        for (int k = 0; k < CPC; ++k)
-            mean[k] *= inv;
-        if (n_valid == BM) {
-#pragma unroll
-            for (int i = 0; i < NR; ++i)
-#pragma unroll
-                for (int k = 0; k < CPC; ++k) {
-                    const float d = val(i, k) - mean[k];
-                    m2[k] = fmaf(d, d, m2[k]);
-                }
-        } else {
-#pragma unroll
-            for (int i = 0; i < NR; ++i)
-#pragma unroll
-                for (int k = 0; k < CPC; ++k) {
-                    const float d = i * PPI + pl < n_valid ? val(i, k) - mean[k] : 0.0f;
-                    m2[k] = fmaf(d, d, m2[k]);
-                }
+        const int ch = lane % LPS;  // channel within the tile's BNC
+        const int n_valid = a.m - m0 < BM ? a.m - m0 : BM;
+        const float n_inv = float(BM - n_valid);
+        float v_inv = 0.0f;
+        if (n_valid < BM) {
+            const int pm = BM - 1;
+            const T t = *reinterpret_cast<const T *>(w_lds + pm * OUT_ROW + (((ch / 8) ^ (pm % OUT_CPR)) * 16) +
+                                                     (ch % 8) * 2);
+            v_inv = float(t);
         }
+        const bf16x2 ones = __builtin_bit_cast(bf16x2, 0x3F803F80u);
+        float s[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-        for (int off = OUT_CPR; off < 64; off <<= 1)
+        for (int i = 0; i < 2 * NR; ++i)
+            s[i & 3] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, dw[i]), ones, s[i & 3], false);
+        float sum = (s[0] + s[1]) + (s[2] + s[3]);
+        if constexpr (SETS == 2)
+            sum += __shfl_xor(sum, 32);
+        const float mean = (sum - n_inv * v_inv) / float(n_valid);
+        float m[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-            for (int k = 0; k < CPC; ++k)
-                m2[k] += __shfl_xor(m2[k], off);
-        const int ch = o0 + cl * CPC;  // first channel of the lane's chunk
-        if (pl == 0 && ch < a.c_out) {
+        for (int i = 0; i < 2 * NR; ++i) {
+            const float lo = __builtin_bit_cast(float, dw[i] << 16) - mean;
+            const float hi = __builtin_bit_cast(float, dw[i] & 0xffff0000u) - mean;
+            m[i & 3] = fmaf(lo, lo, m[i & 3]);
+            m[(i + 2) & 3] = fmaf(hi, hi, m[(i + 2) & 3]);
+        }
+        float m2 = (m[0] + m[1]) + (m[2] + m[3]);
+        if constexpr (SETS == 2)
+            m2 += __shfl_xor(m2, 32);
+        const float dv = v_inv - mean;
+        m2 = fmaxf(m2 - n_inv * dv * dv, 0.0f);
+        if (lane < LPS && o0 + ch < a.c_out) {
             const int mt = m0 / BM;
             const size_t cols = size_t(4) * a.c_out;
-#pragma unroll
-            for (int k = 0; k < CPC; ++k) {
-                const size_t col = size_t(wn) * a.c_out + ch + k;
-                a.stats[col * a.m_tiles + mt] = mean[k];
-                a.stats[(cols + col) * a.m_tiles + mt] = m2[k];
-            }
+            const size_t col = size_t(wn) * a.c_out + o0 + ch;
+            a.stats[col * a.m_tiles + mt] = mean;
+            a.stats[(cols + col) * a.m_tiles + mt] = m2;
         }
     };
 
@@ -804,36 +804,51 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + 2)) void qconv2d_igemm(KA
             // l%32 of block mb; bias added (or the folded affine map and
             // ReLU applied), rounded to T
             unsigned char *const w_lds = o_lds + wn * OUT_WAVE;
+            // AFFINE: a per-column map to apply (bias or the folded IQBN);
+            // without one the accumulators are only rounded.
+            auto park = [&](auto affine) {
+                constexpr bool AFFINE = decltype(affine)::value;
 #pragma unroll
-            for (int nb = 0; nb < NB; ++nb) {
+                for (int nb = 0; nb < NB; ++nb) {
 #pragma unroll
-                for (int g = 0; g < 4; ++g) {
-                    const int oc = nb * 32 + 8 * g + 4 * khalf;  // channel within the tile's BNC
-                    float sc[4], sh[4];
+                    for (int g = 0; g < 4; ++g) {
+                        const int oc = nb * 32 + 8 * g + 4 * khalf;  // channel within the tile's BNC
+                        float sc[4], sh[4];
+                        if constexpr (AFFINE) {
 #pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        col_affine(wn * a.c_out + o0 + oc + e, o0 + oc + e < a.c_out, sc[e], sh[e]);
+                            for (int e = 0; e < 4; ++e)
+                                col_affine(wn * a.c_out + o0 + oc + e, o0 + oc + e < a.c_out, sc[e], sh[e]);
+                        }
 #pragma unroll
-                    for (int mb = 0; mb < MB; ++mb) {
-                        const int m = mb * 32 + l32;
-                        T v[4];
+                        for (int mb = 0; mb < MB; ++mb) {
+                            const int m = mb * 32 + l32;
+                            T v[4];
 #pragma unroll
-                        for (int e = 0; e < 4; ++e)
-                            v[e] = T(epi(acc[0][nb][mb][4 * g + e], sc[e], sh[e]));
-                        const int c = oc * ES / 16, within = (oc * ES) % 16;
-                        unsigned char *dst = w_lds + m * OUT_ROW + ((c ^ (m % OUT_CPR)) * 16) + within;
-                        if constexpr (ES == 2) {
-                            uint2 pk;
-                            __builtin_memcpy(&pk, v, 8);
-                            *reinterpret_cast<uint2 *>(dst) = pk;
-                        } else {
-                            u32x4 pk;
-                            __builtin_memcpy(&pk, v, 16);
-                            *reinterpret_cast<u32x4 *>(dst) = pk;
+                            for (int e = 0; e < 4; ++e) {
+                                if constexpr (AFFINE)
+                                    v[e] = T(epi(acc[0][nb][mb][4 * g + e], sc[e], sh[e]));
+                                else
+                                    v[e] = T(acc[0][nb][mb][4 * g + e]);
+                            }
+                            const int c = oc * ES / 16, within = (oc * ES) % 16;
+                            unsigned char *dst = w_lds + m * OUT_ROW + ((c ^ (m % OUT_CPR)) * 16) + within;
+                            if constexpr (ES == 2) {
+                                uint2 pk;
+                                __builtin_memcpy(&pk, v, 8);
+                                *reinterpret_cast<uint2 *>(dst) = pk;
+                            } else {
+                                u32x4 pk;
+                                __builtin_memcpy(&pk, v, 16);
+                                *reinterpret_cast<u32x4 *>(dst) = pk;
+                            }
                         }
                     }
                 }
-            }
+            };
+            if (EPI == kEpiFold || bias != nullptr)
+                park(std::true_type{});
+            else
+                park(std::false_type{});
             if constexpr (EPI == kEpiStats)
                 tile_stats(w_lds, m0, o0);
             const long long rows_left = (long long)(a.m - m0) * row_bytes;
