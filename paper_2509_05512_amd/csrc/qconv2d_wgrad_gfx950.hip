@@ -11,8 +11,11 @@
 // 64 x 64 tile of (output, input) channels and a contiguous slice of the
 // pixels; it stages 32-pixel chunks of dY (all four components) and of the
 // tap-shifted X (zero outside the image) in LDS, double-buffered, with the
-// global loads issued two chunks ahead, and its four waves each accumulate
-// the four dW_m of one 32 x 32 (o, c) block.  The taps of one (slice, tile)
+// global loads (16-byte buffer loads at 32-bit offsets, zeros past the end,
+// each thread's pixel coordinates advanced incrementally) issued two chunks
+// ahead, and its four waves each accumulate the four dW_m of one 32 x 32
+// (o, c) block, reading the next k-step's fragments while the MFMAs of the
+// current one run; a sign flip is one XOR per fragment dword.  The taps of one (slice, tile)
 // are placed on one XCD (work-group b runs on XCD b % 8), so the nine reads
 // of a slice of dY and its shifted copies of X share that XCD's L2.  MFMA
 // operands need eight consecutive pixels per lane: bf16 fragments come from
@@ -94,6 +97,15 @@ __device__ __forceinline__ u32x4 load_chunk(const T *src, bool valid, int ch0, i
     }
 }
 
+// 16 bytes at byte offset off of the buffer [base, base + bytes); offsets
+// past the end read as zeros.
+__device__ __forceinline__ u32x4 load16(const void *base, unsigned bytes, unsigned off)
+{
+    const __amdgpu_buffer_rsrc_t r =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, 0x00020000);
+    return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+
 template <typename T, bool VEC>
 __global__ __launch_bounds__(kThreads) void qconv2d_wgrad(WArgs a)
 {
@@ -136,24 +148,67 @@ __global__ __launch_bounds__(kThreads) void qconv2d_wgrad(WArgs a)
     struct Staged {
         u32x4 v[2][PASSES][4];  // [tensor][pass][component]
     };
+    // VEC: 16-byte buffer loads at 32-bit offsets from the slice's first
+    // pixel (dY) and first image (X), zeros past a buffer's end; each pass
+    // keeps its pixel's (image, row, column), advanced by one chunk per
+    // fetch, so chunks are fetched in order.
+    const int span = int(pix1 - pix0 > 0 ? pix1 - pix0 : 0);
+    const int64_t img0 = pix0 / hw_out;
+    const T *const dy_s = dy + pix0 * 4 * a.c_out;
+    const T *const x_s = x + img0 * int64_t(a.h) * a.w * 4 * a.c_in;
+    const unsigned dy_bytes = unsigned(int64_t(span) * 4 * a.c_out * ES);
+    const int64_t x_left = (int64_t(a.n) - img0) * a.h * a.w * 4 * a.c_in * ES;
+    const unsigned x_bytes = unsigned(x_left < 0x7fffffffLL ? x_left : 0x7fffffffLL);
+    const bool o_in = o0 + cc * EPC < a.c_out, c_in_ok = c0 + cc * EPC < a.c_in;
+    int cur_img[PASSES], cur_oy[PASSES], cur_ox[PASSES];
+#pragma unroll
+    for (int i = 0; i < PASSES; ++i) {
+        const int64_t pix = pix0 + pr + PXT * i;
+        const int64_t img = pix / hw_out;
+        const int rr = int(pix - img * hw_out);
+        cur_img[i] = int(img - img0);
+        cur_oy[i] = rr / a.w_out;
+        cur_ox[i] = rr - cur_oy[i] * a.w_out;
+    }
     auto fetch = [&](int k, Staged &st) {
 #pragma unroll
         for (int i = 0; i < PASSES; ++i) {
-            int64_t pix = pix0 + int64_t(k) * kChunk + pr + PXT * i;
-            const bool yok = pix < pix1;
-            pix = yok ? pix : pix0;  // keep the address arithmetic in range
-            const int64_t img = pix / hw_out;
-            const int rr = int(pix - img * hw_out);
-            const int oy = rr / a.w_out, ox = rr - (rr / a.w_out) * a.w_out;
-            const int iy = oy * a.s_h - a.p_h + ky * a.d_h, ix = ox * a.s_w - a.p_w + kx * a.d_w;
-            const bool xok = yok && iy >= 0 && iy < a.h && ix >= 0 && ix < a.w;
-            const T *yrow = dy + pix * 4 * a.c_out;
-            const T *xrow = x + ((img * a.h + (xok ? iy : 0)) * a.w + (xok ? ix : 0)) * 4 * a.c_in;
+            const int rel = k * kChunk + pr + PXT * i;  // pixel - pix0
+            const bool yok = rel < span;
+            const int iy = cur_oy[i] * a.s_h - a.p_h + ky * a.d_h, ix = cur_ox[i] * a.s_w - a.p_w + kx * a.d_w;
+            if constexpr (VEC) {
+                const bool xok = yok && c_in_ok && unsigned(iy) < unsigned(a.h) && unsigned(ix) < unsigned(a.w);
+                const unsigned yoff = yok && o_in ? unsigned((rel * 4 * a.c_out + o0 + cc * EPC) * ES) : 0x80000000u;
+                const unsigned xoff =
+                    xok ? unsigned((((cur_img[i] * a.h + iy) * a.w + ix) * 4 * a.c_in + c0 + cc * EPC) * ES)
+                        : 0x80000000u;
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                st.v[0][i][q] = load_chunk<T, VEC>(yrow + q * a.c_out + o0, yok, cc * EPC, a.c_out - o0, dy);
-                st.v[1][i][q] = load_chunk<T, VEC>(xrow + q * a.c_in + c0, xok, cc * EPC, a.c_in - c0, x);
+                for (int q = 0; q < 4; ++q) {
+                    st.v[0][i][q] = load16(dy_s, dy_bytes, yoff + unsigned(q * a.c_out * ES));
+                    st.v[1][i][q] = load16(x_s, x_bytes, xoff + unsigned(q * a.c_in * ES));
+                }
+            } else {
+                const bool xok = yok && iy >= 0 && iy < a.h && ix >= 0 && ix < a.w;
+                const T *yrow = dy_s + int64_t(yok ? rel : 0) * 4 * a.c_out;
+                const T *xrow = x_s + ((int64_t(cur_img[i]) * a.h + (xok ? iy : 0)) * a.w + (xok ? ix : 0)) * 4 * a.c_in;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    st.v[0][i][q] = load_chunk<T, VEC>(yrow + q * a.c_out + o0, yok, cc * EPC, a.c_out - o0, dy);
+                    st.v[1][i][q] = load_chunk<T, VEC>(xrow + q * a.c_in + c0, xok, cc * EPC, a.c_in - c0, x);
+                }
             }
+            // next chunk: kChunk pixels on
+            int ox = cur_ox[i] + kChunk, oy = cur_oy[i], im = cur_img[i];
+            while (ox >= a.w_out) {
+                ox -= a.w_out;
+                if (++oy == a.h_out) {
+                    oy = 0;
+                    ++im;
+                }
+            }
+            cur_ox[i] = ox;
+            cur_oy[i] = oy;
+            cur_img[i] = im;
         }
     };
     auto store = [&](int buf, const Staged &st) {
@@ -200,29 +255,56 @@ __global__ __launch_bounds__(kThreads) void qconv2d_wgrad(WArgs a)
         return f;
     };
     constexpr int KSTEPS = ES == 2 ? kChunk / 16 : kChunk / 2;
-    auto compute = [&](int buf) {
+    typedef typename Frag<T>::type F;
+    struct KFrags {
+        F fy[4], fx[4];
+    };
+    auto read_k = [&](int buf, int ks, KFrags &f) {
         const T *yb = lds + buf * BUF, *xb = yb + TENSOR;
 #pragma unroll
-        for (int ks = 0; ks < KSTEPS; ++ks) {
-            typename Frag<T>::type fy[4], fx[4];
+        for (int q = 0; q < 4; ++q) {
+            f.fy[q] = frag(yb, q, ob, ks);
+            f.fx[q] = frag(xb, q, cb, ks);
+        }
+    };
+    // sign flip of a fragment: the sign bit of every element
+    auto negate = [&](F v) {
+        if constexpr (ES == 2) {
+            u32x4 u = __builtin_bit_cast(u32x4, v);
+            u ^= 0x80008000u;
+            return __builtin_bit_cast(F, u);
+        } else {
+            return __builtin_bit_cast(F, __builtin_bit_cast(unsigned, v) ^ 0x80000000u);
+        }
+    };
+    auto mfmas = [&](const KFrags &f) {
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                fy[q] = frag(yb, q, ob, ks);
-                fx[q] = frag(xb, q, cb, ks);
+        for (int p = 0; p < 4; ++p) {
+            const F pos = f.fy[p], neg = negate(f.fy[p]);
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+                const int q = p ^ m;
+                const bool minus = (kNeg >> (4 * p + q)) & 1u;
+                if constexpr (ES == 2)
+                    acc[m] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(minus ? neg : pos, f.fx[q], acc[m], 0, 0, 0);
+                else
+                    acc[m] = __builtin_amdgcn_mfma_f32_32x32x2f32(minus ? neg : pos, f.fx[q], acc[m], 0, 0, 0);
             }
+        }
+    };
+    // the k-steps of one chunk, reading k-step ks + 1 while ks runs
+    auto compute = [&](int buf) {
+        KFrags fa, fb;
+        read_k(buf, 0, fa);
 #pragma unroll
-            for (int p = 0; p < 4; ++p) {
-                typename Frag<T>::type pos = fy[p], neg = -fy[p];
-#pragma unroll
-                for (int m = 0; m < 4; ++m) {
-                    const int q = p ^ m;
-                    const bool minus = (kNeg >> (4 * p + q)) & 1u;
-                    if constexpr (ES == 2)
-                        acc[m] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(minus ? neg : pos, fx[q], acc[m], 0, 0, 0);
-                    else
-                        acc[m] = __builtin_amdgcn_mfma_f32_32x32x2f32(minus ? neg : pos, fx[q], acc[m], 0, 0, 0);
-                }
-            }
+        for (int ks = 0; ks < KSTEPS; ks += 2) {
+            if (ks + 1 < KSTEPS)
+                read_k(buf, ks + 1, fb);
+            mfmas(fa);
+            if (ks + 2 < KSTEPS)
+                read_k(buf, ks + 2, fa);
+            if (ks + 1 < KSTEPS)
+                mfmas(fb);
         }
     };
 
@@ -459,8 +541,13 @@ hipError_t qconv2d_backward_weight_run(const ConvGeom &g, DType dt, const void *
     a.taps = p.taps;
     a.groups = p.splits * p.c_tiles * p.o_tiles;
     const unsigned blocks = unsigned(int64_t(8) * p.taps * ((a.groups + 7) / 8));
-    const int epc = dt == DType::BF16 ? 8 : 4;
-    const bool vec = g.c_in % epc == 0 && g.c_out % epc == 0;
+    const int epc = dt == DType::BF16 ? 8 : 4, es = dt == DType::BF16 ? 2 : 4;
+    // the 16-byte buffer loads take 32-bit offsets within a slice's pixels
+    // of dY and the images of X it touches
+    const int64_t hw_out = int64_t(g.h_out) * g.w_out;
+    const int64_t dy_span = p.per_split * 4 * g.c_out * es;
+    const int64_t x_span = ((p.per_split + hw_out - 1) / hw_out + 1) * g.h * g.w * 4 * g.c_in * es;
+    const bool vec = g.c_in % epc == 0 && g.c_out % epc == 0 && dy_span < 0x7fffffffLL && x_span < 0x7fffffffLL;
     if (dt == DType::BF16) {
         if (vec)
             hipLaunchKernelGGL((qconv2d_wgrad<__bf16, true>), dim3(blocks), dim3(kThreads), 0, stream, a);
