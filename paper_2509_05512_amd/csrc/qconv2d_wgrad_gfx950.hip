@@ -292,19 +292,37 @@ __global__ __launch_bounds__(kThreads) void qconv2d_wgrad(WArgs a)
             }
         }
     };
-    // the k-steps of one chunk, reading k-step ks + 1 while ks runs
+    // The k-steps of one chunk, reading k-step ks + 1 while ks runs: the
+    // sign flips first, then each MFMA followed by one fragment read.
+    constexpr int NRD = ES == 2 ? 16 : 8;  // LDS reads of one k-step
+    auto sched = [&]() {
+        __builtin_amdgcn_sched_group_barrier(0x002, ES == 2 ? 16 : 4, 0);
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            if (i < NRD)
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+    };
     auto compute = [&](int buf) {
         KFrags fa, fb;
         read_k(buf, 0, fa);
 #pragma unroll
         for (int ks = 0; ks < KSTEPS; ks += 2) {
+            __builtin_amdgcn_sched_barrier(0);
             if (ks + 1 < KSTEPS)
                 read_k(buf, ks + 1, fb);
             mfmas(fa);
+            if (ks + 1 < KSTEPS)
+                sched();
+            __builtin_amdgcn_sched_barrier(0);
             if (ks + 2 < KSTEPS)
                 read_k(buf, ks + 2, fa);
             if (ks + 1 < KSTEPS)
                 mfmas(fb);
+            if (ks + 2 < KSTEPS)
+                sched();
+            __builtin_amdgcn_sched_barrier(0);
         }
     };
 
