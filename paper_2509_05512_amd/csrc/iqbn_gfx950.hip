@@ -32,6 +32,9 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kMaxBlocks = 512;  // partial-statistics blocks per column group (grid.x)
+// blocks per column group of the element-wise passes (normalization and the
+// input gradient), which keep no partials: four work-groups per compute unit
+constexpr int kStreamBlocks = 1024;
 constexpr int kMinRowsPerThread = 24;
 
 template <typename T, int VW>
@@ -52,7 +55,7 @@ struct Layout {
     int64_t rows_per_block;  // contiguous rows of one block
 };
 
-Layout make_layout(int64_t pixels, int c, int vw)
+Layout make_layout(int64_t pixels, int c, int vw, int cap = kMaxBlocks)
 {
     Layout l;
     l.pixels = pixels;
@@ -64,7 +67,7 @@ Layout make_layout(int64_t pixels, int c, int vw)
     l.col_groups = (l.chunks + l.cg - 1) / l.cg;
     const int64_t rows_per_iter_block = int64_t(l.rpi) * kMinRowsPerThread;
     int64_t want = (pixels + rows_per_iter_block - 1) / rows_per_iter_block;
-    int max_blocks = kMaxBlocks;  // per column group
+    int max_blocks = cap;  // per column group
     if (max_blocks < 1)
         max_blocks = 1;
     if (want > max_blocks)
@@ -611,12 +614,14 @@ hipError_t launch_backward(const void *x, const void *dout, const void *y, const
     const int fin_blocks = (l.row_len + kThreads / 64 - 1) / (kThreads / 64);
     hipLaunchKernelGGL(iqbn_bwd_finalize, dim3(fin_blocks), dim3(kThreads), 0, stream, l, (const float *)part,
                        var, gamma, eps, dgamma, dbeta, coef);
+    const Layout ls = make_layout(pixels, c, VW, kStreamBlocks);
+    const dim3 sgrid(ls.blocks, ls.col_groups);
     if (y != nullptr)
-        hipLaunchKernelGGL((iqbn_bwd_apply<T, VW, true>), grid, dim3(kThreads), 0, stream, xt, gt, yt,
-                           static_cast<T *>(dx), l, mean, var, eps, (const float *)coef);
+        hipLaunchKernelGGL((iqbn_bwd_apply<T, VW, true>), sgrid, dim3(kThreads), 0, stream, xt, gt, yt,
+                           static_cast<T *>(dx), ls, mean, var, eps, (const float *)coef);
     else
-        hipLaunchKernelGGL((iqbn_bwd_apply<T, VW, false>), grid, dim3(kThreads), 0, stream, xt, gt, yt,
-                           static_cast<T *>(dx), l, mean, var, eps, (const float *)coef);
+        hipLaunchKernelGGL((iqbn_bwd_apply<T, VW, false>), sgrid, dim3(kThreads), 0, stream, xt, gt, yt,
+                           static_cast<T *>(dx), ls, mean, var, eps, (const float *)coef);
     return hipGetLastError();
 }
 
@@ -634,12 +639,14 @@ hipError_t launch_all(const void *x, const float *gamma, const float *beta, floa
     const int fin_blocks = (l.row_len + kThreads / 64 - 1) / (kThreads / 64);
     hipLaunchKernelGGL((iqbn_finalize<T>), dim3(fin_blocks), dim3(kThreads), 0, stream, xt, l, part,
                        gamma, beta, eps, mean, var, affine);
+    const Layout ls = make_layout(pixels, c, VW, kStreamBlocks);
+    const dim3 sgrid(ls.blocks, ls.col_groups);
     if (relu)
-        hipLaunchKernelGGL((iqbn_affine<T, VW, true>), grid, dim3(kThreads), 0, stream, xt,
-                           static_cast<T *>(out), l, (const float *)affine);
+        hipLaunchKernelGGL((iqbn_affine<T, VW, true>), sgrid, dim3(kThreads), 0, stream, xt,
+                           static_cast<T *>(out), ls, (const float *)affine);
     else
-        hipLaunchKernelGGL((iqbn_affine<T, VW, false>), grid, dim3(kThreads), 0, stream, xt,
-                           static_cast<T *>(out), l, (const float *)affine);
+        hipLaunchKernelGGL((iqbn_affine<T, VW, false>), sgrid, dim3(kThreads), 0, stream, xt,
+                           static_cast<T *>(out), ls, (const float *)affine);
     return hipGetLastError();
 }
 
@@ -652,12 +659,13 @@ hipError_t launch_from_tiles(const float *part, int m_tiles, int tile_rows, cons
     hipLaunchKernelGGL(iqbn_finalize_tiles, dim3(l.row_len), dim3(kThreads), 0, stream, part, m_tiles,
                        tile_rows, pixels, l.row_len, gamma, beta, eps, mean, var, affine);
     T *t = static_cast<T *>(io);
-    const dim3 grid(l.blocks, l.col_groups);
+    const Layout ls = make_layout(pixels, c, VW, kStreamBlocks);
+    const dim3 sgrid(ls.blocks, ls.col_groups);
     if (relu)
-        hipLaunchKernelGGL((iqbn_affine<T, VW, true>), grid, dim3(kThreads), 0, stream, t, t, l,
+        hipLaunchKernelGGL((iqbn_affine<T, VW, true>), sgrid, dim3(kThreads), 0, stream, t, t, ls,
                            (const float *)affine);
     else
-        hipLaunchKernelGGL((iqbn_affine<T, VW, false>), grid, dim3(kThreads), 0, stream, t, t, l,
+        hipLaunchKernelGGL((iqbn_affine<T, VW, false>), sgrid, dim3(kThreads), 0, stream, t, t, ls,
                            (const float *)affine);
     return hipGetLastError();
 }
