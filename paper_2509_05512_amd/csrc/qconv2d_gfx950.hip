@@ -808,17 +808,41 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + 2)) void qconv2d_igemm(KA
             // without one the accumulators are only rounded.
             auto park = [&](auto affine) {
                 constexpr bool AFFINE = decltype(affine)::value;
+                // the lane's per-column map of one 32-channel block, loaded
+                // before any of it is used (one memory latency per block,
+                // not per channel group); the four channels of a group are
+                // all inside c_out or all past it (c_out is a multiple of the
+                // 16-byte chunk here)
 #pragma unroll
                 for (int nb = 0; nb < NB; ++nb) {
+                    float sc[4][4], sh[4][4];
+                    if constexpr (AFFINE) {
+#pragma unroll
+                        for (int g = 0; g < 4; ++g) {
+                            const int oc = nb * 32 + 8 * g + 4 * khalf;
+                            const bool in4 = o0 + oc < a.c_out;
+                            const int col = in4 ? wn * a.c_out + o0 + oc : 0;
+                            if constexpr (EPI == kEpiFold) {
+                                const f32x4 s4 = *reinterpret_cast<const f32x4 *>(a.scale + col);
+                                const f32x4 h4 = *reinterpret_cast<const f32x4 *>(a.shift + col);
+#pragma unroll
+                                for (int e = 0; e < 4; ++e) {
+                                    sc[g][e] = in4 ? s4[e] : 0.0f;
+                                    sh[g][e] = in4 ? h4[e] : 0.0f;
+                                }
+                            } else {
+#pragma unroll
+                                for (int e = 0; e < 4; ++e) {
+                                    sc[g][e] = 1.0f;
+                                    const float b = float(bias[col + e]);
+                                    sh[g][e] = in4 ? b : 0.0f;
+                                }
+                            }
+                        }
+                    }
 #pragma unroll
                     for (int g = 0; g < 4; ++g) {
                         const int oc = nb * 32 + 8 * g + 4 * khalf;  // channel within the tile's BNC
-                        float sc[4], sh[4];
-                        if constexpr (AFFINE) {
-#pragma unroll
-                            for (int e = 0; e < 4; ++e)
-                                col_affine(wn * a.c_out + o0 + oc + e, o0 + oc + e < a.c_out, sc[e], sh[e]);
-                        }
 #pragma unroll
                         for (int mb = 0; mb < MB; ++mb) {
                             const int m = mb * 32 + l32;
@@ -826,7 +850,7 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + 2)) void qconv2d_igemm(KA
 #pragma unroll
                             for (int e = 0; e < 4; ++e) {
                                 if constexpr (AFFINE)
-                                    v[e] = T(epi(acc[0][nb][mb][4 * g + e], sc[e], sh[e]));
+                                    v[e] = T(epi(acc[0][nb][mb][4 * g + e], sc[g][e], sh[g][e]));
                                 else
                                     v[e] = T(acc[0][nb][mb][4 * g + e]);
                             }
