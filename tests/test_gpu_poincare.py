@@ -19,6 +19,8 @@ CASES = [
     (2, 17, 19, 1.0, "fp32"),
     (3, 12, 20, 1.0, "bf16"),     # plane of 240 pixels: four per thread
     (3, 12, 20, 1.0, "fp32"),
+    (2, 12, 21, 1.0, "bf16"),     # plane of 252 pixels (odd width): four per thread
+    (2, 9, 30, 1.0, "fp32"),      # plane of 270 pixels: one per thread
     (1, 1, 1, 1.0, "bf16"),       # one pixel
     (3, 8, 33, 20.0, "fp32"),     # far outside the unit cube: q_r near -1
     (1, 5, 7, 0.0, "bf16"),       # black: q = 1
