@@ -5,7 +5,9 @@ pads, dilations, channel counts off the vector width), its weight and bias
 gradients, and training-mode IQBN's gradients with and without ReLU.  The
 imagenet_stage layer's weight gradient is checked at full size on sampled
 (output, input) channel pairs: each pair's gradient depends only on that
-channel of x and of dy, so the oracle runs on one-channel slices."""
+channel of x and of dy, so the oracle runs on one-channel slices; its input
+gradient on sampled pixels (the oracle on the dy window around each), and
+IQBN's gradients at that size in full."""
 import numpy as np
 import pytest
 import torch
@@ -101,6 +103,64 @@ def test_backward_weight_full_imagenet_layer_sampled():
         assert_close(got[:, o, c], ref[:, 0, 0], torch.float32, f"dW imagenet (o={o}, c={c})")
     ref_b = dy64.sum(axis=(0, 3, 4))
     assert_close(f64(db.cpu()), ref_b, torch.float32, "dbias imagenet")
+
+
+def test_backward_data_full_imagenet_layer_sampled():
+    """The imagenet_stage layer's input gradient at full size (the launch the
+    bench times) on sampled input pixels: dX at (n, iy, ix) only depends on
+    the k x k window of dy around it, so the oracle runs on that window as
+    the gradient of a 1x1 input padded by k - 1 (window entries outside the
+    output are zero)."""
+    say("backward data full-size sampled")
+    from paper_2509_05512_amd import workloads
+    wl = workloads.WORKLOADS["imagenet_stage"]
+    tens = workloads.generate(wl)
+    layer = tens.layers[0]
+    L = wl.layers[0]
+    k, p = L.k, L.pad
+    dev = torch.device("cuda:0")
+    rng = np.random.default_rng(7)
+    dy = torch.from_numpy(rng.standard_normal((wl.n, 4, L.c_out, wl.h, wl.w), dtype=np.float32)).to(torch.bfloat16)
+    w = [layer.weight[q].contiguous() for q in range(4)]
+    dx = quan.quan_qconv2d_backward_data(quan.to_device_layout(dy.to(dev)), *[t.to(dev) for t in w],
+                                         (wl.h, wl.w), stride=1, pad=p)
+    torch.cuda.synchronize()
+    w64 = np.stack([f64(t) for t in w])
+    dy64 = f64(dy)
+    x1 = np.zeros((1, 4, L.c_in, 1, 1))
+    picks = [(0, 0, 0), (0, wl.h - 1, wl.w - 1), (wl.n - 1, 0, wl.w - 1), (wl.n - 1, wl.h - 1, 0)]
+    picks += [(int(rng.integers(wl.n)), int(rng.integers(wl.h)), int(rng.integers(wl.w))) for _ in range(28)]
+    for (n, iy, ix) in picks:
+        win = np.zeros((1, 4, L.c_out, k, k))
+        for a in range(k):
+            for b in range(k):
+                oy, ox = iy + p - (k - 1) + a, ix + p - (k - 1) + b
+                if 0 <= oy < wl.h and 0 <= ox < wl.w:
+                    win[0, :, :, a, b] = dy64[n, :, :, oy, ox]
+        ref, _, _ = oracle.qconv2d_backward(x1, w64, win, 1, k - 1, 1)
+        got = dx[n, :, :, iy, ix].double().cpu().numpy()
+        assert_close(got, ref[0, :, :, 0, 0], torch.bfloat16, f"dX imagenet ({n}, {iy}, {ix})")
+
+
+def test_iqbn_backward_full_imagenet_layer():
+    """Training-mode IQBN gradients at the imagenet_stage layer's full size
+    (64x56x56, 256 real channels, no ReLU) against the oracle in fp64."""
+    say("iqbn backward full size")
+    N, C, H, W = 64, 64, 56, 56
+    rng = np.random.default_rng(11)
+    x = torch.from_numpy((rng.standard_normal((N, 4, C, H, W), dtype=np.float32) * 1.5 + 0.25)).to(torch.bfloat16)
+    g = torch.from_numpy(rng.uniform(0.5, 1.5, (4, C)).astype(np.float32))
+    be = torch.from_numpy((rng.standard_normal((4, C)) * 0.3).astype(np.float32))
+    dout = torch.from_numpy(rng.standard_normal((N, 4, C, H, W), dtype=np.float32)).to(torch.bfloat16)
+    dev = torch.device("cuda:0")
+    xg = quan.to_device_layout(x.to(dev))
+    _, mean, var = quan.quan_iqbn_forward(xg, g.to(dev), be.to(dev))
+    dx, dg, db = quan.quan_iqbn_backward(xg, quan.to_device_layout(dout.to(dev)), mean, var, g.to(dev))
+    torch.cuda.synchronize()
+    ref_dx, ref_dg, ref_db = oracle.iqbn_backward(f64(x), f64(g), f64(be), f64(dout), 1e-5, False)
+    assert_close(f64(dx.cpu()), ref_dx, torch.bfloat16, "iqbn dX full size")
+    assert_close(f64(dg.cpu()), ref_dg, torch.bfloat16, "dgamma full size")
+    assert_close(f64(db.cpu()), ref_db, torch.bfloat16, "dbeta full size")
 
 
 def test_backward_weight_is_deterministic():
