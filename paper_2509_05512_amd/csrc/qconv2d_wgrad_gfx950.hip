@@ -10,18 +10,19 @@
 // both operands stored channels-last.  One work-group takes one tap, a
 // 64 x 64 tile of (output, input) channels and a contiguous slice of the
 // pixels; it stages 32-pixel chunks of dY (all four components) and of the
-// tap-shifted X (zero outside the image) in LDS, double-buffered, with the
-// global loads (16-byte buffer loads at 32-bit offsets, zeros past the end,
-// each thread's pixel coordinates advanced incrementally) issued two chunks
-// ahead, and its four waves each accumulate the four dW_m of one 32 x 32
-// (o, c) block, reading the next k-step's fragments while the MFMAs of the
-// current one run; a sign flip is one XOR per fragment dword.  The taps of one (slice, tile)
-// are placed on one XCD (work-group b runs on XCD b % 8), so the nine reads
-// of a slice of dY and its shifted copies of X share that XCD's L2.  MFMA
-// operands need eight consecutive pixels per lane: bf16 fragments come from
-// the pixel-major rows with two transposing LDS reads (ds_read_b64_tr_b16),
-// fp32 fragments (one pixel per lane) with plain reads.  Slices write fp32
-// partial sums; a second kernel adds them in slice order in fp64
+// tap-shifted X (zero outside the image) in LDS, bank-conflict free (see
+// kRowBf16) and double-buffered, with the global loads (16-byte buffer loads
+// at 32-bit offsets, zeros past the end, each thread's pixel coordinates
+// advanced incrementally) issued two chunks ahead; its four waves each
+// accumulate the four dW_m of one 32 x 32 (o, c) block, reading the next
+// k-step's fragments while the MFMAs of the current one run, a sign flip
+// being one XOR per fragment dword.  The taps of one (slice, tile) are placed
+// on one XCD (work-group b runs on XCD b % 8), so the nine reads of a slice
+// of dY and its shifted copies of X share that XCD's L2.  MFMA operands need
+// eight consecutive pixels per lane: bf16 fragments come from the pixel-major
+// rows with two transposing LDS reads (ds_read_b64_tr_b16), fp32 fragments
+// (one pixel per lane) with plain reads.  Slices write fp32 partial sums; a
+// second kernel adds them in slice order in fp64
 // (deterministic) into dW.  The bias gradient is the column sum of dY.
 #include <hip/hip_runtime.h>
 
@@ -45,7 +46,13 @@ constexpr int kThreads = 256;
 constexpr int kTileO = 64;   // output channels per work-group
 constexpr int kTileC = 64;   // input channels per work-group
 constexpr int kChunk = 32;   // pixels per staged chunk
-constexpr int kRow = 80;     // LDS row length in elements (64 + 16: conflict-free transposing reads)
+// LDS rows of a staged chunk: bf16 rows are 64 elements (128 bytes) with the
+// 16-byte chunks of rows 2..3 mod 4 XOR-swizzled by 4, so that neither the
+// row-wise 16-byte stores nor the transposing 8-byte reads (four rows of
+// one 64-byte column group per 16 lanes) meet in a bank; fp32 rows are
+// padded to 80 elements.
+constexpr int kRowBf16 = 64, kRowF32 = 80;
+__device__ __forceinline__ int chunk_swz(int row) { return 4 * ((row >> 1) & 1); }
 
 struct WArgs {
     const void *x, *dy;
@@ -110,6 +117,7 @@ template <typename T, bool VEC>
 __global__ __launch_bounds__(kThreads) void qconv2d_wgrad(WArgs a)
 {
     constexpr int ES = int(sizeof(T));
+    constexpr int kRow = ES == 2 ? kRowBf16 : kRowF32;
     constexpr int EPC = 16 / ES;               // elements per 16-byte chunk
     constexpr int CPR = kTileO / EPC;          // chunks per (component, pixel) row of the tile
     constexpr int PXT = kThreads / CPR;        // pixels one pass of the threads covers
@@ -219,7 +227,8 @@ __global__ __launch_bounds__(kThreads) void qconv2d_wgrad(WArgs a)
             for (int i = 0; i < PASSES; ++i)
 #pragma unroll
                 for (int q = 0; q < 4; ++q)
-                    *reinterpret_cast<u32x4 *>(base + t * TENSOR + q * COMP + (pr + PXT * i) * kRow + cc * EPC) =
+                    *reinterpret_cast<u32x4 *>(base + t * TENSOR + q * COMP + (pr + PXT * i) * kRow +
+                                               (ES == 2 ? (cc ^ chunk_swz(pr + PXT * i)) : cc) * EPC) =
                         st.v[t][i][q];
     };
 
@@ -241,7 +250,9 @@ __global__ __launch_bounds__(kThreads) void qconv2d_wgrad(WArgs a)
             // two transposing reads of rows 16ks + 8(g/2) + 4r + j, columns
             // col0 + 16(g%2) + 4a (g = l/16, a = l%4, j = (l%16)/4)
             const int g = lane >> 4, aa = lane & 3, j = (lane & 15) >> 2;
-            const T *p0 = base + comp * COMP + (16 * ks + 8 * (g >> 1) + j) * kRow + col0 + 16 * (g & 1) + 4 * aa;
+            const int row = 16 * ks + 8 * (g >> 1) + j, col = col0 + 16 * (g & 1) + 4 * aa;
+            // rows row and row + 4 share the swizzle
+            const T *p0 = base + comp * COMP + row * kRow + (((col >> 3) ^ chunk_swz(row)) << 3) + (col & 7);
             const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
                 (__attribute__((address_space(3))) s16x4 *)(p0));
             const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
