@@ -20,7 +20,8 @@ Prints ONE JSON line:
                dense MFMA peak (2516.6 TFLOP/s)
   iqbn         the stand-alone IQBN (stats + finalize + affine): GB/s of
                algorithmic traffic (two reads + one write of the tensor) and
-               fraction of 8 TB/s
+               fraction of 8 TB/s, in the step (input just written by the
+               convolution) and cold (input evicted from the caches first)
   roofline     the dominant kernel (the convolution) against its roofline,
                timed with HIP events on the stream it runs on
   cpu_baseline the CPU oracle timed on a bounded sample of the same workload
@@ -160,6 +161,30 @@ def time_separable(layers, quan, steps):
     end.record()
     torch.cuda.synchronize()
     return start.elapsed_time(end) * 1e3 / steps
+
+
+def time_iqbn_cold(layers, quan, steps, eps):
+    """The stand-alone IQBN of every layer with its input evicted from the
+    caches first: before each timed rep a 512 MiB buffer is read (twice the
+    256 MB Infinity Cache; a read leaves no dirty lines whose write-back would
+    land inside the timed region).  Median microseconds per step."""
+    import torch
+    dev = layers[0]["y"].device
+    flush_buf = torch.zeros(128 * 2**20, dtype=torch.float32, device=dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    times = []
+    for _ in range(max(steps, 5)):
+        flush_buf.sum()
+        e0.record()
+        for ly in layers:
+            fn = quan.quan_iqbn_relu_forward if ly["spec"].relu else quan.quan_iqbn_forward
+            fn(ly["y"], ly["gamma"], ly["beta"], eps, out=ly["z"], mean=ly["mean"], var=ly["var"])
+        e1.record()
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1) * 1e3)
+    del flush_buf
+    times.sort()
+    return times[len(times) // 2]
 
 
 def time_backward(layers, quan, steps, eps):
@@ -386,6 +411,8 @@ def main():
     conv_tflops = step_flops / (sum(conv_ms) * 1e-3) / 1e12
     peak = MFMA_PEAK_TFLOPS[wl.dtype]
     iqbn_gbps = sum(iqbn_bytes) / (sum(iqbn_ms) * 1e-3) / 1e9
+    iqbn_cold_us = time_iqbn_cold(layers, quan, args.steps, wl.eps)
+    iqbn_cold_gbps = sum(iqbn_bytes) / (iqbn_cold_us * 1e-6) / 1e9
     per_layer = []
     for li, L in enumerate(wl.layers):
         per_layer.append({
@@ -451,9 +478,14 @@ def main():
             "pack_us_per_step": round(sum(pack_ms) * 1e3, 3),
         },
         "iqbn": {
+            # in the step: the tensor was just written by the convolution
             "gbps": round(iqbn_gbps, 1),
             "frac_hbm_peak": round(iqbn_gbps / HBM_PEAK_GBPS, 4),
             "us_per_step": round(sum(iqbn_ms) * 1e3, 3),
+            # with the tensor evicted from L2 and the Infinity Cache first
+            "cold_gbps": round(iqbn_cold_gbps, 1),
+            "cold_frac_hbm_peak": round(iqbn_cold_gbps / HBM_PEAK_GBPS, 4),
+            "cold_us_per_step": round(iqbn_cold_us, 3),
         },
         "per_layer": per_layer,
         "roofline": {
