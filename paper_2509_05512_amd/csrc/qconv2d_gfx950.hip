@@ -24,13 +24,13 @@
 //     block is formed on the LDS->register read: the fragment for (output
 //     component p, input component q) reads kernel p xor q and flips its
 //     sign bits with one XOR;
-//   - the work-group is four compute waves and two producer waves.  The
-//     producers move stages from global memory straight into LDS
-//     (buffer_load ... lds, 1 KB per instruction; each producer moves half
-//     of every stage), three stages ahead of the compute waves, into a
-//     four-stage ring.  One wave can keep at most 63 loads in flight (its
-//     6-bit vmcnt), too few to cover the latency at this bandwidth, hence two
-//     producers.  Rows outside the image
+//   - the work-group is four compute waves and two producer waves (four
+//     for the separable form and narrow tiles).  The producers move stages from global
+//     memory straight into LDS (buffer_load ... lds, 1 KB per instruction;
+//     each producer moves its share of every stage), three stages ahead of
+//     the compute waves, into a four-stage ring.  One wave can keep at most
+//     63 loads in flight (its 6-bit vmcnt), too few to cover the latency at
+//     this bandwidth, hence more than one producer.  Rows outside the image
 //     read past the buffer range and land as zeros.  Compute waves only read
 //     fragments from LDS and issue MFMAs, one fragment read between
 //     consecutive MFMAs (a burst of LDS reads stalls the matrix pipe);
@@ -249,15 +249,30 @@ __device__ __forceinline__ void wait_vmcnt()
 // The tile is BM pixels x BN/4 = 32*NB*WAVES_N output channels, all four
 // output components.
 enum : int { kEpiBias = 0, kEpiStats = 1, kEpiFold = 2 };
+// Producer waves per work-group.  A tile with few MFMAs per stage (the
+// separable form, a quarter of the Hamilton MFMAs; tiles of 32 or fewer
+// output channels) runs at the pace of its activation loads, and four
+// producers, each issuing half as many DMA instructions per stage, make it
+// 3-33% faster; the 64-channel Hamilton tile gains nothing and keeps two.
+// Four need every stage's activation and weight DMAs to split evenly.
+template <typename T, int MB, int NB, int WM, int WN, bool SEP>
+constexpr int producer_waves()
+{
+    constexpr int bnc = SEP ? 32 * NB * WN : 8 * NB * WN;  // output channels per tile
+    constexpr int cs = 128 / (4 * int(sizeof(T)));         // channels per stage
+    constexpr int a_instr = 32 * MB * WM / 8;
+    constexpr int b_instr = 4 * bnc * cs * int(sizeof(T)) / 1024;
+    return ((SEP || bnc <= 32) && a_instr % 4 == 0 && b_instr % 4 == 0) ? 4 : 2;
+}
 template <typename T, int MB, int NB, int WAVES_M, int WAVES_N, bool VEC, int EPI, bool SEP>
-__global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + 2)) void qconv2d_igemm(KArgs a)
+__global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB, WAVES_M, WAVES_N, SEP>())) void qconv2d_igemm(KArgs a)
 {
     constexpr int ES = int(sizeof(T));
     constexpr int EPC = Elem<T>::per_chunk;
     constexpr int CS = stage_channels<T>();
     constexpr int CPQ = CS / EPC;  // 16-byte chunks per component (2)
     constexpr int NCW = WAVES_M * WAVES_N;
-    constexpr int NPROD = 2;                    // producer waves
+    constexpr int NPROD = producer_waves<T, MB, NB, WAVES_M, WAVES_N, SEP>();
     constexpr int WTM = 32 * MB;
     constexpr int WTN = 32 * NB;
     constexpr int BM = WTM * WAVES_M;
@@ -279,6 +294,8 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + 2)) void qconv2d_igemm(KA
     static_assert(BNC % 16 == 0 && kPackCoutAlign % BNC == 0 && B_BYTES % 1024 == 0, "tile geometry");
     static_assert(LOOKAHEAD * PER_STAGE <= 63, "the stages in flight must fit the vmcnt counter");
     static_assert(A_INSTR % NPROD == 0 && B_INSTR % NPROD == 0, "producers split every stage evenly");
+    static_assert(BNC == (SEP ? 32 * NB * WAVES_N : 8 * NB * WAVES_N) && CS == 128 / (4 * ES),
+                  "producer_waves sees the tile geometry");
 
     // Deferred epilogue (DEFER): when a wave holds one output component for
     // all BM pixels, it parks each finished tile in its own LDS region and
@@ -1076,7 +1093,7 @@ constexpr const void *stats_fn()
 #define QCONV_K(T, DT, MB, NB, WM, WN, SEP)                                                            \
     KernelEntry                                                                                        \
     {                                                                                                  \
-        32 * (MB) * (WM), ((SEP) ? 32 : 8) * (NB) * (WN), MB, NB, 64 * ((WM) * (WN) + 2), SEP,         \
+        32 * (MB) * (WM), ((SEP) ? 32 : 8) * (NB) * (WN), MB, NB, 64 * ((WM) * (WN) + producer_waves<T, MB, NB, WM, WN, SEP>()), SEP, \
             QCONV_DEFER(NB, WM, WN, SEP), DT,                                                          \
             {{(const void *)&qconv2d_igemm<T, MB, NB, WM, WN, true, kEpiBias, SEP>,                    \
               (const void *)&qconv2d_igemm<T, MB, NB, WM, WN, false, kEpiBias, SEP>},                  \
