@@ -248,6 +248,15 @@ __device__ __forceinline__ void wait_vmcnt()
 // Hamilton MFMAs), and the epilogue mixes y_p = sum_q S[p][q] c_q in fp32.
 // The tile is BM pixels x BN/4 = 32*NB*WAVES_N output channels, all four
 // output components.
+//
+// PAIR (separable form, bf16, c_in a multiple of 32): a stage's 128-byte
+// activation row is 32 channels of two input components (q = 2*pair,
+// 2*pair + 1) instead of 16 channels of all four, so every 64-byte request
+// the L1 sends to L2 is fully used (half the requests per stage).  The
+// stages of a tap alternate pair 0 and 1 over the 32-channel blocks; the
+// separable form needs only W_q beside x_q, so a stage's weights are still
+// four 16-channel row groups (kernel 2*pair + g/2, channel half g%2).
+// K-step j of a stage then belongs to component 2*pair + j/2.
 enum : int { kEpiBias = 0, kEpiStats = 1, kEpiFold = 2 };
 // Producer waves per work-group.  A tile with few MFMAs per stage (the
 // separable form, a quarter of the Hamilton MFMAs; tiles of 32 or fewer
@@ -264,7 +273,7 @@ constexpr int producer_waves()
     constexpr int b_instr = 4 * bnc * cs * int(sizeof(T)) / 1024;
     return ((SEP || bnc <= 32) && a_instr % 4 == 0 && b_instr % 4 == 0) ? 4 : 2;
 }
-template <typename T, int MB, int NB, int WAVES_M, int WAVES_N, bool VEC, int EPI, bool SEP>
+template <typename T, int MB, int NB, int WAVES_M, int WAVES_N, bool VEC, int EPI, bool SEP, bool PAIR = false>
 __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB, WAVES_M, WAVES_N, SEP>())) void qconv2d_igemm(KArgs a)
 {
     constexpr int ES = int(sizeof(T));
@@ -294,6 +303,7 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
     static_assert(BNC % 16 == 0 && kPackCoutAlign % BNC == 0 && B_BYTES % 1024 == 0, "tile geometry");
     static_assert(LOOKAHEAD * PER_STAGE <= 63, "the stages in flight must fit the vmcnt counter");
     static_assert(A_INSTR % NPROD == 0 && B_INSTR % NPROD == 0, "producers split every stage evenly");
+    static_assert(!PAIR || (SEP && VEC && ES == 2), "paired stages: separable bf16 with 16-byte chunks");
     static_assert(BNC == (SEP ? 32 * NB * WAVES_N : 8 * NB * WAVES_N) && CS == 128 / (4 * ES),
                   "producer_waves sees the tile geometry");
 
@@ -355,6 +365,7 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
         unsigned x_bytes = 0;  // bytes of x from xt on (capped at 2^31 - 1)
         int p_off[A_MINE], p_iy[A_MINE], p_ix[A_MINE], p_cl[A_MINE];
         unsigned p_woff[B_MINE];
+        int p_wodd[B_MINE];  // PAIR: the instruction's channel half
         // Activation DMA i covers rows 8i..8i+7 of the tile: lane l loads
         // row 8i + l/8 into physical chunk l%8, i.e. logical chunk
         // lc = (l%8) ^ swz(row): component lc/2, channels 8*(lc%2).. of the
@@ -375,7 +386,8 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
                 const int i = ii * NPROD + pr;  // instruction index within the stage
                 const int row = 8 * i + (lane >> 3);
                 const int lc = (lane & 7) ^ swz<8>(row);
-                const int comp = lc / CPQ, cin = (lc % CPQ) * EPC;
+                // PAIR: chunks 0-3 are component 2*pair, 4-7 component 2*pair+1
+                const int comp = PAIR ? lc / 4 : lc / CPQ, cin = PAIR ? (lc % 4) * EPC : (lc % CPQ) * EPC;
                 const int m = m0 + row;
                 p_cl[ii] = a.c_in - cin;  // channels of this chunk left before block 0
                 if (m < a.m) {
@@ -401,7 +413,14 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
                 const int row = slot / CPQ;
                 const int lc = (slot % CPQ) ^ swz<CPQ>(row);
                 const int ws = row / BNC, o = row - (row / BNC) * BNC;
-                p_woff[jj] = unsigned(((ws * a.cout_pad + o0 + o) * CS + lc * EPC) * ES);
+                if constexpr (PAIR) {
+                    // row group ws: kernel 2*pair + ws/2 of channel block
+                    // 2*(cblk/2) + ws%2 (one group per instruction)
+                    p_woff[jj] = unsigned((((ws >> 1) * a.cout_pad + o0 + o) * CS + lc * EPC) * ES);
+                    p_wodd[jj] = ws & 1;
+                } else {
+                    p_woff[jj] = unsigned(((ws * a.cout_pad + o0 + o) * CS + lc * EPC) * ES);
+                }
             }
         };
         plan_tile(0);
@@ -411,11 +430,20 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
             const int buf = g & (NBUF - 1);
             const int t = (ky * a.k_w + kx) * a.n_cblk + cblk;  // stage within the tile
 #pragma unroll
-            for (int jj = 0; jj < B_MINE; ++jj)
-                dma16(a.wpack, a.w_bytes, p_woff[jj], unsigned(t) * w_stage_bytes,
-                      b_base + buf * B_BYTES + (jj * NPROD + pr) * 1024);
-            const int dy = ky * a.d_h, dx = kx * a.d_w, cbase = cblk * CS;
-            const int shift = (dy * a.w + dx) * row_elems + cbase;  // elements
+            for (int jj = 0; jj < B_MINE; ++jj) {
+                if constexpr (PAIR)
+                    dma16(a.wpack, a.w_bytes, p_woff[jj],
+                          unsigned(t - (cblk & 1) + p_wodd[jj]) * w_stage_bytes +
+                              unsigned(cblk & 1) * (w_stage_bytes / 2),
+                          b_base + buf * B_BYTES + (jj * NPROD + pr) * 1024);
+                else
+                    dma16(a.wpack, a.w_bytes, p_woff[jj], unsigned(t) * w_stage_bytes,
+                          b_base + buf * B_BYTES + (jj * NPROD + pr) * 1024);
+            }
+            // PAIR: stage cblk is channels 32*(cblk/2).. of components
+            // 2*(cblk%2) and 2*(cblk%2) + 1
+            const int dy = ky * a.d_h, dx = kx * a.d_w, cbase = PAIR ? (cblk >> 1) * 2 * CS : cblk * CS;
+            const int shift = (dy * a.w + dx) * row_elems + cbase + (PAIR ? (cblk & 1) * 2 * a.c_in : 0);  // elements
 #pragma unroll
             for (int ii = 0; ii < A_MINE; ++ii) {
                 const int i = ii * NPROD + pr;
@@ -607,22 +635,27 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
         read_frags(0, 1, f1);
     auto step_sep = [&](auto slot) {
         constexpr int B = decltype(slot)::value;
+        // accumulator set of k-step j: component j, or with paired stages
+        // component 2*pair + j/2, pair = the stage's parity (every tile has
+        // an even number of stages, so it equals the ring slot's)
+        constexpr int QA0 = PAIR ? 2 * (B & 1) : 0, QA1 = PAIR ? 2 * (B & 1) : 1;
+        constexpr int QA2 = PAIR ? 2 * (B & 1) + 1 : 2, QA3 = PAIR ? 2 * (B & 1) + 1 : 3;
         __builtin_amdgcn_sched_barrier(0);
         read_frags(B, 2, fc);
-        mfmas(0, f0);
+        mfmas(QA0, f0);
         interleave_kstep<N_MFMA, 0, N_READ, 1>();
         __builtin_amdgcn_sched_barrier(0);
         read_frags(B, 3, fd);
-        mfmas(1, f1);
+        mfmas(QA1, f1);
         interleave_kstep<N_MFMA, 0, N_READ, 1>();
         __builtin_amdgcn_sched_barrier(0);
         __syncthreads();
         read_frags((B + 1) & (NBUF - 1), 0, f0);
-        mfmas(2, fc);
+        mfmas(QA2, fc);
         interleave_kstep<N_MFMA, 0, N_READ, 1>();
         __builtin_amdgcn_sched_barrier(0);
         read_frags((B + 1) & (NBUF - 1), 1, f1);
-        mfmas(3, fd);
+        mfmas(QA3, fd);
         interleave_kstep<N_MFMA, 0, N_READ, 1>();
         __builtin_amdgcn_sched_barrier(0);
     };
@@ -1071,11 +1104,12 @@ struct KernelEntry {
     bool sep;    // separable convolution (eq. 7) instead of the Hamilton product
     bool defer;  // deferred epilogue (one output component per wave); writes IQBN statistics
     DType dt;
-    // [epilogue kind][masked]: masked = 0 when c_in is a multiple of the
+    // [epilogue kind][variant]: variant 0 when c_in is a multiple of the
     // 16-byte vector (activations move by DMA), 1 for element loads with
-    // channel masking; NULL where the kind does not apply (statistics need
+    // channel masking, 2 for paired stages (separable bf16, c_in a multiple
+    // of 32); NULL where the kind or variant does not apply (statistics need
     // the deferred epilogue).
-    const void *fn[3][2];
+    const void *fn[3][3];
     const char *name;
 };
 
@@ -1090,16 +1124,28 @@ constexpr const void *stats_fn()
         return nullptr;
 }
 #define QCONV_STATS_FN(T, MB, NB, WM, WN, VEC, SEP) stats_fn<T, MB, NB, WM, WN, VEC, SEP>()
+// the paired-stage variant exists only for the separable form in bf16
+template <typename T, int MB, int NB, int WM, int WN, int EPI, bool SEP>
+constexpr const void *pair_fn()
+{
+    if constexpr (SEP && sizeof(T) == 2 && EPI != kEpiStats)
+        return (const void *)&qconv2d_igemm<T, MB, NB, WM, WN, true, EPI, SEP, true>;
+    else
+        return nullptr;
+}
 #define QCONV_K(T, DT, MB, NB, WM, WN, SEP)                                                            \
     KernelEntry                                                                                        \
     {                                                                                                  \
         32 * (MB) * (WM), ((SEP) ? 32 : 8) * (NB) * (WN), MB, NB, 64 * ((WM) * (WN) + producer_waves<T, MB, NB, WM, WN, SEP>()), SEP, \
             QCONV_DEFER(NB, WM, WN, SEP), DT,                                                          \
             {{(const void *)&qconv2d_igemm<T, MB, NB, WM, WN, true, kEpiBias, SEP>,                    \
-              (const void *)&qconv2d_igemm<T, MB, NB, WM, WN, false, kEpiBias, SEP>},                  \
-             {QCONV_STATS_FN(T, MB, NB, WM, WN, true, SEP), QCONV_STATS_FN(T, MB, NB, WM, WN, false, SEP)}, \
+              (const void *)&qconv2d_igemm<T, MB, NB, WM, WN, false, kEpiBias, SEP>,                   \
+              pair_fn<T, MB, NB, WM, WN, kEpiBias, SEP>()},                                              \
+             {QCONV_STATS_FN(T, MB, NB, WM, WN, true, SEP), QCONV_STATS_FN(T, MB, NB, WM, WN, false, SEP), \
+              nullptr},                                                                                  \
              {(const void *)&qconv2d_igemm<T, MB, NB, WM, WN, true, kEpiFold, SEP>,                    \
-              (const void *)&qconv2d_igemm<T, MB, NB, WM, WN, false, kEpiFold, SEP>}},                 \
+              (const void *)&qconv2d_igemm<T, MB, NB, WM, WN, false, kEpiFold, SEP>,                   \
+              pair_fn<T, MB, NB, WM, WN, kEpiFold, SEP>()}},                                             \
             #T "_mb" #MB "x" #WM "_nb" #NB "x" #WN #SEP                                                \
     }
 
@@ -1136,9 +1182,9 @@ int device_cus()
 // at least 1).
 int resident_wgs(const void *fn, int threads)
 {
-    static const void *fns[6 * kNumKernels] = {};
-    static int counts[6 * kNumKernels] = {};
-    for (int i = 0; i < 6 * kNumKernels; ++i) {
+    static const void *fns[9 * kNumKernels] = {};
+    static int counts[9 * kNumKernels] = {};
+    for (int i = 0; i < 9 * kNumKernels; ++i) {
         if (fns[i] == fn)
             return counts[i];
         if (fns[i] == nullptr) {
@@ -1378,7 +1424,8 @@ hipError_t qconv2d_run(const ConvPlan &plan, const PackGeom &pg, const ConvGeom 
         return hipErrorInvalidValue;
     void *args[] = {&a};
     const int epi = stats != nullptr ? kEpiStats : fold != nullptr ? kEpiFold : kEpiBias;
-    const void *fn = k.fn[epi][(g.c_in % epc) == 0 ? 0 : 1];
+    const bool paired = k.fn[epi][2] != nullptr && g.c_in % 32 == 0;
+    const void *fn = k.fn[epi][(g.c_in % epc) != 0 ? 1 : paired ? 2 : 0];
     if (fn == nullptr)
         return hipErrorInvalidValue;
     // Persistent grid: as many work-groups as fit on the device at once, at
