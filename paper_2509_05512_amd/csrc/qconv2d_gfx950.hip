@@ -965,6 +965,63 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
                         dst[e] = v[e];
             }
         };
+        if constexpr (SEP && sizeof(T) == 2 && NB == 2) {
+            if (vec_out && (a.c_out & 7) == 0) {
+                // Separable bf16, 64-channel tile, whole 8-channel groups:
+                // for channel groups g0 = 2t and g1 = 2t+1 lane l (l < 32)
+                // holds channels 8*g0 + 0..3 and 8*g1 + 0..3 of pixel l,
+                // lane l+32 the channels 4..7 of both.  One v_permlane32_swap
+                // per dword hands lane l the upper half of g0 and lane l+32
+                // the lower half of g1, so every lane stores 8 channels (16
+                // bytes): 3-9% faster here, 40% slower on the 32-channel
+                // tile, which keeps the 8-byte stores.
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb) {
+#pragma unroll
+                    for (int t = 0; t < 2; ++t) {
+#pragma unroll
+                        for (int mb = 0; mb < MB; ++mb) {
+                            const int m = m0 + wm * WTM + mb * 32 + l32;
+#pragma unroll
+                            for (int p = 0; p < 4; ++p) {
+                                unsigned h[2][2];  // [g - 2t][dword]: bf16 channel pairs
+#pragma unroll
+                                for (int gh = 0; gh < 2; ++gh) {
+                                    const int g = 2 * t + gh;
+                                    const int o = o0 + wn * WTN + nb * 32 + 8 * g + 4 * khalf;
+                                    T v[4];
+#pragma unroll
+                                    for (int e = 0; e < 4; ++e) {
+                                        // eq. 7: y_p = sum_q S[p][q] c_q, in fp32
+                                        float y = 0.0f;
+#pragma unroll
+                                        for (int q = 0; q < 4; ++q) {
+                                            const float c = acc[q][nb][mb][4 * g + e];
+                                            y = ((kSeparableNeg >> (4 * p + q)) & 1u) ? y - c : y + c;
+                                        }
+                                        float sc, sh;
+                                        col_affine(p * a.c_out + o + e, o + e < a.c_out, sc, sh);
+                                        v[e] = T(epi(y, sc, sh));
+                                    }
+                                    __builtin_memcpy(h[gh], v, 8);
+                                }
+#pragma unroll
+                                for (int d = 0; d < 2; ++d) {
+                                    const auto r = __builtin_amdgcn_permlane32_swap(h[0][d], h[1][d], false, false);
+                                    h[0][d] = r[0];
+                                    h[1][d] = r[1];
+                                }
+                                const int o8 = o0 + wn * WTN + nb * 32 + 8 * (2 * t + khalf);
+                                if (m < a.m && o8 < a.c_out)
+                                    *reinterpret_cast<u32x4 *>(out + ((size_t)m * 4 * a.c_out + p * a.c_out + o8)) =
+                                        u32x4{h[0][0], h[0][1], h[1][0], h[1][1]};
+                            }
+                        }
+                    }
+                }
+                continue;
+            }
+        }
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
 #pragma unroll
