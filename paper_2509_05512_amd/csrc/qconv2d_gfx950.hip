@@ -1185,10 +1185,20 @@ constexpr const void *stats_fn()
 template <typename T, int MB, int NB, int WM, int WN, int EPI, bool SEP>
 constexpr const void *pair_fn()
 {
-    if constexpr (SEP && sizeof(T) == 2 && EPI != kEpiStats)
+    if constexpr (SEP && sizeof(T) == 2 && EPI == kEpiBias)
         return (const void *)&qconv2d_igemm<T, MB, NB, WM, WN, true, EPI, SEP, true>;
     else
         return nullptr;
+}
+// the folded-IQBN epilogue serves the Hamilton form only (inference
+// convolution + IQBN); the separable form has a bias epilogue
+template <typename T, int MB, int NB, int WM, int WN, bool VEC, bool SEP>
+constexpr const void *fold_fn()
+{
+    if constexpr (SEP)
+        return nullptr;
+    else
+        return (const void *)&qconv2d_igemm<T, MB, NB, WM, WN, VEC, kEpiFold, SEP>;
 }
 #define QCONV_K(T, DT, MB, NB, WM, WN, SEP)                                                            \
     KernelEntry                                                                                        \
@@ -1200,8 +1210,8 @@ constexpr const void *pair_fn()
               pair_fn<T, MB, NB, WM, WN, kEpiBias, SEP>()},                                              \
              {QCONV_STATS_FN(T, MB, NB, WM, WN, true, SEP), QCONV_STATS_FN(T, MB, NB, WM, WN, false, SEP), \
               nullptr},                                                                                  \
-             {(const void *)&qconv2d_igemm<T, MB, NB, WM, WN, true, kEpiFold, SEP>,                    \
-              (const void *)&qconv2d_igemm<T, MB, NB, WM, WN, false, kEpiFold, SEP>,                   \
+             {fold_fn<T, MB, NB, WM, WN, true, SEP>(),                                                 \
+              fold_fn<T, MB, NB, WM, WN, false, SEP>(),                                                \
               pair_fn<T, MB, NB, WM, WN, kEpiFold, SEP>()}},                                             \
             #T "_mb" #MB "x" #WM "_nb" #NB "x" #WN #SEP                                                \
     }
