@@ -23,10 +23,14 @@
 // rows with two transposing LDS reads (ds_read_b64_tr_b16), fp32 fragments
 // (one pixel per lane) with plain reads.  Slices write fp32 partial sums; a
 // second kernel adds them in slice order in fp64
-// (deterministic) into dW.  The bias gradient is the column sum of dY.
+// (deterministic) into dW.  Layers of at most 16 channels run the kernel on
+// whole pixel rows (one component of 4*C channels) for the dense product of
+// all sixteen component pairs, and the reduction forms dW from it.  The bias
+// gradient is the column sum of dY.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <type_traits>
 
 #include "quan_launch.h"
 
@@ -113,9 +117,17 @@ __device__ __forceinline__ u32x4 load16(const void *base, unsigned bytes, unsign
     return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
 }
 
-template <typename T, bool VEC>
+// NC: components per pixel row as the kernel sees it.  4: the Hamilton
+// form above.  1 (layers of at most 16 channels): the whole pixel row is one
+// component of 4*C channels (a.c_out, a.c_in are then 4*C), and the kernel
+// computes the dense product G[(p,o)][(q,c)] = sum_pix dY[pix][p][o]
+// X[pix+tap][q][c] of which the reduction forms every dW_m; on a 64 x 64
+// tile this does the useful work once instead of sixteen times.
+template <typename T, bool VEC, int NC>
 __global__ __launch_bounds__(kThreads) void qconv2d_wgrad(WArgs a)
 {
+    static_assert(NC == 4 || NC == 1, "four components or one dense row");
+    constexpr int NM = NC == 4 ? 4 : 1;        // accumulator sets: dW_m, or G
     constexpr int ES = int(sizeof(T));
     constexpr int kRow = ES == 2 ? kRowBf16 : kRowF32;
     constexpr int EPC = 16 / ES;               // elements per 16-byte chunk
@@ -123,7 +135,7 @@ __global__ __launch_bounds__(kThreads) void qconv2d_wgrad(WArgs a)
     constexpr int PXT = kThreads / CPR;        // pixels one pass of the threads covers
     constexpr int PASSES = kChunk / PXT;
     constexpr int COMP = kChunk * kRow;        // elements per component block of a tensor in LDS
-    constexpr int TENSOR = 4 * COMP;
+    constexpr int TENSOR = NC * COMP;
     constexpr int BUF = 2 * TENSOR;            // dY then X
     static_assert(kTileO == kTileC && PXT * PASSES == kChunk, "tile geometry");
     __shared__ __attribute__((aligned(16))) T lds[2 * BUF];
@@ -154,7 +166,7 @@ __global__ __launch_bounds__(kThreads) void qconv2d_wgrad(WArgs a)
     // ---- staging: thread t moves chunk t % CPR of pixel rows t / CPR + PXT * i
     const int cc = tid % CPR, pr = tid / CPR;
     struct Staged {
-        u32x4 v[2][PASSES][4];  // [tensor][pass][component]
+        u32x4 v[2][PASSES][NC];  // [tensor][pass][component]
     };
     // VEC: 16-byte buffer loads at 32-bit offsets from the slice's first
     // pixel (dY) and first image (X), zeros past a buffer's end; each pass
@@ -162,10 +174,10 @@ __global__ __launch_bounds__(kThreads) void qconv2d_wgrad(WArgs a)
     // fetch, so chunks are fetched in order.
     const int span = int(pix1 - pix0 > 0 ? pix1 - pix0 : 0);
     const int64_t img0 = pix0 / hw_out;
-    const T *const dy_s = dy + pix0 * 4 * a.c_out;
-    const T *const x_s = x + img0 * int64_t(a.h) * a.w * 4 * a.c_in;
-    const unsigned dy_bytes = unsigned(int64_t(span) * 4 * a.c_out * ES);
-    const int64_t x_left = (int64_t(a.n) - img0) * a.h * a.w * 4 * a.c_in * ES;
+    const T *const dy_s = dy + pix0 * NC * a.c_out;
+    const T *const x_s = x + img0 * int64_t(a.h) * a.w * NC * a.c_in;
+    const unsigned dy_bytes = unsigned(int64_t(span) * NC * a.c_out * ES);
+    const int64_t x_left = (int64_t(a.n) - img0) * a.h * a.w * NC * a.c_in * ES;
     const unsigned x_bytes = unsigned(x_left < 0x7fffffffLL ? x_left : 0x7fffffffLL);
     const bool o_in = o0 + cc * EPC < a.c_out, c_in_ok = c0 + cc * EPC < a.c_in;
     int cur_img[PASSES], cur_oy[PASSES], cur_ox[PASSES];
@@ -186,21 +198,21 @@ __global__ __launch_bounds__(kThreads) void qconv2d_wgrad(WArgs a)
             const int iy = cur_oy[i] * a.s_h - a.p_h + ky * a.d_h, ix = cur_ox[i] * a.s_w - a.p_w + kx * a.d_w;
             if constexpr (VEC) {
                 const bool xok = yok && c_in_ok && unsigned(iy) < unsigned(a.h) && unsigned(ix) < unsigned(a.w);
-                const unsigned yoff = yok && o_in ? unsigned((rel * 4 * a.c_out + o0 + cc * EPC) * ES) : 0x80000000u;
+                const unsigned yoff = yok && o_in ? unsigned((rel * NC * a.c_out + o0 + cc * EPC) * ES) : 0x80000000u;
                 const unsigned xoff =
-                    xok ? unsigned((((cur_img[i] * a.h + iy) * a.w + ix) * 4 * a.c_in + c0 + cc * EPC) * ES)
+                    xok ? unsigned((((cur_img[i] * a.h + iy) * a.w + ix) * NC * a.c_in + c0 + cc * EPC) * ES)
                         : 0x80000000u;
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
+                for (int q = 0; q < NC; ++q) {
                     st.v[0][i][q] = load16(dy_s, dy_bytes, yoff + unsigned(q * a.c_out * ES));
                     st.v[1][i][q] = load16(x_s, x_bytes, xoff + unsigned(q * a.c_in * ES));
                 }
             } else {
                 const bool xok = yok && iy >= 0 && iy < a.h && ix >= 0 && ix < a.w;
-                const T *yrow = dy_s + int64_t(yok ? rel : 0) * 4 * a.c_out;
-                const T *xrow = x_s + ((int64_t(cur_img[i]) * a.h + (xok ? iy : 0)) * a.w + (xok ? ix : 0)) * 4 * a.c_in;
+                const T *yrow = dy_s + int64_t(yok ? rel : 0) * NC * a.c_out;
+                const T *xrow = x_s + ((int64_t(cur_img[i]) * a.h + (xok ? iy : 0)) * a.w + (xok ? ix : 0)) * NC * a.c_in;
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
+                for (int q = 0; q < NC; ++q) {
                     st.v[0][i][q] = load_chunk<T, VEC>(yrow + q * a.c_out + o0, yok, cc * EPC, a.c_out - o0, dy);
                     st.v[1][i][q] = load_chunk<T, VEC>(xrow + q * a.c_in + c0, xok, cc * EPC, a.c_in - c0, x);
                 }
@@ -226,7 +238,7 @@ __global__ __launch_bounds__(kThreads) void qconv2d_wgrad(WArgs a)
 #pragma unroll
             for (int i = 0; i < PASSES; ++i)
 #pragma unroll
-                for (int q = 0; q < 4; ++q)
+                for (int q = 0; q < NC; ++q)
                     *reinterpret_cast<u32x4 *>(base + t * TENSOR + q * COMP + (pr + PXT * i) * kRow +
                                                (ES == 2 ? (cc ^ chunk_swz(pr + PXT * i)) : cc) * EPC) =
                         st.v[t][i][q];
@@ -234,9 +246,9 @@ __global__ __launch_bounds__(kThreads) void qconv2d_wgrad(WArgs a)
 
     // ---- compute: wave w owns o-block w / 2 and c-block w % 2
     const int ob = (wave >> 1) * 32, cb = (wave & 1) * 32;
-    f32x16 acc[4];
+    f32x16 acc[NM];
 #pragma unroll
-    for (int m = 0; m < 4; ++m)
+    for (int m = 0; m < NM; ++m)
 #pragma unroll
         for (int e = 0; e < 16; ++e)
             acc[m][e] = 0.0f;
@@ -268,12 +280,12 @@ __global__ __launch_bounds__(kThreads) void qconv2d_wgrad(WArgs a)
     constexpr int KSTEPS = ES == 2 ? kChunk / 16 : kChunk / 2;
     typedef typename Frag<T>::type F;
     struct KFrags {
-        F fy[4], fx[4];
+        F fy[NC], fx[NC];
     };
     auto read_k = [&](int buf, int ks, KFrags &f) {
         const T *yb = lds + buf * BUF, *xb = yb + TENSOR;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
+        for (int q = 0; q < NC; ++q) {
             f.fy[q] = frag(yb, q, ob, ks);
             f.fx[q] = frag(xb, q, cb, ks);
         }
@@ -289,17 +301,24 @@ __global__ __launch_bounds__(kThreads) void qconv2d_wgrad(WArgs a)
         }
     };
     auto mfmas = [&](const KFrags &f) {
+        if constexpr (NC == 1) {
+            if constexpr (ES == 2)
+                acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.fy[0], f.fx[0], acc[0], 0, 0, 0);
+            else
+                acc[0] = __builtin_amdgcn_mfma_f32_32x32x2f32(f.fy[0], f.fx[0], acc[0], 0, 0, 0);
+        } else {
 #pragma unroll
-        for (int p = 0; p < 4; ++p) {
-            const F pos = f.fy[p], neg = negate(f.fy[p]);
+            for (int p = 0; p < NC; ++p) {
+                const F pos = f.fy[p], neg = negate(f.fy[p]);
 #pragma unroll
-            for (int m = 0; m < 4; ++m) {
-                const int q = p ^ m;
-                const bool minus = (kNeg >> (4 * p + q)) & 1u;
-                if constexpr (ES == 2)
-                    acc[m] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(minus ? neg : pos, f.fx[q], acc[m], 0, 0, 0);
-                else
-                    acc[m] = __builtin_amdgcn_mfma_f32_32x32x2f32(minus ? neg : pos, f.fx[q], acc[m], 0, 0, 0);
+                for (int m = 0; m < 4; ++m) {
+                    const int q = p ^ m;
+                    const bool minus = (kNeg >> (4 * p + q)) & 1u;
+                    if constexpr (ES == 2)
+                        acc[m] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(minus ? neg : pos, f.fx[q], acc[m], 0, 0, 0);
+                    else
+                        acc[m] = __builtin_amdgcn_mfma_f32_32x32x2f32(minus ? neg : pos, f.fx[q], acc[m], 0, 0, 0);
+                }
             }
         }
     };
@@ -307,6 +326,8 @@ __global__ __launch_bounds__(kThreads) void qconv2d_wgrad(WArgs a)
     // sign flips first, then each MFMA followed by one fragment read.
     constexpr int NRD = ES == 2 ? 16 : 8;  // LDS reads of one k-step
     auto sched = [&]() {
+        if constexpr (NC == 1)
+            return;  // one MFMA per k-step: nothing to interleave
         __builtin_amdgcn_sched_group_barrier(0x002, ES == 2 ? 16 : 4, 0);
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
@@ -370,8 +391,8 @@ __global__ __launch_bounds__(kThreads) void qconv2d_wgrad(WArgs a)
     // 4(l/32) + e, cb + l%32) of the wave's block
     const int c = c0 + cb + (lane & 31);
 #pragma unroll
-    for (int m = 0; m < 4; ++m) {
-        float *dst = a.part + ((int64_t(split) * a.taps + tap) * 4 + m) * a.c_out * a.c_in;
+    for (int m = 0; m < NM; ++m) {
+        float *dst = a.part + ((int64_t(split) * a.taps + tap) * NM + m) * a.c_out * a.c_in;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             const int o = o0 + ob + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
@@ -399,6 +420,40 @@ __global__ __launch_bounds__(kThreads) void qconv2d_wgrad_reduce(const float *__
     double s = 0.0;
     for (int sp = 0; sp < splits; ++sp)
         s += double(part[((int64_t(sp) * taps + tap) * 4 + m) * c_out * c_in + oc]);
+    float *dw = m == 0 ? dw0 : m == 1 ? dw1 : m == 2 ? dw2 : dw3;
+    dw[oc * taps + tap] = float(s);
+}
+
+// Layers of at most 16 channels (the kernel's NC = 1 form): the partials
+// are G[(p,o)][(q,c)] per slice and tap ([splits][taps][4*c_out][4*c_in]), and
+// dW_m[o][c][tap] = sum over slices, then over p in order, of
+// s(p, p xor m) G[(p,o)][(p xor m, c)] (eq. 6's signs), in fp64.
+__global__ __launch_bounds__(kThreads) void qconv2d_wgrad_reduce_dense(const float *__restrict__ part, int splits,
+                                                                       int taps, int c_out, int c_in,
+                                                                       float *__restrict__ dw0,
+                                                                       float *__restrict__ dw1,
+                                                                       float *__restrict__ dw2,
+                                                                       float *__restrict__ dw3)
+{
+    const int64_t oc_n = int64_t(c_out) * c_in;
+    const int64_t idx = int64_t(blockIdx.x) * kThreads + threadIdx.x;  // over [m][tap][o][c]
+    if (idx >= 4 * taps * oc_n)
+        return;
+    const int64_t oc = idx % oc_n;
+    const int o = int(oc / c_in), c = int(oc - int64_t(o) * c_in);
+    const int mt = int(idx / oc_n);
+    const int m = mt / taps, tap = mt - (mt / taps) * taps;
+    const int64_t g_n = int64_t(4 * c_out) * (4 * c_in);  // one slice's G of one tap
+    double s = 0.0;
+    for (int sp = 0; sp < splits; ++sp) {
+        const float *g = part + (int64_t(sp) * taps + tap) * g_n;
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+            const int q = p ^ m;
+            const double v = double(g[int64_t(p * c_out + o) * (4 * c_in) + q * c_in + c]);
+            s += ((kNeg >> (4 * p + q)) & 1u) ? -v : v;
+        }
+    }
     float *dw = m == 0 ? dw0 : m == 1 ? dw1 : m == 2 ? dw2 : dw3;
     dw[oc * taps + tap] = float(s);
 }
@@ -508,11 +563,19 @@ struct WPlan {
     int64_t per_split;
 };
 
+// Layers whose whole pixel rows (4 * C reals) fit one tile take the dense
+// (NC = 1) form of the kernel.
+bool wgrad_dense(const ConvGeom &g)
+{
+    return 4 * g.c_out <= kTileO && 4 * g.c_in <= kTileC;
+}
+
 WPlan wgrad_plan(const ConvGeom &g)
 {
     WPlan p;
-    p.o_tiles = (g.c_out + kTileO - 1) / kTileO;
-    p.c_tiles = (g.c_in + kTileC - 1) / kTileC;
+    const int nc = wgrad_dense(g) ? 4 : 1;  // channels per kernel-side row, in units of C
+    p.o_tiles = (nc * g.c_out + kTileO - 1) / kTileO;
+    p.c_tiles = (nc * g.c_in + kTileC - 1) / kTileC;
     p.taps = g.k_h * g.k_w;
     const int64_t pixels = g.m();
     const int64_t per_split_pass = int64_t(p.o_tiles) * p.c_tiles * p.taps;
@@ -534,7 +597,7 @@ WPlan wgrad_plan(const ConvGeom &g)
 size_t qconv2d_wgrad_work_bytes(const ConvGeom &g)
 {
     const WPlan p = wgrad_plan(g);
-    const size_t dw_part = size_t(p.splits) * p.taps * 4 * g.c_out * g.c_in * sizeof(float);
+    const size_t dw_part = size_t(p.splits) * p.taps * (wgrad_dense(g) ? 16 : 4) * g.c_out * g.c_in * sizeof(float);
     const size_t b_part = size_t(kBiasBlocks) * 4 * g.c_out * sizeof(float);
     return dw_part > b_part ? dw_part : b_part;
 }
@@ -544,15 +607,16 @@ hipError_t qconv2d_backward_weight_run(const ConvGeom &g, DType dt, const void *
                                        hipStream_t stream)
 {
     const WPlan p = wgrad_plan(g);
+    const bool dense = wgrad_dense(g);
     WArgs a;
     a.x = x;
     a.dy = dy;
     a.part = static_cast<float *>(work);
     a.n = g.n;
-    a.c_in = g.c_in;
+    a.c_in = dense ? 4 * g.c_in : g.c_in;  // channels of the kernel's one component
     a.h = g.h;
     a.w = g.w;
-    a.c_out = g.c_out;
+    a.c_out = dense ? 4 * g.c_out : g.c_out;
     a.k_h = g.k_h;
     a.k_w = g.k_w;
     a.s_h = g.s_h;
@@ -576,24 +640,38 @@ hipError_t qconv2d_backward_weight_run(const ConvGeom &g, DType dt, const void *
     const int64_t hw_out = int64_t(g.h_out) * g.w_out;
     const int64_t dy_span = p.per_split * 4 * g.c_out * es;
     const int64_t x_span = ((p.per_split + hw_out - 1) / hw_out + 1) * g.h * g.w * 4 * g.c_in * es;
-    const bool vec = g.c_in % epc == 0 && g.c_out % epc == 0 && dy_span < 0x7fffffffLL && x_span < 0x7fffffffLL;
+    const bool vec = a.c_in % epc == 0 && a.c_out % epc == 0 && dy_span < 0x7fffffffLL && x_span < 0x7fffffffLL;
+    auto launch = [&](auto t, auto v, auto nc) {
+        using T = decltype(t);
+        hipLaunchKernelGGL((qconv2d_wgrad<T, decltype(v)::value, decltype(nc)::value>), dim3(blocks), dim3(kThreads),
+                           0, stream, a);
+    };
+    using VT = std::true_type;
+    using VF = std::false_type;
+    using N4 = std::integral_constant<int, 4>;
+    using N1 = std::integral_constant<int, 1>;
     if (dt == DType::BF16) {
-        if (vec)
-            hipLaunchKernelGGL((qconv2d_wgrad<__bf16, true>), dim3(blocks), dim3(kThreads), 0, stream, a);
+        if (dense)
+            vec ? launch(__bf16{}, VT{}, N1{}) : launch(__bf16{}, VF{}, N1{});
         else
-            hipLaunchKernelGGL((qconv2d_wgrad<__bf16, false>), dim3(blocks), dim3(kThreads), 0, stream, a);
+            vec ? launch(__bf16{}, VT{}, N4{}) : launch(__bf16{}, VF{}, N4{});
     } else {
-        if (vec)
-            hipLaunchKernelGGL((qconv2d_wgrad<float, true>), dim3(blocks), dim3(kThreads), 0, stream, a);
+        if (dense)
+            vec ? launch(float{}, VT{}, N1{}) : launch(float{}, VF{}, N1{});
         else
-            hipLaunchKernelGGL((qconv2d_wgrad<float, false>), dim3(blocks), dim3(kThreads), 0, stream, a);
+            vec ? launch(float{}, VT{}, N4{}) : launch(float{}, VF{}, N4{});
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess)
         return e;
     const int64_t outs = int64_t(4) * g.c_out * g.c_in * p.taps;
-    hipLaunchKernelGGL(qconv2d_wgrad_reduce, dim3(unsigned((outs + kThreads - 1) / kThreads)), dim3(kThreads), 0,
-                       stream, (const float *)a.part, p.splits, p.taps, g.c_out, g.c_in, dw_r, dw_i, dw_j, dw_k);
+    const dim3 rgrid(unsigned((outs + kThreads - 1) / kThreads));
+    if (dense)
+        hipLaunchKernelGGL(qconv2d_wgrad_reduce_dense, rgrid, dim3(kThreads), 0, stream, (const float *)a.part,
+                           p.splits, p.taps, g.c_out, g.c_in, dw_r, dw_i, dw_j, dw_k);
+    else
+        hipLaunchKernelGGL(qconv2d_wgrad_reduce, rgrid, dim3(kThreads), 0, stream, (const float *)a.part, p.splits,
+                           p.taps, g.c_out, g.c_in, dw_r, dw_i, dw_j, dw_k);
     e = hipGetLastError();
     if (e != hipSuccess || db == nullptr)
         return e;
