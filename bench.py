@@ -45,7 +45,7 @@ DEFAULT_WORKLOAD = "imagenet_stage"
 # counter reads for a 512 MiB device copy (FETCH x2.0, WRITE x1.0); the runs are
 # summarised in profiles/qconv2d_<workload>_hbm.md.  A figure is reported only
 # while the kernel source is the one it was measured on (sha256 prefix).
-CONV_TRAFFIC = {"imagenet_stage": {"bytes": 221725622, "kernel_sha256": "673f1c2125108f3c"}}
+CONV_TRAFFIC = {"imagenet_stage": {"bytes": 221713403, "kernel_sha256": "673f1c2125108f3c"}}
 CONV_SOURCE = os.path.join(ROOT, "paper_2509_05512_amd", "csrc", "qconv2d_gfx950.hip")
 
 
