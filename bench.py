@@ -18,10 +18,13 @@ Prints ONE JSON line:
                useful FLOPs = 2 * N*Ho*Wo * 4Cout * 4Cin * k^2 per layer
   qconv2d      the convolution kernel alone: TFLOP/s and fraction of the bf16
                dense MFMA peak (2516.6 TFLOP/s)
-  iqbn         the stand-alone IQBN (stats + finalize + affine): GB/s of
-               algorithmic traffic (two reads + one write of the tensor) and
-               fraction of 8 TB/s, in the step (input just written by the
-               convolution) and cold (input evicted from the caches first)
+  iqbn         the stand-alone IQBN: GB/s of algorithmic traffic (two reads +
+               one write of the tensor) and fraction of 8 TB/s, cold (input
+               evicted from the caches first; the headline) and warm (input
+               just written by the convolution)
+  other_configs  the same figures for the detection pair (3x3 s2 + 1x1) and
+               the deep stack (four 256 -> 256 blocks): fused step, per-layer
+               convolution TFLOP/s and share of the MFMA peak, IQBN cold/warm
   roofline     the dominant kernel (the convolution) against its roofline,
                timed with HIP events on the stream it runs on
   cpu_baseline the CPU oracle timed on a bounded sample of the same workload
@@ -40,6 +43,8 @@ MFMA_PEAK_TFLOPS = {"bf16": 2516.6, "fp32": 157.3}
 HBM_PEAK_GBPS = 8000.0
 METRIC = "qconv2d bf16 TFLOP/s + % MFMA peak; IQBN GB/s + % HBM peak"
 DEFAULT_WORKLOAD = "imagenet_stage"
+# the other configurations the targets apply to, reported as sub-records
+OTHER_CONFIGS = ["detection_pair", "deep_stack"]
 # HBM bytes per launch of the convolution kernel, from rocprofv3 --pmc
 # FETCH_SIZE and WRITE_SIZE runs of this benchmark, each scaled by what the same
 # counter reads for a 512 MiB device copy (FETCH x2.0, WRITE x1.0); the runs are
@@ -68,6 +73,8 @@ def parse_args():
     # this workload take ~15 ms
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--no-other-configs", action="store_true",
+                    help="measure only --workload (profiling runs)")
     ap.add_argument("--no-cpu-baseline", action="store_true",
                     help="skip the CPU oracle leg (profiling runs)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
@@ -164,27 +171,29 @@ def time_separable(layers, quan, steps):
 
 
 def time_iqbn_cold(layers, quan, steps, eps):
-    """The stand-alone IQBN of every layer with its input evicted from the
+    """The stand-alone IQBN of each layer with its input evicted from the
     caches first: before each timed rep a 512 MiB buffer is read (twice the
     256 MB Infinity Cache; a read leaves no dirty lines whose write-back would
-    land inside the timed region).  Median microseconds per step."""
+    land inside the timed region).  Median microseconds per layer."""
     import torch
     dev = layers[0]["y"].device
     flush_buf = torch.zeros(128 * 2**20, dtype=torch.float32, device=dev)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    times = []
-    for _ in range(max(steps, 5)):
-        flush_buf.sum()
-        e0.record()
-        for ly in layers:
-            fn = quan.quan_iqbn_relu_forward if ly["spec"].relu else quan.quan_iqbn_forward
+    med = []
+    for ly in layers:
+        fn = quan.quan_iqbn_relu_forward if ly["spec"].relu else quan.quan_iqbn_forward
+        times = []
+        for _ in range(max(steps, 5)):
+            flush_buf.sum()
+            e0.record()
             fn(ly["y"], ly["gamma"], ly["beta"], eps, out=ly["z"], mean=ly["mean"], var=ly["var"])
-        e1.record()
-        torch.cuda.synchronize()
-        times.append(e0.elapsed_time(e1) * 1e3)
+            e1.record()
+            torch.cuda.synchronize()
+            times.append(e0.elapsed_time(e1) * 1e3)
+        times.sort()
+        med.append(times[len(times) // 2])
     del flush_buf
-    times.sort()
-    return times[len(times) // 2]
+    return med
 
 
 def time_backward(layers, quan, steps, eps):
@@ -272,6 +281,130 @@ def run_step(layers, quan, events=None, eps=1e-5):
             events[li][3].record()
 
 
+def per_kernel_times(layers, quan, steps, eps):
+    """Milliseconds per layer of the pack, the convolution and the three IQBN
+    passes, each launch on its own with HIP events between them on torch's
+    current stream (the stream the kernels run on), averaged over steps."""
+    import torch
+    for _ in range(2):
+        run_step(layers, quan, eps=eps)
+    events = [[[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in layers] for _ in range(steps)]
+    torch.cuda.synchronize()
+    for s in range(steps):
+        run_step(layers, quan, events=events[s], eps=eps)
+    torch.cuda.synchronize()
+    def avg(li, a, b):
+        return sum(events[s][li][a].elapsed_time(events[s][li][b]) for s in range(steps)) / steps
+    return ([avg(li, 0, 1) for li in range(len(layers))], [avg(li, 1, 2) for li in range(len(layers))],
+            [avg(li, 2, 3) for li in range(len(layers))])
+
+
+def time_fused_steps(layers, quan, steps, eps, stats="auto"):
+    """Milliseconds per whole fused step (every layer: pack, convolution with
+    IQBN), HIP events around `steps` back-to-back steps."""
+    import torch
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(steps):
+        run_step_fused(layers, quan, eps=eps, stats=stats)
+    end.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / steps
+
+
+# Targets the measurement is held to: the convolution at >= 50% of the bf16
+# MFMA peak, IQBN at >= 70% of HBM bandwidth.  The detection pair (3x3 s2 +
+# 1x1) is judged as a pair: 73.8 GFLOP at 50% of 2516.6 TFLOP/s = 58.7 us.
+def layer_records(wl, dims, conv_ms, iqbn_ms, cold_us, pack_ms=None):
+    esz = 2 if wl.dtype == "bf16" else 4
+    peak = MFMA_PEAK_TFLOPS[wl.dtype]
+    recs = []
+    for li, L in enumerate(wl.layers):
+        d = dims[li]
+        nbytes = 3 * wl.n * d["ho"] * d["wo"] * 4 * L.c_out * esz
+        tf = d["useful_flops"] / (conv_ms[li] * 1e-3) / 1e12
+        r = {"layer": li, "c_in": L.c_in, "c_out": L.c_out, "k": L.k, "stride": L.stride, "pad": L.pad,
+             "h_out": d["ho"], "w_out": d["wo"]}
+        if pack_ms is not None:
+            r["pack_us"] = round(pack_ms[li] * 1e3, 3)
+        r.update({
+            "qconv2d_us": round(conv_ms[li] * 1e3, 3), "qconv2d_tflops": round(tf, 2),
+            "qconv2d_frac_mfma_peak": round(tf / peak, 4),
+            "iqbn_cold_us": round(cold_us[li], 3),
+            "iqbn_cold_gbps": round(nbytes / (cold_us[li] * 1e-6) / 1e9, 1),
+            "iqbn_cold_frac_hbm_peak": round(nbytes / (cold_us[li] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
+            "iqbn_warm_us": round(iqbn_ms[li] * 1e3, 3),
+            "iqbn_warm_gbps": round(nbytes / (iqbn_ms[li] * 1e-3) / 1e9, 1),
+        })
+        recs.append(r)
+    return recs
+
+
+def measure_config(name, args, dev, quan, workloads):
+    """A sub-record for another target configuration: the fused step, and per
+    layer the convolution alone and IQBN cold and warm."""
+    import torch
+    wl = workloads.WORKLOADS[name]
+    log(f"[bench] config {wl.name}: {wl.description}")
+    tens = workloads.generate(wl)
+    layers = build_layers(wl, tens, dev, quan, torch)
+    for _ in range(args.warmup):
+        run_step_fused(layers, quan, eps=wl.eps)
+    step_ms = time_fused_steps(layers, quan, args.steps, wl.eps)
+    _, conv_ms, iqbn_ms = per_kernel_times(layers, quan, args.steps, wl.eps)
+    cold_us = time_iqbn_cold(layers, quan, args.steps, wl.eps)
+    dims = wl.layer_dims()
+    flops = sum(d["useful_flops"] for d in dims)
+    peak = MFMA_PEAK_TFLOPS[wl.dtype]
+    esz = 2 if wl.dtype == "bf16" else 4
+    nbytes = sum(3 * wl.n * d["ho"] * d["wo"] * 4 * L.c_out * esz for d, L in zip(dims, wl.layers))
+    conv_tf = flops / (sum(conv_ms) * 1e-3) / 1e12
+    rec = {
+        "workload": wl.name, "description": wl.description,
+        "useful_gflop_per_step": round(flops / 1e9, 3),
+        "step_us": round(step_ms * 1e3, 3),
+        "step_tflops": round(flops / (step_ms * 1e-3) / 1e12, 2),
+        "qconv2d": {"us_per_step": round(sum(conv_ms) * 1e3, 3), "tflops": round(conv_tf, 2),
+                    "frac_mfma_peak": round(conv_tf / peak, 4)},
+        "iqbn": {"cold_us_per_step": round(sum(cold_us), 3),
+                 "cold_gbps": round(nbytes / (sum(cold_us) * 1e-6) / 1e9, 1),
+                 "cold_frac_hbm_peak": round(nbytes / (sum(cold_us) * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
+                 "warm_us_per_step": round(sum(iqbn_ms) * 1e3, 3),
+                 "warm_gbps": round(nbytes / (sum(iqbn_ms) * 1e-3) / 1e9, 1)},
+        "per_layer": layer_records(wl, dims, conv_ms, iqbn_ms, cold_us),
+    }
+    if wl.name == "detection_pair":
+        rec["pair_conv_us"] = round(sum(conv_ms) * 1e3, 3)
+        rec["pair_conv_target_us"] = round(flops / (0.5 * peak * 1e12) * 1e6, 1)
+    for r in rec["per_layer"]:
+        log(f"[bench] {wl.name} layer {r}")
+    del layers
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return rec
+
+
+def cpu_model():
+    """The host CPU's model name, as lscpu reports it."""
+    import subprocess
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            if line.startswith("Model name:"):
+                return line.split(":", 1)[1].strip()
+    except (OSError, subprocess.SubprocessError):
+        pass
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(wl, tens, target_s):
     """The oracle on the first images of the batch (all layers, conv + IQBN),
     timed on this host's cores.  Returns the oracle's useful-FLOP rate."""
@@ -304,6 +437,7 @@ def cpu_baseline(wl, tens, target_s):
         "value": f / t / 1e12,
         "unit": "TFLOP/s",
         "cores": threads,
+        "cpu_model": cpu_model(),
         "kind": "oracle",
         "sample": f"first {n_img} of {wl.n} images through every layer (conv + IQBN), fp64, "
                   f"{t:.1f} s, {f / 1e9:.2f} GFLOP",
@@ -389,21 +523,7 @@ def main():
     bwd_iqbn_us, bwd_data_us, bwd_weight_us = time_backward(layers, quan, args.steps, wl.eps)
 
     # per-kernel times: the same steps with every kernel on its own
-    for _ in range(2):
-        run_step(layers, quan, eps=wl.eps)
-    events = [[[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in layers]
-              for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    for s in range(args.steps):
-        run_step(layers, quan, events=events[s], eps=wl.eps)
-    torch.cuda.synchronize()
-
-    pack_ms = [sum(events[s][li][0].elapsed_time(events[s][li][1]) for s in range(args.steps)) / args.steps
-               for li in range(len(layers))]
-    conv_ms = [sum(events[s][li][1].elapsed_time(events[s][li][2]) for s in range(args.steps)) / args.steps
-               for li in range(len(layers))]
-    iqbn_ms = [sum(events[s][li][2].elapsed_time(events[s][li][3]) for s in range(args.steps)) / args.steps
-               for li in range(len(layers))]
+    pack_ms, conv_ms, iqbn_ms = per_kernel_times(layers, quan, args.steps, wl.eps)
     log(f"[bench] {args.steps} steps: {ms_per_step:.4f} ms/step (wall {1e3 * t_wall / args.steps:.4f})")
 
     step_flops = sum(conv_flops)
@@ -411,21 +531,17 @@ def main():
     conv_tflops = step_flops / (sum(conv_ms) * 1e-3) / 1e12
     peak = MFMA_PEAK_TFLOPS[wl.dtype]
     iqbn_gbps = sum(iqbn_bytes) / (sum(iqbn_ms) * 1e-3) / 1e9
-    iqbn_cold_us = time_iqbn_cold(layers, quan, args.steps, wl.eps)
+    cold_us = time_iqbn_cold(layers, quan, args.steps, wl.eps)
+    iqbn_cold_us = sum(cold_us)
     iqbn_cold_gbps = sum(iqbn_bytes) / (iqbn_cold_us * 1e-6) / 1e9
-    per_layer = []
-    for li, L in enumerate(wl.layers):
-        per_layer.append({
-            "layer": li, "c_in": L.c_in, "c_out": L.c_out, "k": L.k, "stride": L.stride,
-            "pad": L.pad, "h_out": dims[li]["ho"], "w_out": dims[li]["wo"],
-            "pack_us": round(pack_ms[li] * 1e3, 3),
-            "qconv2d_us": round(conv_ms[li] * 1e3, 3),
-            "qconv2d_tflops": round(conv_flops[li] / (conv_ms[li] * 1e-3) / 1e12, 2),
-            "iqbn_us": round(iqbn_ms[li] * 1e3, 3),
-            "iqbn_gbps": round(iqbn_bytes[li] / (iqbn_ms[li] * 1e-3) / 1e9, 1),
-        })
+    per_layer = layer_records(wl, dims, conv_ms, iqbn_ms, cold_us, pack_ms)
     for pl in per_layer:
         log(f"[bench] layer {pl}")
+    others = {}
+    if not args.no_other_configs:
+        for name in OTHER_CONFIGS:
+            if name != wl.name:
+                others[name] = measure_config(name, args, dev, quan, workloads)
 
     traffic = conv_traffic(wl.name)
     result = {
@@ -478,16 +594,17 @@ def main():
             "pack_us_per_step": round(sum(pack_ms) * 1e3, 3),
         },
         "iqbn": {
-            # in the step: the tensor was just written by the convolution
-            "gbps": round(iqbn_gbps, 1),
-            "frac_hbm_peak": round(iqbn_gbps / HBM_PEAK_GBPS, 4),
-            "us_per_step": round(sum(iqbn_ms) * 1e3, 3),
-            # with the tensor evicted from L2 and the Infinity Cache first
-            "cold_gbps": round(iqbn_cold_gbps, 1),
-            "cold_frac_hbm_peak": round(iqbn_cold_gbps / HBM_PEAK_GBPS, 4),
-            "cold_us_per_step": round(iqbn_cold_us, 3),
+            # headline: the tensor evicted from L2 and the Infinity Cache first
+            "gbps": round(iqbn_cold_gbps, 1),
+            "frac_hbm_peak": round(iqbn_cold_gbps / HBM_PEAK_GBPS, 4),
+            "us_per_step": round(iqbn_cold_us, 3),
+            # beside it, warm: the tensor just written by the convolution
+            "warm_gbps": round(iqbn_gbps, 1),
+            "warm_frac_hbm_peak": round(iqbn_gbps / HBM_PEAK_GBPS, 4),
+            "warm_us_per_step": round(sum(iqbn_ms) * 1e3, 3),
         },
         "per_layer": per_layer,
+        "other_configs": others,
         "roofline": {
             "bound": "mfma",
             "kernel": "qconv2d_igemm",

@@ -42,7 +42,7 @@
 //     type (RNE) and stores channels-last.
 #include <hip/hip_runtime.h>
 
-#include <cstdlib>
+#include <mutex>
 #include <type_traits>
 
 #include "quan_launch.h"
@@ -1231,13 +1231,17 @@ const KernelEntry kKernels[] = {
 };
 constexpr int kNumKernels = int(sizeof(kKernels) / sizeof(kKernels[0]));
 
-// Compute units of the current device (cached per device).
+// Compute units of the current device (cached per device; the library may
+// be called from several threads, so the caches are guarded).
+std::mutex g_cache_mutex;
+
 int device_cus()
 {
     static int cached[64] = {};
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64)
         return 256;
+    std::lock_guard<std::mutex> lock(g_cache_mutex);
     if (cached[dev] == 0) {
         int n = 0;
         if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
@@ -1251,9 +1255,10 @@ int device_cus()
 // at least 1).
 int resident_wgs(const void *fn, int threads)
 {
-    static const void *fns[9 * kNumKernels] = {};
-    static int counts[9 * kNumKernels] = {};
-    for (int i = 0; i < 9 * kNumKernels; ++i) {
+    static const void *fns[16 * kNumKernels] = {};
+    static int counts[16 * kNumKernels] = {};
+    std::lock_guard<std::mutex> lock(g_cache_mutex);
+    for (int i = 0; i < 16 * kNumKernels; ++i) {
         if (fns[i] == fn)
             return counts[i];
         if (fns[i] == nullptr) {
@@ -1265,7 +1270,10 @@ int resident_wgs(const void *fn, int threads)
             return n;
         }
     }
-    return 1;
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, fn, threads, 0) != hipSuccess || n < 1)
+        n = 1;
+    return n;
 }
 
 // Estimated cycles of a launch: rounds of one tile per CU times the tile's
@@ -1317,14 +1325,6 @@ ConvPlan qconv2d_plan(const ConvGeom &g, DType dt, bool sep)
             id = i;
         }
     }
-#ifdef QUAN_TUNING
-    // Tuning builds only: force a kernel (QUAN_QCONV_KERNEL=<table index>).
-    if (const char *force = getenv("QUAN_QCONV_KERNEL")) {
-        const int f = atoi(force);
-        if (f >= 0 && f < kNumKernels && kKernels[f].dt == dt && kKernels[f].sep == sep)
-            id = f;
-    }
-#endif
     const KernelEntry &k = kKernels[id];
     ConvPlan p;
     p.id = id;

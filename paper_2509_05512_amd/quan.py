@@ -17,8 +17,7 @@ import os
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-# QUAN_LIB_PATH selects another build of the library (default: the in-tree one).
-LIB_PATH = os.environ.get("QUAN_LIB_PATH") or os.path.join(_HERE, "libquan.so")
+LIB_PATH = os.path.join(_HERE, "libquan.so")
 
 QUAN_F32, QUAN_BF16 = 0, 1
 _STATUS = {0: "QUAN_OK", -1: "QUAN_ERR_NULL", -2: "QUAN_ERR_SHAPE", -3: "QUAN_ERR_DTYPE",

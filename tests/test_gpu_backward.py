@@ -105,6 +105,34 @@ def test_backward_weight_full_imagenet_layer_sampled():
     assert_close(f64(db.cpu()), ref_b, torch.float32, "dbias imagenet")
 
 
+def test_backward_weight_full_cifar_layer_sampled():
+    """The cifar layer (128 images of 32x32, 16 -> 16 channels, bf16) at full
+    size: the dense weight-gradient form (one 64-wide operand per pixel row,
+    signs applied in the slice reduction) over all of its pixel slices, on
+    sampled (output, input) channel pairs: each pair's gradient depends only
+    on that channel of x and of dy, so the oracle runs on one-channel slices."""
+    say("backward weight cifar full-size sampled")
+    from paper_2509_05512_amd import workloads
+    wl = workloads.WORKLOADS["cifar"]
+    tens = workloads.generate(wl)
+    L = wl.layers[0]
+    dev = torch.device("cuda:0")
+    rng = np.random.default_rng(2)
+    dy = torch.from_numpy(rng.standard_normal((wl.n, 4, L.c_out, wl.h, wl.w), dtype=np.float32)).to(torch.bfloat16)
+    dws, db = quan.quan_qconv2d_backward_weight(quan.to_device_layout(tens.x.to(dev)),
+                                                quan.to_device_layout(dy.to(dev)), (L.k, L.k), stride=L.stride,
+                                                pad=L.pad)
+    torch.cuda.synchronize()
+    got = np.stack([f64(t.cpu()) for t in dws])  # [4, O, C, 3, 3]
+    x64 = f64(tens.x)
+    dy64 = f64(dy)
+    w1 = np.zeros((4, 1, 1, L.k, L.k))
+    for (o, c) in [(0, 0), (15, 15), (3, 12), (9, 1), (7, 7), (14, 5)]:
+        _, ref, _ = oracle.qconv2d_backward(x64[:, :, c:c + 1], w1, dy64[:, :, o:o + 1], L.stride, L.pad, 1)
+        assert_close(got[:, o, c], ref[:, 0, 0], torch.float32, f"dW cifar (o={o}, c={c})")
+    assert_close(f64(db.cpu()), dy64.sum(axis=(0, 3, 4)), torch.float32, "dbias cifar")
+
+
 def test_backward_data_full_imagenet_layer_sampled():
     """The imagenet_stage layer's input gradient at full size (the launch the
     bench times) on sampled input pixels: dX at (n, iy, ix) only depends on

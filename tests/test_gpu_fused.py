@@ -15,7 +15,7 @@ import torch
 
 import oracle
 from paper_2509_05512_amd import quan
-from parity import assert_close, f64, say
+from parity import assert_close, conv_reference_sampled, f64, sample_pixels, say
 
 pytestmark = pytest.mark.gpu
 
@@ -108,65 +108,78 @@ def test_fused_is_deterministic(stats):
         assert torch.equal(a, c)
 
 
-def _check_layer_statistics(xg, wg, g, be, stride, pad, label, stats="epilogue"):
-    """mean/var of the fused call against fp64 statistics of the GPU
-    convolution output, plus a sample of normalised values."""
-    dev = torch.device("cuda:0")
-    packed = quan.quan_qconv2d_pack_weights(*wg)
-    shape = tuple(wg[0].shape)
-    conv = quan.quan_qconv2d_forward_packed(xg, packed, shape, stride=stride, pad=pad)
-    out, mean, var = quan.quan_qconv2d_iqbn_forward(xg, packed, shape, g, be, stride=stride, pad=pad,
-                                                     stats=stats)
-    torch.cuda.synchronize()
-    c64 = conv.double()  # [N, 4, C, H, W] view of the device tensor, upcast on the GPU
-    ref_mean = c64.mean(dim=(0, 3, 4))
-    ref_var = ((c64 - ref_mean[None, :, :, None, None]) ** 2).mean(dim=(0, 3, 4))
-    assert torch.allclose(mean.double(), ref_mean, rtol=1e-5, atol=1e-6), label
-    assert torch.allclose(var.double(), ref_var, rtol=1e-5, atol=1e-6), label
-    scale = g.double() / torch.sqrt(ref_var + 1e-5)
-    ref = (c64 - ref_mean[None, :, :, None, None]) * scale[None, :, :, None, None] + be.double()[None, :, :, None, None]
-    idx = torch.randint(0, out.numel(), (4096,), generator=torch.Generator().manual_seed(0)).to(dev)
-    got = out.double().reshape(-1)[idx]
-    exp = ref.reshape(-1)[idx]
-    assert torch.all((got - exp).abs() <= 1e-2 + 2e-2 * exp.abs()), label
+def _layer_inputs(case, seed):
+    """Inputs of a large layer case (N, Cin, Cout, H, W, k): N(0,1)
+    activations, N(0, 1/fan_in) kernels, a bias, gamma ~ U(0.5, 1.5), beta
+    ~ N(0, 0.2^2), all rounded to bf16 / fp32 as the GPU receives them."""
+    N, Cin, Cout, H, W, k = case
+    rng = np.random.default_rng(seed)
+    x = torch.from_numpy(rng.standard_normal((N, 4, Cin, H, W), dtype=np.float32)).to(torch.bfloat16)
+    w = torch.from_numpy(rng.standard_normal((4, Cout, Cin, k, k), dtype=np.float32)
+                         / np.float32(np.sqrt(4 * Cin * k * k))).to(torch.bfloat16)
+    b = torch.from_numpy(rng.standard_normal((4, Cout), dtype=np.float32) * np.float32(0.3)).to(torch.bfloat16)
+    g = torch.from_numpy(rng.uniform(0.5, 1.5, (4, Cout)).astype(np.float32))
+    be = torch.from_numpy((rng.standard_normal((4, Cout)) * 0.2).astype(np.float32))
+    return x, w, b, g, be
 
 
+def _check_conv(x64, w64, b64, conv, stride, pad, k, label, full):
+    """The GPU convolution output against the oracle convolution: in full, or
+    (large layers) on sampled output pixels, all channels."""
+    if full:
+        assert_close(f64(conv), oracle.qconv2d(x64, w64, b64, stride, pad, 1), torch.bfloat16, f"conv {label}")
+        return
+    N, _, _, Ho, Wo = conv.shape
+    rng = np.random.default_rng(3)
+    picks = sample_pixels(rng, N, Ho, Wo, 40)
+    ref = conv_reference_sampled(x64, w64, b64, stride, pad, 1, k, picks)
+    got = np.stack([f64(conv[n, :, :, oy, ox]) for (n, oy, ox) in picks])
+    assert_close(got, ref, torch.bfloat16, f"conv {label} (sampled)")
+
+
+def _check_layer_statistics(case, stride, pad, relu, stats, seed, full_conv):
+    """quan_qconv2d_iqbn_forward on a layer with more pixel tiles than
+    work-groups (each persistent work-group gathers several tiles): its conv
+    output against the oracle convolution, and out / mean / var element by
+    element against the oracle's IQBN of that GPU convolution output."""
+    N, Cin, Cout, H, W, k = case
+    label = f"{case} s={stride} relu={relu} stats={stats}"
+    x, w, b, g, be = _layer_inputs(case, seed)
+    conv, out, mean, var = _gpu(x, w, b, g, be, stride, pad, relu, stats)
+    _check_conv(f64(x), f64(w), f64(b), conv, stride, pad, k, label, full_conv)
+    ref_out, ref_mean, ref_var = oracle.iqbn(f64(conv), f64(g), f64(be), 1e-5, relu)
+    assert_close(mean.double().numpy(), ref_mean, torch.float32, f"mean {label}")
+    assert_close(var.double().numpy(), ref_var, torch.float32, f"var {label}")
+    assert_close(f64(out), ref_out, torch.bfloat16, f"out {label}")
+
+
+IMAGENET = (64, 64, 64, 56, 56, 3)   # the imagenet_stage layer: 1568 pixel tiles
+
+
+@pytest.mark.parametrize("relu", [False, True])
 @pytest.mark.parametrize("stats", ["epilogue", "pass"])
-def test_fused_statistics_at_full_layer_size(stats):
-    """The imagenet_stage layer (64x56x56, 64->64): 1568 pixel tiles over the
-    persistent work-groups, several tiles each."""
-    say(f"fused full-size statistics, stats={stats}")
-    from paper_2509_05512_amd import workloads
-    wl = workloads.WORKLOADS["imagenet_stage"]
-    tens = workloads.generate(wl)
-    layer = tens.layers[0]
-    dev = torch.device("cuda:0")
-    xg = quan.to_device_layout(tens.x.to(dev))
-    wg = [layer.weight[q].contiguous().to(dev) for q in range(4)]
-    _check_layer_statistics(xg, wg, layer.gamma.to(dev), layer.beta.to(dev), 1, 1, "imagenet_stage", stats)
+def test_fused_statistics_at_full_layer_size(stats, relu):
+    """The imagenet_stage layer (64x56x56, 64->64) with a bias: 1568 pixel
+    tiles over the persistent work-groups, six or seven each."""
+    say(f"fused full-size statistics, stats={stats} relu={relu}")
+    _check_layer_statistics(IMAGENET, 1, 1, relu, stats, seed=21 + relu, full_conv=False)
 
 
 # (N, Cin, Cout, H, W, k): more pixel tiles than work-groups (each
 # work-group gathers several tiles); ragged last tile.
 MANY_TILES = [
-    (8, 32, 64, 99, 101, 1),  # two stages per tile
+    (8, 32, 64, 99, 101, 1),  # 625 tiles, two stages per tile
     (4, 8, 32, 75, 77, 3),    # nine stages, 32-channel tiles
+    (4, 32, 128, 45, 47, 3),  # two output-channel tiles, 18 stages
 ]
 
 
+@pytest.mark.parametrize("relu", [False, True])
+@pytest.mark.parametrize("stats", ["epilogue", "pass"])
 @pytest.mark.parametrize("case", MANY_TILES, ids=[str(c) for c in MANY_TILES])
-def test_fused_statistics_many_tiles_per_work_group(case):
-    say(f"fused statistics, many tiles {case}")
-    N, Cin, Cout, H, W, k = case
-    dev = torch.device("cuda:0")
-    gen = torch.Generator(device="cpu").manual_seed(N * 1000 + Cin)
-    x = torch.randn((N, 4, Cin, H, W), generator=gen).to(torch.bfloat16)
-    w = (torch.randn((4, Cout, Cin, k, k), generator=gen) / (4 * Cin * k * k) ** 0.5).to(torch.bfloat16)
-    g = torch.rand((4, Cout), generator=gen) + 0.5
-    be = torch.randn((4, Cout), generator=gen) * 0.2
-    xg = quan.to_device_layout(x.to(dev))
-    wg = [w[q].contiguous().to(dev) for q in range(4)]
-    _check_layer_statistics(xg, wg, g.to(dev), be.to(dev), 1, k // 2, str(case))
+def test_fused_statistics_many_tiles_per_work_group(case, stats, relu):
+    say(f"fused statistics, many tiles {case} stats={stats} relu={relu}")
+    _check_layer_statistics(case, 1, case[5] // 2, relu, stats, seed=sum(case) + relu, full_conv=True)
 
 
 # ------------------------- inference IQBN folded in -------------------------
@@ -219,3 +232,48 @@ def test_inference_with_batch_statistics_equals_training():
     # training normalizes the rounded conv output, inference the fp32
     # accumulator: one bf16 rounding apart
     assert_close(f64(inf.cpu()), f64(out), torch.bfloat16, "inference vs training")
+
+
+def _fold_full(case, stride, pad, relu, seed, full_conv):
+    """quan_qconv2d_iqbn_inference on a multi-tile layer against the oracle
+    convolution followed by the oracle's inference IQBN: in full, or on
+    sampled output pixels (each pixel's convolution from its own receptive
+    field, then eq. 12 with the stored statistics)."""
+    N, Cin, Cout, H, W, k = case
+    label = f"{case} relu={relu}"
+    x, w, b, g, be = _layer_inputs(case, seed)
+    rm, rv = _running_stats((0, 0, Cout), seed + 1)
+    dev = torch.device("cuda:0")
+    xg = quan.to_device_layout(x.to(dev))
+    wg = [w[q].contiguous().to(dev) for q in range(4)]
+    packed = quan.quan_qconv2d_pack_weights(*wg)
+    out = quan.quan_qconv2d_iqbn_inference(xg, packed, tuple(wg[0].shape), rm.to(dev), rv.to(dev), g.to(dev),
+                                           be.to(dev), bias=b.to(dev), stride=stride, pad=pad, relu=relu)
+    torch.cuda.synchronize()
+    x64, w64, b64 = f64(x), f64(w), f64(b)
+    if full_conv:
+        ref = oracle.iqbn_inference(oracle.qconv2d(x64, w64, b64, stride, pad, 1), f64(rm), f64(rv), f64(g),
+                                    f64(be), 1e-5, relu)
+        assert_close(f64(out.cpu()), ref, torch.bfloat16, f"inference {label}")
+        return
+    Ho, Wo = out.shape[3], out.shape[4]
+    rng = np.random.default_rng(seed)
+    picks = sample_pixels(rng, N, Ho, Wo, 60)
+    conv = conv_reference_sampled(x64, w64, b64, stride, pad, 1, k, picks)       # [S, 4, Cout]
+    ref = oracle.iqbn_inference(conv[:, :, :, None, None], f64(rm), f64(rv), f64(g), f64(be), 1e-5, relu)
+    got = np.stack([f64(out[n, :, :, oy, ox]) for (n, oy, ox) in picks])
+    assert_close(got, ref[:, :, :, 0, 0], torch.bfloat16, f"inference {label} (sampled)")
+
+
+@pytest.mark.parametrize("relu", [False, True])
+def test_inference_full_layer_size(relu):
+    """The folded epilogue at the imagenet_stage size the bench times."""
+    say(f"inference full size relu={relu}")
+    _fold_full(IMAGENET, 1, 1, relu, seed=31 + relu, full_conv=False)
+
+
+@pytest.mark.parametrize("relu", [False, True])
+@pytest.mark.parametrize("case", MANY_TILES, ids=[str(c) for c in MANY_TILES])
+def test_inference_many_tiles_per_work_group(case, relu):
+    say(f"inference many tiles {case} relu={relu}")
+    _fold_full(case, 1, case[5] // 2, relu, seed=sum(case) + 2 * relu, full_conv=True)
