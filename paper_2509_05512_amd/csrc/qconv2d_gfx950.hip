@@ -101,11 +101,14 @@ struct KArgs {
     int m_tiles, n_tiles;
     unsigned w_bytes;   // bytes of packed weights
     long long x_elems;  // elements of x (n * h * w * 4 * c_in)
-    // Optional IQBN statistics of the output, per M-tile: stats[0][col][mt]
-    // = mean and stats[1][col][mt] = sum of squared deviations of column col
-    // = p * c_out + o over the tile's pixels (after rounding to T).  Written
-    // only by kernels with the deferred epilogue; NULL: none.
+    // Optional IQBN statistics of the output, per run of consecutive output
+    // pixels (an M-tile, or with ALLP waves a tile's 32-pixel sub-tile):
+    // stats[0][col][t] = mean and stats[1][col][t] = sum of squared
+    // deviations of column col = p * c_out + o over run t's pixels (after
+    // rounding to T).  Written only by kernels with the deferred epilogue;
+    // NULL: none.
     float *stats;
+    int stat_tiles;  // partials per column: ceil(m / rows per partial)
     // Optional per-column affine map applied in the epilogue instead of the
     // bias (inference IQBN folded in): out = scale[col] * acc + shift[col],
     // then max(0, .) when relu is non-zero.  NULL scale: out = acc + bias.
@@ -264,30 +267,42 @@ enum : int { kEpiBias = 0, kEpiStats = 1, kEpiFold = 2 };
 // producers, each issuing half as many DMA instructions per stage, make it
 // 3-33% faster; the 64-channel Hamilton tile gains nothing and keeps two.
 // Four need every stage's activation and weight DMAs to split evenly.
-template <typename T, int MB, int NB, int WM, int WN, bool SEP>
+template <typename T, int MB, int NB, int WM, int WN, bool SEP, bool ALLP = false>
 constexpr int producer_waves()
 {
-    constexpr int bnc = SEP ? 32 * NB * WN : 8 * NB * WN;  // output channels per tile
-    constexpr int cs = 128 / (4 * int(sizeof(T)));         // channels per stage
+    constexpr int bnc = (SEP || ALLP) ? 32 * NB * WN : 8 * NB * WN;  // output channels per tile
+    constexpr int cs = 128 / (4 * int(sizeof(T)));                   // channels per stage
     constexpr int a_instr = 32 * MB * WM / 8;
     constexpr int b_instr = 4 * bnc * cs * int(sizeof(T)) / 1024;
     return ((SEP || bnc <= 32) && a_instr % 4 == 0 && b_instr % 4 == 0) ? 4 : 2;
 }
-template <typename T, int MB, int NB, int WAVES_M, int WAVES_N, bool VEC, int EPI, bool SEP, bool PAIR = false>
-__global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB, WAVES_M, WAVES_N, SEP>())) void qconv2d_igemm(KArgs a)
+// ALLP (Hamilton form, bf16): each compute wave holds 32 pixels x all four
+// output components of the tile's BNC = 32*NB channels (4 x NB accumulator
+// blocks), instead of all BM pixels of one component.  A stage's four kernel
+// fragments are then read once and serve all sixteen Hamilton blocks, and
+// one activation fragment (input component q) feeds the four blocks of its
+// column of eq. 6: a quarter of the LDS fragment reads per MFMA of the
+// one-component layout's k-steps for weights, and one activation read per
+// k-step instead of MB.  The MFMAs of a stage run grouped by kernel m = p xor q,
+// so a group needs only W_m: the fragments of W_2 and W_3 are read while the
+// groups of W_0 and W_1 run.  Negative entries of eq. 6 use a sign-flipped
+// copy of the activation fragment (one XOR per dword).
+template <typename T, int MB, int NB, int WAVES_M, int WAVES_N, bool VEC, int EPI, bool SEP, bool PAIR = false,
+          bool ALLP = false>
+__global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB, WAVES_M, WAVES_N, SEP, ALLP>())) void qconv2d_igemm(KArgs a)
 {
     constexpr int ES = int(sizeof(T));
     constexpr int EPC = Elem<T>::per_chunk;
     constexpr int CS = stage_channels<T>();
     constexpr int CPQ = CS / EPC;  // 16-byte chunks per component (2)
     constexpr int NCW = WAVES_M * WAVES_N;
-    constexpr int NPROD = producer_waves<T, MB, NB, WAVES_M, WAVES_N, SEP>();
+    constexpr int NPROD = producer_waves<T, MB, NB, WAVES_M, WAVES_N, SEP, ALLP>();
     constexpr int WTM = 32 * MB;
     constexpr int WTN = 32 * NB;
     constexpr int BM = WTM * WAVES_M;
-    constexpr int BN = (SEP ? 4 : 1) * WTN * WAVES_N;  // output reals per tile
+    constexpr int BN = ((SEP || ALLP) ? 4 : 1) * WTN * WAVES_N;  // output reals per tile
     constexpr int BNC = BN / 4;
-    constexpr int QS = SEP ? 4 : 1;  // accumulator sets per block
+    constexpr int QS = (SEP || ALLP) ? 4 : 1;  // accumulator sets per block
     constexpr int NBUF = 4;                     // stages in the LDS ring
     constexpr int A_BYTES = BM * 128;           // one stage of activations
     constexpr int B_BYTES = 4 * BNC * CS * ES;  // one stage of weights
@@ -304,20 +319,30 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
     static_assert(LOOKAHEAD * PER_STAGE <= 63, "the stages in flight must fit the vmcnt counter");
     static_assert(A_INSTR % NPROD == 0 && B_INSTR % NPROD == 0, "producers split every stage evenly");
     static_assert(!PAIR || (SEP && VEC && ES == 2), "paired stages: separable bf16 with 16-byte chunks");
-    static_assert(BNC == (SEP ? 32 * NB * WAVES_N : 8 * NB * WAVES_N) && CS == 128 / (4 * ES),
+    static_assert(BNC == ((SEP || ALLP) ? 32 * NB * WAVES_N : 8 * NB * WAVES_N) && CS == 128 / (4 * ES),
                   "producer_waves sees the tile geometry");
+    static_assert(!ALLP || (!SEP && !PAIR && ES == 2 && MB == 1 && WAVES_N == 1),
+                  "all-components waves: Hamilton form, bf16, 32 pixels per wave");
 
     // Deferred epilogue (DEFER): when a wave holds one output component for
     // all BM pixels, it parks each finished tile in its own LDS region and
     // drains it with full-line 16-byte stores during the next tile's steps,
     // instead of every work-group writing its tile at the same moment.
-    constexpr bool DEFER = WAVES_M == 1 && WTN == BNC && P_UNIFORM && !SEP;
-    constexpr int OUT_ROW = BNC * ES;     // bytes of one pixel in a wave's region
-    constexpr int OUT_CPR = OUT_ROW / 16;  // 16-byte chunks per pixel
-    constexpr int OUT_WAVE = BM * OUT_ROW;
+    // With ALLP a wave parks its 32 pixels x all four components (rows of
+    // 4 x BNC values, component-major) and drains them itself.  The 16-byte
+    // chunks of one component's BNC values are XOR-swizzled with the pixel
+    // index modulo SWZ (their count), which spreads a wave's park stores
+    // over the banks and leaves the component segments in place.
+    constexpr bool DEFER = ALLP || (WAVES_M == 1 && WTN == BNC && P_UNIFORM && !SEP);
+    constexpr int SWZ = BNC * ES / 16;                  // chunks of one component's channels
+    constexpr int OUT_ROW = (ALLP ? 4 : 1) * BNC * ES;  // bytes of one pixel in a wave's region
+    constexpr int OUT_CPR = OUT_ROW / 16;               // 16-byte chunks per pixel
+    constexpr int OUT_PIX = ALLP ? WTM : BM;            // pixels of a wave's region
+    constexpr int OUT_WAVE = OUT_PIX * OUT_ROW;
     constexpr int N_DRAIN = OUT_WAVE / 1024;  // 1 KB stores per wave per tile
+    constexpr int PPS = 64 / OUT_CPR;         // pixels per drain store
     constexpr int OUT_BYTES = DEFER ? NCW * OUT_WAVE : 0;
-    static_assert(!DEFER || (OUT_CPR >= 2 && (64 / OUT_CPR) % OUT_CPR == 0), "drain geometry");
+    static_assert(!DEFER || (OUT_CPR >= 2 && PPS >= 1 && (ALLP || PPS % OUT_CPR == 0)), "drain geometry");
 
     __shared__ __attribute__((aligned(1024))) unsigned char smem[NBUF * (A_BYTES + B_BYTES) + OUT_BYTES];
     unsigned char *const a_lds = smem;
@@ -520,13 +545,15 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
         a_rd[j] = (wm * WTM + l32) * 128 + (((2 * j + khalf) ^ swz<8>(l32)) * 16);
     // When all N blocks of a wave lie in one output component (SHARED_P),
     // block nb's weight rows are block 0's plus 32*nb: an immediate offset.
-    constexpr bool SHARED_P = SEP || (P_UNIFORM && WTN <= BNC);
+    constexpr bool SHARED_P = SEP || ALLP || (P_UNIFORM && WTN <= BNC);
     constexpr int NB_RD = SHARED_P ? 1 : NB;
     int b_rd[NB_RD][4];
     unsigned flip[NB][4];
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
-        if constexpr (SEP) {
+        if constexpr (SEP || ALLP) {
+            // row j * BNC + o: kernel j (separable: the k-step's own kernel;
+            // ALLP: kernel m = j, read once per stage)
             const int o = wn * WTN + nb * 32 + l32;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
@@ -584,15 +611,62 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
         }
     };
 
+    // ---- all-components waves (ALLP): stage fragments ----
+    // xa0 / xa1: this wave's 32 pixels of input components 0..3 for
+    // alternate stages; xn: sign-flipped copies of the current stage's; wk[m]:
+    // the tile's rows of kernel m.  Block (p, q) of eq. 6 multiplies
+    // W_{p xor q} by x_q into output component p's accumulators.
+    u32x4 xa0[4][MB], xa1[4][MB], xn[4][MB], wk[4][NB];
+    auto rd_act = [&](unsigned off, u32x4 (&dst)[4][MB]) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb)
+                dst[q][mb] = *reinterpret_cast<const u32x4 *>(a_lds + off + mb * 32 * 128 + a_rd[q]);
+    };
+    auto rd_ker = [&](unsigned off, int m, u32x4 (&dst)[NB]) {
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+            dst[nb] = *reinterpret_cast<const u32x4 *>(b_lds + off + b_rd[0][m] + nb * 32 * CPQ * 16);
+    };
+    auto flip_act = [&](const u32x4 (&src)[MB], u32x4 (&dst)[MB]) {
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+            dst[mb] = src[mb] ^ Elem<T>::sign;
+    };
+    // the four blocks (q xor M, q) of kernel M, q = 0..3
+    auto group = [&](auto mc, const u32x4 (&x)[4][MB], const u32x4 (&xneg)[4][MB], const u32x4 (&w)[NB]) {
+        constexpr int M = decltype(mc)::value;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int p = q ^ M;
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                for (int mb = 0; mb < MB; ++mb) {
+                    if ((kHamiltonNeg >> (4 * p + q)) & 1u)
+                        mfma_step<T>(acc[p][nb][mb], w[nb], xneg[q][mb]);
+                    else
+                        mfma_step<T>(acc[p][nb][mb], w[nb], x[q][mb]);
+                }
+        }
+    };
+
     // ---- deferred-epilogue drain ----
-    // Store i of a wave's region covers pixels i*(64/OUT_CPR) + l/OUT_CPR,
-    // chunk l%OUT_CPR (its physical chunk is XOR-swizzled with the pixel).
-    // Stores past N_DRAIN, pixels past M and channels past c_out get an
-    // offset outside the buffer and are dropped.
+    // Store i of a wave's region covers pixels i*PPS + l/OUT_CPR, chunk
+    // l%OUT_CPR (its physical chunk is XOR-swizzled with the pixel).  Stores
+    // past N_DRAIN, pixels past M and channels past c_out get an offset
+    // outside the buffer and are dropped.
     constexpr int CPC = 16 / ES;  // channels per 16-byte chunk
     const bool defer = DEFER && a.c_out % CPC == 0;
+    const int region = ALLP ? wm : wn;  // the wave's parking region
     const int d_pix = lane / OUT_CPR, d_chk = lane % OUT_CPR;
-    const unsigned char *const d_lds = o_lds + wn * OUT_WAVE + d_pix * OUT_ROW + ((d_chk ^ (d_pix % OUT_CPR)) * 16);
+    // ALLP: logical chunk d_chk is component d_chk / SWZ, chunk d_chk % SWZ
+    // of its channels; the swizzle then depends on the store's pixel
+    const int d_p = d_chk / SWZ, d_k = d_chk % SWZ;
+    const unsigned char *const d_lds =
+        ALLP ? o_lds + region * OUT_WAVE
+             : o_lds + region * OUT_WAVE + d_pix * OUT_ROW + ((d_chk ^ (d_pix % OUT_CPR)) * 16);
     const int row_bytes = 4 * a.c_out * ES;
     int d_next = N_DRAIN;        // next store of the pending tile
     const T *d_base = nullptr;   // pending tile: first pixel's output row
@@ -600,7 +674,12 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
     unsigned d_lane = 0;         // lane's byte offset in a store, or out of range
     auto drain_read = [&](int i) {
         const int ic = i < N_DRAIN ? i : N_DRAIN - 1;
-        return *reinterpret_cast<const u32x4 *>(d_lds + ic * 1024);
+        if constexpr (ALLP) {
+            const int pix = ic * PPS + d_pix;
+            return *reinterpret_cast<const u32x4 *>(d_lds + pix * OUT_ROW + ((d_p * SWZ + (d_k ^ (pix % SWZ))) * 16));
+        } else {
+            return *reinterpret_cast<const u32x4 *>(d_lds + ic * 1024);
+        }
     };
     auto drain_store = [&](int i, u32x4 v) {
         const unsigned off = (i < N_DRAIN && d_lane != 0x80000000u)
@@ -625,14 +704,93 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
     //   barrier;
     //   k-step 2 on fc, reading step g+1's k-step 0 into fa;
     //   k-step 3 on fd, reading step g+1's k-step 1 into fb.
+    //
+    // All-components waves (ALLP): a stage's 16 x NB x MB MFMAs run in four
+    // groups by kernel m (group m: blocks (q xor m, q), q = 0..3), with the
+    // stage's activations and W_0, W_1 read during the previous stage:
+    //   group 0 (W_0; sign flips of x_1..x_3), reading W_2;
+    //   group 1 (W_1), reading W_3;
+    //   barrier;
+    //   group 2 (W_2), reading step g+1's x_0..x_3 and W_0;
+    //   group 3 (W_3), reading step g+1's W_1.
     constexpr int N_READ = MB + NB;
     constexpr int N_FLIP = SEP ? 0 : NB * 4;
     Frags f0, f1;
     Frags fc, fd;  // separable form only
     __syncthreads();
-    read_frags(0, 0, f0);
+    if constexpr (ALLP) {
+        rd_act(0, xa0);
+        rd_ker(0, 0, wk[0]);
+        rd_ker(0, 1, wk[1]);
+    } else {
+        read_frags(0, 0, f0);
+    }
     if constexpr (SEP)
         read_frags(0, 1, f1);
+    using G0 = std::integral_constant<int, 0>;
+    using G1 = std::integral_constant<int, 1>;
+    using G2 = std::integral_constant<int, 2>;
+    using G3 = std::integral_constant<int, 3>;
+    constexpr int G_MFMA = 4 * NB * MB;  // MFMAs of one kernel group
+    // ALLP steps keep the ring slot at run time (one wave-uniform value, a
+    // few address adds per stage) rather than unrolling the tile loop per
+    // ring phase: the phase copies of the loop cost more registers than an
+    // ALLP wave has to spare.
+    int slot = 0;  // ring slot of the next ALLP step's stage
+    auto step_allp = [&](const u32x4 (&cur)[4][MB], u32x4 (&nxt)[4][MB]) {
+        const int ns = (slot + 1) & (NBUF - 1);
+        const unsigned cb = unsigned(slot) * B_BYTES;
+        const unsigned na = unsigned(ns) * A_BYTES, nb_ = unsigned(ns) * B_BYTES;
+        u32x4 dv0;
+        if constexpr (DEFER)
+            dv0 = drain_read(d_next);
+        __builtin_amdgcn_sched_barrier(0);
+        rd_ker(cb, 2, wk[2]);
+        flip_act(cur[1], xn[1]);
+        flip_act(cur[2], xn[2]);
+        flip_act(cur[3], xn[3]);
+        group(G0{}, cur, xn, wk[0]);
+        interleave_kstep<G_MFMA, 12 * MB, NB>();
+        __builtin_amdgcn_sched_barrier(0);
+        rd_ker(cb, 3, wk[3]);
+        group(G1{}, cur, xn, wk[1]);
+        interleave_kstep<G_MFMA, 0, NB>();
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (DEFER) {
+            drain_store(d_next, dv0);
+            d_next = d_next < N_DRAIN ? d_next + 1 : N_DRAIN;
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        __syncthreads();
+        rd_act(na, nxt);
+        rd_ker(nb_, 0, wk[0]);
+        group(G2{}, cur, xn, wk[2]);
+        interleave_kstep<G_MFMA, 0, 4 * MB + NB>();
+        __builtin_amdgcn_sched_barrier(0);
+        rd_ker(nb_, 1, wk[1]);
+        group(G3{}, cur, xn, wk[3]);
+        interleave_kstep<G_MFMA, 0, NB>();
+        __builtin_amdgcn_sched_barrier(0);
+        slot = ns;
+    };
+    // One tile: its S steps, two per iteration (activation sets alternate);
+    // an odd last step leaves the next stage's activations in xa1, moved
+    // back to xa0.
+    auto run_tile_allp = [&]() {
+        int t = 0;
+        for (; t + 2 <= S; t += 2) {
+            step_allp(xa0, xa1);
+            step_allp(xa1, xa0);
+        }
+        if (t < S) {
+            step_allp(xa0, xa1);
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+                for (int mb = 0; mb < MB; ++mb)
+                    xa0[q][mb] = xa1[q][mb];
+        }
+    };
     auto step_sep = [&](auto slot) {
         constexpr int B = decltype(slot)::value;
         // accumulator set of k-step j: component j, or with paired stages
@@ -664,6 +822,7 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
             step_sep(slot);
             return;
         }
+
         constexpr int B = decltype(slot)::value;  // ring slot of this step's stage
         // one drain store per step: read from LDS now, stored after k-step 1
         u32x4 dv0;
@@ -796,8 +955,86 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
             const int mt = m0 / BM;
             const size_t cols = size_t(4) * a.c_out;
             const size_t col = size_t(wn) * a.c_out + o0 + ch;
-            a.stats[col * a.m_tiles + mt] = mean;
-            a.stats[(cols + col) * a.m_tiles + mt] = m2;
+            a.stats[col * a.stat_tiles + mt] = mean;
+            a.stats[(cols + col) * a.stat_tiles + mt] = m2;
+        }
+    };
+
+    // The same statistics for an ALLP wave's region: 32 pixels (from mw on)
+    // x four components, each component's BNC channels read back and reduced
+    // as above; one partial per 32-pixel sub-tile (index mw / 32) and column.
+    auto tile_stats_allp = [&](const auto *w_lds, int mw, int o0) {
+        static_assert(ES == 2 && (BNC == 64 || BNC == 32), "statistics read-back geometry");
+        typedef short s16x4 __attribute__((ext_vector_type(4)));
+        typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+        constexpr int NCG = BNC / 4;     // 4-channel groups per component
+        constexpr int LPS = 4 * NCG;     // lanes per pixel set: one per channel
+        constexpr int SETS = 64 / LPS;   // pixel sets read side by side
+        constexpr int PPR = 4 * SETS;    // pixels per read
+        constexpr int NR = WTM / PPR;    // reads per lane and component
+        static_assert(SWZ % PPR == 0 || PPR % SWZ == 0, "swizzle splits into lane and read parts");
+        const int n_valid = a.m - mw < WTM ? a.m - mw : WTM;
+        if (n_valid <= 0)
+            return;  // the whole sub-tile lies past M (wave-uniform)
+        const int q = 4 * (lane >> 4) + (lane & 3);
+        const int cg = q % NCG, set = q / NCG, r = (lane & 15) >> 2;
+        const int p_lane = 4 * set + r;
+        const int ch = lane % LPS;
+        const float n_inv = float(WTM - n_valid);
+        const bf16x2 ones = __builtin_bit_cast(bf16x2, 0x3F803F80u);
+        const int st = mw / WTM;
+        const size_t cols = size_t(4) * a.c_out;
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+            // physical chunk = p * SWZ + (logical ^ (pixel % SWZ)); pixel =
+            // p_lane + PPR * i, whose two parts share no bit below SWZ
+            auto piece = [&](int xr) {
+                return w_lds + p_lane * OUT_ROW + ((p * SWZ + (((cg >> 1) ^ (p_lane % SWZ)) ^ xr)) * 16) +
+                       (cg & 1) * 8;
+            };
+            const unsigned char *const src0 = piece(0);
+            const unsigned char *const src4 = piece(4 % SWZ);
+            unsigned dw[2 * NR];
+#pragma unroll
+            for (int i = 0; i < NR; ++i) {
+                const int xr = (PPR * i) % SWZ;
+                const unsigned char *pp = (xr == 0 ? src0 : src4) + i * PPR * OUT_ROW;
+                const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4 *)(pp));
+                __builtin_memcpy(&dw[2 * i], &v, 8);
+            }
+            float v_inv = 0.0f;
+            if (n_valid < WTM) {
+                const int pm = WTM - 1;
+                const T t = *reinterpret_cast<const T *>(w_lds + pm * OUT_ROW +
+                                                         ((p * SWZ + ((ch / 8) ^ (pm % SWZ))) * 16) + (ch % 8) * 2);
+                v_inv = float(t);
+            }
+            float sacc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int i = 0; i < 2 * NR; ++i)
+                sacc[i & 3] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, dw[i]), ones, sacc[i & 3], false);
+            float sum = (sacc[0] + sacc[1]) + (sacc[2] + sacc[3]);
+            if constexpr (SETS == 2)
+                sum += __shfl_xor(sum, 32);
+            const float mean = (sum - n_inv * v_inv) / float(n_valid);
+            float m[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int i = 0; i < 2 * NR; ++i) {
+                const float lo = __builtin_bit_cast(float, dw[i] << 16) - mean;
+                const float hi = __builtin_bit_cast(float, dw[i] & 0xffff0000u) - mean;
+                m[i & 3] = fmaf(lo, lo, m[i & 3]);
+                m[(i + 2) & 3] = fmaf(hi, hi, m[(i + 2) & 3]);
+            }
+            float m2 = (m[0] + m[1]) + (m[2] + m[3]);
+            if constexpr (SETS == 2)
+                m2 += __shfl_xor(m2, 32);
+            const float dv = v_inv - mean;
+            m2 = fmaxf(m2 - n_inv * dv * dv, 0.0f);
+            if (lane < LPS && o0 + ch < a.c_out) {
+                const size_t col = size_t(p) * a.c_out + o0 + ch;
+                a.stats[col * a.stat_tiles + st] = mean;
+                a.stats[(cols + col) * a.stat_tiles + st] = m2;
+            }
         }
     };
 
@@ -835,15 +1072,19 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
 #pragma unroll
                     for (int e = 0; e < 16; ++e)
                         acc[qs][nb][mb][e] = 0.0f;
-        if (ph == 0)
-            run_tile(P0{});
-        else if (ph == 1)
-            run_tile(P1{});
-        else if (ph == 2)
-            run_tile(P2{});
-        else
-            run_tile(P3{});
-        ph = (ph + S) & 3;
+        if constexpr (ALLP) {
+            run_tile_allp();
+        } else {
+            if (ph == 0)
+                run_tile(P0{});
+            else if (ph == 1)
+                run_tile(P1{});
+            else if (ph == 2)
+                run_tile(P2{});
+            else
+                run_tile(P3{});
+            ph = (ph + S) & 3;
+        }
 
         if (defer) {
             // finish the previous tile's stores before its region is reused
@@ -853,7 +1094,77 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
             // channel 8*g + 4*(l/32) + e of the 32-channel block nb and pixel
             // l%32 of block mb; bias added (or the folded affine map and
             // ReLU applied), rounded to T
-            unsigned char *const w_lds = o_lds + wn * OUT_WAVE;
+            unsigned char *const w_lds = o_lds + region * OUT_WAVE;
+            if constexpr (ALLP) {
+                // the wave's 32 pixels, all four components: row l%32,
+                // component p, chunk nb*4 + g of its channels (swizzled),
+                // half l/32 of it
+                auto park_allp = [&](auto affine) {
+                    constexpr bool AFFINE = decltype(affine)::value;
+#pragma unroll
+                    for (int pb = 0; pb < 4 * NB; ++pb) {
+                        // one 32-channel block of one component; its
+                        // per-column map is loaded before any of it is used
+                        // (one memory latency per block)
+                        const int p = pb / NB, nb = pb % NB;
+                        float sc[4][4], sh[4][4];
+                        if constexpr (AFFINE) {
+#pragma unroll
+                                for (int g = 0; g < 4; ++g) {
+                                    const int oc = nb * 32 + 8 * g + 4 * khalf;
+                                    const bool in4 = o0 + oc < a.c_out;
+                                    const int col = in4 ? p * a.c_out + o0 + oc : 0;
+                                    if constexpr (EPI == kEpiFold) {
+                                        const f32x4 s4 = *reinterpret_cast<const f32x4 *>(a.scale + col);
+                                        const f32x4 h4 = *reinterpret_cast<const f32x4 *>(a.shift + col);
+#pragma unroll
+                                        for (int e = 0; e < 4; ++e) {
+                                            sc[g][e] = in4 ? s4[e] : 0.0f;
+                                            sh[g][e] = in4 ? h4[e] : 0.0f;
+                                        }
+                                    } else {
+#pragma unroll
+                                        for (int e = 0; e < 4; ++e) {
+                                            sc[g][e] = 1.0f;
+                                            const float b = float(bias[col + e]);
+                                            sh[g][e] = in4 ? b : 0.0f;
+                                        }
+                                    }
+                                }
+                        }
+#pragma unroll
+                            for (int g = 0; g < 4; ++g) {
+                                T v[4];
+#pragma unroll
+                                for (int e = 0; e < 4; ++e) {
+                                    if constexpr (AFFINE)
+                                        v[e] = T(epi(acc[p][nb][0][4 * g + e], sc[g][e], sh[g][e]));
+                                    else
+                                        v[e] = T(acc[p][nb][0][4 * g + e]);
+                                }
+                                unsigned char *dst = w_lds + l32 * OUT_ROW +
+                                                     ((p * SWZ + ((nb * 4 + g) ^ (l32 % SWZ))) * 16) + khalf * 8;
+                                uint2 pk;
+                                __builtin_memcpy(&pk, v, 8);
+                                *reinterpret_cast<uint2 *>(dst) = pk;
+                            }
+                    }
+                };
+                if (EPI == kEpiFold || bias != nullptr)
+                    park_allp(std::true_type{});
+                else
+                    park_allp(std::false_type{});
+                const int mw = m0 + wm * WTM;  // the wave's first pixel
+                if constexpr (EPI == kEpiStats)
+                    tile_stats_allp(w_lds, mw, o0);
+                const long long rows_left = (long long)(a.m - mw) * row_bytes;
+                d_base = out + (size_t)mw * 4 * a.c_out;
+                d_bytes = rows_left <= 0 ? 0u : rows_left < 0x7fffffffLL ? unsigned(rows_left) : 0x7fffffffu;
+                const int ch = o0 + d_k * CPC;  // first channel of the lane's chunk
+                d_lane = ch < a.c_out ? unsigned(d_pix * row_bytes + (d_p * a.c_out + ch) * ES) : 0x80000000u;
+                d_next = 0;
+                continue;
+            }
             // AFFINE: a per-column map to apply (bias or the folded IQBN);
             // without one the accumulators are only rounded.
             auto park = [&](auto affine) {
@@ -1026,7 +1337,21 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
         for (int nb = 0; nb < NB; ++nb) {
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
-                if constexpr (SEP) {
+                if constexpr (ALLP) {
+                    // c_out not a whole number of 16-byte chunks: direct stores
+                    const int o = o0 + nb * 32 + 8 * g + 4 * khalf;
+                    const int m = m0 + wm * WTM + l32;
+                    if (o >= a.c_out || m >= a.m)
+                        continue;
+#pragma unroll
+                    for (int p = 0; p < 4; ++p) {
+                        float y[4];
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            y[e] = acc[p][nb][0][4 * g + e];
+                        store4(m, p, o, y);
+                    }
+                } else if constexpr (SEP) {
                     const int o = o0 + wn * WTN + nb * 32 + 8 * g + 4 * khalf;
                     if (o >= a.c_out)
                         continue;
@@ -1160,6 +1485,7 @@ struct KernelEntry {
     int bm, bnc, mb, nb, threads;
     bool sep;    // separable convolution (eq. 7) instead of the Hamilton product
     bool defer;  // deferred epilogue (one output component per wave); writes IQBN statistics
+    int stat_rows;  // output pixels per statistics partial
     DType dt;
     // [epilogue kind][variant]: variant 0 when c_in is a multiple of the
     // 16-byte vector (activations move by DMA), 1 for element loads with
@@ -1204,7 +1530,7 @@ constexpr const void *fold_fn()
     KernelEntry                                                                                        \
     {                                                                                                  \
         32 * (MB) * (WM), ((SEP) ? 32 : 8) * (NB) * (WN), MB, NB, 64 * ((WM) * (WN) + producer_waves<T, MB, NB, WM, WN, SEP>()), SEP, \
-            QCONV_DEFER(NB, WM, WN, SEP), DT,                                                          \
+            QCONV_DEFER(NB, WM, WN, SEP), 32 * (MB) * (WM), DT,                                        \
             {{(const void *)&qconv2d_igemm<T, MB, NB, WM, WN, true, kEpiBias, SEP>,                    \
               (const void *)&qconv2d_igemm<T, MB, NB, WM, WN, false, kEpiBias, SEP>,                   \
               pair_fn<T, MB, NB, WM, WN, kEpiBias, SEP>()},                                              \
@@ -1216,10 +1542,29 @@ constexpr const void *fold_fn()
             #T "_mb" #MB "x" #WM "_nb" #NB "x" #WN #SEP                                                \
     }
 
+// Hamilton product in bf16 with all-components waves (4 waves of 32 pixels
+// x all four components of 32*NB channels); statistics per 32-pixel wave.
+#define QCONV_KA(NB)                                                                                   \
+    KernelEntry                                                                                        \
+    {                                                                                                  \
+        128, 32 * (NB), 1, NB, 64 * (4 + producer_waves<__bf16, 1, NB, 4, 1, false, true>()), false, true, 32, \
+            DType::BF16,                                                                               \
+            {{(const void *)&qconv2d_igemm<__bf16, 1, NB, 4, 1, true, kEpiBias, false, false, true>,    \
+              (const void *)&qconv2d_igemm<__bf16, 1, NB, 4, 1, false, kEpiBias, false, false, true>,   \
+              nullptr},                                                                                \
+             {(const void *)&qconv2d_igemm<__bf16, 1, NB, 4, 1, true, kEpiStats, false, false, true>,   \
+              (const void *)&qconv2d_igemm<__bf16, 1, NB, 4, 1, false, kEpiStats, false, false, true>,  \
+              nullptr},                                                                                \
+             {(const void *)&qconv2d_igemm<__bf16, 1, NB, 4, 1, true, kEpiFold, false, false, true>,    \
+              (const void *)&qconv2d_igemm<__bf16, 1, NB, 4, 1, false, kEpiFold, false, false, true>,   \
+              nullptr}},                                                                               \
+            "bf16_allp_nb" #NB                                                                         \
+    }
+
 const KernelEntry kKernels[] = {
     // Hamilton product (eq. 5)
-    QCONV_K(__bf16, DType::BF16, 4, 2, 1, 4, false),  // 128 px x 64 channels
-    QCONV_K(__bf16, DType::BF16, 4, 1, 1, 4, false),  // 128 px x 32 channels
+    QCONV_KA(2),  // 128 px x 64 channels
+    QCONV_KA(1),  // 128 px x 32 channels
     // (no bf16 16-channel tile: with four producers the 32-channel tile is
     // faster at 16 output channels too: 27.5 vs 32.3 us on 128 images of
     // 32x32, 16 -> 16 channels)
@@ -1332,6 +1677,8 @@ ConvPlan qconv2d_plan(const ConvGeom &g, DType dt, bool sep)
     p.bnc = k.bnc;
     p.n_tiles = (g.c_out + k.bnc - 1) / k.bnc;
     p.m_tiles = int((m + k.bm - 1) / k.bm);
+    p.stat_rows = k.stat_rows;
+    p.stat_tiles = int((m + k.stat_rows - 1) / k.stat_rows);
     p.name = k.name;
     return p;
 }
@@ -1484,6 +1831,7 @@ hipError_t qconv2d_run(const ConvPlan &plan, const PackGeom &pg, const ConvGeom 
     a.w_bytes = unsigned(pg.bytes);
     a.x_elems = (long long)g.n * g.h * g.w * 4 * g.c_in;
     a.stats = stats;
+    a.stat_tiles = plan.stat_tiles;
     a.scale = fold != nullptr ? fold->scale : nullptr;
     a.shift = fold != nullptr ? fold->shift : nullptr;
     a.relu = fold != nullptr && fold->relu ? 1 : 0;

@@ -431,13 +431,13 @@ QUAN_API int quan_qconv2d_iqbn_forward(const void *x, const void *packed, const 
     hipError_t e;
     if (stats != QUAN_STATS_PASS && quan::qconv2d_writes_stats(plan, g, dt)) {
         // statistics gathered in the convolution's epilogue
-        if (int rc = workspace(stream, kIqbnPartials, quan::iqbn_tile_stats_bytes(plan.m_tiles, c_out), &work))
+        if (int rc = workspace(stream, kIqbnPartials, quan::iqbn_tile_stats_bytes(plan.stat_tiles, c_out), &work))
             return rc;
         e = quan::qconv2d_run(plan, pg, g, dt, x, packed, bias, out, static_cast<float *>(work), nullptr, s);
         if (e != hipSuccess)
             return fail_hip(e, "qconv2d launch");
-        e = quan::iqbn_from_tiles_run(static_cast<const float *>(work), plan.m_tiles, plan.bm, gamma, beta,
-                                      eps, relu != 0, out, mean, var, pixels, c_out, dt, s);
+        e = quan::iqbn_from_tiles_run(static_cast<const float *>(work), plan.stat_tiles, plan.stat_rows, gamma,
+                                      beta, eps, relu != 0, out, mean, var, pixels, c_out, dt, s);
     } else {
         if (int rc = workspace(stream, kIqbnPartials, quan::iqbn_workspace_bytes(pixels, c_out), &work))
             return rc;

@@ -38,6 +38,8 @@ struct ConvPlan {
     int id;              // index into the kernel table
     int bm, bnc;         // output pixels, output channels per component
     int m_tiles, n_tiles;
+    int stat_rows;       // output pixels per IQBN statistics partial
+    int stat_tiles;      // statistics partials per column: ceil(m / stat_rows)
     const char *name;
 };
 
@@ -51,10 +53,11 @@ hipError_t qconv2d_pack_weights(const PackGeom &pg, int c_in, int c_out, int k_h
                                 const void *w_k, void *wpack, hipStream_t stream);
 
 // The implicit-GEMM Hamilton convolution.  With `stats` non-NULL (only where
-// qconv2d_writes_stats holds) it also writes per-M-tile IQBN statistics of
-// its output: stats[0][col][mt] = tile mean, stats[1][col][mt] = sum of
-// squared deviations from it, col = p * c_out + o, mt < plan.m_tiles; tile mt
-// covers pixels [mt * plan.bm, min((mt + 1) * plan.bm, m)).
+// qconv2d_writes_stats holds) it also writes IQBN statistics of its output
+// per run of plan.stat_rows consecutive output pixels: stats[0][col][t] =
+// the run's mean, stats[1][col][t] = sum of squared deviations from it,
+// col = p * c_out + o, t < plan.stat_tiles; run t covers pixels
+// [t * stat_rows, min((t + 1) * stat_rows, m)).
 //
 // With `fold` non-NULL the epilogue applies out = scale[col] * acc +
 // shift[col] (fp32, [4][c_out] each, col = p * c_out + o) and max(0, .) when
