@@ -195,6 +195,24 @@ QUAN_API int quan_iqbn_forward(const void *x, const float *gamma, const float *b
                                int32_t n, int32_t c, int32_t h, int32_t w,
                                int32_t dtype, void *stream);
 
+/*
+ * quan_iqbn_forward for callers that cannot allocate device memory: code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  Same arguments, result and validation as quan_iqbn_forward;
+ * the partial statistics live in a fixed 8 MiB array of device memory per
+ * GPU (held until the process ends) instead of a library workspace, so the
+ * call performs no allocation.  It returns QUAN_ERR_UNSUPPORTED, before any
+ * device work, when the tensor needs more scratch than that ((2 * blocks +
+ * 3) * 4c floats, at most 512 blocks: up to 510 channels at any size,
+ * more for small batches).  Every call on one GPU shares that GPU's array:
+ * calls that may overlap in time (other streams, other threads) race, and
+ * must be serialised by the caller.
+ */
+QUAN_API int quan_iqbn_forward_noalloc(const void *x, const float *gamma, const float *beta,
+                                       float eps, void *out, float *mean, float *var,
+                                       int32_t n, int32_t c, int32_t h, int32_t w,
+                                       int32_t dtype, void *stream);
+
 /* As quan_iqbn_forward, followed by a component-wise max(0, .) on out (the
  * IQBN + ReLU pairing of the quaternion networks of Section IV). */
 QUAN_API int quan_iqbn_relu_forward(const void *x, const float *gamma, const float *beta,

@@ -171,11 +171,29 @@ int check_conv(const void *x, const void *bias, int32_t stride_h, int32_t stride
     return QUAN_OK;
 }
 
-int iqbn_common(const void *x, const float *gamma, const float *beta, float eps, void *out,
-                float *mean, float *var, int32_t n, int32_t c, int32_t h, int32_t w, int32_t dtype,
-                void *stream, bool relu)
+}  // namespace
+
+namespace quan {
+
+void clear_error()
 {
     g_last_error.clear();
+}
+
+int report(int code, const char *fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return code;
+}
+
+int iqbn_validate(const void *x, const float *gamma, const float *beta, float eps, const void *out,
+                  const float *mean, const float *var, int32_t n, int32_t c, int32_t h, int32_t w, int32_t dtype)
+{
     if (!x || !gamma || !beta || !out || !mean || !var)
         return fail(QUAN_ERR_NULL, "iqbn: x, gamma, beta, out, mean and var must be non-NULL");
     if (int rc = check_dtype(dtype))
@@ -201,7 +219,21 @@ int iqbn_common(const void *x, const float *gamma, const float *beta, float eps,
         overlaps(var, sbytes, x, xbytes) || overlaps(mean, sbytes, out, xbytes) ||
         overlaps(var, sbytes, out, xbytes))
         return fail(QUAN_ERR_ALIAS, "iqbn: mean/var overlap each other or a tensor");
+    return QUAN_OK;
+}
 
+}  // namespace quan
+
+namespace {
+
+int iqbn_common(const void *x, const float *gamma, const float *beta, float eps, void *out,
+                float *mean, float *var, int32_t n, int32_t c, int32_t h, int32_t w, int32_t dtype,
+                void *stream, bool relu)
+{
+    g_last_error.clear();
+    if (int rc = quan::iqbn_validate(x, gamma, beta, eps, out, mean, var, n, c, h, w, dtype))
+        return rc;
+    const int64_t pixels = int64_t(n) * h * w;
     const quan::DType dt = to_dt(dtype);
     void *work = nullptr;
     if (int rc = workspace(stream, kIqbnPartials, quan::iqbn_workspace_bytes(pixels, c), &work))

@@ -93,6 +93,16 @@ hipError_t qconv2d_backward_weight_run(const ConvGeom &g, DType dt, const void *
                                        float *dw_i, float *dw_j, float *dw_k, float *db, void *work,
                                        hipStream_t stream);
 
+// Error reporting shared by the entry points of every source file: report()
+// stores the thread's last-error message and returns `code`.
+void clear_error();
+int report(int code, const char *fmt, ...);
+
+// Argument checks of quan_iqbn_forward (QUAN_OK, or a QUAN_ERR_* code with
+// the message set); they touch no device state.
+int iqbn_validate(const void *x, const float *gamma, const float *beta, float eps, const void *out,
+                  const float *mean, const float *var, int32_t n, int32_t c, int32_t h, int32_t w, int32_t dtype);
+
 // IQBN.  `work` must hold iqbn_workspace_bytes(...) bytes.
 size_t iqbn_workspace_bytes(int64_t pixels, int c);
 hipError_t iqbn_run(const void *x, const float *gamma, const float *beta, float eps, bool relu,

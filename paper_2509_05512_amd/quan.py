@@ -44,6 +44,7 @@ SIGNATURES = {
     "quan_iqbn_backward": (ctypes.c_int, [_vp] * 6 + [_f32] + [_vp] * 3 + [_i32] * 5 + [_vp]),
     "quan_iqbn_forward": (ctypes.c_int, [_vp, _vp, _vp, _f32, _vp, _vp, _vp] + [_i32] * 5 + [_vp]),
     "quan_iqbn_relu_forward": (ctypes.c_int, [_vp, _vp, _vp, _f32, _vp, _vp, _vp] + [_i32] * 5 + [_vp]),
+    "quan_iqbn_forward_noalloc": (ctypes.c_int, [_vp, _vp, _vp, _f32, _vp, _vp, _vp] + [_i32] * 5 + [_vp]),
     "quan_last_error": (ctypes.c_char_p, []),
     "quan_release": (ctypes.c_int, []),
     "quan_version": (ctypes.c_char_p, []),
@@ -469,6 +470,13 @@ def quan_iqbn_forward(x, gamma, beta, eps=1e-5, out=None, mean=None, var=None):
 def quan_iqbn_relu_forward(x, gamma, beta, eps=1e-5, out=None, mean=None, var=None):
     """IQBN followed by a component-wise ReLU.  Returns (out, mean, var)."""
     return _iqbn("quan_iqbn_relu_forward", x, gamma, beta, eps, out, mean, var)
+
+
+def quan_iqbn_forward_noalloc(x, gamma, beta, eps=1e-5, out=None, mean=None, var=None):
+    """IQBN with the partial statistics in the library's fixed per-GPU scratch
+    array (no device allocation by the call; out, mean and var must then be
+    passed in for an allocation-free call).  Returns (out, mean, var)."""
+    return _iqbn("quan_iqbn_forward_noalloc", x, gamma, beta, eps, out, mean, var)
 
 
 def quan_last_error() -> str:

@@ -61,10 +61,10 @@ def conv(lib, fn="quan_qconv2d_forward", **kw):
     return rc, lib.quan_last_error().decode()
 
 
-def iqbn(lib, relu=False, **kw):
+def iqbn(lib, relu=False, fn_name=None, **kw):
     a = dict(x=X, g=G, b=BE, eps=1e-5, out=OUT, mean=MEAN, var=VAR, n=2, c=4, h=8, w=8, dtype=1)
     a.update(kw)
-    fn = lib.quan_iqbn_relu_forward if relu else lib.quan_iqbn_forward
+    fn = getattr(lib, fn_name) if fn_name else (lib.quan_iqbn_relu_forward if relu else lib.quan_iqbn_forward)
     rc = fn(a["x"], a["g"], a["b"], a["eps"], a["out"], a["mean"], a["var"], a["n"], a["c"],
             a["h"], a["w"], a["dtype"], None)
     return rc, lib.quan_last_error().decode()
@@ -316,12 +316,22 @@ IQBN_ERRORS = [
 ]
 
 
-@pytest.mark.parametrize("relu", [False, True])
+@pytest.mark.parametrize("fn_name", ["quan_iqbn_forward", "quan_iqbn_relu_forward", "quan_iqbn_forward_noalloc"])
 @pytest.mark.parametrize("name,kw,code", IQBN_ERRORS, ids=[c[0] for c in IQBN_ERRORS])
-def test_iqbn_rejects(lib, name, kw, code, relu):
-    rc, msg = iqbn(lib, relu=relu, **kw)
+def test_iqbn_rejects(lib, name, kw, code, fn_name):
+    rc, msg = iqbn(lib, fn_name=fn_name, **kw)
     assert rc == code, (name, rc, msg)
     assert msg
+
+
+def test_iqbn_noalloc_rejects_more_scratch_than_it_holds(lib):
+    """12288 rows of 4000 columns: 512 statistics blocks per column group
+    need (2 * 512 + 3) * 4000 floats = 16.4 MB of scratch, beyond the fixed
+    8 MiB array; refused before any device work, with a message naming the
+    sizes.  quan_iqbn_forward (which allocates) accepts the same arguments
+    up to the same point, i.e. the shape itself is valid."""
+    rc, msg = iqbn(lib, fn_name="quan_iqbn_forward_noalloc", n=1, c=1000, h=128, w=96)
+    assert rc == E_UNSUP and "scratch" in msg, (rc, msg)
 
 
 def test_error_message_is_per_call(lib):
