@@ -24,6 +24,8 @@ SHAPES = [
     (7, 2, 1, 1),
     (1, 1, 1, 1),          # one value per column
     (64, 8, 32, 16),       # many rows, many blocks
+    (32, 256, 14, 14),     # the deep-stack layer
+    (64, 16, 32, 32),      # 86 statistics blocks per column group
 ]
 
 
@@ -107,3 +109,38 @@ def test_iqbn_deterministic(dtype):
     o2, m2, v2 = _run(x, g, b, 1e-5, False)
     assert torch.equal(o1.cpu(), o2.cpu()) and torch.equal(m1.cpu(), m2.cpu()) \
         and torch.equal(v1.cpu(), v2.cpu())
+
+
+@pytest.mark.parametrize("case", [("bf16", True), ("fp32", False)])
+def test_iqbn_two_column_groups_many_block_groups(case):
+    """18432 rows of 2400 columns: two column groups of 512 statistics blocks
+    each, merged per column in block order."""
+    dtype, relu = case
+    say(f"iqbn column groups x block groups {dtype} relu={relu}")
+    dt = DT[dtype]
+    x, g, b = _case((8, 600, 48, 48), dt, seed=21)
+    out, mean, var = _run(x, g, b, 1e-5, relu)
+    ref, rmean, rvar = oracle.iqbn(f64(x), f64(g), f64(b), 1e-5, relu)
+    assert_close(f64(mean), rmean, dt, "mean")
+    assert_close(f64(var), rvar, dt, "var")
+    assert_close(f64(out), ref, dt, "out")
+
+
+def test_iqbn_repeated_calls_reuse_counters():
+    """Calls of different shapes one after another on one stream sharing one
+    workspace: every call matches the oracle, and repeating a call repeats
+    its result bit for bit."""
+    say("iqbn repeated calls")
+    shapes = [(64, 16, 32, 32), (32, 256, 14, 14), (64, 16, 32, 32), (2, 4, 16, 16), (64, 16, 32, 32)]
+    first = None
+    for i, shape in enumerate(shapes):
+        x, g, b = _case(shape, torch.bfloat16, seed=40 + (i % 2))
+        out, mean, var = _run(x, g, b, 1e-5, False)
+        ref, rmean, rvar = oracle.iqbn(f64(x), f64(g), f64(b), 1e-5, False)
+        assert_close(f64(var), rvar, torch.bfloat16, f"var call {i}")
+        assert_close(f64(out), ref, torch.bfloat16, f"out call {i}")
+        if shape == shapes[0]:
+            if first is None:
+                first = (out.cpu(), mean.cpu(), var.cpu())
+            elif i == 4:
+                assert torch.equal(first[0], out.cpu()) and torch.equal(first[2], var.cpu())
