@@ -2,7 +2,7 @@
 
 Slow, plain fp64 reference implementations, written from the paper in C
 (quan_oracle.c): the quaternion convolution (Section III-B, eqs. 5/6) and its
-gradients, the separable convolution (eq. 7), Independent Quaternion Batch
+gradients, the separable convolution (eq. 7) and its gradients (eqs. 8-10), Independent Quaternion Batch
 Normalization (Section III-C, eqs. 11/12) in training and inference form and
 its gradients, and the Poincare input mapping (Section III-A, eq. 4).
 Only the tests, the smoke check and the benchmark's CPU-baseline leg may import
@@ -59,6 +59,8 @@ class Oracle:
         lib.quan_oracle_poincare.restype = None
         lib.quan_oracle_qconv2d_backward.argtypes = [_D] * 6 + [_I64] * 13
         lib.quan_oracle_qconv2d_backward.restype = None
+        lib.quan_oracle_qconv2d_separable_backward.argtypes = [_D] * 6 + [_I64] * 13
+        lib.quan_oracle_qconv2d_separable_backward.restype = None
         lib.quan_oracle_iqbn_backward.argtypes = [_D, _D, _D, ctypes.c_double, ctypes.c_int,
                                                   _D, _D, _D, _D] + [_I64] * 4
         lib.quan_oracle_iqbn_backward.restype = None
@@ -132,6 +134,17 @@ class Oracle:
         dx, dwt, db = np.empty_like(x), np.empty_like(w), np.empty((4, dims[4]))
         self.lib.quan_oracle_qconv2d_backward(_ptr(x), _ptr(w), _ptr(dy), _ptr(dx), _ptr(dwt), _ptr(db),
                                               *dims)
+        return dx, dwt, db
+
+    def qconv2d_separable_backward(self, x, w, dy, stride=1, pad=0, dilation=1):
+        """Gradients of qconv2d_separable (eq. 7) for dL/dY = dy, by eqs. 8-10
+        with the printed mixing matrix M: returns (dx, dw, db)."""
+        x, w, dy = _f64(x), _f64(w), _f64(dy)
+        dims, Ho, Wo = self._conv_dims(x, w, stride, pad, dilation)
+        assert dy.shape == (dims[0], 4, dims[4], Ho, Wo)
+        dx, dwt, db = np.empty_like(x), np.empty_like(w), np.empty((4, dims[4]))
+        self.lib.quan_oracle_qconv2d_separable_backward(_ptr(x), _ptr(w), _ptr(dy), _ptr(dx), _ptr(dwt),
+                                                        _ptr(db), *dims)
         return dx, dwt, db
 
     def iqbn_inference(self, x, mean, var, gamma, beta, eps=1e-5, relu=False):
@@ -220,6 +233,10 @@ def qconv2d_separable(x, w, bias=None, stride=1, pad=0, dilation=1):
 
 def qconv2d_backward(x, w, dy, stride=1, pad=0, dilation=1):
     return default().qconv2d_backward(x, w, dy, stride, pad, dilation)
+
+
+def qconv2d_separable_backward(x, w, dy, stride=1, pad=0, dilation=1):
+    return default().qconv2d_separable_backward(x, w, dy, stride, pad, dilation)
 
 
 def iqbn_inference(x, mean, var, gamma, beta, eps=1e-5, relu=False):

@@ -225,6 +225,119 @@ void quan_oracle_qconv2d_separable(const double *x, const double *w, const doubl
 }
 
 /* ------------------------------------------------------------------------ */
+/* Backward pass of the separable convolution, Section III-B, eqs. 8-10.  The
+ * gradients keep eq. 7's separable structure: the output gradients are
+ * mixed by the matrix M printed with eq. 9, and each mixed component z_q
+ * then meets only its own kernel W_q and input x_q:
+ *
+ *   z_q[n,o,oy,ox] = sum_p M[q][p] dy_p[n,o,oy,ox]
+ *   dx_q[n,c,iy,ix] += W_q[o,c,ky,kx] z_q[n,o,oy,ox]     (a transposed conv)
+ *   dW_q[o,c,ky,kx] += x_q[n,c,iy,ix] z_q[n,o,oy,ox]      (a correlation)
+ *   db_p[o]         += dy_p[n,o,oy,ox]
+ *
+ * over every (n, o, oy, ox, c, ky, kx) whose tap lies inside the image.  The
+ * printed equations index M_q^T ambiguously; read as M[q][p] = S[p][q]
+ * (M is eq. 7's sign matrix transposed), this is the exact adjoint of
+ * quan_oracle_qconv2d_separable.  dx, dw and db are overwritten; any may be
+ * NULL (not computed). */
+static const double kMixing[4][4] = {
+    {1.0, 1.0, 1.0, 1.0},
+    {-1.0, 1.0, -1.0, 1.0},
+    {-1.0, 1.0, 1.0, -1.0},
+    {-1.0, -1.0, 1.0, 1.0},
+};
+
+void quan_oracle_qconv2d_separable_backward(const double *x, const double *w, const double *dy,
+                                            double *dx, double *dwt, double *db,
+                                            int64_t N, int64_t Cin, int64_t H, int64_t W,
+                                            int64_t Cout, int64_t KH, int64_t KW,
+                                            int64_t sh, int64_t sw, int64_t ph, int64_t pw,
+                                            int64_t dh, int64_t dw)
+{
+    const int64_t Ho = quan_oracle_out_size(H, KH, sh, ph, dh);
+    const int64_t Wo = quan_oracle_out_size(W, KW, sw, pw, dw);
+    const int64_t wq = Cout * Cin * KH * KW;
+    const int64_t xq = Cin * H * W;
+    const int64_t yq = Cout * Ho * Wo;
+
+    if (dx) {
+        for (int64_t i = 0; i < N * 4 * xq; ++i)
+            dx[i] = 0.0;
+        /* each image's input gradient is written by one thread */
+#pragma omp parallel for schedule(dynamic)
+        for (int64_t n = 0; n < N; ++n) {
+            for (int64_t o = 0; o < Cout; ++o)
+                for (int64_t oy = 0; oy < Ho; ++oy)
+                    for (int64_t ox = 0; ox < Wo; ++ox) {
+                        double z[4];
+                        for (int q = 0; q < 4; ++q) {
+                            z[q] = 0.0;
+                            for (int p = 0; p < 4; ++p)
+                                z[q] += kMixing[q][p] * dy[n * 4 * yq + p * yq + (o * Ho + oy) * Wo + ox];
+                        }
+                        for (int q = 0; q < 4; ++q)
+                            for (int64_t c = 0; c < Cin; ++c)
+                                for (int64_t ky = 0; ky < KH; ++ky) {
+                                    const int64_t iy = oy * sh - ph + ky * dh;
+                                    if (iy < 0 || iy >= H)
+                                        continue;
+                                    for (int64_t kx = 0; kx < KW; ++kx) {
+                                        const int64_t ix = ox * sw - pw + kx * dw;
+                                        if (ix < 0 || ix >= W)
+                                            continue;
+                                        dx[n * 4 * xq + q * xq + (c * H + iy) * W + ix] +=
+                                            w[q * wq + ((o * Cin + c) * KH + ky) * KW + kx] * z[q];
+                                    }
+                                }
+                    }
+        }
+    }
+    if (dwt) {
+        /* each output channel's weight gradient is written by one thread */
+#pragma omp parallel for schedule(dynamic)
+        for (int64_t o = 0; o < Cout; ++o) {
+            for (int q = 0; q < 4; ++q)
+                for (int64_t t = 0; t < Cin * KH * KW; ++t)
+                    dwt[q * wq + o * Cin * KH * KW + t] = 0.0;
+            for (int64_t n = 0; n < N; ++n)
+                for (int64_t oy = 0; oy < Ho; ++oy)
+                    for (int64_t ox = 0; ox < Wo; ++ox) {
+                        double z[4];
+                        for (int q = 0; q < 4; ++q) {
+                            z[q] = 0.0;
+                            for (int p = 0; p < 4; ++p)
+                                z[q] += kMixing[q][p] * dy[n * 4 * yq + p * yq + (o * Ho + oy) * Wo + ox];
+                        }
+                        for (int q = 0; q < 4; ++q)
+                            for (int64_t c = 0; c < Cin; ++c)
+                                for (int64_t ky = 0; ky < KH; ++ky) {
+                                    const int64_t iy = oy * sh - ph + ky * dh;
+                                    if (iy < 0 || iy >= H)
+                                        continue;
+                                    for (int64_t kx = 0; kx < KW; ++kx) {
+                                        const int64_t ix = ox * sw - pw + kx * dw;
+                                        if (ix < 0 || ix >= W)
+                                            continue;
+                                        dwt[q * wq + ((o * Cin + c) * KH + ky) * KW + kx] +=
+                                            x[n * 4 * xq + q * xq + (c * H + iy) * W + ix] * z[q];
+                                    }
+                                }
+                    }
+        }
+    }
+    if (db) {
+        for (int p = 0; p < 4; ++p)
+            for (int64_t o = 0; o < Cout; ++o) {
+                double s = 0.0;
+                for (int64_t n = 0; n < N; ++n)
+                    for (int64_t t = 0; t < Ho * Wo; ++t)
+                        s += dy[n * 4 * yq + p * yq + o * Ho * Wo + t];
+                db[p * Cout + o] = s;
+            }
+    }
+}
+
+/* ------------------------------------------------------------------------ */
 /* IQBN with given statistics (inference: eq. 12 with stored running mean and
  * variance in place of the batch statistics of eq. 11):
  *

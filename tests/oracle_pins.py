@@ -654,6 +654,67 @@ def pin_poincare_special_points(orc):
     _close(q, np.array([UNIT["1"], UNIT["i"], UNIT["j"], UNIT["k"]]), 0, "special points")
 
 
+# --------------------------- separable conv gradients --------------------------
+
+def pin_separable_backward_adjoint(orc):
+    """eq. 7 is linear in x and in W: <sep(x; W), G> = <x, dx> = <W, dW> for
+    the oracle's gradients at dL/dY = G; dbias is G summed."""
+    rng = _rng(35)
+    for (N, Cin, Cout, H, W, k, s, p, d) in CONV_SWEEP:
+        x = rng.standard_normal((N, 4, Cin, H, W))
+        w = rng.standard_normal((4, Cout, Cin, k, k))
+        y = orc.qconv2d_separable(x, w, None, s, p, d)
+        g = rng.standard_normal(y.shape)
+        dx, dw, db = orc.qconv2d_separable_backward(x, w, g, s, p, d)
+        lhs = float(np.sum(y * g))
+        tag = str((N, Cin, Cout, H, W, k, s, p, d))
+        _close(np.sum(x * dx), lhs, 1e-12, f"separable <X, dX> {tag}")
+        _close(np.sum(w * dw), lhs, 1e-12, f"separable <W, dW> {tag}")
+        _close(db, g.sum(axis=(0, 3, 4)), 1e-13, f"separable dbias {tag}")
+
+
+def pin_separable_backward_autograd(orc):
+    """Gradients equal torch autograd (fp64) through conv2d of the real block
+    weight whose block (p, q) is S[p, q] * W_q, S from the eq. 7 fixture."""
+    S = eq7_signs()
+    rng = _rng(36)
+    for (N, Cin, Cout, H, W, k, s, p, d) in CONV_SWEEP:
+        x = rng.standard_normal((N, 4, Cin, H, W))
+        w = rng.standard_normal((4, Cout, Cin, k, k))
+        b = rng.standard_normal((4, Cout))
+        xt = torch.from_numpy(x.reshape(N, 4 * Cin, H, W).copy()).requires_grad_(True)
+        wt = torch.from_numpy(w.copy()).requires_grad_(True)
+        bt = torch.from_numpy(b.copy()).requires_grad_(True)
+        wb = torch.cat([torch.cat([float(S[pp, q]) * wt[q] for q in range(4)], dim=1) for pp in range(4)], dim=0)
+        y = F.conv2d(xt, wb, bt.reshape(-1), stride=s, padding=p, dilation=d)
+        g = rng.standard_normal(tuple(y.shape))
+        y.backward(torch.from_numpy(g))
+        dx, dw, db = orc.qconv2d_separable_backward(x, w, g.reshape(N, 4, Cout, y.shape[2], y.shape[3]), s, p, d)
+        tag = str((N, Cin, Cout, H, W, k, s, p, d))
+        _close(dx, xt.grad.numpy().reshape(x.shape), 1e-12, f"separable autograd dX {tag}")
+        _close(dw, wt.grad.numpy(), 1e-12, f"separable autograd dW {tag}")
+        _close(db, bt.grad.numpy(), 1e-12, f"separable autograd dbias {tag}")
+
+
+def pin_separable_backward_mixing(orc):
+    """With every W_q = 1 (one 1x1 channel) the input gradient of component q
+    is sum_p M[q][p] dY_p: probing with unit output gradients reproduces the
+    printed matrix M of eq. 9 column by column, and the weight gradient of
+    W_q for x = e_q is that same mixed component."""
+    M = eq9_mixing()
+    w = np.ones((4, 1, 1, 1, 1))
+    got_x, got_w = np.zeros((4, 4)), np.zeros((4, 4))
+    for pp in range(4):
+        g = np.eye(4)[pp].reshape(1, 4, 1, 1, 1)
+        dx, _, _ = orc.qconv2d_separable_backward(np.zeros((1, 4, 1, 1, 1)), w, g)
+        got_x[:, pp] = dx.reshape(4)
+        for q in range(4):
+            _, dw, _ = orc.qconv2d_separable_backward(np.eye(4)[q].reshape(1, 4, 1, 1, 1), w, g)
+            got_w[q, pp] = dw.reshape(4)[q]
+    _close(got_x, M, 0, "dX mixing = M (eq. 9)")
+    _close(got_w, M, 0, "dW mixing = M (eq. 9)")
+
+
 ALL_PINS = [
     pin_eq2_unit_relations, pin_unit_table_derived, pin_complex_model, pin_eq6_matrix,
     pin_eq5_expansion, pin_orientation, pin_identity_kernel, pin_norm, pin_conjugate_adjoint,
@@ -663,6 +724,7 @@ ALL_PINS = [
     pin_separable_eq7_terms, pin_separable_mixing_transpose, pin_separable_real_row,
     pin_separable_block_matrix,
     pin_backward_adjoint, pin_backward_autograd, pin_backward_conjugate_kernel,
+    pin_separable_backward_adjoint, pin_separable_backward_autograd, pin_separable_backward_mixing,
     pin_iqbn_inference_batch_norm, pin_iqbn_inference_batch_stats,
     pin_iqbn_backward_autograd, pin_iqbn_backward_zero_sum,
     pin_poincare_unit_norm, pin_poincare_inverse, pin_poincare_special_points,

@@ -64,6 +64,14 @@ MUTANTS = [
     ("dX stride dropped", "const int64_t iy = oy * sh - ph + ky * dh;\n                                if (iy < 0 || iy >= H)\n                                    continue;\n                                for (int64_t kx = 0; kx < KW; ++kx) {\n                                    const int64_t ix = ox * sw - pw + kx * dw;\n                                    if (ix < 0 || ix >= W)\n                                        continue;\n                                    double wv[4], L[4][4];",
      "const int64_t iy = oy - ph + ky * dh;\n                                if (iy < 0 || iy >= H)\n                                    continue;\n                                for (int64_t kx = 0; kx < KW; ++kx) {\n                                    const int64_t ix = ox * sw - pw + kx * dw;\n                                    if (ix < 0 || ix >= W)\n                                        continue;\n                                    double wv[4], L[4][4];"),
     ("dbias one component", "s += dy[n * 4 * yq + q * yq + o * Ho * Wo + t];", "s += dy[n * 4 * yq + o * Ho * Wo + t];"),
+    # separable conv gradients (eqs. 8-10)
+    ("M transposed", "z[q] += kMixing[q][p] * dy[n * 4 * yq + p * yq + (o * Ho + oy) * Wo + ox];\n                        }\n                        for (int q = 0; q < 4; ++q)\n                            for (int64_t c = 0; c < Cin; ++c)\n                                for (int64_t ky = 0; ky < KH; ++ky) {\n                                    const int64_t iy = oy * sh - ph + ky * dh;\n                                    if (iy < 0 || iy >= H)\n                                        continue;\n                                    for (int64_t kx = 0; kx < KW; ++kx) {\n                                        const int64_t ix = ox * sw - pw + kx * dw;\n                                        if (ix < 0 || ix >= W)\n                                            continue;\n                                        dx[",
+     "z[q] += kMixing[p][q] * dy[n * 4 * yq + p * yq + (o * Ho + oy) * Wo + ox];\n                        }\n                        for (int q = 0; q < 4; ++q)\n                            for (int64_t c = 0; c < Cin; ++c)\n                                for (int64_t ky = 0; ky < KH; ++ky) {\n                                    const int64_t iy = oy * sh - ph + ky * dh;\n                                    if (iy < 0 || iy >= H)\n                                        continue;\n                                    for (int64_t kx = 0; kx < KW; ++kx) {\n                                        const int64_t ix = ox * sw - pw + kx * dw;\n                                        if (ix < 0 || ix >= W)\n                                            continue;\n                                        dx["),
+    ("M sign", "{-1.0, 1.0, 1.0, -1.0},\n    {-1.0, -1.0, 1.0, 1.0},\n};", "{-1.0, 1.0, -1.0, -1.0},\n    {-1.0, -1.0, 1.0, 1.0},\n};"),
+    ("separable dX wrong kernel", "w[q * wq + ((o * Cin + c) * KH + ky) * KW + kx] * z[q];", "w[((q + 1) & 3) * wq + ((o * Cin + c) * KH + ky) * KW + kx] * z[q];"),
+    ("separable dW unmixed", "x[n * 4 * xq + q * xq + (c * H + iy) * W + ix] * z[q];", "x[n * 4 * xq + q * xq + (c * H + iy) * W + ix] * dy[n * 4 * yq + q * yq + (o * Ho + oy) * Wo + ox];"),
+    ("separable dX kernel not flipped back", "dx[n * 4 * xq + q * xq + (c * H + iy) * W + ix] +=\n                                            w[q * wq + ((o * Cin + c) * KH + ky) * KW + kx] * z[q];",
+     "dx[n * 4 * xq + q * xq + (c * H + iy) * W + ix] +=\n                                            w[q * wq + ((o * Cin + c) * KH + (KH - 1 - ky)) * KW + (KW - 1 - kx)] * z[q];"),
     # IQBN inference and backward
     ("inference eps outside sqrt", "const double inv = 1.0 / sqrt(var[q * C + c] + eps);",
      "const double inv = 1.0 / (sqrt(var[q * C + c]) + eps);"),
