@@ -170,6 +170,39 @@ def time_separable(layers, quan, steps):
     return start.elapsed_time(end) * 1e3 / steps
 
 
+def time_separable_backward(layers, quan, steps):
+    """The separable form's gradients (eqs. 8-10) of every layer for a seeded
+    dL/dy: microseconds per step of the input gradient and of the weight +
+    bias gradients."""
+    import torch
+    g = torch.Generator(device="cpu").manual_seed(7)
+    grads = [quan.to_device_layout(torch.randn(tuple(ly["y"].shape), generator=g).to(ly["y"].dtype)
+                                   .to(ly["y"].device)) for ly in layers]
+    e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+
+    def once():
+        for ly, dy in zip(layers, grads):
+            L = ly["spec"]
+            quan.quan_qconv2d_separable_backward_data(dy, *ly["w"], (ly["x"].shape[3], ly["x"].shape[4]),
+                                                      stride=L.stride, pad=L.pad, dilation=L.dilation)
+        e[1].record()
+        for ly, dy in zip(layers, grads):
+            L = ly["spec"]
+            quan.quan_qconv2d_separable_backward_weight(ly["x"], dy, (L.k, L.k), stride=L.stride, pad=L.pad,
+                                                        dilation=L.dilation)
+    once()
+    torch.cuda.synchronize()
+    tot = [0.0, 0.0]
+    for _ in range(steps):
+        e[0].record()
+        once()
+        e[2].record()
+        torch.cuda.synchronize()
+        tot[0] += e[0].elapsed_time(e[1]) * 1e3
+        tot[1] += e[1].elapsed_time(e[2]) * 1e3
+    return [t / steps for t in tot]
+
+
 def time_iqbn_cold(layers, quan, steps, eps):
     """The stand-alone IQBN of each layer with its input evicted from the
     caches first: before each timed rep a 512 MiB buffer is read (twice the
@@ -518,6 +551,7 @@ def main():
     inference_ms = start.elapsed_time(end) / args.steps
     poincare = time_poincare(quan, args.steps, dev)
     separable_us = time_separable(layers, quan, args.steps)
+    sep_bwd_data_us, sep_bwd_weight_us = time_separable_backward(layers, quan, args.steps)
     # the separate-kernel forward leaves y (conv), z (IQBN) and the statistics
     run_step(layers, quan, eps=wl.eps)
     bwd_iqbn_us, bwd_data_us, bwd_weight_us = time_backward(layers, quan, args.steps, wl.eps)
@@ -585,6 +619,11 @@ def main():
             # eq. 7 does a quarter of the Hamilton product's multiply-adds
             "tflops": round(step_flops / 4 / (separable_us * 1e-6) / 1e12, 2),
             "frac_mfma_peak": round(step_flops / 4 / (separable_us * 1e-6) / 1e12 / peak, 4),
+            # its gradients (eqs. 8-10): the input gradient runs the mixing
+            # inside a Hamilton-shaped block product (16 blocks), the weight
+            # gradient sixteen component-pair products; useful FLOPs as eq. 7's
+            "backward_data_us": round(sep_bwd_data_us, 3),
+            "backward_weight_us": round(sep_bwd_weight_us, 3),
         },
         "separate_kernels_us_per_step": round((sum(pack_ms) + sum(conv_ms) + sum(iqbn_ms)) * 1e3, 3),
         "qconv2d": {

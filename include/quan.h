@@ -362,6 +362,46 @@ QUAN_API int quan_qconv2d_backward_weight(const void *x, const void *dy,
                                           int32_t dtype, void *stream);
 
 /*
+ * Gradients of the separable convolution (quan_qconv2d_separable_forward,
+ * eq. 7) by Section III-B's eqs. 8-10: the output gradients are mixed by the
+ * backward matrix M printed with eq. 9 (M = S^T for eq. 7's sign matrix S),
+ * and each mixed component meets only its own kernel and input,
+ *
+ *   z_q = sum_p M[q][p] dy_p                      (per pixel and channel)
+ *   dx_q[n,c,iy,ix] = sum over (o, ky, kx, oy, ox) with iy = oy*stride_h -
+ *                     pad_h + ky*dilation_h (ix likewise) of
+ *                     W_q[o,c,ky,kx] * z_q[n,o,oy,ox]
+ *   dW_q[o,c,ky,kx] = sum over (n, oy, ox) of z_q[n,o,oy,ox] * x_q[n,c,iy,ix]
+ *   db_p[o]         = sum over (n, oy, ox) of dy_p[n,o,oy,ox]
+ *
+ * with every argument, layout, limit and error as in
+ * quan_qconv2d_backward_data / quan_qconv2d_backward_weight.  The input
+ * gradient runs as one convolution of dy (for strides above 1, staged with
+ * zeros inserted) whose 4x4 block weight holds M[p][q] W'_p in block
+ * (p, q), W'_p the transposed, spatially flipped real kernel: the mixing is
+ * accumulated in fp32 with the products and rounded once.  Weight gradients
+ * are fp32, deterministic.
+ */
+QUAN_API int quan_qconv2d_separable_backward_data(const void *dy, const void *w_r, const void *w_i,
+                                                  const void *w_j, const void *w_k,
+                                                  int32_t stride_h, int32_t stride_w,
+                                                  int32_t pad_h, int32_t pad_w,
+                                                  int32_t dilation_h, int32_t dilation_w, void *dx,
+                                                  int32_t n, int32_t c_in, int32_t h, int32_t w,
+                                                  int32_t c_out, int32_t k_h, int32_t k_w,
+                                                  int32_t dtype, void *stream);
+
+QUAN_API int quan_qconv2d_separable_backward_weight(const void *x, const void *dy,
+                                                    int32_t stride_h, int32_t stride_w,
+                                                    int32_t pad_h, int32_t pad_w,
+                                                    int32_t dilation_h, int32_t dilation_w,
+                                                    float *dw_r, float *dw_i, float *dw_j,
+                                                    float *dw_k, float *db, int32_t n, int32_t c_in,
+                                                    int32_t h, int32_t w, int32_t c_out, int32_t k_h,
+                                                    int32_t k_w, int32_t dtype, void *stream);
+
+/*
+ * Gradient of training-mode IQBN (eqs. 11 and 12) with respect to its/*
  * Gradient of training-mode IQBN (eqs. 11 and 12) with respect to its
  * input, gamma and beta, given the batch statistics the forward call
  * returned.  Per component and channel, over the P = n*h*w values, with

@@ -287,8 +287,15 @@ constexpr int producer_waves()
 // so a group needs only W_m: the fragments of W_2 and W_3 are read while the
 // groups of W_0 and W_1 run.  Negative entries of eq. 6 use a sign-flipped
 // copy of the activation fragment (one XOR per dword).
+// FORM (Hamilton layouts, not SEP): which signed kernel block (p, q) of the
+// 4x4 block weight holds.  kFormHamilton: eq. 6, kernel p xor q with the
+// Hamilton sign.  kFormSepGrad: the input gradient of the separable form
+// (eqs. 8-10), dX_p = sum_q M[p][q] (W'_p (*) dY_q) with the backward mixing
+// matrix M = S^T (S eq. 7's signs): kernel p with sign M[p][q] = S[q][p], so
+// the mixing is accumulated in fp32 with the products.
+enum : int { kFormHamilton = 0, kFormSepGrad = 1 };
 template <typename T, int MB, int NB, int WAVES_M, int WAVES_N, bool VEC, int EPI, bool SEP, bool PAIR = false,
-          bool ALLP = false>
+          bool ALLP = false, int FORM = kFormHamilton>
 __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB, WAVES_M, WAVES_N, SEP, ALLP>())) void qconv2d_igemm(KArgs a)
 {
     constexpr int ES = int(sizeof(T));
@@ -323,6 +330,12 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
                   "producer_waves sees the tile geometry");
     static_assert(!ALLP || (!SEP && !PAIR && ES == 2 && MB == 1 && WAVES_N == 1),
                   "all-components waves: Hamilton form, bf16, 32 pixels per wave");
+    static_assert(FORM == kFormHamilton || (!SEP && EPI == kEpiBias), "block tables: Hamilton layouts, bias epilogue");
+    // kernel component and sign of block (output p, input q)
+    auto blk_kernel = [](int p, int q) { return FORM == kFormHamilton ? (p ^ q) : p; };
+    auto blk_neg = [](int p, int q) -> bool {
+        return FORM == kFormHamilton ? ((kHamiltonNeg >> (4 * p + q)) & 1u) : ((kSeparableNeg >> (4 * q + p)) & 1u);
+    };
 
     // Deferred epilogue (DEFER): when a wave holds one output component for
     // all BM pixels, it parks each finished tile in its own LDS region and
@@ -567,10 +580,10 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
             const int o = tn % BNC;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                const int row = (p ^ j) * BNC + o;
+                const int row = blk_kernel(p, j) * BNC + o;
                 if (nb < NB_RD)
                     b_rd[nb][j] = row * CPQ * 16 + ((khalf ^ swz<CPQ>(o)) * 16);
-                flip[nb][j] = ((kHamiltonNeg >> (4 * p + j)) & 1u) ? Elem<T>::sign : 0u;
+                flip[nb][j] = blk_neg(p, j) ? Elem<T>::sign : 0u;
             }
         }
     }
@@ -634,17 +647,18 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
         for (int mb = 0; mb < MB; ++mb)
             dst[mb] = src[mb] ^ Elem<T>::sign;
     };
-    // the four blocks (q xor M, q) of kernel M, q = 0..3
+    // the four blocks of kernel M: (q xor M, q) for the Hamilton product,
+    // (M, q) for the separable input gradient, q = 0..3
     auto group = [&](auto mc, const u32x4 (&x)[4][MB], const u32x4 (&xneg)[4][MB], const u32x4 (&w)[NB]) {
         constexpr int M = decltype(mc)::value;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-            const int p = q ^ M;
+            const int p = FORM == kFormHamilton ? q ^ M : M;
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
                 for (int mb = 0; mb < MB; ++mb) {
-                    if ((kHamiltonNeg >> (4 * p + q)) & 1u)
+                    if (blk_neg(p, q))
                         mfma_step<T>(acc[p][nb][mb], w[nb], xneg[q][mb]);
                     else
                         mfma_step<T>(acc[p][nb][mb], w[nb], x[q][mb]);
@@ -746,11 +760,13 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
             dv0 = drain_read(d_next);
         __builtin_amdgcn_sched_barrier(0);
         rd_ker(cb, 2, wk[2]);
+        if constexpr (FORM != kFormHamilton)
+            flip_act(cur[0], xn[0]);  // eq. 6 never negates input component r
         flip_act(cur[1], xn[1]);
         flip_act(cur[2], xn[2]);
         flip_act(cur[3], xn[3]);
         group(G0{}, cur, xn, wk[0]);
-        interleave_kstep<G_MFMA, 12 * MB, NB>();
+        interleave_kstep<G_MFMA, (FORM == kFormHamilton ? 12 : 16) * MB, NB>();
         __builtin_amdgcn_sched_barrier(0);
         rd_ker(cb, 3, wk[3]);
         group(G1{}, cur, xn, wk[1]);
@@ -1406,13 +1422,15 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
 
 // Packs W_r, W_i, W_j, W_k (each OIHW) into [tap][cblk][kernel][cout_pad][CS]
 // so that one stage of one N-tile is four contiguous runs; padding is zero.
-// c_in, c_out are the packed convolution's.  TRANSPOSED packs the kernel of
-// the input-gradient convolution instead: with W [c_in][c_out] of the
-// forward layer (c_in, c_out here being the forward's c_out, c_in), entry
-// (o, c, ky, kx) is the conjugate (w_r, -w_i, -w_j, -w_k) of the forward
-// kernel W[c][o] at the flipped tap (k_h-1-ky, k_w-1-kx), since the Hamilton
-// matrix of the conjugate is the transpose.
-template <typename T, bool TRANSPOSED>
+// c_in, c_out are the packed convolution's.  The transposed modes pack the
+// kernel of an input-gradient convolution instead: with W [c_in][c_out] of
+// the forward layer (c_in, c_out here being the forward's c_out, c_in),
+// entry (o, c, ky, kx) is the forward kernel W[c][o] at the flipped tap
+// (k_h-1-ky, k_w-1-kx); kPackHamiltonGrad takes its conjugate (w_r, -w_i,
+// -w_j, -w_k), since the Hamilton matrix of the conjugate is the transpose,
+// kPackSeparableGrad the four real kernels as they are.
+enum : int { kPackForward = 0, kPackHamiltonGrad = 1, kPackSeparableGrad = 2 };
+template <typename T, int MODE>
 __global__ __launch_bounds__(256) void qconv2d_pack(const T *__restrict__ w0, const T *__restrict__ w1,
                                                     const T *__restrict__ w2, const T *__restrict__ w3,
                                                     T *__restrict__ wp, int c_in, int c_out, int k_h,
@@ -1436,9 +1454,9 @@ __global__ __launch_bounds__(256) void qconv2d_pack(const T *__restrict__ w0, co
     const T *src = ws == 0 ? w0 : ws == 1 ? w1 : ws == 2 ? w2 : w3;
     T v = T(0);
     if (o < c_out && c < c_in) {
-        if constexpr (TRANSPOSED) {
+        if constexpr (MODE != kPackForward) {
             const T u = src[((c * c_out + o) * k_h + (k_h - 1 - ky)) * k_w + (k_w - 1 - kx)];
-            v = ws == 0 ? u : T(-float(u));
+            v = (MODE == kPackSeparableGrad || ws == 0) ? u : T(-float(u));
         } else {
             v = src[((o * c_in + c) * k_h + ky) * k_w + kx];
         }
@@ -1483,7 +1501,7 @@ __global__ __launch_bounds__(256) void qconv2d_grad_dilate(const T *__restrict__
 
 struct KernelEntry {
     int bm, bnc, mb, nb, threads;
-    bool sep;    // separable convolution (eq. 7) instead of the Hamilton product
+    int form;    // a ConvForm: Hamilton product, separable (eq. 7), separable unmixed
     bool defer;  // deferred epilogue (one output component per wave); writes IQBN statistics
     int stat_rows;  // output pixels per statistics partial
     DType dt;
@@ -1529,7 +1547,7 @@ constexpr const void *fold_fn()
 #define QCONV_K(T, DT, MB, NB, WM, WN, SEP)                                                            \
     KernelEntry                                                                                        \
     {                                                                                                  \
-        32 * (MB) * (WM), ((SEP) ? 32 : 8) * (NB) * (WN), MB, NB, 64 * ((WM) * (WN) + producer_waves<T, MB, NB, WM, WN, SEP>()), SEP, \
+        32 * (MB) * (WM), ((SEP) ? 32 : 8) * (NB) * (WN), MB, NB, 64 * ((WM) * (WN) + producer_waves<T, MB, NB, WM, WN, SEP>()), (SEP) ? 1 : 0, \
             QCONV_DEFER(NB, WM, WN, SEP), 32 * (MB) * (WM), DT,                                        \
             {{(const void *)&qconv2d_igemm<T, MB, NB, WM, WN, true, kEpiBias, SEP>,                    \
               (const void *)&qconv2d_igemm<T, MB, NB, WM, WN, false, kEpiBias, SEP>,                   \
@@ -1547,7 +1565,7 @@ constexpr const void *fold_fn()
 #define QCONV_KA(NB)                                                                                   \
     KernelEntry                                                                                        \
     {                                                                                                  \
-        128, 32 * (NB), 1, NB, 64 * (4 + producer_waves<__bf16, 1, NB, 4, 1, false, true>()), false, true, 32, \
+        128, 32 * (NB), 1, NB, 64 * (4 + producer_waves<__bf16, 1, NB, 4, 1, false, true>()), 0, true, 32, \
             DType::BF16,                                                                               \
             {{(const void *)&qconv2d_igemm<__bf16, 1, NB, 4, 1, true, kEpiBias, false, false, true>,    \
               (const void *)&qconv2d_igemm<__bf16, 1, NB, 4, 1, false, kEpiBias, false, false, true>,   \
@@ -1559,6 +1577,22 @@ constexpr const void *fold_fn()
               (const void *)&qconv2d_igemm<__bf16, 1, NB, 4, 1, false, kEpiFold, false, false, true>,   \
               nullptr}},                                                                               \
             "bf16_allp_nb" #NB                                                                         \
+    }
+
+// The input gradient of the separable form (eqs. 8-10) on the Hamilton
+// layouts with the kFormSepGrad block table: bias epilogue only.
+#define QCONV_KG(T, DT, MB, NB, WM, WN, ALLPW)                                                         \
+    KernelEntry                                                                                        \
+    {                                                                                                  \
+        32 * (MB) * (WM), ((ALLPW) ? 32 : 8) * (NB) * (WN), MB, NB,                                    \
+            64 * ((WM) * (WN) + producer_waves<T, MB, NB, WM, WN, false, ALLPW>()), 2, false,          \
+            32 * (MB) * (WM), DT,                                                                      \
+            {{(const void *)&qconv2d_igemm<T, MB, NB, WM, WN, true, kEpiBias, false, false, ALLPW, kFormSepGrad>,  \
+              (const void *)&qconv2d_igemm<T, MB, NB, WM, WN, false, kEpiBias, false, false, ALLPW, kFormSepGrad>, \
+              nullptr},                                                                                \
+             {nullptr, nullptr, nullptr},                                                              \
+             {nullptr, nullptr, nullptr}},                                                             \
+            #T "_sepgrad_mb" #MB "x" #WM "_nb" #NB "x" #WN                                             \
     }
 
 const KernelEntry kKernels[] = {
@@ -1573,6 +1607,10 @@ const KernelEntry kKernels[] = {
     QCONV_K(__bf16, DType::BF16, 1, 2, 4, 1, true),   // 128 px x 64 channels
     QCONV_K(__bf16, DType::BF16, 1, 1, 4, 1, true),   // 128 px x 32 channels
     QCONV_K(float, DType::F32, 1, 1, 4, 1, true),     // 128 px x 32 channels
+    // the separable form's input gradient (kernel p, sign M[p][q])
+    QCONV_KG(__bf16, DType::BF16, 1, 2, 4, 1, true),  // 128 px x 64 channels, all-components waves
+    QCONV_KG(__bf16, DType::BF16, 1, 1, 4, 1, true),  // 128 px x 32 channels
+    QCONV_KG(float, DType::F32, 1, 1, 2, 2, false),   // 64 px x 16 channels
 };
 constexpr int kNumKernels = int(sizeof(kKernels) / sizeof(kKernels[0]));
 
@@ -1647,8 +1685,9 @@ PackGeom qconv2d_pack_geom(int c_in, int c_out, int k_h, int k_w, DType dt)
     return pg;
 }
 
-ConvPlan qconv2d_plan(const ConvGeom &g, DType dt, bool sep)
+ConvPlan qconv2d_plan(const ConvGeom &g, DType dt, ConvForm form)
 {
+    const bool sep = form != ConvForm::Hamilton;
     const int64_t m = g.m();
     const int pk = dt == DType::BF16 ? 16 : 8;
     const int stages = g.k_h * g.k_w * ((g.c_in + pk - 1) / pk);
@@ -1657,7 +1696,7 @@ ConvPlan qconv2d_plan(const ConvGeom &g, DType dt, bool sep)
     const int cus = device_cus();
     for (int i = 0; i < kNumKernels; ++i) {
         const KernelEntry &k = kKernels[i];
-        if (k.dt != dt || k.sep != sep)
+        if (k.dt != dt || k.form != int(form))
             continue;
         // the narrow tile only where the output channels leave a wide one idle
         if (dt == DType::BF16 && k.bnc == 64 && g.c_out <= 32)
@@ -1684,19 +1723,19 @@ ConvPlan qconv2d_plan(const ConvGeom &g, DType dt, bool sep)
 }
 
 namespace {
-template <bool TRANSPOSED>
+template <int MODE>
 hipError_t pack_weights(const PackGeom &pg, int c_in, int c_out, int k_h, int k_w, DType dt, const void *w_r,
                         const void *w_i, const void *w_j, const void *w_k, void *wpack, hipStream_t stream)
 {
     const int total = int(pg.bytes / (dt == DType::BF16 ? 2 : 4));
     const int blocks = (total + 255) / 256;
     if (dt == DType::BF16)
-        hipLaunchKernelGGL((qconv2d_pack<__bf16, TRANSPOSED>), dim3(blocks), dim3(256), 0, stream,
+        hipLaunchKernelGGL((qconv2d_pack<__bf16, MODE>), dim3(blocks), dim3(256), 0, stream,
                            (const __bf16 *)w_r, (const __bf16 *)w_i, (const __bf16 *)w_j,
                            (const __bf16 *)w_k, (__bf16 *)wpack, c_in, c_out, k_h, k_w, pg.n_cblk,
                            pg.cout_pad, total);
     else
-        hipLaunchKernelGGL((qconv2d_pack<float, TRANSPOSED>), dim3(blocks), dim3(256), 0, stream,
+        hipLaunchKernelGGL((qconv2d_pack<float, MODE>), dim3(blocks), dim3(256), 0, stream,
                            (const float *)w_r, (const float *)w_i, (const float *)w_j,
                            (const float *)w_k, (float *)wpack, c_in, c_out, k_h, k_w, pg.n_cblk,
                            pg.cout_pad, total);
@@ -1708,7 +1747,7 @@ hipError_t qconv2d_pack_weights(const PackGeom &pg, int c_in, int c_out, int k_h
                                 const void *w_r, const void *w_i, const void *w_j, const void *w_k,
                                 void *wpack, hipStream_t stream)
 {
-    return pack_weights<false>(pg, c_in, c_out, k_h, k_w, dt, w_r, w_i, w_j, w_k, wpack, stream);
+    return pack_weights<kPackForward>(pg, c_in, c_out, k_h, k_w, dt, w_r, w_i, w_j, w_k, wpack, stream);
 }
 
 ConvGeom qconv2d_grad_data_geom(const ConvGeom &g)
@@ -1741,13 +1780,16 @@ size_t qconv2d_grad_data_stage_bytes(const ConvGeom &g, DType dt)
 
 hipError_t qconv2d_backward_data_run(const ConvGeom &g, DType dt, const void *dy, const void *w_r, const void *w_i,
                                      const void *w_j, const void *w_k, void *dx, void *wpack, void *stage,
-                                     hipStream_t stream)
+                                     hipStream_t stream, bool sep)
 {
     const ConvGeom t = qconv2d_grad_data_geom(g);
     if (t.p_h < 0 || t.p_w < 0 || t.h < 1 || t.w < 1)
         return hipErrorInvalidValue;
     const PackGeom pg = qconv2d_pack_geom(t.c_in, t.c_out, t.k_h, t.k_w, dt);
-    hipError_t e = pack_weights<true>(pg, t.c_in, t.c_out, t.k_h, t.k_w, dt, w_r, w_i, w_j, w_k, wpack, stream);
+    hipError_t e = sep ? pack_weights<kPackSeparableGrad>(pg, t.c_in, t.c_out, t.k_h, t.k_w, dt, w_r, w_i, w_j, w_k,
+                                                          wpack, stream)
+                       : pack_weights<kPackHamiltonGrad>(pg, t.c_in, t.c_out, t.k_h, t.k_w, dt, w_r, w_i, w_j, w_k,
+                                                         wpack, stream);
     if (e != hipSuccess)
         return e;
     const void *z = dy;
@@ -1780,7 +1822,8 @@ hipError_t qconv2d_backward_data_run(const ConvGeom &g, DType dt, const void *dy
             return e;
         z = stage;
     }
-    return qconv2d_run(qconv2d_plan(t, dt, false), pg, t, dt, z, wpack, nullptr, dx, nullptr, nullptr, stream);
+    return qconv2d_run(qconv2d_plan(t, dt, sep ? ConvForm::SeparableGradData : ConvForm::Hamilton), pg, t, dt, z,
+                       wpack, nullptr, dx, nullptr, nullptr, stream);
 }
 
 bool qconv2d_writes_stats(const ConvPlan &plan, const ConvGeom &g, DType dt)

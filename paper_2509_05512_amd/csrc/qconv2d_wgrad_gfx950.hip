@@ -45,6 +45,10 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 // Bit 4*p + q is set when entry (p, q) of the Hamilton matrix (eq. 6) is
 // negative.  Row r: + - - -, row i: + + - +, row j: + + + -, row k: + - + +.
 constexpr unsigned kNeg = (1u << 1) | (1u << 2) | (1u << 3) | (1u << 6) | (1u << 11) | (1u << 13);
+// Bit 4*p + q is set when the separable form (eq. 7) subtracts W_q (*) x_q
+// from output component p: S[p][q] = -1.  Row r: + - - -, row i: + + + -,
+// row j: + - + +, row k: + + - +.
+constexpr unsigned kSepNeg = (1u << 1) | (1u << 2) | (1u << 3) | (1u << 7) | (1u << 9) | (1u << 14);
 
 constexpr int kThreads = 256;
 constexpr int kTileO = 64;   // output channels per work-group
@@ -123,7 +127,10 @@ __device__ __forceinline__ u32x4 load16(const void *base, unsigned bytes, unsign
 // computes the dense product G[(p,o)][(q,c)] = sum_pix dY[pix][p][o]
 // X[pix+tap][q][c] of which the reduction forms every dW_m; on a 64 x 64
 // tile this does the useful work once instead of sixteen times.
-template <typename T, bool VEC, int NC>
+// SEP (NC = 4): the separable form's gradients (eqs. 8-10), dW_q = sum_p
+// S[p][q] dY_p X_q: the same sixteen component pairs, each added into the
+// accumulator of its input component q with eq. 7's sign.
+template <typename T, bool VEC, int NC, bool SEP = false>
 __global__ __launch_bounds__(kThreads) void qconv2d_wgrad(WArgs a)
 {
     static_assert(NC == 4 || NC == 1, "four components or one dense row");
@@ -313,11 +320,12 @@ __global__ __launch_bounds__(kThreads) void qconv2d_wgrad(WArgs a)
 #pragma unroll
                 for (int m = 0; m < 4; ++m) {
                     const int q = p ^ m;
-                    const bool minus = (kNeg >> (4 * p + q)) & 1u;
+                    const int d = SEP ? q : m;  // the gradient this pair adds into
+                    const bool minus = ((SEP ? kSepNeg : kNeg) >> (4 * p + q)) & 1u;
                     if constexpr (ES == 2)
-                        acc[m] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(minus ? neg : pos, f.fx[q], acc[m], 0, 0, 0);
+                        acc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(minus ? neg : pos, f.fx[q], acc[d], 0, 0, 0);
                     else
-                        acc[m] = __builtin_amdgcn_mfma_f32_32x32x2f32(minus ? neg : pos, f.fx[q], acc[m], 0, 0, 0);
+                        acc[d] = __builtin_amdgcn_mfma_f32_32x32x2f32(minus ? neg : pos, f.fx[q], acc[d], 0, 0, 0);
                 }
             }
         }
@@ -427,9 +435,10 @@ __global__ __launch_bounds__(kThreads) void qconv2d_wgrad_reduce(const float *__
 // Layers of at most 16 channels (the kernel's NC = 1 form): the partials
 // are G[(p,o)][(q,c)] per slice and tap ([splits][taps][4*c_out][4*c_in]), and
 // dW_m[o][c][tap] = sum over slices, then over p in order, of
-// s(p, p xor m) G[(p,o)][(p xor m, c)] (eq. 6's signs), in fp64.
+// s(p, p xor m) G[(p,o)][(p xor m, c)] (eq. 6's signs), in fp64; with sep
+// (the separable form) dW_m = sum of S[p][m] G[(p,o)][(m,c)] (eq. 7's signs).
 __global__ __launch_bounds__(kThreads) void qconv2d_wgrad_reduce_dense(const float *__restrict__ part, int splits,
-                                                                       int taps, int c_out, int c_in,
+                                                                       int taps, int c_out, int c_in, int sep,
                                                                        float *__restrict__ dw0,
                                                                        float *__restrict__ dw1,
                                                                        float *__restrict__ dw2,
@@ -449,9 +458,9 @@ __global__ __launch_bounds__(kThreads) void qconv2d_wgrad_reduce_dense(const flo
         const float *g = part + (int64_t(sp) * taps + tap) * g_n;
 #pragma unroll
         for (int p = 0; p < 4; ++p) {
-            const int q = p ^ m;
+            const int q = sep ? m : p ^ m;
             const double v = double(g[int64_t(p * c_out + o) * (4 * c_in) + q * c_in + c]);
-            s += ((kNeg >> (4 * p + q)) & 1u) ? -v : v;
+            s += (((sep ? kSepNeg : kNeg) >> (4 * p + q)) & 1u) ? -v : v;
         }
     }
     float *dw = m == 0 ? dw0 : m == 1 ? dw1 : m == 2 ? dw2 : dw3;
@@ -604,7 +613,7 @@ size_t qconv2d_wgrad_work_bytes(const ConvGeom &g)
 
 hipError_t qconv2d_backward_weight_run(const ConvGeom &g, DType dt, const void *x, const void *dy, float *dw_r,
                                        float *dw_i, float *dw_j, float *dw_k, float *db, void *work,
-                                       hipStream_t stream)
+                                       hipStream_t stream, bool sep)
 {
     const WPlan p = wgrad_plan(g);
     const bool dense = wgrad_dense(g);
@@ -643,8 +652,13 @@ hipError_t qconv2d_backward_weight_run(const ConvGeom &g, DType dt, const void *
     const bool vec = a.c_in % epc == 0 && a.c_out % epc == 0 && dy_span < 0x7fffffffLL && x_span < 0x7fffffffLL;
     auto launch = [&](auto t, auto v, auto nc) {
         using T = decltype(t);
-        hipLaunchKernelGGL((qconv2d_wgrad<T, decltype(v)::value, decltype(nc)::value>), dim3(blocks), dim3(kThreads),
-                           0, stream, a);
+        constexpr int NC = decltype(nc)::value;
+        if (sep && NC == 4)
+            hipLaunchKernelGGL((qconv2d_wgrad<T, decltype(v)::value, NC, NC == 4>), dim3(blocks), dim3(kThreads), 0,
+                               stream, a);
+        else
+            hipLaunchKernelGGL((qconv2d_wgrad<T, decltype(v)::value, NC>), dim3(blocks), dim3(kThreads), 0, stream,
+                               a);
     };
     using VT = std::true_type;
     using VF = std::false_type;
@@ -668,7 +682,7 @@ hipError_t qconv2d_backward_weight_run(const ConvGeom &g, DType dt, const void *
     const dim3 rgrid(unsigned((outs + kThreads - 1) / kThreads));
     if (dense)
         hipLaunchKernelGGL(qconv2d_wgrad_reduce_dense, rgrid, dim3(kThreads), 0, stream, (const float *)a.part,
-                           p.splits, p.taps, g.c_out, g.c_in, dw_r, dw_i, dw_j, dw_k);
+                           p.splits, p.taps, g.c_out, g.c_in, sep ? 1 : 0, dw_r, dw_i, dw_j, dw_k);
     else
         hipLaunchKernelGGL(qconv2d_wgrad_reduce, rgrid, dim3(kThreads), 0, stream, (const float *)a.part, p.splits,
                            p.taps, g.c_out, g.c_in, dw_r, dw_i, dw_j, dw_k);

@@ -274,7 +274,7 @@ int conv_packed(const char *name, bool sep, const void *x, const void *packed, c
         return fail(QUAN_ERR_ALIAS, "%s: out overlaps the packed weights", name);
     const quan::DType dt = to_dt(dtype);
     const quan::PackGeom pg = quan::qconv2d_pack_geom(c_in, c_out, k_h, k_w, dt);
-    const quan::ConvPlan plan = quan::qconv2d_plan(g, dt, sep);
+    const quan::ConvPlan plan = quan::qconv2d_plan(g, dt, sep ? quan::ConvForm::Separable : quan::ConvForm::Hamilton);
     hipError_t e = quan::qconv2d_run(plan, pg, g, dt, x, packed, bias, out, nullptr, nullptr,
                                      static_cast<hipStream_t>(stream));
     if (e != hipSuccess)
@@ -319,7 +319,8 @@ int conv_unpacked(const char *name, bool sep, const void *x, const void *w_r, co
                                               wpack, s);
     if (e != hipSuccess)
         return fail_hip(e, "qconv2d weight pack launch");
-    e = quan::qconv2d_run(quan::qconv2d_plan(g, dt, sep), pg, g, dt, x, wpack, bias, out, nullptr, nullptr, s);
+    e = quan::qconv2d_run(quan::qconv2d_plan(g, dt, sep ? quan::ConvForm::Separable : quan::ConvForm::Hamilton), pg,
+                          g, dt, x, wpack, bias, out, nullptr, nullptr, s);
     if (e != hipSuccess)
         return fail_hip(e, "qconv2d launch");
     return QUAN_OK;
@@ -456,7 +457,7 @@ QUAN_API int quan_qconv2d_iqbn_forward(const void *x, const void *packed, const 
 
     const quan::DType dt = to_dt(dtype);
     const quan::PackGeom pg = quan::qconv2d_pack_geom(c_in, c_out, k_h, k_w, dt);
-    const quan::ConvPlan plan = quan::qconv2d_plan(g, dt, false);
+    const quan::ConvPlan plan = quan::qconv2d_plan(g, dt, quan::ConvForm::Hamilton);
     const int64_t pixels = g.m();
     hipStream_t s = static_cast<hipStream_t>(stream);
     void *work = nullptr;
@@ -530,7 +531,8 @@ QUAN_API int quan_qconv2d_iqbn_inference(const void *x, const void *packed, cons
     if (e != hipSuccess)
         return fail_hip(e, "iqbn fold launch");
     const quan::ConvFold fold{scale, shift, relu != 0};
-    e = quan::qconv2d_run(quan::qconv2d_plan(g, dt, false), pg, g, dt, x, packed, bias, out, nullptr, &fold, s);
+    e = quan::qconv2d_run(quan::qconv2d_plan(g, dt, quan::ConvForm::Hamilton), pg, g, dt, x, packed, bias, out,
+                          nullptr, &fold, s);
     if (e != hipSuccess)
         return fail_hip(e, "qconv2d launch");
     return QUAN_OK;
@@ -561,15 +563,17 @@ QUAN_API int quan_poincare_map(const void *rgb, void *out, int32_t n, int32_t h,
     return QUAN_OK;
 }
 
-QUAN_API int quan_qconv2d_backward_data(const void *dy, const void *w_r, const void *w_i, const void *w_j,
-                                        const void *w_k, int32_t stride_h, int32_t stride_w, int32_t pad_h,
-                                        int32_t pad_w, int32_t dilation_h, int32_t dilation_w, void *dx, int32_t n,
-                                        int32_t c_in, int32_t h, int32_t w, int32_t c_out, int32_t k_h, int32_t k_w,
-                                        int32_t dtype, void *stream)
+namespace {
+
+// Input gradient of the Hamilton (sep false) or separable (sep true) form.
+int backward_data(const char *name, bool sep, const void *dy, const void *w_r, const void *w_i, const void *w_j,
+                  const void *w_k, int32_t stride_h, int32_t stride_w, int32_t pad_h, int32_t pad_w,
+                  int32_t dilation_h, int32_t dilation_w, void *dx, int32_t n, int32_t c_in, int32_t h, int32_t w,
+                  int32_t c_out, int32_t k_h, int32_t k_w, int32_t dtype, void *stream)
 {
     g_last_error.clear();
     if (!dy || !w_r || !w_i || !w_j || !w_k || !dx)
-        return fail(QUAN_ERR_NULL, "qconv2d_backward_data: dy, w_r, w_i, w_j, w_k and dx must be non-NULL");
+        return fail(QUAN_ERR_NULL, "%s: dy, w_r, w_i, w_j, w_k and dx must be non-NULL", name);
     // the forward layer's geometry, with dx in the place of x and dy of out
     quan::ConvGeom g;
     size_t xb = 0, ob = 0;
@@ -577,21 +581,21 @@ QUAN_API int quan_qconv2d_backward_data(const void *dy, const void *w_r, const v
                             w, c_out, k_h, k_w, dtype, &g, &xb, &ob))
         return rc;
     if (pad_h > dilation_h * (k_h - 1) || pad_w > dilation_w * (k_w - 1))
-        return fail(QUAN_ERR_UNSUPPORTED, "qconv2d_backward_data: padding beyond the dilated kernel span");
+        return fail(QUAN_ERR_UNSUPPORTED, "%s: padding beyond the dilated kernel span", name);
     const size_t es = elem_size(dtype);
     if (misaligned(w_r, es) || misaligned(w_i, es) || misaligned(w_j, es) || misaligned(w_k, es))
-        return fail(QUAN_ERR_ALIGN, "qconv2d_backward_data: kernels must be aligned to their element size");
+        return fail(QUAN_ERR_ALIGN, "%s: kernels must be aligned to their element size", name);
     const size_t wb = size_t(c_out) * c_in * k_h * k_w * es;
     if (overlaps(dx, xb, w_r, wb) || overlaps(dx, xb, w_i, wb) || overlaps(dx, xb, w_j, wb) ||
         overlaps(dx, xb, w_k, wb))
-        return fail(QUAN_ERR_ALIAS, "qconv2d_backward_data: dx overlaps dy or a kernel");
+        return fail(QUAN_ERR_ALIAS, "%s: dx overlaps dy or a kernel", name);
     const quan::DType dt = to_dt(dtype);
     const quan::ConvGeom t = quan::qconv2d_grad_data_geom(g);
     // the gradient convolution's own limits (its input is dy or the staged,
     // zero-inserted dy)
     const int64_t t_img = int64_t(t.h) * t.w * 4 * t.c_in * int64_t(es);
     if (int64_t(t.n) * t.h * t.w * 4 * t.c_in > kMaxElems || t_img * (256 / (int64_t(h) * w) + 2) > kMaxElems)
-        return fail(QUAN_ERR_UNSUPPORTED, "qconv2d_backward_data: staged gradient too large for 32-bit offsets");
+        return fail(QUAN_ERR_UNSUPPORTED, "%s: staged gradient too large for 32-bit offsets", name);
     const int64_t need = quan_qconv2d_packed_bytes(c_out, c_in, k_h, k_w, dtype);
     if (need < 0)
         return int(need);
@@ -604,21 +608,47 @@ QUAN_API int quan_qconv2d_backward_data(const void *dy, const void *w_r, const v
             return rc;
     }
     const hipError_t e = quan::qconv2d_backward_data_run(g, dt, dy, w_r, w_i, w_j, w_k, dx, wpack, stage,
-                                                         static_cast<hipStream_t>(stream));
+                                                         static_cast<hipStream_t>(stream), sep);
     if (e != hipSuccess)
-        return fail_hip(e, "qconv2d backward data launch");
+        return fail_hip(e, "backward data launch");
     return QUAN_OK;
 }
 
-QUAN_API int quan_qconv2d_backward_weight(const void *x, const void *dy, int32_t stride_h, int32_t stride_w,
-                                          int32_t pad_h, int32_t pad_w, int32_t dilation_h, int32_t dilation_w,
-                                          float *dw_r, float *dw_i, float *dw_j, float *dw_k, float *db, int32_t n,
-                                          int32_t c_in, int32_t h, int32_t w, int32_t c_out, int32_t k_h,
-                                          int32_t k_w, int32_t dtype, void *stream)
+}  // namespace
+
+QUAN_API int quan_qconv2d_backward_data(const void *dy, const void *w_r, const void *w_i, const void *w_j,
+                                        const void *w_k, int32_t stride_h, int32_t stride_w, int32_t pad_h,
+                                        int32_t pad_w, int32_t dilation_h, int32_t dilation_w, void *dx, int32_t n,
+                                        int32_t c_in, int32_t h, int32_t w, int32_t c_out, int32_t k_h, int32_t k_w,
+                                        int32_t dtype, void *stream)
+{
+    return backward_data("qconv2d_backward_data", false, dy, w_r, w_i, w_j, w_k, stride_h, stride_w, pad_h, pad_w,
+                         dilation_h, dilation_w, dx, n, c_in, h, w, c_out, k_h, k_w, dtype, stream);
+}
+
+QUAN_API int quan_qconv2d_separable_backward_data(const void *dy, const void *w_r, const void *w_i,
+                                                  const void *w_j, const void *w_k, int32_t stride_h,
+                                                  int32_t stride_w, int32_t pad_h, int32_t pad_w,
+                                                  int32_t dilation_h, int32_t dilation_w, void *dx, int32_t n,
+                                                  int32_t c_in, int32_t h, int32_t w, int32_t c_out, int32_t k_h,
+                                                  int32_t k_w, int32_t dtype, void *stream)
+{
+    return backward_data("qconv2d_separable_backward_data", true, dy, w_r, w_i, w_j, w_k, stride_h, stride_w, pad_h,
+                         pad_w, dilation_h, dilation_w, dx, n, c_in, h, w, c_out, k_h, k_w, dtype, stream);
+}
+
+
+namespace {
+
+// Weight and bias gradients of the Hamilton (sep false) or separable form.
+int backward_weight(const char *name, bool sep, const void *x, const void *dy, int32_t stride_h, int32_t stride_w,
+                    int32_t pad_h, int32_t pad_w, int32_t dilation_h, int32_t dilation_w, float *dw_r, float *dw_i,
+                    float *dw_j, float *dw_k, float *db, int32_t n, int32_t c_in, int32_t h, int32_t w,
+                    int32_t c_out, int32_t k_h, int32_t k_w, int32_t dtype, void *stream)
 {
     g_last_error.clear();
     if (!x || !dy || !dw_r || !dw_i || !dw_j || !dw_k)
-        return fail(QUAN_ERR_NULL, "qconv2d_backward_weight: x, dy and dw_r..dw_k must be non-NULL");
+        return fail(QUAN_ERR_NULL, "%s: x, dy and dw_r..dw_k must be non-NULL", name);
     quan::ConvGeom g;
     size_t xb = 0, ob = 0;
     if (int rc = check_conv(x, nullptr, stride_h, stride_w, pad_h, pad_w, dilation_h, dilation_w, dy, n, c_in, h, w,
@@ -631,23 +661,49 @@ QUAN_API int quan_qconv2d_backward_weight(const void *x, const void *dy, int32_t
             continue;
         const size_t bi = i < 4 ? wb : bb;
         if (misaligned(outs[i], 4))
-            return fail(QUAN_ERR_ALIGN, "qconv2d_backward_weight: dw_* and db must be 4-byte aligned");
+            return fail(QUAN_ERR_ALIGN, "%s: dw_* and db must be 4-byte aligned", name);
         if (overlaps(outs[i], bi, x, xb) || overlaps(outs[i], bi, dy, ob))
-            return fail(QUAN_ERR_ALIAS, "qconv2d_backward_weight: a gradient overlaps x or dy");
+            return fail(QUAN_ERR_ALIAS, "%s: a gradient overlaps x or dy", name);
         for (int j = 0; j < i; ++j) {
             if (outs[j] && overlaps(outs[i], bi, outs[j], j < 4 ? wb : bb))
-                return fail(QUAN_ERR_ALIAS, "qconv2d_backward_weight: gradients overlap each other");
+                return fail(QUAN_ERR_ALIAS, "%s: gradients overlap each other", name);
         }
     }
     void *work = nullptr;
     if (int rc = workspace(stream, kWgrad, quan::qconv2d_wgrad_work_bytes(g), &work))
         return rc;
     const hipError_t e = quan::qconv2d_backward_weight_run(g, to_dt(dtype), x, dy, dw_r, dw_i, dw_j, dw_k, db, work,
-                                                           static_cast<hipStream_t>(stream));
+                                                           static_cast<hipStream_t>(stream), sep);
     if (e != hipSuccess)
-        return fail_hip(e, "qconv2d backward weight launch");
+        return fail_hip(e, "backward weight launch");
     return QUAN_OK;
 }
+
+}  // namespace
+
+QUAN_API int quan_qconv2d_backward_weight(const void *x, const void *dy, int32_t stride_h, int32_t stride_w,
+                                          int32_t pad_h, int32_t pad_w, int32_t dilation_h, int32_t dilation_w,
+                                          float *dw_r, float *dw_i, float *dw_j, float *dw_k, float *db, int32_t n,
+                                          int32_t c_in, int32_t h, int32_t w, int32_t c_out, int32_t k_h,
+                                          int32_t k_w, int32_t dtype, void *stream)
+{
+    return backward_weight("qconv2d_backward_weight", false, x, dy, stride_h, stride_w, pad_h, pad_w, dilation_h,
+                           dilation_w, dw_r, dw_i, dw_j, dw_k, db, n, c_in, h, w, c_out, k_h, k_w, dtype, stream);
+}
+
+QUAN_API int quan_qconv2d_separable_backward_weight(const void *x, const void *dy, int32_t stride_h,
+                                                    int32_t stride_w, int32_t pad_h, int32_t pad_w,
+                                                    int32_t dilation_h, int32_t dilation_w, float *dw_r,
+                                                    float *dw_i, float *dw_j, float *dw_k, float *db, int32_t n,
+                                                    int32_t c_in, int32_t h, int32_t w, int32_t c_out, int32_t k_h,
+                                                    int32_t k_w, int32_t dtype, void *stream)
+{
+    return backward_weight("qconv2d_separable_backward_weight", true, x, dy, stride_h, stride_w, pad_h, pad_w,
+                           dilation_h, dilation_w, dw_r, dw_i, dw_j, dw_k, db, n, c_in, h, w, c_out, k_h, k_w, dtype,
+                           stream);
+}
+
+
 
 QUAN_API int quan_iqbn_backward(const void *x, const void *dout, const void *y, const float *mean,
                                 const float *var, const float *gamma, float eps, void *dx, float *dgamma,

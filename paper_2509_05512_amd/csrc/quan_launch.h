@@ -43,9 +43,13 @@ struct ConvPlan {
     const char *name;
 };
 
-// Pick a tile configuration for the convolution: the Hamilton product
-// (eq. 5) or, with sep, the separable form (eq. 7).
-ConvPlan qconv2d_plan(const ConvGeom &g, DType dt, bool sep);
+// What a convolution launch computes: the Hamilton product (eq. 5), the
+// separable form (eq. 7), or the separable form's input gradient (eqs.
+// 8-10: block (p, q) of the 4x4 block weight is M[p][q] W'_p).
+enum class ConvForm : int { Hamilton = 0, Separable = 1, SeparableGradData = 2 };
+
+// Pick a tile configuration for the convolution.
+ConvPlan qconv2d_plan(const ConvGeom &g, DType dt, ConvForm form);
 
 // Pack W_r..W_k (OIHW) into the PackGeom layout, zero padded.
 hipError_t qconv2d_pack_weights(const PackGeom &pg, int c_in, int c_out, int k_h, int k_w, DType dt,
@@ -78,20 +82,25 @@ hipError_t qconv2d_run(const ConvPlan &plan, const PackGeom &pg, const ConvGeom 
 // flipped kernel (packed into `wpack`: qconv2d_pack_geom of the gradient
 // geometry), stride 1, pad d(k-1) - p (must be >= 0).  g is the forward
 // layer's geometry; dy [n][h_out][w_out][4][c_out], dx [n][h][w][4][c_in].
+// With sep, the separable form's input gradient (eqs. 8-10) instead:
+// dX_p = sum_q M[p][q] (W'_p (*) Z_q), W'_p the transposed, flipped real
+// kernel and M the backward mixing matrix, accumulated in fp32.
 ConvGeom qconv2d_grad_data_geom(const ConvGeom &g);
 size_t qconv2d_grad_data_stage_bytes(const ConvGeom &g, DType dt);
 hipError_t qconv2d_backward_data_run(const ConvGeom &g, DType dt, const void *dy, const void *w_r, const void *w_i,
                                      const void *w_j, const void *w_k, void *dx, void *wpack, void *stage,
-                                     hipStream_t stream);
+                                     hipStream_t stream, bool sep = false);
 
 // Weight and bias gradients of the Hamilton convolution for dL/dY = dy:
 // dw_r..dw_k [c_out][c_in][k_h][k_w] and db [4][c_out] (NULL: skipped), all
 // fp32; x [n][h][w][4][c_in], dy [n][h_out][w_out][4][c_out].  `work` must
 // hold qconv2d_wgrad_work_bytes(g) bytes.
+// With sep, the gradients of the separable form instead (eqs. 8-10):
+// dW_q = sum_p S[p][q] sum_pix dY_p X_q (S the sign matrix of eq. 7).
 size_t qconv2d_wgrad_work_bytes(const ConvGeom &g);
 hipError_t qconv2d_backward_weight_run(const ConvGeom &g, DType dt, const void *x, const void *dy, float *dw_r,
                                        float *dw_i, float *dw_j, float *dw_k, float *db, void *work,
-                                       hipStream_t stream);
+                                       hipStream_t stream, bool sep = false);
 
 // Error reporting shared by the entry points of every source file: report()
 // stores the thread's last-error message and returns `code`.

@@ -41,6 +41,9 @@ SIGNATURES = {
     "quan_poincare_map": (ctypes.c_int, [_vp, _vp] + [_i32] * 4 + [_vp]),
     "quan_qconv2d_backward_data": (ctypes.c_int, [_vp] * 5 + [_i32] * 6 + [_vp] + [_i32] * 8 + [_vp]),
     "quan_qconv2d_backward_weight": (ctypes.c_int, [_vp] * 2 + [_i32] * 6 + [_vp] * 5 + [_i32] * 8 + [_vp]),
+    "quan_qconv2d_separable_backward_data": (ctypes.c_int, [_vp] * 5 + [_i32] * 6 + [_vp] + [_i32] * 8 + [_vp]),
+    "quan_qconv2d_separable_backward_weight": (ctypes.c_int, [_vp] * 2 + [_i32] * 6 + [_vp] * 5 + [_i32] * 8
+                                               + [_vp]),
     "quan_iqbn_backward": (ctypes.c_int, [_vp] * 6 + [_f32] + [_vp] * 3 + [_i32] * 5 + [_vp]),
     "quan_iqbn_forward": (ctypes.c_int, [_vp, _vp, _vp, _f32, _vp, _vp, _vp] + [_i32] * 5 + [_vp]),
     "quan_iqbn_relu_forward": (ctypes.c_int, [_vp, _vp, _vp, _f32, _vp, _vp, _vp] + [_i32] * 5 + [_vp]),
@@ -355,7 +358,8 @@ def quan_poincare_map(rgb, out=None):
     return out
 
 
-def quan_qconv2d_backward_data(dy, w_r, w_i, w_j, w_k, input_hw, stride=1, pad=0, dilation=1, dx=None):
+def quan_qconv2d_backward_data(dy, w_r, w_i, w_j, w_k, input_hw, stride=1, pad=0, dilation=1, dx=None,
+                               _fn="quan_qconv2d_backward_data"):
     """Input gradient of quan_qconv2d_forward for dL/dY = dy ([N, 4, Cout, Ho,
     Wo], device layout); input_hw = (H, W) of the forward input.  Returns dx
     [N, 4, Cin, H, W] in device layout."""
@@ -377,14 +381,15 @@ def quan_qconv2d_backward_data(dy, w_r, w_i, w_j, w_k, input_hw, stride=1, pad=0
     elif not is_device_layout(dx) or tuple(dx.shape) != (n, 4, c_in, h, w) or dx.dtype != dy.dtype:
         raise ValueError("dx must be [N, 4, Cin, H, W] in device layout with dy's dtype")
     with torch.cuda.device(dy.device):
-        rc = lib.quan_qconv2d_backward_data(_ptr(dy), _ptr(w_r), _ptr(w_i), _ptr(w_j), _ptr(w_k), sh, sw, ph, pw,
-                                            dh, dw, _ptr(dx), n, c_in, h, w, c_out, k_h, k_w, _dtype_code(dy),
-                                            _stream(dy.device))
+        rc = getattr(lib, _fn)(_ptr(dy), _ptr(w_r), _ptr(w_i), _ptr(w_j), _ptr(w_k), sh, sw, ph, pw,
+                               dh, dw, _ptr(dx), n, c_in, h, w, c_out, k_h, k_w, _dtype_code(dy),
+                               _stream(dy.device))
     _check(rc)
     return dx
 
 
-def quan_qconv2d_backward_weight(x, dy, kernel_hw, stride=1, pad=0, dilation=1, with_bias=True):
+def quan_qconv2d_backward_weight(x, dy, kernel_hw, stride=1, pad=0, dilation=1, with_bias=True,
+                                 _fn="quan_qconv2d_backward_weight"):
     """Weight (and bias) gradients of quan_qconv2d_forward for dL/dY = dy:
     returns ([dW_r, dW_i, dW_j, dW_k] each fp32 [Cout, Cin, kh, kw], db fp32
     [4, Cout] or None)."""
@@ -405,11 +410,25 @@ def quan_qconv2d_backward_weight(x, dy, kernel_hw, stride=1, pad=0, dilation=1, 
     dws = [torch.empty((c_out, c_in, k_h, k_w), dtype=torch.float32, device=x.device) for _ in range(4)]
     db = torch.empty((4, c_out), dtype=torch.float32, device=x.device) if with_bias else None
     with torch.cuda.device(x.device):
-        rc = lib.quan_qconv2d_backward_weight(_ptr(x), _ptr(dy), sh, sw, ph, pw, dh, dw_, *[_ptr(t) for t in dws],
-                                              _ptr(db), n, c_in, h, w, c_out, k_h, k_w, _dtype_code(x),
-                                              _stream(x.device))
+        rc = getattr(lib, _fn)(_ptr(x), _ptr(dy), sh, sw, ph, pw, dh, dw_, *[_ptr(t) for t in dws],
+                               _ptr(db), n, c_in, h, w, c_out, k_h, k_w, _dtype_code(x),
+                               _stream(x.device))
     _check(rc)
     return dws, db
+
+
+def quan_qconv2d_separable_backward_data(dy, w_r, w_i, w_j, w_k, input_hw, stride=1, pad=0, dilation=1, dx=None):
+    """Input gradient of quan_qconv2d_separable_forward (eqs. 8-10); arguments
+    and result as in quan_qconv2d_backward_data."""
+    return quan_qconv2d_backward_data(dy, w_r, w_i, w_j, w_k, input_hw, stride, pad, dilation, dx,
+                                      _fn="quan_qconv2d_separable_backward_data")
+
+
+def quan_qconv2d_separable_backward_weight(x, dy, kernel_hw, stride=1, pad=0, dilation=1, with_bias=True):
+    """Weight (and bias) gradients of quan_qconv2d_separable_forward (eqs.
+    8-10); arguments and result as in quan_qconv2d_backward_weight."""
+    return quan_qconv2d_backward_weight(x, dy, kernel_hw, stride, pad, dilation, with_bias,
+                                        _fn="quan_qconv2d_separable_backward_weight")
 
 
 def quan_iqbn_backward(x, dout, mean, var, gamma, y=None, eps=1e-5, dx=None):

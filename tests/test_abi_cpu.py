@@ -203,21 +203,21 @@ DX, DG, DB = 0xA0000000, 0xA8000000, 0xA8100000
 DW0, DW1, DW2, DW3 = (0xB0000000 + 0x100000 * i for i in range(4))
 
 
-def bwd_data(lib, **kw):
+def bwd_data(lib, fn="quan_qconv2d_backward_data", **kw):
     a = dict(dy=OUT, wr=WR, wi=WI, wj=WJ, wk=WK, sh=1, sw=1, ph=1, pw=1, dh=1, dw=1, dx=DX, n=2, cin=4, h=16, w=16,
              cout=4, kh=3, kw=3, dtype=1)
     a.update(kw)
-    rc = lib.quan_qconv2d_backward_data(a["dy"], a["wr"], a["wi"], a["wj"], a["wk"], a["sh"], a["sw"], a["ph"],
+    rc = getattr(lib, fn)(a["dy"], a["wr"], a["wi"], a["wj"], a["wk"], a["sh"], a["sw"], a["ph"],
                                         a["pw"], a["dh"], a["dw"], a["dx"], a["n"], a["cin"], a["h"], a["w"],
                                         a["cout"], a["kh"], a["kw"], a["dtype"], None)
     return rc, lib.quan_last_error().decode()
 
 
-def bwd_weight(lib, **kw):
+def bwd_weight(lib, fn="quan_qconv2d_backward_weight", **kw):
     a = dict(x=X, dy=OUT, sh=1, sw=1, ph=1, pw=1, dh=1, dw=1, d0=DW0, d1=DW1, d2=DW2, d3=DW3, db=DB, n=2, cin=4,
              h=16, w=16, cout=4, kh=3, kw=3, dtype=1)
     a.update(kw)
-    rc = lib.quan_qconv2d_backward_weight(a["x"], a["dy"], a["sh"], a["sw"], a["ph"], a["pw"], a["dh"], a["dw"],
+    rc = getattr(lib, fn)(a["x"], a["dy"], a["sh"], a["sw"], a["ph"], a["pw"], a["dh"], a["dw"],
                                           a["d0"], a["d1"], a["d2"], a["d3"], a["db"], a["n"], a["cin"], a["h"],
                                           a["w"], a["cout"], a["kh"], a["kw"], a["dtype"], None)
     return rc, lib.quan_last_error().decode()
@@ -237,9 +237,10 @@ BWD_DATA_ERRORS = [
 ]
 
 
+@pytest.mark.parametrize("fn", ["quan_qconv2d_backward_data", "quan_qconv2d_separable_backward_data"])
 @pytest.mark.parametrize("name,kw,code", BWD_DATA_ERRORS, ids=[c[0] for c in BWD_DATA_ERRORS])
-def test_backward_data_rejects(lib, name, kw, code):
-    rc, msg = bwd_data(lib, **kw)
+def test_backward_data_rejects(lib, name, kw, code, fn):
+    rc, msg = bwd_data(lib, fn=fn, **kw)
     assert rc == code, (name, rc, msg)
     assert msg
 
@@ -257,9 +258,10 @@ BWD_WEIGHT_ERRORS = [
 ]
 
 
+@pytest.mark.parametrize("fn", ["quan_qconv2d_backward_weight", "quan_qconv2d_separable_backward_weight"])
 @pytest.mark.parametrize("name,kw,code", BWD_WEIGHT_ERRORS, ids=[c[0] for c in BWD_WEIGHT_ERRORS])
-def test_backward_weight_rejects(lib, name, kw, code):
-    rc, msg = bwd_weight(lib, **kw)
+def test_backward_weight_rejects(lib, name, kw, code, fn):
+    rc, msg = bwd_weight(lib, fn=fn, **kw)
     assert rc == code, (name, rc, msg)
     assert msg
 

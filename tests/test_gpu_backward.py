@@ -2,7 +2,8 @@
 fp64 gradients (the adjoint of the forward, pinned by autograd and adjoint
 identities): the Hamilton convolution's input gradient (strides 1 and 2,
 pads, dilations, channel counts off the vector width), its weight and bias
-gradients, and training-mode IQBN's gradients with and without ReLU.  The
+gradients, the same for the separable form (eqs. 8-10, mixing matrix M),
+and training-mode IQBN's gradients with and without ReLU.  The
 imagenet_stage layer's weight gradient is checked at full size on sampled
 (output, input) channel pairs: each pair's gradient depends only on that
 channel of x and of dy, so the oracle runs on one-channel slices; its input
@@ -80,6 +81,88 @@ def test_backward_weight_matches_oracle(shape, dtype):
     got_w = np.stack([f64(t.cpu()) for t in dws])
     assert_close(got_w, ref_w, torch.float32, f"dW {dtype} {shape}")
     assert_close(f64(db.cpu()), ref_b, torch.float32, f"dbias {dtype} {shape}")
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("shape", SHAPES, ids=[str(s) for s in SHAPES])
+def test_separable_backward_data_matches_oracle(shape, dtype):
+    say(f"separable backward data {dtype} {shape}")
+    dt = DT[dtype]
+    N, Cin, Cout, H, W, k, s, p, d = shape
+    x, w, dy = _case(shape, dt, seed=hash(shape) % 1000 + 7)
+    dev = torch.device("cuda:0")
+    dx = quan.empty_qmap(N, Cin, H, W, dt, dev)
+    dx.fill_(float("nan"))
+    quan.quan_qconv2d_separable_backward_data(quan.to_device_layout(dy.to(dev)),
+                                              *[w[q].contiguous().to(dev) for q in range(4)], (H, W), stride=s,
+                                              pad=p, dilation=d, dx=dx)
+    torch.cuda.synchronize()
+    ref, _, _ = oracle.qconv2d_separable_backward(f64(x), f64(w), f64(dy), s, p, d)
+    # bf16: the mixed gradient z (a sum of four values) is rounded once to
+    # bf16 before the convolution, as the forward rounds its input
+    assert_close(f64(dx.cpu()), ref, dt, f"separable dX {dtype} {shape}")
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("shape", SHAPES, ids=[str(s) for s in SHAPES])
+def test_separable_backward_weight_matches_oracle(shape, dtype):
+    say(f"separable backward weight {dtype} {shape}")
+    dt = DT[dtype]
+    N, Cin, Cout, H, W, k, s, p, d = shape
+    x, w, dy = _case(shape, dt, seed=hash(shape) % 1000 + 8)
+    dev = torch.device("cuda:0")
+    dws, db = quan.quan_qconv2d_separable_backward_weight(quan.to_device_layout(x.to(dev)),
+                                                          quan.to_device_layout(dy.to(dev)), (k, k), stride=s,
+                                                          pad=p, dilation=d)
+    torch.cuda.synchronize()
+    _, ref_w, ref_b = oracle.qconv2d_separable_backward(f64(x), f64(w), f64(dy), s, p, d)
+    got_w = np.stack([f64(t.cpu()) for t in dws])
+    assert_close(got_w, ref_w, torch.float32, f"separable dW {dtype} {shape}")
+    assert_close(f64(db.cpu()), ref_b, torch.float32, f"separable dbias {dtype} {shape}")
+
+
+def test_separable_backward_full_imagenet_layer_sampled():
+    """The imagenet_stage layer's separable gradients at full size: dW on
+    sampled (output, input) channel pairs (the oracle on one-channel slices:
+    the mixing acts per channel), dX on sampled input pixels (the oracle on
+    the k x k window of dy around each)."""
+    say("separable backward full-size sampled")
+    from paper_2509_05512_amd import workloads
+    wl = workloads.WORKLOADS["imagenet_stage"]
+    tens = workloads.generate(wl)
+    layer = tens.layers[0]
+    L = wl.layers[0]
+    k, p = L.k, L.pad
+    dev = torch.device("cuda:0")
+    rng = np.random.default_rng(9)
+    dy = torch.from_numpy(rng.standard_normal((wl.n, 4, L.c_out, wl.h, wl.w), dtype=np.float32)).to(torch.bfloat16)
+    dyg = quan.to_device_layout(dy.to(dev))
+    w = [layer.weight[q].contiguous() for q in range(4)]
+    dws, db = quan.quan_qconv2d_separable_backward_weight(quan.to_device_layout(tens.x.to(dev)), dyg, (k, k),
+                                                          stride=1, pad=p)
+    dx = quan.quan_qconv2d_separable_backward_data(dyg, *[t.to(dev) for t in w], (wl.h, wl.w), stride=1, pad=p)
+    torch.cuda.synchronize()
+    x64, dy64 = f64(tens.x), f64(dy)
+    got = np.stack([f64(t.cpu()) for t in dws])
+    w1 = np.zeros((4, 1, 1, k, k))
+    for (o, c) in [(0, 0), (63, 63), (7, 40), (41, 3), (20, 20)]:
+        _, ref, _ = oracle.qconv2d_separable_backward(x64[:, :, c:c + 1], w1, dy64[:, :, o:o + 1], 1, p, 1)
+        assert_close(got[:, o, c], ref[:, 0, 0], torch.float32, f"separable dW imagenet (o={o}, c={c})")
+    assert_close(f64(db.cpu()), dy64.sum(axis=(0, 3, 4)), torch.float32, "separable dbias imagenet")
+    w64 = np.stack([f64(t) for t in w])
+    x1 = np.zeros((1, 4, L.c_in, 1, 1))
+    picks = [(0, 0, 0), (wl.n - 1, wl.h - 1, wl.w - 1)]
+    picks += [(int(rng.integers(wl.n)), int(rng.integers(wl.h)), int(rng.integers(wl.w))) for _ in range(14)]
+    for (n, iy, ix) in picks:
+        win = np.zeros((1, 4, L.c_out, k, k))
+        for a in range(k):
+            for b in range(k):
+                oy, ox = iy + p - (k - 1) + a, ix + p - (k - 1) + b
+                if 0 <= oy < wl.h and 0 <= ox < wl.w:
+                    win[0, :, :, a, b] = dy64[n, :, :, oy, ox]
+        ref, _, _ = oracle.qconv2d_separable_backward(x1, w64, win, 1, k - 1, 1)
+        assert_close(dx[n, :, :, iy, ix].double().cpu().numpy(), ref[0, :, :, 0, 0], torch.bfloat16,
+                     f"separable dX imagenet ({n}, {iy}, {ix})")
 
 
 def test_backward_weight_full_imagenet_layer_sampled():
