@@ -272,7 +272,9 @@ def time_backward(layers, quan, steps, eps):
 def time_poincare(quan, steps, dev):
     """The Poincare input mapping of one ImageNet-sized bf16 batch
     (64 x 3 x 224 x 224): microseconds per launch and algorithmic GB/s
-    (3 reads + 4 writes of a 2-byte element per pixel)."""
+    (3 reads + 4 writes of a 2-byte element per pixel); and a stem
+    convolution on it with the map fused into its loads against the two
+    separate passes."""
     import torch
     n, h, w = 64, 224, 224
     g = torch.Generator(device="cpu").manual_seed(5)
@@ -289,8 +291,41 @@ def time_poincare(quan, steps, dev):
     torch.cuda.synchronize()
     us = start.elapsed_time(end) * 1e3 / steps
     gbps = n * h * w * 7 * 2 / (us * 1e-6) / 1e9
+    # the stem convolution on the mapped batch (3x3, stride 2, pad 1, 16
+    # quaternion channels): the map fused into the convolution's loads,
+    # against the map followed by the convolution
+    c_out, k = 16, 3
+    w = [(torch.randn((c_out, 1, k, k), generator=g) / 6.0).to(torch.bfloat16).to(dev) for _ in range(4)]
+    packed = quan.quan_qconv2d_pack_weights(*w)
+    shape = (c_out, 1, k, k)
+    y = quan.quan_qconv2d_poincare_forward(rgb, packed, shape, stride=2, pad=1)
+
+    def fused():
+        quan.quan_qconv2d_poincare_forward(rgb, packed, shape, stride=2, pad=1, out=y)
+
+    def two_pass():
+        quan.quan_poincare_map(rgb, out=q)
+        quan.quan_qconv2d_forward_packed(q, packed, shape, stride=2, pad=1, out=y)
+
+    times = {}
+    for name, fn in (("fused", fused), ("two_pass", two_pass), ("fused2", fused), ("two_pass2", two_pass)):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        start.record()
+        for _ in range(steps):
+            fn()
+        end.record()
+        torch.cuda.synchronize()
+        times[name] = start.elapsed_time(end) * 1e3 / steps
+    stem_flops = 2 * n * y.shape[3] * y.shape[4] * 4 * c_out * 4 * 1 * k * k
+    fused_us = min(times["fused"], times["fused2"])
     return {"workload": "64x3x224x224 bf16", "us": round(us, 3), "gbps": round(gbps, 1),
-            "frac_hbm_peak": round(gbps / HBM_PEAK_GBPS, 4)}
+            "frac_hbm_peak": round(gbps / HBM_PEAK_GBPS, 4),
+            "stem": {"conv": "3x3 stride 2 pad 1, 1 -> 16 quaternion channels",
+                     "fused_us": round(fused_us, 3),
+                     "two_pass_us": round(min(times["two_pass"], times["two_pass2"]), 3),
+                     "fused_tflops": round(stem_flops / (fused_us * 1e-6) / 1e12, 2)}}
 
 
 def run_step(layers, quan, events=None, eps=1e-5):

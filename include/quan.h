@@ -301,6 +301,29 @@ QUAN_API int quan_poincare_map(const void *rgb, void *out, int32_t n, int32_t h,
                                int32_t dtype, void *stream);
 
 /*
+ * The first convolution of a network on RGB input with the Poincare mapping
+ * of eq. 4 fused into its loads: out = quan_qconv2d_forward_packed(
+ * quan_poincare_map(rgb), packed, bias, ...) of a one-channel (c_in = 1)
+ * layer, without the quaternion map ever reaching memory.  The kernel
+ * forms each tap's input quaternion from the three colour samples in fp32
+ * and rounds it once to dtype, as quan_poincare_map does.
+ *
+ *   rgb     [n, 3, h, w] colour planes (dtype, aligned to its element).
+ *   packed  quan_qconv2d_pack_weights of the four [c_out, 1, k_h, k_w]
+ *           kernels (c_in = 1).
+ *   out     [n, 4, c_out, Ho, Wo] channels-last by component, 16-byte
+ *           aligned, overlapping neither rgb, packed nor bias.
+ * Every other argument, rule and error is quan_qconv2d_forward_packed's.
+ */
+QUAN_API int quan_qconv2d_poincare_forward(const void *rgb, const void *packed, const void *bias,
+                                           int32_t stride_h, int32_t stride_w,
+                                           int32_t pad_h, int32_t pad_w,
+                                           int32_t dilation_h, int32_t dilation_w, void *out,
+                                           int32_t n, int32_t h, int32_t w, int32_t c_out,
+                                           int32_t k_h, int32_t k_w, int32_t dtype, void *stream);
+
+/*
+ * Input gradient of the Hamilton convolution (the backward pass of/*
  * Input gradient of the Hamilton convolution (the backward pass of
  * quan_qconv2d_forward with respect to x): for dL/dY = dy,
  *

@@ -294,8 +294,14 @@ constexpr int producer_waves()
 // matrix M = S^T (S eq. 7's signs): kernel p with sign M[p][q] = S[q][p], so
 // the mixing is accumulated in fp32 with the products.
 enum : int { kFormHamilton = 0, kFormSepGrad = 1 };
+// POINCARE (the stem layer, one input channel, element-wise loads): x is
+// the colour planes [N][3][H][W] of the input images, and the producer
+// forms the input quaternion of eq. 4 at each tap pixel, q = ((1 - n2), 2r,
+// 2g, 2b) / (1 + n2) with n2 = r^2 + g^2 + b^2, in fp32 rounded once to T,
+// instead of reading a mapped activation: the quaternion map never goes to
+// memory.
 template <typename T, int MB, int NB, int WAVES_M, int WAVES_N, bool VEC, int EPI, bool SEP, bool PAIR = false,
-          bool ALLP = false, int FORM = kFormHamilton>
+          bool ALLP = false, int FORM = kFormHamilton, bool POINCARE = false>
 __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB, WAVES_M, WAVES_N, SEP, ALLP>())) void qconv2d_igemm(KArgs a)
 {
     constexpr int ES = int(sizeof(T));
@@ -331,6 +337,7 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
     static_assert(!ALLP || (!SEP && !PAIR && ES == 2 && MB == 1 && WAVES_N == 1),
                   "all-components waves: Hamilton form, bf16, 32 pixels per wave");
     static_assert(FORM == kFormHamilton || (!SEP && EPI == kEpiBias), "block tables: Hamilton layouts, bias epilogue");
+    static_assert(!POINCARE || (!VEC && !SEP && EPI == kEpiBias), "Poincare stem: element loads, bias epilogue");
     // kernel component and sign of block (output p, input q)
     auto blk_kernel = [](int p, int q) { return FORM == kFormHamilton ? (p ^ q) : p; };
     auto blk_neg = [](int p, int q) -> bool {
@@ -402,6 +409,7 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
         const T *xt = nullptr;
         unsigned x_bytes = 0;  // bytes of x from xt on (capped at 2^31 - 1)
         int p_off[A_MINE], p_iy[A_MINE], p_ix[A_MINE], p_cl[A_MINE];
+        int p_comp[A_MINE];  // POINCARE: the quaternion component of the lane's chunk
         unsigned p_woff[B_MINE];
         int p_wodd[B_MINE];  // PAIR: the instruction's channel half
         // Activation DMA i covers rows 8i..8i+7 of the tile: lane l loads
@@ -416,7 +424,7 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
             const int m0 = (tile / a.n_tiles) * BM;
             const int o0 = (tile % a.n_tiles) * BNC;
             const int img0 = m0 / hw_out;
-            xt = static_cast<const T *>(a.x) + img0 * img_elems;
+            xt = static_cast<const T *>(a.x) + img0 * (POINCARE ? 3LL * a.h * a.w : img_elems);
             const long long rest = (a.x_elems - img0 * img_elems) * ES;
             x_bytes = rest <= 0 ? 0u : (rest < 0x7fffffffLL ? unsigned(rest) : 0x7fffffffu);
 #pragma unroll
@@ -428,6 +436,7 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
                 const int comp = PAIR ? lc / 4 : lc / CPQ, cin = PAIR ? (lc % 4) * EPC : (lc % CPQ) * EPC;
                 const int m = m0 + row;
                 p_cl[ii] = a.c_in - cin;  // channels of this chunk left before block 0
+                p_comp[ii] = comp;
                 if (m < a.m) {
                     const int img = m / hw_out;
                     const int rr = m - img * hw_out;
@@ -438,6 +447,8 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
                     const int e = (((img - img0) * a.h + p_iy[ii]) * a.w + p_ix[ii]) * row_elems +
                                   comp * a.c_in + cin;
                     p_off[ii] = VEC ? e * ES : e;
+                    if constexpr (POINCARE)  // the pixel's red sample in the planes [img][3][h][w]
+                        p_off[ii] = ((img - img0) * 3 * a.h + p_iy[ii]) * a.w + p_ix[ii];
                 } else {
                     p_iy[ii] = -0x20000000;  // rows past M never load
                     p_ix[ii] = 0;
@@ -490,6 +501,26 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
                 if constexpr (VEC) {
                     const unsigned off = inside ? unsigned(p_off[ii] + shift * ES) : 0x80000000u;
                     dma16(xt, x_bytes, off, 0u, a_base + buf * A_BYTES + i * 1024);
+                } else if constexpr (POINCARE) {
+                    // one input channel: the lane of component q's first chunk
+                    // holds q's value in element 0, everything else is zero
+                    u32x4 v = {0u, 0u, 0u, 0u};
+                    if (inside) {
+                        const int hw = a.h * a.w;
+                        const T *px = xt + p_off[ii] + dy * a.w + dx;
+                        const float r = float(px[0]), g = float(px[hw]), b = float(px[2 * hw]);
+                        const float n2 = r * r + g * g + b * b;
+                        const float den = 1.0f + n2;
+                        const int qc = p_comp[ii];
+                        const float num = qc == 0 ? 1.0f - n2 : 2.0f * (qc == 1 ? r : qc == 2 ? g : b);
+                        T e[Elem<T>::per_chunk];
+#pragma unroll
+                        for (int k = 0; k < Elem<T>::per_chunk; ++k)
+                            e[k] = T(0);
+                        e[0] = T(num / den);
+                        __builtin_memcpy(&v, e, 16);
+                    }
+                    *reinterpret_cast<u32x4 *>(a_lds + buf * A_BYTES + i * 1024 + lane * 16) = v;
                 } else {
                     u32x4 v = {0u, 0u, 0u, 0u};
                     if (inside)
@@ -1508,9 +1539,10 @@ struct KernelEntry {
     // [epilogue kind][variant]: variant 0 when c_in is a multiple of the
     // 16-byte vector (activations move by DMA), 1 for element loads with
     // channel masking, 2 for paired stages (separable bf16, c_in a multiple
-    // of 32); NULL where the kind or variant does not apply (statistics need
+    // of 32), 3 for the Poincare stem (element loads of eq. 4 from colour
+    // planes); NULL where the kind or variant does not apply (statistics need
     // the deferred epilogue).
-    const void *fn[3][3];
+    const void *fn[3][4];
     const char *name;
 };
 
@@ -1534,6 +1566,15 @@ constexpr const void *pair_fn()
     else
         return nullptr;
 }
+// the Poincare stem variant exists for the Hamilton form
+template <typename T, int MB, int NB, int WM, int WN, bool SEP>
+constexpr const void *stem_fn()
+{
+    if constexpr (SEP)
+        return nullptr;
+    else
+        return (const void *)&qconv2d_igemm<T, MB, NB, WM, WN, false, kEpiBias, SEP, false, false, kFormHamilton, true>;
+}
 // the folded-IQBN epilogue serves the Hamilton form only (inference
 // convolution + IQBN); the separable form has a bias epilogue
 template <typename T, int MB, int NB, int WM, int WN, bool VEC, bool SEP>
@@ -1551,12 +1592,12 @@ constexpr const void *fold_fn()
             QCONV_DEFER(NB, WM, WN, SEP), 32 * (MB) * (WM), DT,                                        \
             {{(const void *)&qconv2d_igemm<T, MB, NB, WM, WN, true, kEpiBias, SEP>,                    \
               (const void *)&qconv2d_igemm<T, MB, NB, WM, WN, false, kEpiBias, SEP>,                   \
-              pair_fn<T, MB, NB, WM, WN, kEpiBias, SEP>()},                                              \
+              pair_fn<T, MB, NB, WM, WN, kEpiBias, SEP>(), stem_fn<T, MB, NB, WM, WN, SEP>()},           \
              {QCONV_STATS_FN(T, MB, NB, WM, WN, true, SEP), QCONV_STATS_FN(T, MB, NB, WM, WN, false, SEP), \
-              nullptr},                                                                                  \
+              nullptr, nullptr},                                                                         \
              {fold_fn<T, MB, NB, WM, WN, true, SEP>(),                                                 \
               fold_fn<T, MB, NB, WM, WN, false, SEP>(),                                                \
-              pair_fn<T, MB, NB, WM, WN, kEpiFold, SEP>()}},                                             \
+              pair_fn<T, MB, NB, WM, WN, kEpiFold, SEP>(), nullptr}},                                    \
             #T "_mb" #MB "x" #WM "_nb" #NB "x" #WN #SEP                                                \
     }
 
@@ -1569,13 +1610,15 @@ constexpr const void *fold_fn()
             DType::BF16,                                                                               \
             {{(const void *)&qconv2d_igemm<__bf16, 1, NB, 4, 1, true, kEpiBias, false, false, true>,    \
               (const void *)&qconv2d_igemm<__bf16, 1, NB, 4, 1, false, kEpiBias, false, false, true>,   \
-              nullptr},                                                                                \
+              nullptr,                                                                                 \
+              (const void *)&qconv2d_igemm<__bf16, 1, NB, 4, 1, false, kEpiBias, false, false, true,    \
+                                           kFormHamilton, true>},                                      \
              {(const void *)&qconv2d_igemm<__bf16, 1, NB, 4, 1, true, kEpiStats, false, false, true>,   \
               (const void *)&qconv2d_igemm<__bf16, 1, NB, 4, 1, false, kEpiStats, false, false, true>,  \
-              nullptr},                                                                                \
+              nullptr, nullptr},                                                                       \
              {(const void *)&qconv2d_igemm<__bf16, 1, NB, 4, 1, true, kEpiFold, false, false, true>,    \
               (const void *)&qconv2d_igemm<__bf16, 1, NB, 4, 1, false, kEpiFold, false, false, true>,   \
-              nullptr}},                                                                               \
+              nullptr, nullptr}},                                                                      \
             "bf16_allp_nb" #NB                                                                         \
     }
 
@@ -1589,9 +1632,9 @@ constexpr const void *fold_fn()
             32 * (MB) * (WM), DT,                                                                      \
             {{(const void *)&qconv2d_igemm<T, MB, NB, WM, WN, true, kEpiBias, false, false, ALLPW, kFormSepGrad>,  \
               (const void *)&qconv2d_igemm<T, MB, NB, WM, WN, false, kEpiBias, false, false, ALLPW, kFormSepGrad>, \
-              nullptr},                                                                                \
-             {nullptr, nullptr, nullptr},                                                              \
-             {nullptr, nullptr, nullptr}},                                                             \
+              nullptr, nullptr},                                                                       \
+             {nullptr, nullptr, nullptr, nullptr},                                                     \
+             {nullptr, nullptr, nullptr, nullptr}},                                                    \
             #T "_sepgrad_mb" #MB "x" #WM "_nb" #NB "x" #WN                                             \
     }
 
@@ -1837,7 +1880,7 @@ bool qconv2d_writes_stats(const ConvPlan &plan, const ConvGeom &g, DType dt)
 
 hipError_t qconv2d_run(const ConvPlan &plan, const PackGeom &pg, const ConvGeom &g, DType dt,
                        const void *x, const void *wpack, const void *bias, void *out,
-                       float *stats, const ConvFold *fold, hipStream_t stream)
+                       float *stats, const ConvFold *fold, hipStream_t stream, bool poincare)
 {
     if (plan.id < 0 || plan.id >= kNumKernels)
         return hipErrorInvalidValue;
@@ -1885,7 +1928,9 @@ hipError_t qconv2d_run(const ConvPlan &plan, const PackGeom &pg, const ConvGeom 
     void *args[] = {&a};
     const int epi = stats != nullptr ? kEpiStats : fold != nullptr ? kEpiFold : kEpiBias;
     const bool paired = k.fn[epi][2] != nullptr && g.c_in % 32 == 0;
-    const void *fn = k.fn[epi][(g.c_in % epc) != 0 ? 1 : paired ? 2 : 0];
+    if (poincare && (g.c_in != 1 || epi != kEpiBias))
+        return hipErrorInvalidValue;
+    const void *fn = k.fn[epi][poincare ? 3 : (g.c_in % epc) != 0 ? 1 : paired ? 2 : 0];
     if (fn == nullptr)
         return hipErrorInvalidValue;
     // Persistent grid: as many work-groups as fit on the device at once, at

@@ -115,10 +115,12 @@ quan::DType to_dt(int32_t dtype)
 // Validation shared by the two convolution entry points (everything except
 // the weights): sizes, output extent, limits, alignment of x/out/bias and
 // overlap of out with x and the bias.  Fills the geometry on success.
+// rgb_planes: x is the colour planes [n][3][h][w] of a Poincare stem (c_in
+// 1), aligned to its element and sized as such.
 int check_conv(const void *x, const void *bias, int32_t stride_h, int32_t stride_w, int32_t pad_h,
                int32_t pad_w, int32_t dilation_h, int32_t dilation_w, const void *out, int32_t n,
                int32_t c_in, int32_t h, int32_t w, int32_t c_out, int32_t k_h, int32_t k_w,
-               int32_t dtype, quan::ConvGeom *g, size_t *xb, size_t *ob)
+               int32_t dtype, quan::ConvGeom *g, size_t *xb, size_t *ob, bool rgb_planes = false)
 {
     if (int rc = check_dtype(dtype))
         return rc;
@@ -133,7 +135,7 @@ int check_conv(const void *x, const void *bias, int32_t stride_h, int32_t stride
     if (span_h < 0 || span_w < 0)
         return fail(QUAN_ERR_SHAPE, "qconv2d: empty output (kernel span exceeds padded input)");
     const int64_t ho = span_h / stride_h + 1, wo = span_w / stride_w + 1;
-    const int64_t x_elems = int64_t(n) * h * w * 4 * c_in;
+    const int64_t x_elems = int64_t(n) * h * w * (rgb_planes ? 3 : 4 * c_in);
     const int64_t o_elems = int64_t(n) * ho * wo * 4 * c_out;
     const int64_t w_elems = int64_t(c_out) * c_in * k_h * k_w;
     if (x_elems > kMaxElems || o_elems > kMaxElems || w_elems * 4 * 4 > kMaxElems)
@@ -145,8 +147,9 @@ int check_conv(const void *x, const void *bias, int32_t stride_h, int32_t stride
     const int64_t img_bytes = int64_t(h) * w * 4 * c_in * int64_t(es);
     if (img_bytes * (256 / (ho * wo) + 2) > kMaxElems)
         return fail(QUAN_ERR_UNSUPPORTED, "qconv2d: images of x too large for 32-bit tile offsets");
-    if (misaligned(x, 16) || misaligned(out, 16))
-        return fail(QUAN_ERR_ALIGN, "qconv2d: x and out must be 16-byte aligned");
+    if (misaligned(x, rgb_planes ? es : 16) || misaligned(out, 16))
+        return fail(QUAN_ERR_ALIGN, rgb_planes ? "qconv2d: rgb must be aligned to its element, out to 16 bytes"
+                                               : "qconv2d: x and out must be 16-byte aligned");
     if (bias && misaligned(bias, es))
         return fail(QUAN_ERR_ALIGN, "qconv2d: weights and bias must be aligned to their element size");
     *xb = size_t(x_elems) * es;
@@ -535,6 +538,38 @@ QUAN_API int quan_qconv2d_iqbn_inference(const void *x, const void *packed, cons
                           nullptr, &fold, s);
     if (e != hipSuccess)
         return fail_hip(e, "qconv2d launch");
+    return QUAN_OK;
+}
+
+QUAN_API int quan_qconv2d_poincare_forward(const void *rgb, const void *packed, const void *bias,
+                                           int32_t stride_h, int32_t stride_w, int32_t pad_h, int32_t pad_w,
+                                           int32_t dilation_h, int32_t dilation_w, void *out, int32_t n,
+                                           int32_t h, int32_t w, int32_t c_out, int32_t k_h, int32_t k_w,
+                                           int32_t dtype, void *stream)
+{
+    g_last_error.clear();
+    if (!rgb || !packed || !out)
+        return fail(QUAN_ERR_NULL, "qconv2d_poincare: rgb, packed and out must be non-NULL");
+    // the layer's geometry as a one-channel convolution of the planes
+    quan::ConvGeom g;
+    size_t xb = 0, ob = 0;
+    if (int rc = check_conv(rgb, bias, stride_h, stride_w, pad_h, pad_w, dilation_h, dilation_w, out, n, 1, h, w,
+                            c_out, k_h, k_w, dtype, &g, &xb, &ob, true))
+        return rc;
+    const int64_t need = quan_qconv2d_packed_bytes(1, c_out, k_h, k_w, dtype);
+    if (need < 0)
+        return int(need);
+    if (misaligned(packed, 16))
+        return fail(QUAN_ERR_ALIGN, "qconv2d_poincare: packed must be 16-byte aligned");
+    if (overlaps(out, ob, packed, size_t(need)))
+        return fail(QUAN_ERR_ALIAS, "qconv2d_poincare: out overlaps the packed weights");
+    const quan::DType dt = to_dt(dtype);
+    const quan::PackGeom pg = quan::qconv2d_pack_geom(1, c_out, k_h, k_w, dt);
+    const hipError_t e = quan::qconv2d_run(quan::qconv2d_plan(g, dt, quan::ConvForm::Hamilton), pg, g, dt, rgb,
+                                           packed, bias, out, nullptr, nullptr, static_cast<hipStream_t>(stream),
+                                           true);
+    if (e != hipSuccess)
+        return fail_hip(e, "qconv2d_poincare launch");
     return QUAN_OK;
 }
 

@@ -71,10 +71,14 @@ struct ConvFold {
     const float *shift;
     bool relu;
 };
+//
+// With `poincare` (a stem layer: g.c_in == 1, bias epilogue) x is the colour
+// planes [n][3][h][w] of the input images, mapped to quaternions by eq. 4
+// as the convolution loads them.
 bool qconv2d_writes_stats(const ConvPlan &plan, const ConvGeom &g, DType dt);
 hipError_t qconv2d_run(const ConvPlan &plan, const PackGeom &pg, const ConvGeom &g, DType dt,
                        const void *x, const void *wpack, const void *bias, void *out,
-                       float *stats, const ConvFold *fold, hipStream_t stream);
+                       float *stats, const ConvFold *fold, hipStream_t stream, bool poincare = false);
 
 // Input gradient of the Hamilton convolution: dX = conv(Z, W'), Z = dY (stride
 // 1) or dY scattered with s-1 zeros between rows/columns (staged in `stage`,

@@ -39,6 +39,7 @@ SIGNATURES = {
     "quan_qconv2d_iqbn_inference": (ctypes.c_int, [_vp] * 3 + [_i32] * 6 + [_vp] * 4 + [_f32, _i32, _vp]
                                     + [_i32] * 8 + [_vp]),
     "quan_poincare_map": (ctypes.c_int, [_vp, _vp] + [_i32] * 4 + [_vp]),
+    "quan_qconv2d_poincare_forward": (ctypes.c_int, [_vp] * 3 + [_i32] * 6 + [_vp] + [_i32] * 7 + [_vp]),
     "quan_qconv2d_backward_data": (ctypes.c_int, [_vp] * 5 + [_i32] * 6 + [_vp] + [_i32] * 8 + [_vp]),
     "quan_qconv2d_backward_weight": (ctypes.c_int, [_vp] * 2 + [_i32] * 6 + [_vp] * 5 + [_i32] * 8 + [_vp]),
     "quan_qconv2d_separable_backward_data": (ctypes.c_int, [_vp] * 5 + [_i32] * 6 + [_vp] + [_i32] * 8 + [_vp]),
@@ -354,6 +355,37 @@ def quan_poincare_map(rgb, out=None):
         raise ValueError("out must be [N, 4, 1, H, W] in device layout with rgb's dtype")
     with torch.cuda.device(rgb.device):
         rc = lib.quan_poincare_map(_ptr(rgb), _ptr(out), n, h, w, _dtype_code(rgb), _stream(rgb.device))
+    _check(rc)
+    return out
+
+
+def quan_qconv2d_poincare_forward(rgb, packed, weight_shape, bias=None, stride=1, pad=0, dilation=1, out=None):
+    """The stem convolution on RGB images [N, 3, H, W] (contiguous) with the
+    Poincare map (eq. 4) fused into its loads: equals quan_qconv2d_forward_packed
+    of quan_poincare_map(rgb).  weight_shape: (Cout, 1, kh, kw) of the packed
+    kernels.  Returns out [N, 4, Cout, Ho, Wo] in device layout."""
+    lib = load_library()
+    if rgb.dim() != 4 or rgb.shape[1] != 3 or not rgb.is_contiguous():
+        raise ValueError("rgb must be a contiguous [N, 3, H, W] tensor")
+    n, _, h, w = rgb.shape
+    c_out, c_in, k_h, k_w = (int(v) for v in weight_shape)
+    if c_in != 1:
+        raise ValueError("the Poincare stem has one input quaternion channel (weight_shape[1] == 1)")
+    if bias is not None and (tuple(bias.shape) != (4, c_out) or not bias.is_contiguous()
+                             or bias.dtype != rgb.dtype or bias.device != rgb.device):
+        raise ValueError("bias must be a contiguous [4, Cout] tensor like rgb")
+    sh, sw = _pair(stride)
+    ph, pw = _pair(pad)
+    dh, dw = _pair(dilation)
+    ho, wo = conv_out_size(h, k_h, sh, ph, dh), conv_out_size(w, k_w, sw, pw, dw)
+    if out is None:
+        out = empty_qmap(n, c_out, ho, wo, rgb.dtype, rgb.device)
+    elif not is_device_layout(out) or tuple(out.shape) != (n, 4, c_out, ho, wo) or out.dtype != rgb.dtype:
+        raise ValueError("out must be [N, 4, Cout, Ho, Wo] in device layout with rgb's dtype")
+    with torch.cuda.device(rgb.device):
+        rc = lib.quan_qconv2d_poincare_forward(_ptr(rgb), _ptr(packed), _ptr(bias), sh, sw, ph, pw, dh, dw,
+                                               _ptr(out), n, h, w, c_out, k_h, k_w, _dtype_code(rgb),
+                                               _stream(rgb.device))
     _check(rc)
     return out
 

@@ -203,6 +203,37 @@ DX, DG, DB = 0xA0000000, 0xA8000000, 0xA8100000
 DW0, DW1, DW2, DW3 = (0xB0000000 + 0x100000 * i for i in range(4))
 
 
+def stem(lib, **kw):
+    a = dict(rgb=X, packed=WR, bias=B, sh=2, sw=2, ph=1, pw=1, dh=1, dw=1, out=OUT, n=2, h=16, w=16, cout=16,
+             kh=3, kw=3, dtype=1)
+    a.update(kw)
+    rc = lib.quan_qconv2d_poincare_forward(a["rgb"], a["packed"], a["bias"], a["sh"], a["sw"], a["ph"], a["pw"],
+                                           a["dh"], a["dw"], a["out"], a["n"], a["h"], a["w"], a["cout"], a["kh"],
+                                           a["kw"], a["dtype"], None)
+    return rc, lib.quan_last_error().decode()
+
+
+STEM_ERRORS = [
+    ("null rgb", dict(rgb=None), E_NULL),
+    ("null packed", dict(packed=None), E_NULL),
+    ("bad dtype", dict(dtype=2), E_DTYPE),
+    ("c_out = 0", dict(cout=0), E_SHAPE),
+    ("empty output", dict(h=1, ph=0), E_SHAPE),
+    ("rgb off its element", dict(rgb=X + 1), E_ALIGN),
+    ("out misaligned", dict(out=OUT + 8), E_ALIGN),
+    ("packed misaligned", dict(packed=WR + 8), E_ALIGN),
+    ("out overlaps rgb", dict(out=X + 256), E_ALIAS),
+    ("out overlaps packed", dict(out=WR - 256), E_ALIAS),
+]
+
+
+@pytest.mark.parametrize("name,kw,code", STEM_ERRORS, ids=[c[0] for c in STEM_ERRORS])
+def test_poincare_stem_rejects(lib, name, kw, code):
+    rc, msg = stem(lib, **kw)
+    assert rc == code, (name, rc, msg)
+    assert msg
+
+
 def bwd_data(lib, fn="quan_qconv2d_backward_data", **kw):
     a = dict(dy=OUT, wr=WR, wi=WI, wj=WJ, wk=WK, sh=1, sw=1, ph=1, pw=1, dh=1, dw=1, dx=DX, n=2, cin=4, h=16, w=16,
              cout=4, kh=3, kw=3, dtype=1)
