@@ -61,7 +61,8 @@ enum quan_status {
     QUAN_ERR_ALIAS = -5,       /* an output overlaps an input it may not overlap */
     QUAN_ERR_UNSUPPORTED = -6, /* a size exceeds the library's limits */
     QUAN_ERR_HIP = -7,         /* the HIP runtime reported an error */
-    QUAN_ERR_NOMEM = -8        /* the workspace could not be allocated */
+    QUAN_ERR_NOMEM = -8,       /* the workspace could not be allocated */
+    QUAN_ERR_LAYOUT = -9       /* a descriptor's strides are not the layout required */
 };
 
 /*
@@ -220,6 +221,63 @@ QUAN_API int quan_iqbn_relu_forward(const void *x, const float *gamma, const flo
                                     int32_t n, int32_t c, int32_t h, int32_t w,
                                     int32_t dtype, void *stream);
 
+/*
+ * Tensor descriptors
+ * ------------------
+ * The same convolution and IQBN (Section III-B eqs. 5/6, Section III-C eqs.
+ * 11/12) for callers that hold tensors as (pointer, shape, strides) and want
+ * the library, not themselves, to check the memory layout.  A descriptor
+ * names a device buffer owned by the caller, its element type, and per axis
+ * the logical extent and the distance in ELEMENTS between neighbours along
+ * that axis.  An axis of extent 1 is never stepped, so its stride is not
+ * checked (as in PyTorch's contiguity rule).
+ *
+ *   activation   ndim 5, logical [N, 4, C, H, W], strides (H*W*4*C, C, 1,
+ *                W*4*C, 4*C): channels-last by component, the dense
+ *                [N][H][W][4][C] array of every entry point above
+ *   conv weight  ndim 4, [C_out, C_in, k_h, k_w], dense OIHW strides
+ *                (C_in*k_h*k_w, k_h*k_w, k_w, 1)
+ *   conv bias    ndim 2, [4, C_out], strides (C_out, 1)
+ *   IQBN gamma, beta, mean, var   ndim 2, [4, C], strides (C, 1), QUAN_F32
+ *
+ * Any other strides (e.g. NCHW-ordered [N, 4, C, H, W] memory) return
+ * QUAN_ERR_LAYOUT; a wrong ndim or extent returns QUAN_ERR_SHAPE; a dtype
+ * that differs from x's (or is not QUAN_F32 for the IQBN parameters and
+ * statistics) returns QUAN_ERR_DTYPE; a NULL descriptor or data pointer
+ * returns QUAN_ERR_NULL (bias: a NULL descriptor means no bias).  An extent
+ * of 2^31 or more returns QUAN_ERR_UNSUPPORTED.  All of this is checked on
+ * the host before any HIP call; the call then behaves exactly like the
+ * plain-pointer entry point named below, including its alignment and
+ * overlap checks and its asynchronous completion on `stream`.
+ */
+typedef struct quan_tensor {
+    void *data;
+    int32_t dtype;
+    int32_t ndim;
+    int64_t shape[5];
+    int64_t strides[5];
+} quan_tensor;
+
+/* quan_qconv2d_forward on descriptors: x [N, 4, C_in, H, W], w_r..w_k
+ * [C_out, C_in, k_h, k_w], bias [4, C_out] or NULL, out [N, 4, C_out, Ho,
+ * Wo]; stride, pad and dilation are (h, w) pairs. */
+QUAN_API int quan_qconv2d_forward_desc(const quan_tensor *x,
+                                       const quan_tensor *w_r, const quan_tensor *w_i,
+                                       const quan_tensor *w_j, const quan_tensor *w_k,
+                                       const quan_tensor *bias,
+                                       const int32_t stride[2], const int32_t pad[2],
+                                       const int32_t dilation[2],
+                                       quan_tensor *out, void *stream);
+
+/* quan_iqbn_forward and quan_iqbn_relu_forward on descriptors: x and out
+ * [N, 4, C, H, W] (out may be x), gamma, beta, mean, var [4, C] fp32. */
+QUAN_API int quan_iqbn_forward_desc(const quan_tensor *x, const quan_tensor *gamma,
+                                    const quan_tensor *beta, float eps, quan_tensor *out,
+                                    quan_tensor *mean, quan_tensor *var, void *stream);
+QUAN_API int quan_iqbn_relu_forward_desc(const quan_tensor *x, const quan_tensor *gamma,
+                                         const quan_tensor *beta, float eps, quan_tensor *out,
+                                         quan_tensor *mean, quan_tensor *var, void *stream);
+
 /* Where quan_qconv2d_iqbn_forward gathers the batch statistics. */
 enum quan_stats_mode {
     QUAN_STATS_AUTO = 0,     /* the library's choice: the epilogue where the tiles allow */
@@ -323,7 +381,6 @@ QUAN_API int quan_qconv2d_poincare_forward(const void *rgb, const void *packed, 
                                            int32_t k_h, int32_t k_w, int32_t dtype, void *stream);
 
 /*
- * Input gradient of the Hamilton convolution (the backward pass of/*
  * Input gradient of the Hamilton convolution (the backward pass of
  * quan_qconv2d_forward with respect to x): for dL/dY = dy,
  *
@@ -424,7 +481,6 @@ QUAN_API int quan_qconv2d_separable_backward_weight(const void *x, const void *d
                                                     int32_t k_w, int32_t dtype, void *stream);
 
 /*
- * Gradient of training-mode IQBN (eqs. 11 and 12) with respect to its/*
  * Gradient of training-mode IQBN (eqs. 11 and 12) with respect to its
  * input, gamma and beta, given the batch statistics the forward call
  * returned.  Per component and channel, over the P = n*h*w values, with

@@ -682,6 +682,9 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
     // (M, q) for the separable input gradient, q = 0..3
     auto group = [&](auto mc, const u32x4 (&x)[4][MB], const u32x4 (&xneg)[4][MB], const u32x4 (&w)[NB]) {
         constexpr int M = decltype(mc)::value;
+        // (compiled into the all-components kernels only; the others hold
+        // one component's accumulators and never call it)
+        if constexpr (ALLP)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const int p = FORM == kFormHamilton ? q ^ M : M;

@@ -800,6 +800,170 @@ QUAN_API int quan_iqbn_relu_forward(const void *x, const float *gamma, const flo
     return iqbn_common(x, gamma, beta, eps, out, mean, var, n, c, h, w, dtype, stream, true);
 }
 
+namespace {
+
+// ---- descriptor entry points: checks of quan_tensor, all on the host ------
+
+int desc_present(const quan_tensor *t, const char *fn, const char *what)
+{
+    if (t == nullptr || t->data == nullptr)
+        return fail(QUAN_ERR_NULL, "%s: %s descriptor or its data pointer is NULL", fn, what);
+    return QUAN_OK;
+}
+
+// ndim, extents (want[i] < 0: any extent >= 1) and dtype of a descriptor.
+int desc_shape(const quan_tensor *t, const char *fn, const char *what, int ndim, const int64_t *want,
+               int32_t dtype)
+{
+    if (t->ndim != ndim)
+        return fail(QUAN_ERR_SHAPE, "%s: %s has ndim %d, expected %d", fn, what, t->ndim, ndim);
+    for (int i = 0; i < ndim; ++i) {
+        if (t->shape[i] < 1)
+            return fail(QUAN_ERR_SHAPE, "%s: %s extent %lld on axis %d must be >= 1", fn, what,
+                        (long long)t->shape[i], i);
+        if (t->shape[i] > INT32_MAX)
+            return fail(QUAN_ERR_UNSUPPORTED, "%s: %s extent %lld on axis %d exceeds 2^31-1", fn, what,
+                        (long long)t->shape[i], i);
+        if (want[i] >= 0 && t->shape[i] != want[i])
+            return fail(QUAN_ERR_SHAPE, "%s: %s extent %lld on axis %d, expected %lld", fn, what,
+                        (long long)t->shape[i], i, (long long)want[i]);
+    }
+    if (t->dtype != dtype)
+        return fail(QUAN_ERR_DTYPE, "%s: %s has dtype %d, expected %d", fn, what, t->dtype, dtype);
+    return QUAN_OK;
+}
+
+// Strides against the required ones; an axis of extent 1 is never stepped.
+int desc_strides(const quan_tensor *t, const char *fn, const char *what, const int64_t *want,
+                 const char *layout)
+{
+    for (int i = 0; i < t->ndim; ++i)
+        if (t->shape[i] != 1 && t->strides[i] != want[i])
+            return fail(QUAN_ERR_LAYOUT, "%s: %s is not %s (axis %d: stride %lld, expected %lld)", fn, what,
+                        layout, i, (long long)t->strides[i], (long long)want[i]);
+    return QUAN_OK;
+}
+
+// A quaternion map [N, 4, C, H, W] stored channels-last by component.
+int desc_activation(const quan_tensor *t, const char *fn, const char *what, const int64_t *want, int32_t dtype)
+{
+    if (int rc = desc_present(t, fn, what))
+        return rc;
+    if (int rc = desc_shape(t, fn, what, 5, want, dtype))
+        return rc;
+    const int64_t c = t->shape[2], h = t->shape[3], w = t->shape[4];
+    const int64_t strides[5] = {h * w * 4 * c, c, 1, w * 4 * c, 4 * c};
+    return desc_strides(t, fn, what, strides, "channels-last by component ([N][H][W][4][C] in memory)");
+}
+
+// A dense row-major tensor of the given extents.
+int desc_dense(const quan_tensor *t, const char *fn, const char *what, int ndim, const int64_t *want,
+               int32_t dtype)
+{
+    if (int rc = desc_present(t, fn, what))
+        return rc;
+    if (int rc = desc_shape(t, fn, what, ndim, want, dtype))
+        return rc;
+    int64_t strides[5];
+    int64_t step = 1;
+    for (int i = ndim - 1; i >= 0; --i) {
+        strides[i] = step;
+        step *= t->shape[i];
+    }
+    return desc_strides(t, fn, what, strides, "dense row-major");
+}
+
+int iqbn_desc(const char *fn, const quan_tensor *x, const quan_tensor *gamma, const quan_tensor *beta,
+              float eps, quan_tensor *out, quan_tensor *mean, quan_tensor *var, void *stream, bool relu)
+{
+    g_last_error.clear();
+    if (int rc = desc_present(x, fn, "x"))
+        return rc;
+    if (int rc = check_dtype(x->dtype))
+        return rc;
+    const int64_t any5[5] = {-1, 4, -1, -1, -1};
+    if (int rc = desc_activation(x, fn, "x", any5, x->dtype))
+        return rc;
+    const int64_t stat[2] = {4, x->shape[2]};
+    const quan_tensor *params[4] = {gamma, beta, mean, var};
+    const char *names[4] = {"gamma", "beta", "mean", "var"};
+    for (int i = 0; i < 4; ++i)
+        if (int rc = desc_dense(params[i], fn, names[i], 2, stat, QUAN_F32))
+            return rc;
+    if (int rc = desc_activation(out, fn, "out", x->shape, x->dtype))
+        return rc;
+    return iqbn_common(x->data, static_cast<const float *>(gamma->data), static_cast<const float *>(beta->data),
+                       eps, out->data, static_cast<float *>(mean->data), static_cast<float *>(var->data),
+                       int32_t(x->shape[0]), int32_t(x->shape[2]), int32_t(x->shape[3]), int32_t(x->shape[4]),
+                       x->dtype, stream, relu);
+}
+
+}  // namespace
+
+QUAN_API int quan_qconv2d_forward_desc(const quan_tensor *x, const quan_tensor *w_r, const quan_tensor *w_i,
+                                       const quan_tensor *w_j, const quan_tensor *w_k, const quan_tensor *bias,
+                                       const int32_t stride[2], const int32_t pad[2], const int32_t dilation[2],
+                                       quan_tensor *out, void *stream)
+{
+    const char *fn = "qconv2d_forward_desc";
+    g_last_error.clear();
+    if (int rc = desc_present(x, fn, "x"))
+        return rc;
+    if (int rc = check_dtype(x->dtype))
+        return rc;
+    const int64_t any5[5] = {-1, 4, -1, -1, -1};
+    if (int rc = desc_activation(x, fn, "x", any5, x->dtype))
+        return rc;
+    if (int rc = desc_present(w_r, fn, "w_r"))
+        return rc;
+    const int64_t wshape[4] = {w_r->ndim == 4 ? w_r->shape[0] : -1, x->shape[2], w_r->ndim == 4 ? w_r->shape[2] : -1,
+                               w_r->ndim == 4 ? w_r->shape[3] : -1};
+    const quan_tensor *ws[4] = {w_r, w_i, w_j, w_k};
+    const char *wn[4] = {"w_r", "w_i", "w_j", "w_k"};
+    for (int i = 0; i < 4; ++i)
+        if (int rc = desc_dense(ws[i], fn, wn[i], 4, wshape, x->dtype))
+            return rc;
+    const int64_t c_out = w_r->shape[0], k_h = w_r->shape[2], k_w = w_r->shape[3];
+    if (bias != nullptr) {
+        const int64_t bshape[2] = {4, c_out};
+        if (int rc = desc_dense(bias, fn, "bias", 2, bshape, x->dtype))
+            return rc;
+    }
+    if (stride == nullptr || pad == nullptr || dilation == nullptr)
+        return fail(QUAN_ERR_NULL, "%s: stride, pad and dilation must point to (h, w) pairs", fn);
+    int64_t o_hw[2];
+    for (int i = 0; i < 2; ++i) {
+        const int64_t k = i == 0 ? k_h : k_w, in = x->shape[3 + i];
+        if (stride[i] < 1 || dilation[i] < 1 || pad[i] < 0)
+            return fail(QUAN_ERR_SHAPE, "%s: stride/dilation must be >= 1 and pad >= 0", fn);
+        const int64_t span = in + 2 * int64_t(pad[i]) - int64_t(dilation[i]) * (k - 1) - 1;
+        if (span < 0)
+            return fail(QUAN_ERR_SHAPE, "%s: empty output (kernel span exceeds padded input)", fn);
+        o_hw[i] = span / stride[i] + 1;
+    }
+    const int64_t oshape[5] = {x->shape[0], 4, c_out, o_hw[0], o_hw[1]};
+    if (int rc = desc_activation(out, fn, "out", oshape, x->dtype))
+        return rc;
+    return conv_unpacked("qconv2d", false, x->data, w_r->data, w_i->data, w_j->data, w_k->data,
+                         bias ? bias->data : nullptr, stride[0], stride[1], pad[0], pad[1], dilation[0],
+                         dilation[1], out->data, int32_t(x->shape[0]), int32_t(x->shape[2]),
+                         int32_t(x->shape[3]), int32_t(x->shape[4]), int32_t(c_out), int32_t(k_h), int32_t(k_w),
+                         x->dtype, stream);
+}
+
+QUAN_API int quan_iqbn_forward_desc(const quan_tensor *x, const quan_tensor *gamma, const quan_tensor *beta,
+                                    float eps, quan_tensor *out, quan_tensor *mean, quan_tensor *var, void *stream)
+{
+    return iqbn_desc("iqbn_forward_desc", x, gamma, beta, eps, out, mean, var, stream, false);
+}
+
+QUAN_API int quan_iqbn_relu_forward_desc(const quan_tensor *x, const quan_tensor *gamma, const quan_tensor *beta,
+                                         float eps, quan_tensor *out, quan_tensor *mean, quan_tensor *var,
+                                         void *stream)
+{
+    return iqbn_desc("iqbn_relu_forward_desc", x, gamma, beta, eps, out, mean, var, stream, true);
+}
+
 QUAN_API const char *quan_last_error(void)
 {
     return g_last_error.c_str();

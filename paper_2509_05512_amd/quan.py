@@ -22,12 +22,40 @@ LIB_PATH = os.path.join(_HERE, "libquan.so")
 QUAN_F32, QUAN_BF16 = 0, 1
 _STATUS = {0: "QUAN_OK", -1: "QUAN_ERR_NULL", -2: "QUAN_ERR_SHAPE", -3: "QUAN_ERR_DTYPE",
            -4: "QUAN_ERR_ALIGN", -5: "QUAN_ERR_ALIAS", -6: "QUAN_ERR_UNSUPPORTED",
-           -7: "QUAN_ERR_HIP", -8: "QUAN_ERR_NOMEM"}
+           -7: "QUAN_ERR_HIP", -8: "QUAN_ERR_NOMEM", -9: "QUAN_ERR_LAYOUT"}
+QUAN_ERR_LAYOUT = -9
+
+
+class QuanTensor(ctypes.Structure):
+    """struct quan_tensor: device pointer, dtype, and up to 5 (extent, stride
+    in elements) axes."""
+    _fields_ = [("data", ctypes.c_void_p), ("dtype", ctypes.c_int32), ("ndim", ctypes.c_int32),
+                ("shape", ctypes.c_int64 * 5), ("strides", ctypes.c_int64 * 5)]
+
+
+def describe(t):
+    """A quan_tensor for a torch tensor (its real shape and strides), or None."""
+    if t is None:
+        return None
+    if t.dim() > 5:
+        raise ValueError("quan_tensor holds at most 5 axes")
+    d = QuanTensor()
+    d.data = t.data_ptr()
+    d.dtype = _dtype_code(t)
+    d.ndim = t.dim()
+    for i, (n, st) in enumerate(zip(t.shape, t.stride())):
+        d.shape[i] = n
+        d.strides[i] = st
+    return d
 
 # Every symbol include/quan.h declares, with its ctypes signature.
 _vp, _i32, _f32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_float
 SIGNATURES = {
     "quan_qconv2d_forward": (ctypes.c_int, [_vp] * 6 + [_i32] * 6 + [_vp] + [_i32] * 8 + [_vp]),
+    "quan_qconv2d_forward_desc": (ctypes.c_int, [ctypes.c_void_p] * 6 + [ctypes.POINTER(ctypes.c_int32)] * 3
+                                  + [ctypes.c_void_p, _vp]),
+    "quan_iqbn_forward_desc": (ctypes.c_int, [_vp] * 3 + [_f32] + [_vp] * 4),
+    "quan_iqbn_relu_forward_desc": (ctypes.c_int, [_vp] * 3 + [_f32] + [_vp] * 4),
     "quan_qconv2d_packed_bytes": (ctypes.c_int64, [_i32] * 5),
     "quan_qconv2d_pack_weights": (ctypes.c_int, [_vp] * 4 + [_i32] * 5 + [_vp, ctypes.c_int64, _vp]),
     "quan_qconv2d_forward_packed": (ctypes.c_int, [_vp] * 3 + [_i32] * 6 + [_vp] + [_i32] * 8 + [_vp]),
@@ -130,12 +158,39 @@ def conv_out_size(n, k, stride, pad, dil):
     return (n + 2 * pad - dil * (k - 1) - 1) // stride + 1
 
 
+def _ref(d):
+    return ctypes.byref(d) if d is not None else None
+
+
 def quan_qconv2d_forward(x, w_r, w_i, w_j, w_k, bias=None, stride=1, pad=0, dilation=1, out=None):
     """Quaternion convolution Y = W (x) X + b (Section III-B, eqs. 5/6).
 
     x: [N, 4, Cin, H, W] in device layout; w_*: [Cout, Cin, kh, kw] contiguous;
-    bias: [4, Cout] or None.  Returns out [N, 4, Cout, Ho, Wo] (device layout)."""
-    return _conv("quan_qconv2d_forward", x, w_r, w_i, w_j, w_k, bias, stride, pad, dilation, out)
+    bias: [4, Cout] or None.  Returns out [N, 4, Cout, Ho, Wo] (device layout).
+    The tensors go to the library as descriptors with their real strides: the
+    library checks shapes, dtypes and layouts (QuanError QUAN_ERR_LAYOUT for
+    a map that is not channels-last by component)."""
+    lib = load_library()
+    if x.dim() != 5 or w_r.dim() != 4:
+        raise ValueError("x must be [N, 4, Cin, H, W] and w_r [Cout, Cin, kh, kw]")
+    for t in (w_r, w_i, w_j, w_k, bias, out):
+        if t is not None and t.device != x.device:
+            raise ValueError("all tensors must be on x's device")
+    n, _, _, h, w = x.shape
+    c_out, _, k_h, k_w = w_r.shape
+    sh, sw = _pair(stride)
+    ph, pw = _pair(pad)
+    dh, dw = _pair(dilation)
+    if out is None:
+        ho, wo = conv_out_size(h, k_h, sh, ph, dh), conv_out_size(w, k_w, sw, pw, dw)
+        out = empty_qmap(n, c_out, max(ho, 1), max(wo, 1), x.dtype, x.device)
+    pair = ctypes.c_int32 * 2
+    descs = [describe(t) for t in (x, w_r, w_i, w_j, w_k, bias, out)]
+    with torch.cuda.device(x.device):
+        rc = lib.quan_qconv2d_forward_desc(*[_ref(d) for d in descs[:6]], pair(sh, sw), pair(ph, pw),
+                                           pair(dh, dw), _ref(descs[6]), _stream(x.device))
+    _check(rc)
+    return out
 
 
 def quan_qconv2d_separable_forward(x, w_r, w_i, w_j, w_k, bias=None, stride=1, pad=0, dilation=1,
@@ -513,14 +568,37 @@ def _iqbn(fn_name, x, gamma, beta, eps, out, mean, var):
     return out, mean, var
 
 
+def _iqbn_desc(fn_name, x, gamma, beta, eps, out, mean, var):
+    lib = load_library()
+    if x.dim() != 5:
+        raise ValueError("x must be [N, 4, C, H, W]")
+    n, _, c, h, w = x.shape
+    if out is None:
+        out = empty_qmap(n, c, h, w, x.dtype, x.device)
+    if mean is None:
+        mean = torch.empty(4, c, dtype=torch.float32, device=x.device)
+    if var is None:
+        var = torch.empty(4, c, dtype=torch.float32, device=x.device)
+    for t in (gamma, beta, out, mean, var):
+        if t.device != x.device:
+            raise ValueError("all tensors must be on x's device")
+    descs = [describe(t) for t in (x, gamma, beta, out, mean, var)]
+    with torch.cuda.device(x.device):
+        rc = getattr(lib, fn_name)(_ref(descs[0]), _ref(descs[1]), _ref(descs[2]), float(eps),
+                                   _ref(descs[3]), _ref(descs[4]), _ref(descs[5]), _stream(x.device))
+    _check(rc)
+    return out, mean, var
+
+
 def quan_iqbn_forward(x, gamma, beta, eps=1e-5, out=None, mean=None, var=None):
-    """IQBN (Section III-C, eqs. 11/12).  Returns (out, mean, var)."""
-    return _iqbn("quan_iqbn_forward", x, gamma, beta, eps, out, mean, var)
+    """IQBN (Section III-C, eqs. 11/12).  Returns (out, mean, var).  Tensors
+    go to the library as descriptors; it checks their shapes and layouts."""
+    return _iqbn_desc("quan_iqbn_forward_desc", x, gamma, beta, eps, out, mean, var)
 
 
 def quan_iqbn_relu_forward(x, gamma, beta, eps=1e-5, out=None, mean=None, var=None):
     """IQBN followed by a component-wise ReLU.  Returns (out, mean, var)."""
-    return _iqbn("quan_iqbn_relu_forward", x, gamma, beta, eps, out, mean, var)
+    return _iqbn_desc("quan_iqbn_relu_forward_desc", x, gamma, beta, eps, out, mean, var)
 
 
 def quan_iqbn_forward_noalloc(x, gamma, beta, eps=1e-5, out=None, mean=None, var=None):

@@ -388,3 +388,135 @@ def test_binding_layout_helpers():
     assert y.stride() == quan.device_strides(2, 3, 5, 6)
     e = quan.empty_qmap(2, 3, 5, 6, torch.float32, "cpu")
     assert quan.is_device_layout(e) and tuple(e.shape) == (2, 4, 3, 5, 6)
+
+
+# ---- descriptor entry points: layout, shape and dtype from (shape, strides) --
+
+E_LAYOUT = -9
+
+
+def qt(addr, shape, strides=None, dtype=1):
+    """A quan_tensor with dense row-major strides unless given."""
+    d = quan.QuanTensor()
+    d.data = addr or 0
+    d.dtype = dtype
+    d.ndim = len(shape)
+    if strides is None:
+        strides, step = [0] * len(shape), 1
+        for i in range(len(shape) - 1, -1, -1):
+            strides[i] = step
+            step *= shape[i]
+    for i, (n, st) in enumerate(zip(shape, strides)):
+        d.shape[i] = n
+        d.strides[i] = st
+    return d
+
+
+def qmap(addr, n, c, h, w, dtype=1):
+    """A [N, 4, C, H, W] map stored channels-last by component."""
+    return qt(addr, (n, 4, c, h, w), quan.device_strides(n, c, h, w), dtype)
+
+
+def conv_desc(lib, **kw):
+    a = dict(x=qmap(X, 2, 4, 16, 16), wr=qt(WR, (4, 4, 3, 3)), wi=qt(WI, (4, 4, 3, 3)),
+             wj=qt(WJ, (4, 4, 3, 3)), wk=qt(WK, (4, 4, 3, 3)), bias=qt(B, (4, 4)),
+             stride=(1, 1), pad=(1, 1), dil=(1, 1), out=qmap(OUT, 2, 4, 16, 16))
+    a.update(kw)
+    ref = lambda d: ctypes.byref(d) if d is not None else None
+    pair = lambda p: (ctypes.c_int32 * 2)(*p) if p is not None else None
+    rc = lib.quan_qconv2d_forward_desc(ref(a["x"]), ref(a["wr"]), ref(a["wi"]), ref(a["wj"]), ref(a["wk"]),
+                                       ref(a["bias"]), pair(a["stride"]), pair(a["pad"]), pair(a["dil"]),
+                                       ref(a["out"]), None)
+    return rc, lib.quan_last_error().decode()
+
+
+CONV_DESC_ERRORS = [
+    ("x NCHW-ordered memory", dict(x=qt(X, (2, 4, 4, 16, 16))), E_LAYOUT),
+    ("x NHWC but component-minor", dict(x=qt(X, (2, 4, 4, 16, 16), (4096, 1, 4, 256, 16))), E_LAYOUT),
+    ("out NCHW-ordered memory", dict(out=qt(OUT, (2, 4, 4, 16, 16))), E_LAYOUT),
+    ("w_k OHWI strides", dict(wk=qt(WK, (4, 4, 3, 3), (36, 1, 12, 4))), E_LAYOUT),
+    ("bias transposed", dict(bias=qt(B, (4, 4), (1, 4))), E_LAYOUT),
+    ("x ndim 4", dict(x=qt(X, (2, 16, 16, 16))), E_SHAPE),
+    ("x 3 components", dict(x=qt(X, (2, 3, 4, 16, 16), (3072, 4, 1, 192, 12))), E_SHAPE),
+    ("w_i c_in mismatch", dict(wi=qt(WI, (4, 5, 3, 3))), E_SHAPE),
+    ("w_j k mismatch", dict(wj=qt(WJ, (4, 4, 5, 5))), E_SHAPE),
+    ("bias extent", dict(bias=qt(B, (4, 5))), E_SHAPE),
+    ("out wrong Ho", dict(out=qmap(OUT, 2, 4, 15, 16)), E_SHAPE),
+    ("out wrong c_out", dict(out=qmap(OUT, 2, 8, 16, 16)), E_SHAPE),
+    ("empty output", dict(pad=(0, 0), x=qmap(X, 2, 4, 2, 16), out=qmap(OUT, 2, 4, 1, 14)), E_SHAPE),
+    ("stride 0", dict(stride=(0, 1)), E_SHAPE),
+    ("x bad dtype", dict(x=qmap(X, 2, 4, 16, 16, dtype=5)), E_DTYPE),
+    ("w_j f32 with bf16 x", dict(wj=qt(WJ, (4, 4, 3, 3), dtype=0)), E_DTYPE),
+    ("out f32 with bf16 x", dict(out=qmap(OUT, 2, 4, 16, 16, dtype=0)), E_DTYPE),
+    ("NULL x descriptor", dict(x=None), E_NULL),
+    ("NULL x data", dict(x=qmap(0, 2, 4, 16, 16)), E_NULL),
+    ("NULL w_r descriptor", dict(wr=None), E_NULL),
+    ("NULL out", dict(out=None), E_NULL),
+    ("NULL stride", dict(stride=None), E_NULL),
+    ("extent 2^31", dict(x=qmap(X, 2 ** 31, 4, 16, 16)), E_UNSUP),
+    # descriptors accepted, then the plain entry point's own checks
+    ("x misaligned", dict(x=qmap(X + 2, 2, 4, 16, 16)), E_ALIGN),
+    ("out overlaps x", dict(out=qmap(X + 256, 2, 4, 16, 16)), E_ALIAS),
+    # an axis of extent 1 is never stepped: its stride is not checked
+    ("unit axis, any stride", dict(x=qt(X + 2, (1, 4, 4, 16, 16), (7, 4, 1, 256, 16)),
+                                   out=qmap(OUT, 1, 4, 16, 16)), E_ALIGN),
+]
+
+
+@pytest.mark.parametrize("name,kw,code", CONV_DESC_ERRORS, ids=[c[0] for c in CONV_DESC_ERRORS])
+def test_qconv2d_desc_rejects(lib, name, kw, code):
+    rc, msg = conv_desc(lib, **kw)
+    assert rc == code, (name, rc, msg)
+    assert msg
+
+
+def iqbn_desc(lib, relu=False, **kw):
+    a = dict(x=qmap(X, 2, 4, 8, 8), g=qt(G, (4, 4), dtype=0), b=qt(BE, (4, 4), dtype=0), eps=1e-5,
+             out=qmap(OUT, 2, 4, 8, 8), mean=qt(MEAN, (4, 4), dtype=0), var=qt(VAR, (4, 4), dtype=0))
+    a.update(kw)
+    ref = lambda d: ctypes.byref(d) if d is not None else None
+    fn = lib.quan_iqbn_relu_forward_desc if relu else lib.quan_iqbn_forward_desc
+    rc = fn(ref(a["x"]), ref(a["g"]), ref(a["b"]), a["eps"], ref(a["out"]), ref(a["mean"]), ref(a["var"]),
+            None)
+    return rc, lib.quan_last_error().decode()
+
+
+IQBN_DESC_ERRORS = [
+    ("x NCHW-ordered memory", dict(x=qt(X, (2, 4, 4, 8, 8))), E_LAYOUT),
+    ("out NCHW-ordered memory", dict(out=qt(OUT, (2, 4, 4, 8, 8))), E_LAYOUT),
+    ("gamma transposed", dict(g=qt(G, (4, 4), (1, 4), dtype=0)), E_LAYOUT),
+    ("var strided", dict(var=qt(VAR, (4, 4), (8, 1), dtype=0)), E_LAYOUT),
+    ("x ndim 3", dict(x=qt(X, (2, 4, 64))), E_SHAPE),
+    ("out shape differs", dict(out=qmap(OUT, 2, 4, 8, 9)), E_SHAPE),
+    ("mean extent", dict(mean=qt(MEAN, (4, 5), dtype=0)), E_SHAPE),
+    ("beta ndim", dict(b=qt(BE, (16,), dtype=0)), E_SHAPE),
+    ("gamma bf16", dict(g=qt(G, (4, 4), dtype=1)), E_DTYPE),
+    ("out dtype differs", dict(out=qmap(OUT, 2, 4, 8, 8, dtype=0)), E_DTYPE),
+    ("x bad dtype", dict(x=qmap(X, 2, 4, 8, 8, dtype=9)), E_DTYPE),
+    ("NULL var", dict(var=None), E_NULL),
+    ("NULL gamma data", dict(g=qt(0, (4, 4), dtype=0)), E_NULL),
+    ("eps 0", dict(eps=0.0), E_SHAPE),
+    ("x misaligned", dict(x=qmap(X + 8, 2, 4, 8, 8)), E_ALIGN),
+    ("mean overlaps var", dict(mean=qt(VAR + 4, (4, 4), dtype=0)), E_ALIAS),
+]
+
+
+@pytest.mark.parametrize("relu", [False, True])
+@pytest.mark.parametrize("name,kw,code", IQBN_DESC_ERRORS, ids=[c[0] for c in IQBN_DESC_ERRORS])
+def test_iqbn_desc_rejects(lib, name, kw, code, relu):
+    rc, msg = iqbn_desc(lib, relu=relu, **kw)
+    assert rc == code, (name, rc, msg)
+    assert msg
+
+
+def test_descriptor_of_torch_tensors():
+    import torch
+    x = quan.empty_qmap(2, 3, 5, 6, torch.bfloat16, "cpu")
+    d = quan.describe(x)
+    assert d.ndim == 5 and d.dtype == quan.QUAN_BF16
+    assert tuple(d.shape[:5]) == (2, 4, 3, 5, 6)
+    assert tuple(d.strides[:5]) == quan.device_strides(2, 3, 5, 6)
+    w = torch.zeros(4, 3, 3, 3)
+    dw = quan.describe(w)
+    assert dw.ndim == 4 and dw.dtype == quan.QUAN_F32 and tuple(dw.strides[:4]) == (27, 9, 3, 1)
+    assert quan.describe(None) is None

@@ -120,13 +120,23 @@ def test_deterministic(dtype):
     assert torch.equal(o1, o2)
 
 
-def test_binding_rejects_wrong_layout():
-    say("qconv2d layout rejection")
+def test_library_rejects_wrong_layout():
+    # the descriptors carry torch's real strides; the library refuses them
+    say("qconv2d / iqbn layout rejection")
     dev = torch.device("cuda:0")
     x = torch.randn(1, 4, 4, 5, 5, device=dev)          # plain contiguous: wrong layout
     w = [torch.randn(4, 4, 3, 3, device=dev) for _ in range(4)]
-    with pytest.raises(ValueError):
+    with pytest.raises(quan.QuanError) as ei:
         quan.quan_qconv2d_forward(x, *w, stride=1, pad=1)
+    assert ei.value.code == quan.QUAN_ERR_LAYOUT
+    g = torch.ones(4, 4, device=dev)
+    with pytest.raises(quan.QuanError) as ei:
+        quan.quan_iqbn_forward(x, g, g)
+    assert ei.value.code == quan.QUAN_ERR_LAYOUT
+    wt = [t.permute(0, 2, 3, 1).contiguous().permute(0, 3, 1, 2) for t in w]   # OHWI memory
+    with pytest.raises(quan.QuanError) as ei:
+        quan.quan_qconv2d_forward(quan.to_device_layout(x), *wt, stride=1, pad=1)
+    assert ei.value.code == quan.QUAN_ERR_LAYOUT
 
 
 def test_abi_error_from_device_tensors():
