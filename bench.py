@@ -4,14 +4,15 @@
 One step = one pass of the whole hot path over one batch of a workload: for
 every layer, pack the four real kernels, then the quaternion (Hamilton)
 convolution with IQBN (+ReLU where the layer has it) behind it
-(quan_qconv2d_iqbn_forward with the library's default statistics mode: per
-output tile in the convolution's epilogue), through libquan's C ABI on
-torch's current stream.  Inputs are seeded synthetic tensors already resident
-in HBM when the timed region starts.  The same steps are then timed with a
-separate statistics pass and in inference form (stored statistics folded into
-the convolution's epilogue), and run with every kernel on its own (pack,
-convolution, the three IQBN passes) for per-kernel times; the Poincare input
-mapping is timed on an ImageNet-sized batch.
+(quan_qconv2d_iqbn_forward with the library's default statistics mode: the
+one-launch IQBN after the plain convolution where the tensor takes it, else
+per-tile statistics in the convolution's epilogue), through libquan's C ABI
+on torch's current stream.  Inputs are seeded synthetic tensors already
+resident in HBM when the timed region starts.  The same steps are then timed
+with each statistics mode forced (epilogue, separate pass) and in inference
+form (stored statistics folded into the convolution's epilogue), and run
+with every kernel on its own (pack, convolution, IQBN) for per-kernel times;
+the Poincare input mapping is timed on an ImageNet-sized batch.
 
 Prints ONE JSON line:
   value        useful convolution TFLOP/s over whole steps (pack + conv + IQBN);
@@ -563,16 +564,19 @@ def main():
     total_ms = start.elapsed_time(end)
     ms_per_step = total_ms / args.steps
 
-    # the same steps with a separate statistics pass
-    for _ in range(2):
-        run_step_fused(layers, quan, eps=wl.eps, stats="pass")
-    torch.cuda.synchronize()
-    start.record()
-    for s in range(args.steps):
-        run_step_fused(layers, quan, eps=wl.eps, stats="pass")
-    end.record()
-    torch.cuda.synchronize()
-    pass_ms = start.elapsed_time(end) / args.steps
+    # the same steps with each statistics mode forced
+    mode_ms = {}
+    for mode in ("epilogue", "pass"):
+        for _ in range(2):
+            run_step_fused(layers, quan, eps=wl.eps, stats=mode)
+        torch.cuda.synchronize()
+        start.record()
+        for s in range(args.steps):
+            run_step_fused(layers, quan, eps=wl.eps, stats=mode)
+        end.record()
+        torch.cuda.synchronize()
+        mode_ms[mode] = start.elapsed_time(end) / args.steps
+    pass_ms = mode_ms["pass"]
 
     # the step in inference form (stored statistics folded into the conv)
     for _ in range(2):
@@ -633,8 +637,10 @@ def main():
                         "pad": L.pad, "iqbn_relu": L.relu} for L in wl.layers],
             "useful_gflop_per_step": round(step_flops / 1e9, 3),
         },
-        "step": "per layer: pack the four kernels, then quan_qconv2d_iqbn_forward "
-                "(convolution with IQBN statistics in its epilogue, normalization)",
+        "step": "per layer: pack the four kernels, then quan_qconv2d_iqbn_forward with "
+                "QUAN_STATS_AUTO (the plain convolution and the one-launch IQBN where the "
+                "tensor takes it, else IQBN statistics in the convolution's epilogue)",
+        "stats_epilogue_us_per_step": round(mode_ms["epilogue"] * 1e3, 3),
         "stats_pass_us_per_step": round(pass_ms * 1e3, 3),
         "inference_us_per_step": round(inference_ms * 1e3, 3),
         "inference_tflops": round(step_flops / (inference_ms * 1e-3) / 1e12, 2),

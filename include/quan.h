@@ -280,7 +280,7 @@ QUAN_API int quan_iqbn_relu_forward_desc(const quan_tensor *x, const quan_tensor
 
 /* Where quan_qconv2d_iqbn_forward gathers the batch statistics. */
 enum quan_stats_mode {
-    QUAN_STATS_AUTO = 0,     /* the library's choice: the epilogue where the tiles allow */
+    QUAN_STATS_AUTO = 0,     /* the library's choice (see quan_qconv2d_iqbn_forward) */
     QUAN_STATS_EPILOGUE = 1, /* per-tile statistics in the convolution's epilogue */
     QUAN_STATS_PASS = 2      /* a separate statistics pass over out */
 };
@@ -300,11 +300,15 @@ enum quan_stats_mode {
  *           costs one read and one write of out); tiles that cannot gather
  *           them (fewer than 32 output channels, or c_out not a multiple of
  *           8 for bf16 / 4 for fp32) use the separate pass instead.
- *           QUAN_STATS_PASS reads out once more for the statistics.  The
- *           epilogue's vector arithmetic pauses the matrix cores for about
- *           as long as the extra read takes; measured alternately on MI355X
- *           the epilogue is 1-3% faster per layer, so QUAN_STATS_AUTO picks
- *           it.  Both are deterministic.
+ *           QUAN_STATS_PASS runs the plain convolution and then
+ *           quan_iqbn_forward's normalisation on out: on tensors of 16 MiB
+ *           or more that one work-group per compute unit can hold (about
+ *           100 MB on MI355X), one launch that reads out once and writes it
+ *           once; otherwise three launches that read it twice.
+ *           QUAN_STATS_AUTO picks the pass where that one launch applies
+ *           (measured on MI355X: 261 against 270 us for the 64 x 56 x 56,
+ *           64-channel layer) and the epilogue elsewhere.  All modes are
+ *           deterministic.
  */
 QUAN_API int quan_qconv2d_iqbn_forward(const void *x, const void *packed, const void *bias,
                                        int32_t stride_h, int32_t stride_w,

@@ -25,6 +25,9 @@
 // normalization then costs one read and one write of the tensor.
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+#include <type_traits>
+
 #include "quan_launch.h"
 
 namespace quan {
@@ -412,6 +415,377 @@ __global__ __launch_bounds__(kThreads) void iqbn_affine(const T *x, T *out, Layo
     }
 }
 
+// ------------------------ one-launch resident IQBN ------------------------
+// Where the tensor fits in the registers and LDS of one work-group per
+// compute unit (up to about 100 MB on 256 CUs), IQBN runs as ONE launch that
+// reads x from memory once:
+//
+//   phase 1  work-group w copies its contiguous rows [w * R, (w + 1) * R) into
+//            VGPRs (the first kResRegChunks 16-byte chunks of each thread) and
+//            LDS (the next kResLdsChunks, by direct global->LDS loads), and
+//            reduces the shifted sums s1 = sum(x - K), s2 = sum((x - K)^2)
+//            of every column over its rows (K = the column's value in row
+//            0, as in iqbn_stats) in a fixed order: one (s1, s2) pair per
+//            column per work-group.
+//   barrier  every work-group has published its partials.
+//   phase 2  work-group w merges its ceil(L / G) columns over the G partials
+//            in fp64, in work-group order, and publishes mean and scale.
+//   barrier  every column's mean and scale are published.
+//   phase 3  every work-group normalises the rows it holds and writes them.
+//
+// The grid is one work-group per compute unit and each work-group needs a
+// whole compute unit's LDS, so all G are resident together.  Partials,
+// coefficients and barrier flags are read by other XCDs (each XCD has its own
+// L2): they are written and read with system-scope atomic stores and loads,
+// which go to memory, and every thread waits for its own stores to complete
+// before its work-group raises its flag.  The barrier has no read-modify-
+// write: work-group w raises only its own flag, flags[w], and waits until
+// every flag has reached the same value; each launch raises every flag by
+// exactly two, so a work-group takes its targets from its own flag at the
+// start.  The wait is bounded (kSpinLimit polls, about a second): a work-group
+// that gives up writes NaN where its results would be, so a launch that could
+// not run all its work-groups at once shows as NaNs, never as a hang.
+constexpr int kResThreads = 512;
+constexpr int kResRegChunks = 36;  // 16-byte chunks per thread held in VGPRs
+constexpr int kResLdsChunks = 15;  // ... and in LDS
+constexpr int kResChunks = kResRegChunks + kResLdsChunks;
+constexpr int kResMaxGroups = 512;
+constexpr int kResMaxCols = 16;     // columns merged per work-group in phase 2
+constexpr int kFlagStride = 32;     // unsigned ints between flags: one 128-byte line each
+constexpr long kSpinLimit = 1L << 20;
+// Below 16 MiB the three launches are as fast (measured on MI355X: 12.8 MB
+// tensors take 21-24 us either way, 16.8 MB 22.1 against 23.7, 52 MB 34.4
+// against 37.7, 103 MB 54.6 against 59.4, cold), so only larger tensors rely
+// on all work-groups being resident together.
+constexpr int64_t kResMinBytes = int64_t(16) << 20;
+
+typedef unsigned int res_u32x4 __attribute__((ext_vector_type(4)));
+
+struct ResArgs {
+    const void *x;
+    void *out;
+    const float *gamma, *beta;
+    float eps;
+    float *mean, *var;
+    float *part;      // [2][G][L] partial (s1, s2) per work-group
+    float *coef;      // [2][L] mean, scale
+    unsigned *flags;  // [kResMaxGroups][kFlagStride]
+    int64_t pixels;
+    int row_len;      // L = 4*C
+    int cpr;          // 16-byte chunks per row
+    int rpi;          // rows per pass of the work-group: kResThreads / cpr
+    int rows_per_wg;  // R
+    int chunks;       // chunks per thread: ceil(R / rpi) <= kResChunks
+    int groups;       // G
+    int cols_per_wg;  // ceil(L / G) <= kResMaxCols
+    int tpc;          // phase-2 threads per column: kResThreads / next power of two >= cols_per_wg
+};
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t res_rsrc(const void *base, unsigned bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+// 16 bytes per lane from byte offset voff of [base, base + bytes) straight
+// into LDS at m0 + 16 * lane (offsets past the end land as zeros).  The
+// issuing wave waits for it with s_waitcnt vmcnt(0) before it reads the LDS.
+__device__ __forceinline__ void res_dma16(const void *base, unsigned bytes, unsigned voff, unsigned m0)
+{
+    const unsigned long long b = (unsigned long long)base;
+    const unsigned lo = __builtin_amdgcn_readfirstlane(unsigned(b));
+    const unsigned hi = __builtin_amdgcn_readfirstlane(unsigned(b >> 32));
+    const __amdgpu_buffer_rsrc_t rsrc =
+        res_rsrc((const void *)(((unsigned long long)hi << 32) | lo), __builtin_amdgcn_readfirstlane(bytes));
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds" ::"v"(voff), "s"(rsrc),
+                 "s"(__builtin_amdgcn_readfirstlane(m0))
+                 : "memory");
+}
+
+__device__ __forceinline__ void res_store(float *p, float v)
+{
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
+__device__ __forceinline__ float res_load(const float *p)
+{
+    return __hip_atomic_load(const_cast<float *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
+__device__ __forceinline__ unsigned res_flag(const unsigned *p)
+{
+    return __hip_atomic_load(const_cast<unsigned *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
+// This work-group raises its flag to `target` and waits until all G flags
+// have reached it.  False (in every thread) if the wait gave up.
+__device__ __forceinline__ bool res_barrier(unsigned *flags, int groups, unsigned target)
+{
+    __builtin_amdgcn_s_waitcnt(0);  // this thread's stores have completed
+    __syncthreads();
+    if (threadIdx.x == 0)
+        __hip_atomic_store(flags + blockIdx.x * kFlagStride, target, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    int late = 0;
+    for (int b = threadIdx.x; b < groups; b += kResThreads) {
+        long i = 0;
+        while (int(res_flag(flags + b * kFlagStride) - target) < 0) {
+            if (++i >= kSpinLimit) {
+                late = 1;
+                break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+        }
+    }
+    return __syncthreads_or(late) == 0;
+}
+
+template <typename T>
+__device__ __forceinline__ void res_unpack(const res_u32x4 &v, float (&f)[16 / sizeof(T)])
+{
+    if constexpr (sizeof(T) == 2) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            f[2 * i] = __builtin_bit_cast(float, v[i] << 16);
+            f[2 * i + 1] = __builtin_bit_cast(float, v[i] & 0xffff0000u);
+        }
+    } else {
+        // (each element through a scalar first: a bit-cast of a vector
+        // element read the vector's first element here)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const unsigned u = v[i];
+            f[i] = __builtin_bit_cast(float, u);
+        }
+    }
+}
+
+template <typename T>
+__device__ __forceinline__ res_u32x4 res_pack(const float (&f)[16 / sizeof(T)])
+{
+    Vec<T, 16 / sizeof(T)> o;
+#pragma unroll
+    for (int e = 0; e < 16 / int(sizeof(T)); ++e)
+        o.v[e] = T(f[e]);
+    return __builtin_bit_cast(res_u32x4, o);
+}
+
+template <typename T, bool RELU>
+__global__ __launch_bounds__(kResThreads) void iqbn_resident(ResArgs a)
+{
+    constexpr int VW = 16 / sizeof(T);
+    constexpr int NV = kResRegChunks, NL = kResLdsChunks;
+    constexpr int NW = kResThreads / 64;
+    __shared__ res_u32x4 held[NL][kResThreads];
+    __shared__ float red[2 * VW][kResThreads + 1];  // +1: the pass over it reads eight rows at once
+    __shared__ double wsum[2][NW];
+    __shared__ unsigned base_flag;
+
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const int wg = blockIdx.x;
+    const int L = a.row_len, G = a.groups;
+    const int cc = t % a.cpr, rl = t / a.cpr;
+    const bool active = rl < a.rpi;
+    const int64_t r0 = int64_t(wg) * a.rows_per_wg;
+    const int nrows = r0 < a.pixels ? int(min(int64_t(a.rows_per_wg), a.pixels - r0)) : 0;
+    const T *xw = static_cast<const T *>(a.x) + (nrows > 0 ? r0 : 0) * L;
+    const unsigned wbytes = unsigned(nrows) * unsigned(L) * unsigned(sizeof(T));
+    const unsigned kOut = 0x80000000u;  // an offset past every work-group's rows: loads give zero
+    auto chunk_off = [&](int k) {
+        const int lr = rl + k * a.rpi;
+        return active && lr < nrows ? unsigned(lr * L + cc * VW) * unsigned(sizeof(T)) : kOut;
+    };
+    auto chunk_valid = [&](int k) { return active && rl + k * a.rpi < nrows; };
+    if (t == 0)
+        base_flag = res_flag(a.flags + wg * kFlagStride);
+    // phase 2's column of this thread, with its shift value and gamma loaded
+    // now, off the path between the two barriers
+    const int ci = t / a.tpc, j = t % a.tpc;
+    const int col = wg * a.cols_per_wg + ci;
+    const bool mine = ci < a.cols_per_wg && col < L;
+    const float k0 = mine ? float(static_cast<const T *>(a.x)[col]) : 0.0f;
+    const float g0 = mine ? a.gamma[col] : 0.0f;
+    float beta0[VW];
+#pragma unroll
+    for (int e = 0; e < VW; ++e)
+        beta0[e] = a.beta[cc * VW + e];
+
+    // ---- phase 1: rows into LDS (direct loads) and VGPRs; shifted sums
+#pragma unroll
+    for (int k = 0; k < NL; ++k)
+        if (NV + k < a.chunks)
+            res_dma16(xw, wbytes, chunk_off(NV + k),
+                      unsigned((size_t)(const __attribute__((address_space(3))) void *)&held[k][wave * 64]));
+    const __amdgpu_buffer_rsrc_t src = res_rsrc(xw, wbytes);
+    res_u32x4 v[NV];
+#pragma unroll
+    for (int k = 0; k < NV; ++k)
+        v[k] = k < a.chunks ? __builtin_amdgcn_raw_buffer_load_b128(src, chunk_off(k), 0, 0) : res_u32x4{0, 0, 0, 0};
+    float shift[VW];
+    {
+        const res_u32x4 kv = *reinterpret_cast<const res_u32x4 *>(static_cast<const T *>(a.x) + cc * VW);
+        res_unpack<T>(kv, shift);
+    }
+    float s1[VW], s2[VW];
+#pragma unroll
+    for (int e = 0; e < VW; ++e)
+        s1[e] = s2[e] = 0.0f;
+    auto accumulate = [&](const res_u32x4 &c) {
+        float f[VW];
+        res_unpack<T>(c, f);
+#pragma unroll
+        for (int e = 0; e < VW; ++e) {
+            const float d = f[e] - shift[e];
+            s1[e] += d;
+            s2[e] = fmaf(d, d, s2[e]);
+        }
+    };
+#pragma unroll
+    for (int k = 0; k < NV; ++k)
+        if (k < a.chunks && chunk_valid(k))
+            accumulate(v[k]);
+    __builtin_amdgcn_s_waitcnt(0);  // the direct-to-LDS loads have landed
+    asm volatile("" ::: "memory");
+#pragma unroll
+    for (int k = 0; k < NL; ++k)
+        if (NV + k < a.chunks && chunk_valid(NV + k))
+            accumulate(held[k][t]);
+    // one (s1, s2) per column of this work-group: the rpi threads of a
+    // column chunk are added in row order, and the partials go out as
+    // contiguous rows of L floats
+#pragma unroll
+    for (int e = 0; e < VW; ++e) {
+        red[e][t] = s1[e];
+        red[VW + e][t] = s2[e];
+    }
+    __syncthreads();
+    const unsigned target1 = base_flag + 1, target2 = base_flag + 2;
+    for (int p = t; p < 2 * L; p += kResThreads) {
+        const int which = p / L, col = p % L;  // which: 0 = s1, 1 = s2
+        const int pc = col / VW, pe = which * VW + col % VW;
+        float sum = 0.0f;
+        for (int j = 0; j < a.rpi; ++j)
+            sum += red[pe][pc + j * a.cpr];
+        res_store(a.part + (size_t(which) * G + wg) * L + col, sum);
+    }
+    bool ok = res_barrier(a.flags, G, target1);
+
+    // ---- phase 2: this work-group's columns merged over the G partials (fp64)
+    {
+        // NU = ceil(G / tpc) partials per thread, all loads issued (at
+        // in-range addresses) before any is added
+        double d1 = 0.0, d2 = 0.0;
+        auto gather = [&](auto nu) {
+            constexpr int NU = decltype(nu)::value;
+            const int cl = mine ? col : 0;
+            float p1[NU], p2[NU];
+#pragma unroll
+            for (int u = 0; u < NU; ++u) {
+                const int b = min(j + u * a.tpc, G - 1);
+                p1[u] = res_load(a.part + size_t(b) * L + cl);
+                p2[u] = res_load(a.part + (size_t(G) + b) * L + cl);
+            }
+#pragma unroll
+            for (int u = 0; u < NU; ++u)
+                if (mine && j + u * a.tpc < G) {
+                    d1 += double(p1[u]);
+                    d2 += double(p2[u]);
+                }
+        };
+        const int nu = (G + a.tpc - 1) / a.tpc;
+        if (nu <= 1)
+            gather(std::integral_constant<int, 1>{});
+        else if (nu <= 2)
+            gather(std::integral_constant<int, 2>{});
+        else if (nu <= 4)
+            gather(std::integral_constant<int, 4>{});
+        else if (nu <= 8)
+            gather(std::integral_constant<int, 8>{});
+        else
+            gather(std::integral_constant<int, 16>{});
+        // the tpc threads of a column: a butterfly within the wave, then the
+        // column's waves in order
+        for (int off = (a.tpc < 64 ? a.tpc : 64) >> 1; off > 0; off >>= 1) {
+            d1 += __shfl_xor(d1, off);
+            d2 += __shfl_xor(d2, off);
+        }
+        if (lane == 0) {
+            wsum[0][wave] = d1;
+            wsum[1][wave] = d2;
+        }
+        __syncthreads();
+        if (mine && j == 0) {
+            double t1 = d1, t2 = d2;
+            if (a.tpc > 64) {
+                t1 = t2 = 0.0;
+                for (int q = 0; q < a.tpc / 64; ++q) {
+                    t1 += wsum[0][wave + q];
+                    t2 += wsum[1][wave + q];
+                }
+            }
+            const double n = double(a.pixels);
+            const double d = t1 / n;      // mean - K
+            double var = t2 / n - d * d;  // biased variance
+            if (var < 0.0)
+                var = 0.0;
+            const double mu = double(k0) + d;
+            const double sc = double(g0) / sqrt(var + double(a.eps));
+            a.mean[col] = ok ? float(mu) : __builtin_nanf("");
+            a.var[col] = ok ? float(var) : __builtin_nanf("");
+            res_store(a.coef + col, float(mu));
+            res_store(a.coef + L + col, float(sc));
+        }
+    }
+    ok = res_barrier(a.flags, G, target2) && ok;
+
+    // ---- phase 3: normalise the held rows and write them
+    if (!active)
+        return;
+    float mu[VW], sc[VW], be[VW];
+    {
+        // 16-byte loads with the cache policy of the system-scope loads
+        // above (sc0 sc1: from memory, past the L2)
+        constexpr int kSysCoherent = 17;
+        const __amdgpu_buffer_rsrc_t crs = res_rsrc(a.coef, unsigned(2 * L) * unsigned(sizeof(float)));
+#pragma unroll
+        for (int h = 0; h < VW / 4; ++h) {
+            const res_u32x4 m = __builtin_amdgcn_raw_buffer_load_b128(crs, unsigned(cc * VW + 4 * h) * 4u, 0, kSysCoherent);
+            const res_u32x4 q =
+                __builtin_amdgcn_raw_buffer_load_b128(crs, unsigned(L + cc * VW + 4 * h) * 4u, 0, kSysCoherent);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const unsigned mi = m[i], qi = q[i];
+                mu[4 * h + i] = __builtin_bit_cast(float, mi);
+                sc[4 * h + i] = __builtin_bit_cast(float, qi);
+            }
+        }
+#pragma unroll
+        for (int e = 0; e < VW; ++e)
+            be[e] = beta0[e];
+    }
+    T *ow = static_cast<T *>(a.out) + (nrows > 0 ? r0 : 0) * L;
+    auto emit = [&](int k, const res_u32x4 &c) {
+        float f[VW];
+        res_unpack<T>(c, f);
+#pragma unroll
+        for (int e = 0; e < VW; ++e) {
+            float y = fmaf(f[e] - mu[e], sc[e], be[e]);
+            if (RELU)
+                y = fmaxf(y, 0.0f);
+            f[e] = ok ? y : __builtin_nanf("");
+        }
+        const int lr = rl + k * a.rpi;
+        __builtin_nontemporal_store(res_pack<T>(f),
+                                    reinterpret_cast<res_u32x4 *>(ow + size_t(lr) * L + cc * VW));
+    };
+#pragma unroll
+    for (int k = 0; k < NV; ++k)
+        if (k < a.chunks && chunk_valid(k))
+            emit(k, v[k]);
+#pragma unroll
+    for (int k = 0; k < NL; ++k)
+        if (NV + k < a.chunks && chunk_valid(NV + k))
+            emit(NV + k, held[k][t]);
+}
+
 // ------------------------------ backward ------------------------------
 // Gradient of training-mode IQBN (eqs. 11, 12) given the saved batch mean
 // and biased variance: per column, with s = sqrt(var + eps), xhat = (x - mean)
@@ -670,6 +1044,108 @@ hipError_t launch_backward(const void *x, const void *dout, const void *y, const
     return hipGetLastError();
 }
 
+// Geometry of the resident launch for this tensor on the current device, or
+// false where it does not apply (chunks that are not 16 bytes, rows longer
+// than kResThreads chunks, more rows per work-group than it can hold, more
+// than kResMaxCols columns per work-group to merge).
+struct ResPlan {
+    int groups, cpr, rpi, rows_per_wg, chunks, cols_per_wg, tpc;
+};
+
+std::mutex g_res_mutex;
+int g_res_groups[64];
+bool g_res_known[64];
+
+// Work-groups of the resident launch on the current device: one per compute
+// unit, where a compute unit holds exactly one (0: not available).
+int resident_groups()
+{
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64)
+        return 0;
+    std::lock_guard<std::mutex> lock(g_res_mutex);
+    if (!g_res_known[dev]) {
+        int cus = 0, per_cu = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+            cus = 0;
+        // every instantiation holds the same LDS and thread count
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, iqbn_resident<__bf16, false>, kResThreads, 0) !=
+            hipSuccess)
+            per_cu = 0;
+        g_res_groups[dev] = per_cu == 1 && cus > 0 && cus <= kResMaxGroups ? cus : 0;
+        g_res_known[dev] = true;
+    }
+    return g_res_groups[dev];
+}
+
+bool resident_plan(int64_t pixels, int c, DType dt, ResPlan *rp)
+{
+    const int es = dt == DType::BF16 ? 2 : 4;
+    const int row_bytes = 4 * c * es;
+    if (row_bytes % 16 != 0)
+        return false;
+    const int cpr = row_bytes / 16;
+    if (cpr > kResThreads || pixels * row_bytes < kResMinBytes)
+        return false;
+    const int groups = resident_groups();
+    if (groups <= 0)
+        return false;
+    const int rpi = kResThreads / cpr;
+    const int64_t rows_per_wg = (pixels + groups - 1) / groups;
+    const int64_t chunks = (rows_per_wg + rpi - 1) / rpi;
+    const int cols_per_wg = (4 * c + groups - 1) / groups;
+    if (chunks > kResChunks || cols_per_wg > kResMaxCols)
+        return false;
+    int pow2 = 1;
+    while (pow2 < cols_per_wg)
+        pow2 *= 2;
+    rp->groups = groups;
+    rp->cpr = cpr;
+    rp->rpi = rpi;
+    rp->rows_per_wg = int(rows_per_wg);
+    rp->chunks = int(chunks);
+    rp->cols_per_wg = cols_per_wg;
+    rp->tpc = kResThreads / pow2;
+    return true;
+}
+
+size_t resident_bytes(const ResPlan &rp, int c)
+{
+    return (size_t(2) * rp.groups + 2) * 4 * size_t(c) * sizeof(float);
+}
+
+template <typename T>
+hipError_t launch_resident(const ResPlan &rp, const void *x, const float *gamma, const float *beta, float eps,
+                           bool relu, void *out, float *mean, float *var, int64_t pixels, int c, void *work,
+                           unsigned *flags, hipStream_t stream)
+{
+    ResArgs a;
+    a.x = x;
+    a.out = out;
+    a.gamma = gamma;
+    a.beta = beta;
+    a.eps = eps;
+    a.mean = mean;
+    a.var = var;
+    a.part = static_cast<float *>(work);
+    a.coef = a.part + size_t(2) * 4 * c * rp.groups;
+    a.flags = flags;
+    a.pixels = pixels;
+    a.row_len = 4 * c;
+    a.cpr = rp.cpr;
+    a.rpi = rp.rpi;
+    a.rows_per_wg = rp.rows_per_wg;
+    a.chunks = rp.chunks;
+    a.groups = rp.groups;
+    a.cols_per_wg = rp.cols_per_wg;
+    a.tpc = rp.tpc;
+    if (relu)
+        hipLaunchKernelGGL((iqbn_resident<T, true>), dim3(rp.groups), dim3(kResThreads), 0, stream, a);
+    else
+        hipLaunchKernelGGL((iqbn_resident<T, false>), dim3(rp.groups), dim3(kResThreads), 0, stream, a);
+    return hipGetLastError();
+}
+
 template <typename T, int VW>
 hipError_t launch_all(const void *x, const float *gamma, const float *beta, float eps, bool relu,
                       void *out, float *mean, float *var, int64_t pixels, int c, void *work,
@@ -776,10 +1252,26 @@ hipError_t iqbn_from_tiles_run(const float *part, int m_tiles, int tile_rows, co
                                        pixels, c, affine, stream);
 }
 
+bool iqbn_one_launch(int64_t pixels, int c, DType dt)
+{
+    ResPlan rp;
+    return resident_plan(pixels, c, dt, &rp);
+}
+
+size_t iqbn_barrier_bytes()
+{
+    return size_t(kResMaxGroups) * kFlagStride * sizeof(unsigned);
+}
+
 size_t iqbn_workspace_bytes(int64_t pixels, int c)
 {
-    // Largest over the vector widths the dispatcher may pick.
+    // Largest over the vector widths the dispatcher may pick, and the
+    // resident launch where it applies.
     size_t best = 0;
+    ResPlan rp;
+    for (DType dt : {DType::BF16, DType::F32})
+        if (resident_plan(pixels, c, dt, &rp) && resident_bytes(rp, c) > best)
+            best = resident_bytes(rp, c);
     for (int vw : {1, 4, 8}) {
         if ((4 * c) % vw)
             continue;
@@ -812,8 +1304,14 @@ hipError_t iqbn_backward_run(const void *x, const void *dout, const void *y, con
 
 hipError_t iqbn_run(const void *x, const float *gamma, const float *beta, float eps, bool relu,
                     void *out, float *mean, float *var, int64_t pixels, int c, DType dt, void *work,
-                    hipStream_t stream)
+                    unsigned *flags, hipStream_t stream)
 {
+    ResPlan rp;
+    if (flags != nullptr && resident_plan(pixels, c, dt, &rp))
+        return dt == DType::BF16 ? launch_resident<__bf16>(rp, x, gamma, beta, eps, relu, out, mean, var, pixels,
+                                                           c, work, flags, stream)
+                                 : launch_resident<float>(rp, x, gamma, beta, eps, relu, out, mean, var, pixels, c,
+                                                          work, flags, stream);
     const int vw = vec_width(c, dt);
     if (dt == DType::BF16) {
         if (vw == 8)

@@ -46,7 +46,15 @@ struct Workspace {
 std::mutex g_ws_mutex;
 std::map<std::pair<int, std::pair<void *, int>>, Workspace> g_ws;
 
-enum Purpose { kWeightPack = 0, kIqbnPartials = 1, kIqbnFold = 2, kGradPack = 3, kGradStage = 4, kWgrad = 5 };
+enum Purpose {
+    kWeightPack = 0,
+    kIqbnPartials = 1,
+    kIqbnFold = 2,
+    kGradPack = 3,
+    kGradStage = 4,
+    kWgrad = 5,
+    kIqbnBarrier = 6  // the one-launch IQBN's grid-barrier flags: zeroed once, when allocated
+};
 
 // Returns a device buffer of at least `bytes` for (current device, stream,
 // purpose).  Growing it first waits for the device to finish with the old one.
@@ -77,8 +85,23 @@ int workspace(void *stream, Purpose purpose, size_t bytes, void **out)
             return fail(QUAN_ERR_NOMEM, "hipMalloc(%zu) for workspace: %s", want, hipGetErrorString(e));
         }
         ws.bytes = want;
+        if (purpose == kIqbnBarrier) {
+            e = hipMemsetAsync(ws.ptr, 0, want, static_cast<hipStream_t>(stream));
+            if (e != hipSuccess)
+                return fail_hip(e, "hipMemsetAsync (barrier flags)");
+        }
     }
     *out = ws.ptr;
+    return QUAN_OK;
+}
+
+// The grid-barrier flags of the one-launch IQBN on this (device, stream).
+int iqbn_flags(void *stream, unsigned **out)
+{
+    void *p = nullptr;
+    if (int rc = workspace(stream, kIqbnBarrier, quan::iqbn_barrier_bytes(), &p))
+        return rc;
+    *out = static_cast<unsigned *>(p);
     return QUAN_OK;
 }
 
@@ -241,7 +264,10 @@ int iqbn_common(const void *x, const float *gamma, const float *beta, float eps,
     void *work = nullptr;
     if (int rc = workspace(stream, kIqbnPartials, quan::iqbn_workspace_bytes(pixels, c), &work))
         return rc;
-    hipError_t e = quan::iqbn_run(x, gamma, beta, eps, relu, out, mean, var, pixels, c, dt, work,
+    unsigned *flags = nullptr;
+    if (int rc = iqbn_flags(stream, &flags))
+        return rc;
+    hipError_t e = quan::iqbn_run(x, gamma, beta, eps, relu, out, mean, var, pixels, c, dt, work, flags,
                                   static_cast<hipStream_t>(stream));
     if (e != hipSuccess)
         return fail_hip(e, "iqbn launch");
@@ -465,7 +491,12 @@ QUAN_API int quan_qconv2d_iqbn_forward(const void *x, const void *packed, const 
     hipStream_t s = static_cast<hipStream_t>(stream);
     void *work = nullptr;
     hipError_t e;
-    if (stats != QUAN_STATS_PASS && quan::qconv2d_writes_stats(plan, g, dt)) {
+    // AUTO: a one-launch IQBN pass after the plain convolution where the
+    // tensor takes it (it reads out once, like the epilogue's normalisation,
+    // and spares the epilogue's statistics work), else the epilogue
+    const bool epilogue = stats == QUAN_STATS_EPILOGUE ||
+                          (stats == QUAN_STATS_AUTO && !quan::iqbn_one_launch(pixels, c_out, dt));
+    if (epilogue && quan::qconv2d_writes_stats(plan, g, dt)) {
         // statistics gathered in the convolution's epilogue
         if (int rc = workspace(stream, kIqbnPartials, quan::iqbn_tile_stats_bytes(plan.stat_tiles, c_out), &work))
             return rc;
@@ -477,10 +508,13 @@ QUAN_API int quan_qconv2d_iqbn_forward(const void *x, const void *packed, const 
     } else {
         if (int rc = workspace(stream, kIqbnPartials, quan::iqbn_workspace_bytes(pixels, c_out), &work))
             return rc;
+        unsigned *flags = nullptr;
+        if (int rc = iqbn_flags(stream, &flags))
+            return rc;
         e = quan::qconv2d_run(plan, pg, g, dt, x, packed, bias, out, nullptr, nullptr, s);
         if (e != hipSuccess)
             return fail_hip(e, "qconv2d launch");
-        e = quan::iqbn_run(out, gamma, beta, eps, relu != 0, out, mean, var, pixels, c_out, dt, work, s);
+        e = quan::iqbn_run(out, gamma, beta, eps, relu != 0, out, mean, var, pixels, c_out, dt, work, flags, s);
     }
     if (e != hipSuccess)
         return fail_hip(e, "iqbn launch");

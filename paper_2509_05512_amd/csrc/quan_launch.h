@@ -116,11 +116,18 @@ int report(int code, const char *fmt, ...);
 int iqbn_validate(const void *x, const float *gamma, const float *beta, float eps, const void *out,
                   const float *mean, const float *var, int32_t n, int32_t c, int32_t h, int32_t w, int32_t dtype);
 
-// IQBN.  `work` must hold iqbn_workspace_bytes(...) bytes.
+// IQBN.  `work` must hold iqbn_workspace_bytes(...) bytes.  `flags` holds the
+// grid-barrier flags of the one-launch form: iqbn_barrier_bytes() of device
+// memory, zero when first allocated, used by no other code and by one stream
+// at a time (NULL: always the three-launch form).
 size_t iqbn_workspace_bytes(int64_t pixels, int c);
+size_t iqbn_barrier_bytes();
+// Whether iqbn_run (given flags) normalises this tensor in one launch that
+// reads it once, on the current device.
+bool iqbn_one_launch(int64_t pixels, int c, DType dt);
 hipError_t iqbn_run(const void *x, const float *gamma, const float *beta, float eps, bool relu,
                     void *out, float *mean, float *var, int64_t pixels, int c, DType dt,
-                    void *work, hipStream_t stream);
+                    void *work, unsigned *flags, hipStream_t stream);
 
 // Gradient of training-mode IQBN given the forward's saved mean and biased
 // variance ([4][c] fp32): dx (dtype dt, x's layout), dgamma, dbeta ([4][c]

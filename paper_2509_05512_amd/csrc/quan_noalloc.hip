@@ -18,9 +18,14 @@
 
 namespace {
 
-// 8 MiB per device: the statistics pass needs (2 * blocks + 3) * 4C floats
-// with at most 512 blocks, e.g. 1.0 MiB for 256 real channels.
+// 8 MiB per device.  Its first 64 KiB hold the grid-barrier flags of the
+// one-launch IQBN (zero at module load, used by nothing else); the rest holds
+// the partial statistics: (2 * blocks + 3) * 4C floats with at most 512
+// blocks for the three-launch form (1.0 MiB for 256 real channels), (2 * G +
+// 2) * 4C floats for the one-launch form on G compute units.
 constexpr size_t kScratchBytes = size_t(8) << 20;
+constexpr size_t kFlagBytes = size_t(64) << 10;
+static_assert(kFlagBytes >= 512 * 32 * sizeof(unsigned), "room for the barrier flags");
 
 static __device__ __align__(256) unsigned char scratch[kScratchBytes];
 
@@ -62,7 +67,7 @@ extern "C" QUAN_API int quan_iqbn_forward_noalloc(const void *x, const float *ga
     if (int rc = quan::iqbn_validate(x, gamma, beta, eps, out, mean, var, n, c, h, w, dtype))
         return rc;
     const int64_t pixels = int64_t(n) * h * w;
-    const size_t need = quan::iqbn_workspace_bytes(pixels, c);
+    const size_t need = quan::iqbn_workspace_bytes(pixels, c) + kFlagBytes;
     if (need > kScratchBytes)
         return quan::report(QUAN_ERR_UNSUPPORTED,
                             "iqbn_forward_noalloc: needs %zu bytes of scratch, the fixed array holds %zu "
@@ -71,8 +76,10 @@ extern "C" QUAN_API int quan_iqbn_forward_noalloc(const void *x, const float *ga
     void *work = nullptr;
     if (int rc = scratch_address(&work))
         return rc;
+    unsigned char *base = static_cast<unsigned char *>(work);
     const hipError_t e = quan::iqbn_run(x, gamma, beta, eps, false, out, mean, var, pixels, c,
-                                        dtype == QUAN_BF16 ? quan::DType::BF16 : quan::DType::F32, work,
+                                        dtype == QUAN_BF16 ? quan::DType::BF16 : quan::DType::F32,
+                                        base + kFlagBytes, reinterpret_cast<unsigned *>(base),
                                         static_cast<hipStream_t>(stream));
     if (e != hipSuccess)
         return quan::report(QUAN_ERR_HIP, "iqbn_forward_noalloc launch: %s (%d)", hipGetErrorString(e), int(e));

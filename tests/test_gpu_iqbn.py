@@ -144,3 +144,67 @@ def test_iqbn_repeated_calls_reuse_counters():
                 first = (out.cpu(), mean.cpu(), var.cpu())
             elif i == 4:
                 assert torch.equal(first[0], out.cpu()) and torch.equal(first[2], var.cpu())
+
+
+# ---- the one-launch form (tensors of 16 MiB and more that fit the registers
+# and LDS of one work-group per compute unit) --------------------------------
+
+def _cus():
+    return torch.cuda.get_device_properties(0).multi_processor_count
+
+
+# (N, C, H, W), dtype, relu: 16 MiB and up; narrow rows (8 chunks), 256-byte
+# rows with 32 and 64 chunks, 4 KB and 8 KB rows (several columns merged per
+# work-group), the detection-pair layer and the full ImageNet-stage layer
+RESIDENT = [
+    ((128, 16, 32, 32), "bf16", True),
+    ((32, 64, 32, 32), "bf16", False),
+    ((16, 64, 32, 32), "fp32", True),
+    ((4, 512, 32, 32), "bf16", False),
+    ((2, 1024, 32, 64), "bf16", True),
+    ((16, 64, 80, 80), "bf16", False),
+    ((64, 64, 56, 56), "bf16", True),
+]
+
+
+@pytest.mark.parametrize("shape,dtype,relu", RESIDENT, ids=[f"{s}-{d}-relu{int(r)}" for s, d, r in RESIDENT])
+def test_iqbn_one_launch_matches_oracle(shape, dtype, relu):
+    say(f"iqbn one-launch {dtype} {shape} relu={relu}")
+    dt = DT[dtype]
+    x, g, b = _case(shape, dt, seed=sum(shape) + 5)
+    out, mean, var = _run(x, g, b, 1e-5, relu)
+    ref, rmean, rvar = oracle.iqbn(f64(x), f64(g), f64(b), 1e-5, relu)
+    assert_close(f64(mean), rmean, dt, "mean")
+    assert_close(f64(var), rvar, dt, "var")
+    assert_close(f64(out), ref, dt, "out")
+
+
+@pytest.mark.parametrize("extra", [0, 16])
+def test_iqbn_one_launch_capacity_edge(extra):
+    """256-element bf16 rows: 16 rows per pass of a work-group, at most 51
+    passes held per work-group.  The largest tensor held (51 passes on every
+    compute unit) and one just past it (the three launches) both match."""
+    P = _cus() * 16 * 51 + extra
+    say(f"iqbn capacity edge P={P}")
+    x, g, b = _case((1, 64, 1, P), torch.bfloat16, seed=77 + extra)
+    out, mean, var = _run(x, g, b, 1e-5, False)
+    ref, rmean, rvar = oracle.iqbn(f64(x), f64(g), f64(b), 1e-5, False)
+    assert_close(f64(var), rvar, torch.bfloat16, "var")
+    assert_close(f64(out), ref, torch.bfloat16, "out")
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_iqbn_one_launch_in_place_and_repeatable(dtype):
+    """In place (every work-group reads all its rows before any is written),
+    and bit-identical across calls (fixed-order merges; the barrier flags
+    advance by two per call)."""
+    say(f"iqbn one-launch in-place {dtype}")
+    dt = DT[dtype]
+    x, g, b = _case((32, 64, 32, 32), dt, seed=91)
+    o1, m1, v1 = _run(x, g, b, 1e-5, True, inplace=True)
+    ref, rmean, rvar = oracle.iqbn(f64(x), f64(g), f64(b), 1e-5, True)
+    assert_close(f64(o1), ref, dt, "in-place out")
+    for _ in range(3):
+        o2, m2, v2 = _run(x, g, b, 1e-5, True, inplace=True)
+        assert torch.equal(o1.cpu(), o2.cpu()) and torch.equal(m1.cpu(), m2.cpu()) \
+            and torch.equal(v1.cpu(), v2.cpu())
