@@ -12,8 +12,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libquan.so")
-SOURCES = ["qconv2d_gfx950.hip", "qconv2d_wgrad_gfx950.hip", "iqbn_gfx950.hip", "poincare_gfx950.hip",
-           "quan_noalloc.hip", "quan_api.cpp"]
+SOURCES = ["qconv2d_gfx950.hip", "qconv2d_wgrad_gfx950.hip", "stem_gfx950.hip", "iqbn_gfx950.hip",
+           "poincare_gfx950.hip", "quan_noalloc.hip", "quan_api.cpp"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -55,10 +55,6 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-// Bit 4*p + q is set when entry (p, q) of the Hamilton matrix (eq. 6) is
-// negative.  Row r: + - - -, row i: + + - +, row j: + + + -, row k: + - + +.
-constexpr unsigned kHamiltonNeg =
-    (1u << 1) | (1u << 2) | (1u << 3) | (1u << 6) | (1u << 11) | (1u << 13);
 
 // Bit 4*p + q is set when the separable form (eq. 7) subtracts W_q (*) x_q
 // from output component p.  Row r: + - - -, row i: + + + -, row j: + - + +,

@@ -599,9 +599,12 @@ QUAN_API int quan_qconv2d_poincare_forward(const void *rgb, const void *packed, 
         return fail(QUAN_ERR_ALIAS, "qconv2d_poincare: out overlaps the packed weights");
     const quan::DType dt = to_dt(dtype);
     const quan::PackGeom pg = quan::qconv2d_pack_geom(1, c_out, k_h, k_w, dt);
-    const hipError_t e = quan::qconv2d_run(quan::qconv2d_plan(g, dt, quan::ConvForm::Hamilton), pg, g, dt, rgb,
-                                           packed, bias, out, nullptr, nullptr, static_cast<hipStream_t>(stream),
-                                           true);
+    // the stem kernel where it takes the layer, else the implicit-GEMM
+    // kernel with the map in its loads
+    hipError_t e = quan::qconv2d_stem_run(pg, g, dt, rgb, packed, bias, out, static_cast<hipStream_t>(stream));
+    if (e == hipErrorNotSupported)
+        e = quan::qconv2d_run(quan::qconv2d_plan(g, dt, quan::ConvForm::Hamilton), pg, g, dt, rgb, packed, bias, out,
+                              nullptr, nullptr, static_cast<hipStream_t>(stream), true);
     if (e != hipSuccess)
         return fail_hip(e, "qconv2d_poincare launch");
     return QUAN_OK;

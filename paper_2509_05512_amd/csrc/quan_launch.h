@@ -11,6 +11,11 @@ namespace quan {
 
 enum class DType : int { F32 = 0, BF16 = 1 };
 
+// Bit 4*p + q is set when entry (p, q) of the Hamilton matrix (eq. 6) is
+// negative.  Row r: + - - -, row i: + + - +, row j: + + + -, row k: + - + +.
+constexpr unsigned kHamiltonNeg =
+    (1u << 1) | (1u << 2) | (1u << 3) | (1u << 6) | (1u << 11) | (1u << 13);
+
 // Geometry of one quaternion convolution (quaternion channel counts).
 struct ConvGeom {
     int n, c_in, h, w, c_out, k_h, k_w;
@@ -79,6 +84,16 @@ bool qconv2d_writes_stats(const ConvPlan &plan, const ConvGeom &g, DType dt);
 hipError_t qconv2d_run(const ConvPlan &plan, const PackGeom &pg, const ConvGeom &g, DType dt,
                        const void *x, const void *wpack, const void *bias, void *out,
                        float *stats, const ConvFold *fold, hipStream_t stream, bool poincare = false);
+
+// The stem layer (g.c_in == 1, bf16) as its own kernel: rgb is the colour
+// planes [n][3][h][w], mapped to quaternions by eq. 4 as they are loaded;
+// wpack the packed weights (qconv2d_pack_weights); out as qconv2d_run.
+// Returns hipErrorNotSupported, before any launch, where the layer is not
+// one it takes: fp32, more than 64 output channels, or more than 32 MFMA
+// weight fragments (B * ceil(taps / 4), B = ceil(4 c_out / 32) rounded up
+// to a power of two).
+hipError_t qconv2d_stem_run(const PackGeom &pg, const ConvGeom &g, DType dt, const void *rgb, const void *wpack,
+                            const void *bias, void *out, hipStream_t stream);
 
 // Input gradient of the Hamilton convolution: dX = conv(Z, W'), Z = dY (stride
 // 1) or dY scattered with s-1 zeros between rows/columns (staged in `stage`,

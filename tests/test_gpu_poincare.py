@@ -84,6 +84,10 @@ STEM_CASES = [
     (2, 23, 21, 16, 7, 2, 3, 1.0, "bf16"),    # 7x7 stride 2 (a classification stem)
     (2, 9, 11, 12, 3, 1, 1, 1.0, "bf16"),     # 12 channels: not whole 16-byte output chunks
     (1, 8, 9, 32, 3, 1, 0, 15.0, "bf16"),     # colours far outside the unit cube
+    # past the stem kernel's weight table: the implicit-GEMM kernel with the
+    # map in its loads
+    (2, 10, 12, 80, 3, 1, 1, 1.0, "bf16"),    # 80 channels: ten 32-row blocks
+    (2, 13, 11, 64, 5, 1, 2, 1.0, "bf16"),    # 5x5, 64 channels: 8 x 7 fragments
 ]
 
 
