@@ -46,12 +46,17 @@ METRIC = "qconv2d bf16 TFLOP/s + % MFMA peak; IQBN GB/s + % HBM peak"
 DEFAULT_WORKLOAD = "imagenet_stage"
 # the other configurations the targets apply to, reported as sub-records
 OTHER_CONFIGS = ["detection_pair", "deep_stack"]
-# HBM bytes per launch of the convolution kernel, from rocprofv3 --pmc
-# FETCH_SIZE and WRITE_SIZE runs of this benchmark, each scaled by what the same
-# counter reads for a 512 MiB device copy (FETCH x2.0, WRITE x1.0); the runs are
-# summarised in profiles/qconv2d_<workload>_hbm.md.  A figure is reported only
-# while the kernel source is the one it was measured on (sha256 prefix).
-CONV_TRAFFIC = {"imagenet_stage": {"bytes": 221713403, "kernel_sha256": "673f1c2125108f3c"}}
+# HBM bytes per step of the convolution kernel (all layers of the workload),
+# from rocprofv3 --pmc FETCH_SIZE and WRITE_SIZE runs of this benchmark, each
+# scaled by what the same counter reads for a 512 MiB device copy (FETCH x2.0,
+# WRITE x1.0); the runs are summarised in profiles/qconv2d_<workload>_hbm.md.
+# A figure is reported only while the kernel source is the one it was
+# measured on (sha256 prefix).
+CONV_TRAFFIC = {
+    "imagenet_stage": {"bytes": 221711945, "kernel_sha256": "a761e11818b239b5"},
+    "detection_pair": {"bytes": 289684248, "kernel_sha256": "a761e11818b239b5"},
+    "deep_stack": {"bytes": 259758004, "kernel_sha256": "a761e11818b239b5"},
+}
 CONV_SOURCE = os.path.join(ROOT, "paper_2509_05512_amd", "csrc", "qconv2d_gfx950.hip")
 
 
@@ -435,7 +440,9 @@ def measure_config(name, args, dev, quan, workloads):
         "step_us": round(step_ms * 1e3, 3),
         "step_tflops": round(flops / (step_ms * 1e-3) / 1e12, 2),
         "qconv2d": {"us_per_step": round(sum(conv_ms) * 1e3, 3), "tflops": round(conv_tf, 2),
-                    "frac_mfma_peak": round(conv_tf / peak, 4)},
+                    "frac_mfma_peak": round(conv_tf / peak, 4),
+                    # HBM bytes per step of the convolution launches (profiles/), or None
+                    "traffic": conv_traffic(name)},
         "iqbn": {"cold_us_per_step": round(sum(cold_us), 3),
                  "cold_gbps": round(nbytes / (sum(cold_us) * 1e-6) / 1e9, 1),
                  "cold_frac_hbm_peak": round(nbytes / (sum(cold_us) * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
