@@ -1460,11 +1460,17 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
 // -w_j, -w_k), since the Hamilton matrix of the conjugate is the transpose,
 // kPackSeparableGrad the four real kernels as they are.
 enum : int { kPackForward = 0, kPackHamiltonGrad = 1, kPackSeparableGrad = 2 };
+//
+// A transposed mode may pack a sub-kernel instead (one output phase of a
+// strided layer's input gradient): tap (ky, kx) of the k_h x k_w sub-kernel
+// is tap (ky0 + ky * step_h, kx0 + kx * step_w) of the full_kh x full_kw
+// transposed kernel.
 template <typename T, int MODE>
 __global__ __launch_bounds__(256) void qconv2d_pack(const T *__restrict__ w0, const T *__restrict__ w1,
                                                     const T *__restrict__ w2, const T *__restrict__ w3,
                                                     T *__restrict__ wp, int c_in, int c_out, int k_h,
-                                                    int k_w, int n_cblk, int cout_pad, int total)
+                                                    int k_w, int n_cblk, int cout_pad, int total, int ky0,
+                                                    int kx0, int step_h, int step_w, int full_kh, int full_kw)
 {
     constexpr int CS = stage_channels<T>();
     const int idx = blockIdx.x * blockDim.x + threadIdx.x;
@@ -1485,7 +1491,8 @@ __global__ __launch_bounds__(256) void qconv2d_pack(const T *__restrict__ w0, co
     T v = T(0);
     if (o < c_out && c < c_in) {
         if constexpr (MODE != kPackForward) {
-            const T u = src[((c * c_out + o) * k_h + (k_h - 1 - ky)) * k_w + (k_w - 1 - kx)];
+            const int kyf = ky0 + ky * step_h, kxf = kx0 + kx * step_w;
+            const T u = src[((c * c_out + o) * full_kh + (full_kh - 1 - kyf)) * full_kw + (full_kw - 1 - kxf)];
             v = (MODE == kPackSeparableGrad || ws == 0) ? u : T(-float(u));
         } else {
             v = src[((o * c_in + c) * k_h + ky) * k_w + kx];
@@ -1525,6 +1532,48 @@ __global__ __launch_bounds__(256) void qconv2d_grad_dilate(const T *__restrict__
             c.e[e] = T(0);
     }
     reinterpret_cast<Chunk *>(z)[idx] = c;
+}
+
+// The output phases of a strided layer's input gradient, computed apart:
+// phase (ry, rx) holds dX at rows ry, ry + s_h, ... and columns rx, rx + s_w,
+// ... as a dense [n][hp][wp][row] block `off` elements into the stage buffer;
+// hp == 0 marks a phase that no kernel tap reaches (its pixels are zero).
+constexpr int kMaxPhases = 16;
+struct PhaseMap {
+    int64_t off[kMaxPhases];
+    int hp[kMaxPhases], wp[kMaxPhases];
+};
+
+// Interleaves the phases into dX [n][h][w][row].  One thread per VW elements.
+template <typename T, int VW>
+__global__ __launch_bounds__(256) void qconv2d_grad_interleave(const T *__restrict__ stage, T *__restrict__ dx,
+                                                               PhaseMap pm, int h, int w, int s_h, int s_w,
+                                                               int row_vecs, int64_t total)
+{
+    const int64_t idx = int64_t(blockIdx.x) * 256 + threadIdx.x;
+    if (idx >= total)
+        return;
+    int64_t t = idx;
+    const int v = int(t % row_vecs);
+    t /= row_vecs;
+    const int ix = int(t % w);
+    t /= w;
+    const int iy = int(t % h);
+    const int64_t n = t / h;
+    struct alignas(sizeof(T) * VW) Chunk {
+        T e[VW];
+    };
+    Chunk c;
+    const int ph = (iy % s_h) * s_w + ix % s_w;
+    if (pm.hp[ph] > 0) {
+        const int64_t at = ((n * pm.hp[ph] + iy / s_h) * pm.wp[ph] + ix / s_w) * row_vecs + v;
+        c = reinterpret_cast<const Chunk *>(stage + pm.off[ph])[at];
+    } else {
+#pragma unroll
+        for (int e = 0; e < VW; ++e)
+            c.e[e] = T(0);
+    }
+    reinterpret_cast<Chunk *>(dx)[idx] = c;
 }
 
 // ----------------------------- kernel table -------------------------------
@@ -1765,22 +1814,30 @@ ConvPlan qconv2d_plan(const ConvGeom &g, DType dt, ConvForm form)
 }
 
 namespace {
+// (ky0, kx0, step_h, step_w, full_kh, full_kw): the sub-kernel of a
+// transposed mode (the whole kernel: 0, 0, 1, 1, k_h, k_w)
 template <int MODE>
 hipError_t pack_weights(const PackGeom &pg, int c_in, int c_out, int k_h, int k_w, DType dt, const void *w_r,
-                        const void *w_i, const void *w_j, const void *w_k, void *wpack, hipStream_t stream)
+                        const void *w_i, const void *w_j, const void *w_k, void *wpack, hipStream_t stream,
+                        int ky0 = 0, int kx0 = 0, int step_h = 1, int step_w = 1, int full_kh = 0,
+                        int full_kw = 0)
 {
     const int total = int(pg.bytes / (dt == DType::BF16 ? 2 : 4));
     const int blocks = (total + 255) / 256;
+    if (full_kh == 0) {
+        full_kh = k_h;
+        full_kw = k_w;
+    }
     if (dt == DType::BF16)
         hipLaunchKernelGGL((qconv2d_pack<__bf16, MODE>), dim3(blocks), dim3(256), 0, stream,
                            (const __bf16 *)w_r, (const __bf16 *)w_i, (const __bf16 *)w_j,
                            (const __bf16 *)w_k, (__bf16 *)wpack, c_in, c_out, k_h, k_w, pg.n_cblk,
-                           pg.cout_pad, total);
+                           pg.cout_pad, total, ky0, kx0, step_h, step_w, full_kh, full_kw);
     else
         hipLaunchKernelGGL((qconv2d_pack<float, MODE>), dim3(blocks), dim3(256), 0, stream,
                            (const float *)w_r, (const float *)w_i, (const float *)w_j,
                            (const float *)w_k, (float *)wpack, c_in, c_out, k_h, k_w, pg.n_cblk,
-                           pg.cout_pad, total);
+                           pg.cout_pad, total, ky0, kx0, step_h, step_w, full_kh, full_kw);
     return hipGetLastError();
 }
 }  // namespace
@@ -1817,8 +1874,114 @@ size_t qconv2d_grad_data_stage_bytes(const ConvGeom &g, DType dt)
     if (g.s_h == 1 && g.s_w == 1)
         return 0;
     const ConvGeom t = qconv2d_grad_data_geom(g);
-    return size_t(t.n) * t.h * t.w * 4 * t.c_in * (dt == DType::BF16 ? 2 : 4);
+    const size_t es = dt == DType::BF16 ? 2 : 4;
+    // the zero-inserted gradient (dilated layers), or the output phases (dX's size)
+    const size_t z = size_t(t.n) * t.h * t.w * 4 * t.c_in * es;
+    // (each phase starts on a 16-byte boundary)
+    const size_t phases = size_t(g.n) * g.h * g.w * 4 * g.c_in * es + size_t(16) * kMaxPhases;
+    return z > phases ? z : phases;
 }
+
+namespace {
+// One output phase of a strided layer's input gradient along one axis: with
+// the transposed kernel W'[u] = W[k-1-u] and its stride-1 padding
+// tp = k-1-p, dX[s*j + r] = sum over taps u = u0 + m*s (u < k) of
+// W'[u] dY[j + c + m] for c = (r - tp + u0) / s, u0 = (tp - r) mod s:
+// a stride-1 correlation of dY with the sub-kernel of `taps` taps and
+// padding -c.  (Unit dilation.)
+struct AxisPhase {
+    int u0, taps, pad, size;
+};
+AxisPhase axis_phase(int k, int p, int s, int in, int r)
+{
+    AxisPhase a;
+    const int tp = k - 1 - p;
+    a.u0 = ((tp - r) % s + s) % s;
+    a.taps = a.u0 < k ? (k - 1 - a.u0) / s + 1 : 0;
+    a.pad = -((r - tp + a.u0) / s);  // exact: r - tp + u0 is a multiple of s
+    a.size = in > r ? (in - r + s - 1) / s : 0;
+    return a;
+}
+
+// The strided input gradient as s_h x s_w stride-1 convolutions of dY, one
+// per output phase (only the taps that reach it: the MFMA work of the layer
+// once, where the zero-inserted gradient does it s_h * s_w times), then one
+// pass that interleaves the phases into dX.
+hipError_t backward_data_phases(const ConvGeom &g, DType dt, const void *dy, const void *w_r, const void *w_i,
+                                const void *w_j, const void *w_k, void *dx, void *wpack, void *stage,
+                                hipStream_t stream, bool sep)
+{
+    const size_t es = dt == DType::BF16 ? 2 : 4;
+    const int row = 4 * g.c_in;
+    PhaseMap pm;
+    int64_t off = 0;          // elements into the stage buffer
+    size_t wp_off = 0;        // bytes into the packed-weight buffer
+    for (int ry = 0; ry < g.s_h; ++ry)
+        for (int rx = 0; rx < g.s_w; ++rx) {
+            const int ph = ry * g.s_w + rx;
+            const AxisPhase ay = axis_phase(g.k_h, g.p_h, g.s_h, g.h, ry);
+            const AxisPhase ax = axis_phase(g.k_w, g.p_w, g.s_w, g.w, rx);
+            pm.off[ph] = off;
+            pm.hp[ph] = pm.wp[ph] = 0;
+            if (ay.size == 0 || ax.size == 0 || ay.taps == 0 || ax.taps == 0)
+                continue;  // no pixels, or no tap reaches them: zeros
+            ConvGeom t;
+            t.n = g.n;
+            t.c_in = g.c_out;
+            t.c_out = g.c_in;
+            t.k_h = ay.taps;
+            t.k_w = ax.taps;
+            t.s_h = t.s_w = 1;
+            t.d_h = t.d_w = 1;
+            t.p_h = ay.pad;
+            t.p_w = ax.pad;
+            t.h = g.h_out;
+            t.w = g.w_out;
+            t.h_out = ay.size;
+            t.w_out = ax.size;
+            const PackGeom pg = qconv2d_pack_geom(t.c_in, t.c_out, t.k_h, t.k_w, dt);
+            void *wp = static_cast<unsigned char *>(wpack) + wp_off;
+            hipError_t e = sep ? pack_weights<kPackSeparableGrad>(pg, t.c_in, t.c_out, t.k_h, t.k_w, dt, w_r, w_i,
+                                                                   w_j, w_k, wp, stream, ay.u0, ax.u0, g.s_h, g.s_w,
+                                                                   g.k_h, g.k_w)
+                               : pack_weights<kPackHamiltonGrad>(pg, t.c_in, t.c_out, t.k_h, t.k_w, dt, w_r, w_i,
+                                                                  w_j, w_k, wp, stream, ay.u0, ax.u0, g.s_h, g.s_w,
+                                                                  g.k_h, g.k_w);
+            if (e != hipSuccess)
+                return e;
+            e = qconv2d_run(qconv2d_plan(t, dt, sep ? ConvForm::SeparableGradData : ConvForm::Hamilton), pg, t, dt,
+                            dy, wp, nullptr, static_cast<unsigned char *>(stage) + size_t(off) * es, nullptr,
+                            nullptr, stream);
+            if (e != hipSuccess)
+                return e;
+            pm.hp[ph] = ay.size;
+            pm.wp[ph] = ax.size;
+            // the next phase starts on a 16-byte boundary
+            off += int64_t(g.n) * ay.size * ax.size * row;
+            off = (off * int64_t(es) + 15) / 16 * 16 / int64_t(es);
+            wp_off += pg.bytes;
+        }
+    const int vw = row % (dt == DType::BF16 ? 8 : 4) == 0 ? (dt == DType::BF16 ? 8 : 4) : 1;
+    const int64_t total = int64_t(g.n) * g.h * g.w * (row / vw);
+    const unsigned blocks = unsigned((total + 255) / 256);
+    if (dt == DType::BF16) {
+        if (vw == 8)
+            hipLaunchKernelGGL((qconv2d_grad_interleave<__bf16, 8>), dim3(blocks), dim3(256), 0, stream,
+                               (const __bf16 *)stage, (__bf16 *)dx, pm, g.h, g.w, g.s_h, g.s_w, row / vw, total);
+        else
+            hipLaunchKernelGGL((qconv2d_grad_interleave<__bf16, 1>), dim3(blocks), dim3(256), 0, stream,
+                               (const __bf16 *)stage, (__bf16 *)dx, pm, g.h, g.w, g.s_h, g.s_w, row, total);
+    } else {
+        if (vw == 4)
+            hipLaunchKernelGGL((qconv2d_grad_interleave<float, 4>), dim3(blocks), dim3(256), 0, stream,
+                               (const float *)stage, (float *)dx, pm, g.h, g.w, g.s_h, g.s_w, row / vw, total);
+        else
+            hipLaunchKernelGGL((qconv2d_grad_interleave<float, 1>), dim3(blocks), dim3(256), 0, stream,
+                               (const float *)stage, (float *)dx, pm, g.h, g.w, g.s_h, g.s_w, row, total);
+    }
+    return hipGetLastError();
+}
+}  // namespace
 
 hipError_t qconv2d_backward_data_run(const ConvGeom &g, DType dt, const void *dy, const void *w_r, const void *w_i,
                                      const void *w_j, const void *w_k, void *dx, void *wpack, void *stage,
@@ -1834,6 +1997,8 @@ hipError_t qconv2d_backward_data_run(const ConvGeom &g, DType dt, const void *dy
                                                          wpack, stream);
     if (e != hipSuccess)
         return e;
+    if ((g.s_h != 1 || g.s_w != 1) && g.d_h == 1 && g.d_w == 1 && g.s_h * g.s_w <= kMaxPhases)
+        return backward_data_phases(g, dt, dy, w_r, w_i, w_j, w_k, dx, wpack, stage, stream, sep);
     const void *z = dy;
     if (g.s_h != 1 || g.s_w != 1) {
         const int row = 4 * g.c_out;

@@ -32,6 +32,12 @@ SHAPES = [
     (1, 24, 40, 17, 19, 3, 2, 0, 1),     # stride 2, pad 0, ragged output
     (1, 72, 80, 9, 8, 3, 1, 1, 1),       # several channel tiles with tails
     (3, 8, 16, 7, 7, 5, 1, 2, 1),        # 5x5
+    # strided input gradients as one stride-1 convolution per output phase
+    (1, 8, 16, 11, 13, 1, 2, 0, 1),      # 1x1 stride 2: odd rows and columns get no tap
+    (2, 8, 8, 12, 12, 4, 2, 1, 1),       # even kernel
+    (1, 16, 8, 15, 14, 3, 3, 1, 1),      # stride 3
+    (1, 8, 16, 10, 10, 5, 2, 2, 1),      # 5x5 stride 2
+    (1, 8, 8, 9, 9, 3, 2, 1, 2),         # stride 2 with dilation 2: the zero-inserted gradient
 ]
 
 
