@@ -190,6 +190,16 @@ QUAN_API int quan_qconv2d_separable_forward_packed(const void *x, const void *pa
  *   mean, var     [4, c] fp32 device arrays receiving the batch statistics used
  *                 for normalisation.  Running statistics are the caller's.
  *   eps           > 0.
+ *
+ * Tensors of 16 MiB or more whose rows fit the registers and LDS of one
+ * work-group per compute unit (about 100 MB on MI355X) are normalised in
+ * one launch that reads x once; its work-groups exchange partial sums
+ * through device memory and wait for each other, so the launch needs every
+ * compute unit of the device at once.  If other work holds compute units
+ * for more than about a second meanwhile, the waits give up and the rows
+ * and statistics of the work-groups that gave up come back as NaN (never a
+ * hang).  Smaller or larger tensors run in three launches with no such
+ * wait.
  */
 QUAN_API int quan_iqbn_forward(const void *x, const float *gamma, const float *beta,
                                float eps, void *out, float *mean, float *var,

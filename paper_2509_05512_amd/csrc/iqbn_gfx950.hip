@@ -735,6 +735,11 @@ __global__ __launch_bounds__(kResThreads) void iqbn_resident(ResArgs a)
         }
     }
     ok = res_barrier(a.flags, G, target2) && ok;
+    if (!ok && mine && j == 0) {
+        // a wait gave up: this work-group's statistics are marked too
+        a.mean[col] = __builtin_nanf("");
+        a.var[col] = __builtin_nanf("");
+    }
 
     // ---- phase 3: normalise the held rows and write them
     if (!active)

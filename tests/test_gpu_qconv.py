@@ -167,3 +167,23 @@ def test_packed_path_equals_forward(dtype):
         got = quan.quan_qconv2d_forward_packed(xg, packed, tuple(wg[0].shape), bias=bg, stride=s, pad=1)
         torch.cuda.synchronize()
         assert torch.equal(got.cpu(), ref.cpu())
+
+
+def test_descriptor_unit_axis_takes_any_stride():
+    """An axis of extent 1 is never stepped: the library accepts any stride
+    for it, and the result is the one of the dense tensor."""
+    say("descriptor: extent-1 axis with an odd stride")
+    dev = torch.device("cuda:0")
+    g = torch.Generator().manual_seed(5)
+    x = quan.to_device_layout(torch.randn(1, 4, 8, 9, 7, generator=g).to(torch.bfloat16).to(dev))
+    w = [(torch.randn(8, 8, 3, 3, generator=g) * 0.1).to(torch.bfloat16).to(dev) for _ in range(4)]
+    x_odd = x.as_strided(x.shape, (12345,) + tuple(x.stride()[1:]))
+    y_ref = quan.quan_qconv2d_forward(x, *w, stride=1, pad=1)
+    y_odd = quan.quan_qconv2d_forward(x_odd, *w, stride=1, pad=1)
+    torch.cuda.synchronize()
+    assert torch.equal(y_ref.cpu(), y_odd.cpu())
+    gm, bt = torch.ones(4, 8, device=dev), torch.zeros(4, 8, device=dev)
+    o_ref, m_ref, v_ref = quan.quan_iqbn_forward(x, gm, bt)
+    o_odd, m_odd, v_odd = quan.quan_iqbn_forward(x_odd, gm, bt)
+    torch.cuda.synchronize()
+    assert torch.equal(o_ref.cpu(), o_odd.cpu()) and torch.equal(m_ref.cpu(), m_odd.cpu())
