@@ -725,11 +725,19 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
             return *reinterpret_cast<const u32x4 *>(d_lds + ic * 1024);
         }
     };
+    // The stores carry device scope (sc1): each line goes on to memory as it
+    // is written, instead of every dirty line of the L2 being written back
+    // by the release at the kernel's end (measured on MI355X: 3x3 stride-2
+    // layer 76-79 -> 71-74 us, 1x1 layer 30.6-31.6 -> 29.1 us, the
+    // 64 x 56 x 56 layer with IQBN behind it 271.7 -> 269 us; non-temporal
+    // stores were as fast alone but slowed the IQBN pass that reads them).
+    constexpr int kStoreDeviceScope = 16;
     auto drain_store = [&](int i, u32x4 v) {
         const unsigned off = (i < N_DRAIN && d_lane != 0x80000000u)
                                  ? d_lane + unsigned(i * (64 / OUT_CPR) * row_bytes)
                                  : 0x80000000u;
-        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), make_rsrc(d_base, d_bytes), off, 0, 0);
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), make_rsrc(d_base, d_bytes), off, 0,
+                                               kStoreDeviceScope);
     };
 
     // Step g (its stage in ring slot g % 4):
