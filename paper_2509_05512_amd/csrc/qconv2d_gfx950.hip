@@ -95,6 +95,21 @@ struct KArgs {
     int n_cblk;
     int cout_pad;
     int m_tiles, n_tiles;
+    // Work split of a persistent launch: the first full_tiles tiles are
+    // dealt to the work-groups (full_tiles = m_tiles * n_tiles unless
+    // tail_blocks is non-zero).  tail_blocks (all-components waves, Hamilton
+    // form, one N-tile, full_tiles a multiple of the grid of at least one
+    // tile per work-group, tail_blocks <= grid): the 32-pixel blocks past
+    // those tiles; each work-group claims one once its tiles are nearly
+    // done, so the first to get there take them, and its four waves then
+    // compute one output component of the block each.  claim (tail_blocks >
+    // 0): claim[0] the claim counter, zero when the launch starts and left
+    // zero by its last claimant; claim[1 + b] work-group b's mailbox, its
+    // ticket posted as (epoch << 16) | ticket; epoch: the launch's tag (16
+    // bits, not 0), which tells a post of this launch from an earlier one.
+    int full_tiles, tail_blocks;
+    unsigned *claim;
+    unsigned epoch;
     unsigned w_bytes;   // bytes of packed weights
     long long x_elems;  // elements of x (n * h * w * 4 * c_in)
     // Optional IQBN statistics of the output, per run of consecutive output
@@ -112,6 +127,10 @@ struct KArgs {
     const float *shift;
     int relu;
 };
+
+// Work-groups a launch with tail blocks may have (the claim buffer's
+// mailboxes).
+constexpr int kClaimMaxGroups = 2048;
 
 // XOR swizzle of the 16-byte chunk index within an LDS row of CPR chunks.
 // A ds_read_b128 from a wave reads one chunk from each of 16 consecutive rows
@@ -379,15 +398,19 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
     const int xcd = bid & 7, xslot = bid >> 3;
     const int cnt_x = (n_wg >> 3) + (xcd < (n_wg & 7) ? 1 : 0);
     const int before_x = xcd * (n_wg >> 3) + (xcd < (n_wg & 7) ? xcd : (n_wg & 7));
-    const int tiles = a.m_tiles * a.n_tiles;
+    const int tiles = a.full_tiles;
     const int x_lo = int((long long)tiles * before_x / n_wg);
     const int x_hi = int((long long)tiles * (before_x + cnt_x) / n_wg);
     const int n_mine = x_hi - x_lo > xslot ? (x_hi - x_lo - xslot + cnt_x - 1) / cnt_x : 0;
+    // (with tail blocks every work-group has at least one tile, so none
+    // leaves here and every one takes part in the claims)
     if (n_mine == 0)
         return;  // the whole work-group leaves: no barrier is pending
     auto tile_of = [&](int k) { return x_lo + xslot + k * cnt_x; };
+    const bool tails = ALLP && FORM == kFormHamilton && a.tail_blocks > 0;
+    // first pixel of tail block c
+    auto tail_m0 = [&](int c) { return ((BM / WTM) * a.full_tiles + c) * WTM; };
     const int S = a.stages;
-    const int total = n_mine * S;  // steps of this work-group, all tiles
 
     if (wave >= NCW) {
         // ================= producer waves =================
@@ -402,6 +425,7 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
         // Issue cursor: tile k (of this work-group), stage t of that tile at
         // tap (ky, kx) and channel block cblk, and the tile's DMA plan.
         int k = 0, ky = 0, kx = 0, cblk = 0;
+        int n_items = n_mine;  // items known so far: the tiles, then each claimed tail block
         const T *xt = nullptr;
         unsigned x_bytes = 0;  // bytes of x from xt on (capped at 2^31 - 1)
         int p_off[A_MINE], p_iy[A_MINE], p_ix[A_MINE], p_cl[A_MINE];
@@ -415,10 +439,10 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
         // relative to the first image of the tile.  Weight DMA j covers LDS
         // slots 64j..64j+63 of the stage's weights: slot = row * 2 +
         // physical chunk, row = kernel * BNC + o.
-        auto plan_tile = [&](int kt) {
-            const int tile = tile_of(kt);
-            const int m0 = (tile / a.n_tiles) * BM;
-            const int o0 = (tile % a.n_tiles) * BNC;
+        // (item kt past the tiles: tail block c)
+        auto plan_tile = [&](int kt, int c) {
+            const int m0 = kt < n_mine ? (tile_of(kt) / a.n_tiles) * BM : tail_m0(c);
+            const int o0 = kt < n_mine ? (tile_of(kt) % a.n_tiles) * BNC : 0;
             const int img0 = m0 / hw_out;
             xt = static_cast<const T *>(a.x) + img0 * (POINCARE ? 3LL * a.h * a.w : img_elems);
             const long long rest = (a.x_elems - img0 * img_elems) * ES;
@@ -468,9 +492,36 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
                 }
             }
         };
-        plan_tile(0);
+        // Tail block: when its cursor passes the end of its last tile,
+        // producer 0 claims one: lane 0 takes a ticket from the counter and
+        // posts it, with the launch tag, in the work-group's mailbox.  Both
+        // atomics return before the producer goes on, so the post is in
+        // memory before its next barrier; after that barrier both producers
+        // read it (at the top of their next iteration: resolve_claim) and
+        // the compute waves (after the last tile).  A ticket below
+        // tail_blocks is the block; the last of the grid's tickets (every
+        // work-group claims once) sets the counter back to zero for the next
+        // launch.  (System scope, as every access to the claim buffer.)  The
+        // claim comes at step n_mine * S - 1, issued in iteration n_mine * S
+        // - 4 >= 0 (the host takes tail blocks only then), so a barrier
+        // always lies between post and read.
+        unsigned *const mbox = a.claim + 1 + bid;
+        bool pending = false;  // cursor past the last tile, the claim not yet read
+        auto post_claim = [&]() {
+            unsigned c = 0;
+            if (lane == 0)
+                c = __hip_atomic_fetch_add(a.claim, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+            c = __builtin_amdgcn_readfirstlane(c);
+            unsigned posted = 0;
+            if (lane == 0)
+                posted = __hip_atomic_exchange(mbox, (a.epoch << 16) | c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+            asm volatile("" ::"v"(posted));  // wait for the exchange
+            if (c == unsigned(n_wg) - 1 && lane == 0)
+                __hip_atomic_exchange(a.claim, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        };
+        plan_tile(0, 0);
         // Issues the cursor's stage into ring slot g % NBUF and advances the
-        // cursor (to the next tile after its last stage).
+        // cursor (to the next item after its last stage).
         auto issue = [&](int g) {
             const int buf = g & (NBUF - 1);
             const int t = (ky * a.k_w + kx) * a.n_cblk + cblk;  // stage within the tile
@@ -493,7 +544,8 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
             for (int ii = 0; ii < A_MINE; ++ii) {
                 const int i = ii * NPROD + pr;
                 const bool inside = ((unsigned)(p_iy[ii] + dy) < (unsigned)a.h) &
-                                    ((unsigned)(p_ix[ii] + dx) < (unsigned)a.w) & (cbase < p_cl[ii]);
+                                    ((unsigned)(p_ix[ii] + dx) < (unsigned)a.w) & (cbase < p_cl[ii]) &
+                                    (k < n_mine || i < WTM / 8);
                 if constexpr (VEC) {
                     const unsigned off = inside ? unsigned(p_off[ii] + shift * ES) : 0x80000000u;
                     dma16(xt, x_bytes, off, 0u, a_base + buf * A_BYTES + i * 1024);
@@ -528,9 +580,16 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
                 cblk = 0;
                 if (++kx == a.k_w) {
                     kx = 0;
-                    if (++ky == a.k_h && ++k < n_mine) {
-                        ky = 0;
-                        plan_tile(k);
+                    if (++ky == a.k_h) {
+                        ++k;
+                        if (k < n_items) {
+                            ky = 0;
+                            plan_tile(k, 0);
+                        } else if (tails && k == n_mine) {
+                            if (pr == 0)
+                                post_claim();
+                            pending = true;
+                        }
                     }
                 }
             }
@@ -549,20 +608,37 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
                 wait_vmcnt<0>();
             }
         };
+        // steps of the items known so far (claims add to them as the
+        // cursor reaches the end of the tiles)
+        auto total = [&]() { return n_items * S; };
         // prologue: steps 0..2; step 0 lands before the first barrier
-        for (int g = 0; g < LOOKAHEAD && g < total; ++g)
+        for (int g = 0; g < LOOKAHEAD && g < total(); ++g)
             issue(g);
-        wait_landed(total - 1 < LOOKAHEAD - 1 ? total - 1 : LOOKAHEAD - 1);
+        wait_landed(total() - 1 < LOOKAHEAD - 1 ? total() - 1 : LOOKAHEAD - 1);
         __syncthreads();
         // Iteration g: step g+3 goes into the slot step g-1 left before the
         // barrier of step g-1; step g+1 lands before the barrier of step g,
         // after which the compute waves first read it.  Steps run on across
         // tiles, so the next tile's first stages arrive during this tile's
         // last steps and epilogue.
-        for (int g = 0; g < total; ++g) {
-            if (g + LOOKAHEAD < total)
+        // the claim posted before the last barrier: a block is item k
+        auto resolve_claim = [&]() {
+            const unsigned v = __builtin_amdgcn_readfirstlane(
+                __hip_atomic_load(mbox, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM));
+            const unsigned c = v & 0xffffu;
+            pending = false;
+            if ((v >> 16) == a.epoch && c < unsigned(a.tail_blocks)) {
+                ++n_items;
+                ky = 0;
+                plan_tile(k, int(c));
+            }
+        };
+        for (int g = 0; g < total(); ++g) {
+            if (pending)
+                resolve_claim();
+            if (g + LOOKAHEAD < total())
                 issue(g + LOOKAHEAD);
-            wait_landed(g + 3 < total ? 2 : (g + 2 < total ? 1 : 0));
+            wait_landed(g + 3 < total() ? 2 : (g + 2 < total() ? 1 : 0));
             __syncthreads();
         }
         return;
@@ -827,17 +903,64 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
         __builtin_amdgcn_sched_barrier(0);
         slot = ns;
     };
+    // Tail block (ALLP, Hamilton form): the work-group's 32 pixels sit in
+    // rows 0..31 of the stage and wave wm computes output component p = wm
+    // alone, block (p, q = p xor m) of each kernel group m: activation set
+    // entry m holds input component p xor m, and t_flip[m] the sign of eq. 6
+    // for that block (a quarter of a tile's MFMAs per wave).
+    auto rd_act_tail = [&](unsigned off, u32x4 (&dst)[4][MB]) {
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+            const int q = wm ^ m;
+            dst[m][0] = *reinterpret_cast<const u32x4 *>(a_lds + off + l32 * 128 +
+                                                        (((2 * q + khalf) ^ swz<8>(l32)) * 16));
+        }
+    };
+    auto step_tail = [&](const u32x4 (&cur)[4][MB], u32x4 (&nxt)[4][MB]) {
+        const int ns = (slot + 1) & (NBUF - 1);
+        const unsigned cb = unsigned(slot) * B_BYTES;
+        const unsigned na = unsigned(ns) * A_BYTES, nb_ = unsigned(ns) * B_BYTES;
+        auto tail_group = [&](int m, const u32x4 (&w)[NB]) {
+            const unsigned fl = ((kHamiltonNeg >> (4 * wm + (wm ^ m))) & 1u) ? Elem<T>::sign : 0u;
+            const u32x4 x = cur[m][0] ^ fl;
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+                mfma_step<T>(acc[0][nb][0], w[nb], x);
+        };
+        u32x4 dv0;
+        if constexpr (DEFER)
+            dv0 = drain_read(d_next);
+        __builtin_amdgcn_sched_barrier(0);
+        rd_ker(cb, 2, wk[2]);
+        tail_group(0, wk[0]);
+        rd_ker(cb, 3, wk[3]);
+        tail_group(1, wk[1]);
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (DEFER) {
+            drain_store(d_next, dv0);
+            d_next = d_next < N_DRAIN ? d_next + 1 : N_DRAIN;
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        __syncthreads();
+        rd_act_tail(na, nxt);
+        rd_ker(nb_, 0, wk[0]);
+        tail_group(2, wk[2]);
+        rd_ker(nb_, 1, wk[1]);
+        tail_group(3, wk[3]);
+        __builtin_amdgcn_sched_barrier(0);
+        slot = ns;
+    };
     // One tile: its S steps, two per iteration (activation sets alternate);
     // an odd last step leaves the next stage's activations in xa1, moved
     // back to xa0.
-    auto run_tile_allp = [&]() {
+    auto run_tile_allp = [&](auto stepf) {
         int t = 0;
         for (; t + 2 <= S; t += 2) {
-            step_allp(xa0, xa1);
-            step_allp(xa1, xa0);
+            stepf(xa0, xa1);
+            stepf(xa1, xa0);
         }
         if (t < S) {
-            step_allp(xa0, xa1);
+            stepf(xa0, xa1);
 #pragma unroll
             for (int q = 0; q < 4; ++q)
 #pragma unroll
@@ -1017,7 +1140,8 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
     // The same statistics for an ALLP wave's region: 32 pixels (from mw on)
     // x four components, each component's BNC channels read back and reduced
     // as above; one partial per 32-pixel sub-tile (index mw / 32) and column.
-    auto tile_stats_allp = [&](const auto *w_lds, int mw, int o0) {
+    // p_only >= 0 (a tail block): that component alone.
+    auto tile_stats_allp = [&](const auto *w_lds, int mw, int o0, int p_only) {
         static_assert(ES == 2 && (BNC == 64 || BNC == 32), "statistics read-back geometry");
         typedef short s16x4 __attribute__((ext_vector_type(4)));
         typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -1040,6 +1164,8 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
         const size_t cols = size_t(4) * a.c_out;
 #pragma unroll
         for (int p = 0; p < 4; ++p) {
+            if (p_only >= 0 && p != p_only)
+                continue;
             // physical chunk = p * SWZ + (logical ^ (pixel % SWZ)); pixel =
             // p_lane + PPR * i, whose two parts share no bit below SWZ
             auto piece = [&](int xr) {
@@ -1112,6 +1238,112 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
         return y;
     };
     const bool vec_out = (a.c_out & 3) == 0;
+    // ALLP deferred epilogue: parks the wave's 32 pixels from mw on in its
+    // LDS region w_lds (row l%32, component p, chunk nb*4 + g of its
+    // channels, swizzled, half l/32 of it) with the bias added (or the
+    // folded map and ReLU applied), rounded to T, takes the statistics and
+    // sets up the drain.  TAIL: accumulator set 0 is output component wm
+    // alone, parked in place of that component; the region's other chunks
+    // keep stale values, which are never read for statistics nor stored.
+    auto park_allp_at = [&](unsigned char *w_lds, int mw, int o0, auto tailc) {
+        constexpr bool TAIL = decltype(tailc)::value;
+        auto park = [&](auto affine) {
+            constexpr bool AFFINE = decltype(affine)::value;
+#pragma unroll
+            for (int pb = 0; pb < (TAIL ? 1 : 4) * NB; ++pb) {
+                // one 32-channel block of one component; its per-column map
+                // is loaded before any of it is used (one memory latency per
+                // block)
+                const int pa = pb / NB, nb = pb % NB;
+                const int p = TAIL ? wm : pa;
+                float sc[4][4], sh[4][4];
+                if constexpr (AFFINE) {
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) {
+                        const int oc = nb * 32 + 8 * g + 4 * khalf;
+                        const bool in4 = o0 + oc < a.c_out;
+                        const int col = in4 ? p * a.c_out + o0 + oc : 0;
+                        if constexpr (EPI == kEpiFold) {
+                            const f32x4 s4 = *reinterpret_cast<const f32x4 *>(a.scale + col);
+                            const f32x4 h4 = *reinterpret_cast<const f32x4 *>(a.shift + col);
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) {
+                                sc[g][e] = in4 ? s4[e] : 0.0f;
+                                sh[g][e] = in4 ? h4[e] : 0.0f;
+                            }
+                        } else {
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) {
+                                sc[g][e] = 1.0f;
+                                const float b = float(bias[col + e]);
+                                sh[g][e] = in4 ? b : 0.0f;
+                            }
+                        }
+                    }
+                }
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    T v[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        if constexpr (AFFINE)
+                            v[e] = T(epi(acc[pa][nb][0][4 * g + e], sc[g][e], sh[g][e]));
+                        else
+                            v[e] = T(acc[pa][nb][0][4 * g + e]);
+                    }
+                    unsigned char *dst =
+                        w_lds + l32 * OUT_ROW + ((p * SWZ + ((nb * 4 + g) ^ (l32 % SWZ))) * 16) + khalf * 8;
+                    uint2 pk;
+                    __builtin_memcpy(&pk, v, 8);
+                    *reinterpret_cast<uint2 *>(dst) = pk;
+                }
+            }
+        };
+        if (EPI == kEpiFold || bias != nullptr)
+            park(std::true_type{});
+        else
+            park(std::false_type{});
+        if constexpr (EPI == kEpiStats)
+            tile_stats_allp(w_lds, mw, o0, TAIL ? wm : -1);
+        const long long rows_left = (long long)(a.m - mw) * row_bytes;
+        d_base = out + (size_t)mw * 4 * a.c_out;
+        d_bytes = rows_left <= 0 ? 0u : rows_left < 0x7fffffffLL ? unsigned(rows_left) : 0x7fffffffu;
+        const int ch = o0 + d_k * CPC;  // first channel of the lane's chunk
+        d_lane = (ch < a.c_out && (!TAIL || d_p == wm)) ? unsigned(d_pix * row_bytes + (d_p * a.c_out + ch) * ES)
+                                                        : 0x80000000u;
+        d_next = 0;
+    };
+    // ---- epilogue: bias, round, channels-last store ----
+    // Accumulator register 4*g + e of lane l holds output channel row
+    // 8*g + 4*(l/32) + e of the 32x32 block and pixel column l%32.
+    // Writes the four channels o..o+3 of component p at pixel m.
+    auto store4 = [&](int m, int p, int o, const float *y) {
+        float sc[4], sh[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            col_affine(p * a.c_out + o + e, o + e < a.c_out, sc[e], sh[e]);
+        T *dst = out + ((size_t)m * 4 * a.c_out + p * a.c_out + o);
+        T v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            v[e] = T(epi(y[e], sc[e], sh[e]));
+        if (vec_out) {
+            if constexpr (sizeof(T) == 2) {
+                uint2 pk;
+                __builtin_memcpy(&pk, v, 8);
+                *reinterpret_cast<uint2 *>(dst) = pk;
+            } else {
+                float4 pk;
+                __builtin_memcpy(&pk, v, 16);
+                *reinterpret_cast<float4 *>(dst) = pk;
+            }
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (o + e < a.c_out)
+                    dst[e] = v[e];
+        }
+    };
     int ph = 0;  // ring slot of the current tile's first stage
     for (int kt = 0; kt < n_mine; ++kt) {
         const int tile = tile_of(kt);
@@ -1127,7 +1359,7 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
                     for (int e = 0; e < 16; ++e)
                         acc[qs][nb][mb][e] = 0.0f;
         if constexpr (ALLP) {
-            run_tile_allp();
+            run_tile_allp(step_allp);
         } else {
             if (ph == 0)
                 run_tile(P0{});
@@ -1150,73 +1382,7 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
             // ReLU applied), rounded to T
             unsigned char *const w_lds = o_lds + region * OUT_WAVE;
             if constexpr (ALLP) {
-                // the wave's 32 pixels, all four components: row l%32,
-                // component p, chunk nb*4 + g of its channels (swizzled),
-                // half l/32 of it
-                auto park_allp = [&](auto affine) {
-                    constexpr bool AFFINE = decltype(affine)::value;
-#pragma unroll
-                    for (int pb = 0; pb < 4 * NB; ++pb) {
-                        // one 32-channel block of one component; its
-                        // per-column map is loaded before any of it is used
-                        // (one memory latency per block)
-                        const int p = pb / NB, nb = pb % NB;
-                        float sc[4][4], sh[4][4];
-                        if constexpr (AFFINE) {
-#pragma unroll
-                                for (int g = 0; g < 4; ++g) {
-                                    const int oc = nb * 32 + 8 * g + 4 * khalf;
-                                    const bool in4 = o0 + oc < a.c_out;
-                                    const int col = in4 ? p * a.c_out + o0 + oc : 0;
-                                    if constexpr (EPI == kEpiFold) {
-                                        const f32x4 s4 = *reinterpret_cast<const f32x4 *>(a.scale + col);
-                                        const f32x4 h4 = *reinterpret_cast<const f32x4 *>(a.shift + col);
-#pragma unroll
-                                        for (int e = 0; e < 4; ++e) {
-                                            sc[g][e] = in4 ? s4[e] : 0.0f;
-                                            sh[g][e] = in4 ? h4[e] : 0.0f;
-                                        }
-                                    } else {
-#pragma unroll
-                                        for (int e = 0; e < 4; ++e) {
-                                            sc[g][e] = 1.0f;
-                                            const float b = float(bias[col + e]);
-                                            sh[g][e] = in4 ? b : 0.0f;
-                                        }
-                                    }
-                                }
-                        }
-#pragma unroll
-                            for (int g = 0; g < 4; ++g) {
-                                T v[4];
-#pragma unroll
-                                for (int e = 0; e < 4; ++e) {
-                                    if constexpr (AFFINE)
-                                        v[e] = T(epi(acc[p][nb][0][4 * g + e], sc[g][e], sh[g][e]));
-                                    else
-                                        v[e] = T(acc[p][nb][0][4 * g + e]);
-                                }
-                                unsigned char *dst = w_lds + l32 * OUT_ROW +
-                                                     ((p * SWZ + ((nb * 4 + g) ^ (l32 % SWZ))) * 16) + khalf * 8;
-                                uint2 pk;
-                                __builtin_memcpy(&pk, v, 8);
-                                *reinterpret_cast<uint2 *>(dst) = pk;
-                            }
-                    }
-                };
-                if (EPI == kEpiFold || bias != nullptr)
-                    park_allp(std::true_type{});
-                else
-                    park_allp(std::false_type{});
-                const int mw = m0 + wm * WTM;  // the wave's first pixel
-                if constexpr (EPI == kEpiStats)
-                    tile_stats_allp(w_lds, mw, o0);
-                const long long rows_left = (long long)(a.m - mw) * row_bytes;
-                d_base = out + (size_t)mw * 4 * a.c_out;
-                d_bytes = rows_left <= 0 ? 0u : rows_left < 0x7fffffffLL ? unsigned(rows_left) : 0x7fffffffu;
-                const int ch = o0 + d_k * CPC;  // first channel of the lane's chunk
-                d_lane = ch < a.c_out ? unsigned(d_pix * row_bytes + (d_p * a.c_out + ch) * ES) : 0x80000000u;
-                d_next = 0;
+                park_allp_at(w_lds, m0 + wm * WTM, o0, std::false_type{});
                 continue;
             }
             // AFFINE: a per-column map to apply (bias or the folded IQBN);
@@ -1299,37 +1465,6 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
             continue;
         }
 
-        // ---- epilogue: bias, round, channels-last store ----
-        // Accumulator register 4*g + e of lane l holds output channel row
-        // 8*g + 4*(l/32) + e of the 32x32 block and pixel column l%32.
-        // Writes the four channels o..o+3 of component p at pixel m.
-        auto store4 = [&](int m, int p, int o, const float *y) {
-            float sc[4], sh[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-                col_affine(p * a.c_out + o + e, o + e < a.c_out, sc[e], sh[e]);
-            T *dst = out + ((size_t)m * 4 * a.c_out + p * a.c_out + o);
-            T v[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-                v[e] = T(epi(y[e], sc[e], sh[e]));
-            if (vec_out) {
-                if constexpr (sizeof(T) == 2) {
-                    uint2 pk;
-                    __builtin_memcpy(&pk, v, 8);
-                    *reinterpret_cast<uint2 *>(dst) = pk;
-                } else {
-                    float4 pk;
-                    __builtin_memcpy(&pk, v, 16);
-                    *reinterpret_cast<float4 *>(dst) = pk;
-                }
-            } else {
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    if (o + e < a.c_out)
-                        dst[e] = v[e];
-            }
-        };
         if constexpr (SEP && sizeof(T) == 2 && NB == 2) {
             if (vec_out && (a.c_out & 7) == 0) {
                 // Separable bf16, 64-channel tile, whole 8-channel groups:
@@ -1448,6 +1583,50 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
                             y[e] = acc[0][nb][mb][4 * g + e];
                         store4(m, p, o, y);
                     }
+                }
+            }
+        }
+    }
+    // tail block: wave wm computes output component wm of the block's 32
+    // pixels (all four waves read the same activation rows).  The claim was
+    // posted before the producers' barrier of step n_mine * S - 4 and is
+    // read here after the barrier of step n_mine * S - 1.
+    if constexpr (ALLP && FORM == kFormHamilton) {
+        if (tails) {
+            const unsigned v = __builtin_amdgcn_readfirstlane(
+                __hip_atomic_load(a.claim + 1 + bid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM));
+            const unsigned c = v & 0xffffu;
+            // (a post of another launch cannot be read here; were it, the
+            // block would be left undone rather than the barriers broken)
+            if ((v >> 16) == a.epoch && c < unsigned(a.tail_blocks)) {
+                const int m0 = tail_m0(int(c));
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e)
+                        acc[0][nb][0][e] = 0.0f;
+                // its first stage was read as a tile's
+                rd_act_tail(unsigned(slot) * A_BYTES, xa0);
+                run_tile_allp(step_tail);
+                if (defer) {
+                    for (; d_next < N_DRAIN; ++d_next)
+                        drain_store(d_next, drain_read(d_next));
+                    park_allp_at(o_lds + region * OUT_WAVE, m0, 0, std::true_type{});
+                } else {
+                    const int m = m0 + l32;
+#pragma unroll
+                    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                        for (int g = 0; g < 4; ++g) {
+                            const int o = nb * 32 + 8 * g + 4 * khalf;
+                            if (o >= a.c_out || m >= a.m)
+                                continue;
+                            float y[4];
+#pragma unroll
+                            for (int e = 0; e < 4; ++e)
+                                y[e] = acc[0][nb][0][4 * g + e];
+                            store4(m, wm, o, y);
+                        }
                 }
             }
         }
@@ -1600,6 +1779,7 @@ struct KernelEntry {
     // the deferred epilogue).
     const void *fn[3][4];
     const char *name;
+    bool allp;   // all-components waves in the Hamilton form: takes tail blocks
 };
 
 #define QCONV_DEFER(NB, WM, WN, SEP) (!(SEP) && (WM) == 1 && (WN) == 4 && 8 * (NB) * (WN) >= 32)
@@ -1675,7 +1855,7 @@ constexpr const void *fold_fn()
              {(const void *)&qconv2d_igemm<__bf16, 1, NB, 4, 1, true, kEpiFold, false, false, true>,    \
               (const void *)&qconv2d_igemm<__bf16, 1, NB, 4, 1, false, kEpiFold, false, false, true>,   \
               nullptr, nullptr}},                                                                      \
-            "bf16_allp_nb" #NB                                                                         \
+            "bf16_allp_nb" #NB, true                                                                   \
     }
 
 // The input gradient of the separable form (eqs. 8-10) on the Hamilton
@@ -2050,9 +2230,14 @@ bool qconv2d_writes_stats(const ConvPlan &plan, const ConvGeom &g, DType dt)
     return k.defer && g.c_out % (dt == DType::BF16 ? 8 : 4) == 0;
 }
 
+size_t qconv2d_claim_bytes()
+{
+    return sizeof(unsigned) * (1 + size_t(kClaimMaxGroups));
+}
+
 hipError_t qconv2d_run(const ConvPlan &plan, const PackGeom &pg, const ConvGeom &g, DType dt,
                        const void *x, const void *wpack, const void *bias, void *out,
-                       float *stats, const ConvFold *fold, hipStream_t stream, bool poincare)
+                       float *stats, const ConvFold *fold, hipStream_t stream, bool poincare, const ConvClaim *claim)
 {
     if (plan.id < 0 || plan.id >= kNumKernels)
         return hipErrorInvalidValue;
@@ -2110,6 +2295,27 @@ hipError_t qconv2d_run(const ConvPlan &plan, const PackGeom &pg, const ConvGeom 
     const long long tiles = (long long)plan.m_tiles * plan.n_tiles;
     const long long slots = (long long)device_cus() * resident_wgs(fn, k.threads);
     const unsigned blocks = unsigned(tiles < slots ? tiles : slots);
+    // With all-components waves and one N-tile, a last round that would
+    // leave work-groups idle goes out as 32-pixel tail blocks instead:
+    // every work-group takes `full` tiles, then claims one tail block (a
+    // quarter of a tile's MFMAs) while any are left, so the work-groups that
+    // finish first take them.
+    a.full_tiles = int(tiles);
+    a.tail_blocks = 0;
+    a.claim = claim != nullptr ? claim->buf : nullptr;
+    // 1..65535: never the zero of a mailbox that was never written
+    a.epoch = claim != nullptr ? claim->epoch % 0xffffu + 1u : 0u;
+    if (k.allp && plan.n_tiles == 1 && a.claim != nullptr && blocks <= unsigned(kClaimMaxGroups)) {
+        const long long blk = (a.m + 31) / 32;
+        const long long full = blk / (4LL * blocks);
+        const long long rest = blk - full * 4 * blocks;
+        // (at least 4 steps of tiles per work-group: the first claim then
+        // falls after the producers' first barrier)
+        if (full >= 1 && rest > 0 && rest <= blocks && full * a.stages >= 4) {
+            a.full_tiles = int(full * blocks);
+            a.tail_blocks = int(rest);
+        }
+    }
     return hipLaunchKernel(fn, dim3(blocks), dim3(k.threads), args, 0, stream);
 }
 

@@ -41,6 +41,7 @@ int fail_hip(hipError_t e, const char *what)
 struct Workspace {
     void *ptr = nullptr;
     size_t bytes = 0;
+    unsigned uses = 0;  // calls that took it (the claim buffer's launch tags)
 };
 
 std::mutex g_ws_mutex;
@@ -53,12 +54,13 @@ enum Purpose {
     kGradPack = 3,
     kGradStage = 4,
     kWgrad = 5,
-    kIqbnBarrier = 6  // the one-launch IQBN's grid-barrier flags: zeroed once, when allocated
+    kIqbnBarrier = 6,  // the one-launch IQBN's grid-barrier flags: zeroed once, when allocated
+    kConvClaim = 7     // the convolution's tail-block claims: zeroed once, when allocated
 };
 
 // Returns a device buffer of at least `bytes` for (current device, stream,
 // purpose).  Growing it first waits for the device to finish with the old one.
-int workspace(void *stream, Purpose purpose, size_t bytes, void **out)
+int workspace(void *stream, Purpose purpose, size_t bytes, void **out, unsigned *uses = nullptr)
 {
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
@@ -85,13 +87,15 @@ int workspace(void *stream, Purpose purpose, size_t bytes, void **out)
             return fail(QUAN_ERR_NOMEM, "hipMalloc(%zu) for workspace: %s", want, hipGetErrorString(e));
         }
         ws.bytes = want;
-        if (purpose == kIqbnBarrier) {
+        if (purpose == kIqbnBarrier || purpose == kConvClaim) {
             e = hipMemsetAsync(ws.ptr, 0, want, static_cast<hipStream_t>(stream));
             if (e != hipSuccess)
-                return fail_hip(e, "hipMemsetAsync (barrier flags)");
+                return fail_hip(e, "hipMemsetAsync (barrier flags, claim counter)");
         }
     }
     *out = ws.ptr;
+    if (uses != nullptr)
+        *uses = ws.uses++;
     return QUAN_OK;
 }
 
@@ -102,6 +106,17 @@ int iqbn_flags(void *stream, unsigned **out)
     if (int rc = workspace(stream, kIqbnBarrier, quan::iqbn_barrier_bytes(), &p))
         return rc;
     *out = static_cast<unsigned *>(p);
+    return QUAN_OK;
+}
+
+// The claim counter and mailboxes of the convolution's tail blocks on this
+// (device, stream): every launch leaves the counter zero.
+int conv_claim(void *stream, quan::ConvClaim *out)
+{
+    void *p = nullptr;
+    if (int rc = workspace(stream, kConvClaim, quan::qconv2d_claim_bytes(), &p, &out->epoch))
+        return rc;
+    out->buf = static_cast<unsigned *>(p);
     return QUAN_OK;
 }
 
@@ -304,8 +319,11 @@ int conv_packed(const char *name, bool sep, const void *x, const void *packed, c
     const quan::DType dt = to_dt(dtype);
     const quan::PackGeom pg = quan::qconv2d_pack_geom(c_in, c_out, k_h, k_w, dt);
     const quan::ConvPlan plan = quan::qconv2d_plan(g, dt, sep ? quan::ConvForm::Separable : quan::ConvForm::Hamilton);
+    quan::ConvClaim claim{};
+    if (int rc = conv_claim(stream, &claim))
+        return rc;
     hipError_t e = quan::qconv2d_run(plan, pg, g, dt, x, packed, bias, out, nullptr, nullptr,
-                                     static_cast<hipStream_t>(stream));
+                                     static_cast<hipStream_t>(stream), false, &claim);
     if (e != hipSuccess)
         return fail_hip(e, "qconv2d launch");
     return QUAN_OK;
@@ -348,8 +366,11 @@ int conv_unpacked(const char *name, bool sep, const void *x, const void *w_r, co
                                               wpack, s);
     if (e != hipSuccess)
         return fail_hip(e, "qconv2d weight pack launch");
+    quan::ConvClaim claim{};
+    if (int rc = conv_claim(stream, &claim))
+        return rc;
     e = quan::qconv2d_run(quan::qconv2d_plan(g, dt, sep ? quan::ConvForm::Separable : quan::ConvForm::Hamilton), pg,
-                          g, dt, x, wpack, bias, out, nullptr, nullptr, s);
+                          g, dt, x, wpack, bias, out, nullptr, nullptr, s, false, &claim);
     if (e != hipSuccess)
         return fail_hip(e, "qconv2d launch");
     return QUAN_OK;
@@ -490,6 +511,9 @@ QUAN_API int quan_qconv2d_iqbn_forward(const void *x, const void *packed, const 
     const int64_t pixels = g.m();
     hipStream_t s = static_cast<hipStream_t>(stream);
     void *work = nullptr;
+    quan::ConvClaim claim{};
+    if (int rc = conv_claim(stream, &claim))
+        return rc;
     hipError_t e;
     // AUTO: a one-launch IQBN pass after the plain convolution where the
     // tensor takes it (it reads out once, like the epilogue's normalisation,
@@ -500,7 +524,8 @@ QUAN_API int quan_qconv2d_iqbn_forward(const void *x, const void *packed, const 
         // statistics gathered in the convolution's epilogue
         if (int rc = workspace(stream, kIqbnPartials, quan::iqbn_tile_stats_bytes(plan.stat_tiles, c_out), &work))
             return rc;
-        e = quan::qconv2d_run(plan, pg, g, dt, x, packed, bias, out, static_cast<float *>(work), nullptr, s);
+        e = quan::qconv2d_run(plan, pg, g, dt, x, packed, bias, out, static_cast<float *>(work), nullptr, s, false,
+                              &claim);
         if (e != hipSuccess)
             return fail_hip(e, "qconv2d launch");
         e = quan::iqbn_from_tiles_run(static_cast<const float *>(work), plan.stat_tiles, plan.stat_rows, gamma,
@@ -511,7 +536,7 @@ QUAN_API int quan_qconv2d_iqbn_forward(const void *x, const void *packed, const 
         unsigned *flags = nullptr;
         if (int rc = iqbn_flags(stream, &flags))
             return rc;
-        e = quan::qconv2d_run(plan, pg, g, dt, x, packed, bias, out, nullptr, nullptr, s);
+        e = quan::qconv2d_run(plan, pg, g, dt, x, packed, bias, out, nullptr, nullptr, s, false, &claim);
         if (e != hipSuccess)
             return fail_hip(e, "qconv2d launch");
         e = quan::iqbn_run(out, gamma, beta, eps, relu != 0, out, mean, var, pixels, c_out, dt, work, flags, s);
@@ -568,8 +593,11 @@ QUAN_API int quan_qconv2d_iqbn_inference(const void *x, const void *packed, cons
     if (e != hipSuccess)
         return fail_hip(e, "iqbn fold launch");
     const quan::ConvFold fold{scale, shift, relu != 0};
+    quan::ConvClaim claim{};
+    if (int rc = conv_claim(stream, &claim))
+        return rc;
     e = quan::qconv2d_run(quan::qconv2d_plan(g, dt, quan::ConvForm::Hamilton), pg, g, dt, x, packed, bias, out,
-                          nullptr, &fold, s);
+                          nullptr, &fold, s, false, &claim);
     if (e != hipSuccess)
         return fail_hip(e, "qconv2d launch");
     return QUAN_OK;
@@ -602,9 +630,13 @@ QUAN_API int quan_qconv2d_poincare_forward(const void *rgb, const void *packed, 
     // the stem kernel where it takes the layer, else the implicit-GEMM
     // kernel with the map in its loads
     hipError_t e = quan::qconv2d_stem_run(pg, g, dt, rgb, packed, bias, out, static_cast<hipStream_t>(stream));
-    if (e == hipErrorNotSupported)
+    if (e == hipErrorNotSupported) {
+        quan::ConvClaim claim{};
+        if (int rc = conv_claim(stream, &claim))
+            return rc;
         e = quan::qconv2d_run(quan::qconv2d_plan(g, dt, quan::ConvForm::Hamilton), pg, g, dt, rgb, packed, bias, out,
-                              nullptr, nullptr, static_cast<hipStream_t>(stream), true);
+                              nullptr, nullptr, static_cast<hipStream_t>(stream), true, &claim);
+    }
     if (e != hipSuccess)
         return fail_hip(e, "qconv2d_poincare launch");
     return QUAN_OK;

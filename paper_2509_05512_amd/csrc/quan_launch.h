@@ -81,9 +81,23 @@ struct ConvFold {
 // planes [n][3][h][w] of the input images, mapped to quaternions by eq. 4
 // as the convolution loads them.
 bool qconv2d_writes_stats(const ConvPlan &plan, const ConvGeom &g, DType dt);
+//
+// `claim` (optional): buf, qconv2d_claim_bytes() of device memory, zero
+// before the first launch that uses it, which every launch leaves zero
+// again (the launches that use one buffer must not overlap: one buffer per
+// stream); epoch, a tag that differs between consecutive launches on the
+// buffer.  With it a layer whose last round of tiles would leave
+// work-groups idle ends in 32-pixel tail blocks that the work-groups claim
+// as they finish; NULL: whole tiles only.
+struct ConvClaim {
+    unsigned *buf;
+    unsigned epoch;
+};
 hipError_t qconv2d_run(const ConvPlan &plan, const PackGeom &pg, const ConvGeom &g, DType dt,
                        const void *x, const void *wpack, const void *bias, void *out,
-                       float *stats, const ConvFold *fold, hipStream_t stream, bool poincare = false);
+                       float *stats, const ConvFold *fold, hipStream_t stream, bool poincare = false,
+                       const ConvClaim *claim = nullptr);
+size_t qconv2d_claim_bytes();
 
 // The stem layer (g.c_in == 1, bf16) as its own kernel: rgb is the colour
 // planes [n][3][h][w], mapped to quaternions by eq. 4 as they are loaded;
