@@ -341,6 +341,15 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
     constexpr int PER_STAGE = (A_INSTR + NPROD - 1) / NPROD + (B_INSTR + NPROD - 1) / NPROD;
     constexpr int LOOKAHEAD = 3;                // stages issued ahead of the one being read
     constexpr int N_MFMA = MB * NB * (ES == 2 ? 1 : 4);  // MFMA instructions per k-step
+    // Tail blocks of the 64-channel DMA tile (two producers) carry two
+    // K-blocks per ring slot: a tail stage fills only rows 0..31 of the slot's
+    // activation region, so K-block t's activations go to rows 0..31, K-block
+    // t+1's to rows 32..63 and K-block t+1's weights (laid out as in the
+    // weight region) to the region's upper half, which the A instructions
+    // of rows 64..127 load instead.  A producer issues as many instructions
+    // per step as for a tile, and a tail block takes ceil(S / 2) steps.
+    constexpr bool TAIL2 = ALLP && FORM == kFormHamilton && VEC && !POINCARE && NPROD == 2 &&
+                           A_INSTR == 2 * B_INSTR && A_BYTES == 2 * B_BYTES;
     constexpr bool P_UNIFORM = BNC >= 32;       // a 32-wide N block lies in one output component
     static_assert(CPQ == 2 && CS * 4 * ES == 128, "stage row is 128 bytes");
     static_assert(BNC % 16 == 0 && kPackCoutAlign % BNC == 0 && B_BYTES % 1024 == 0, "tile geometry");
@@ -411,6 +420,7 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
     // first pixel of tail block c
     auto tail_m0 = [&](int c) { return ((BM / WTM) * a.full_tiles + c) * WTM; };
     const int S = a.stages;
+    const int ST = TAIL2 ? (S + 1) / 2 : S;  // steps of a tail block
 
     if (wave >= NCW) {
         // ================= producer waves =================
@@ -454,7 +464,9 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
                 const int lc = (lane & 7) ^ swz<8>(row);
                 // PAIR: chunks 0-3 are component 2*pair, 4-7 component 2*pair+1
                 const int comp = PAIR ? lc / 4 : lc / CPQ, cin = PAIR ? (lc % 4) * EPC : (lc % CPQ) * EPC;
-                const int m = m0 + row;
+                // (TAIL2 tail block: rows 32..63 hold the block's rows 0..31
+                // again, for the second K-block; the same swizzle)
+                const int m = m0 + ((TAIL2 && kt >= n_mine) ? 8 * (i & 3) + (lane >> 3) : row);
                 p_cl[ii] = a.c_in - cin;  // channels of this chunk left before block 0
                 p_comp[ii] = comp;
                 if (m < a.m) {
@@ -522,8 +534,88 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
         plan_tile(0, 0);
         // Issues the cursor's stage into ring slot g % NBUF and advances the
         // cursor (to the next item after its last stage).
+        // The cursor one K-block on; past an item's last one, to the next
+        // item (or, past the last tile, the claim of a tail block).
+        auto advance = [&]() {
+            if (++cblk == a.n_cblk) {
+                cblk = 0;
+                if (++kx == a.k_w) {
+                    kx = 0;
+                    if (++ky == a.k_h) {
+                        ++k;
+                        if (k < n_items) {
+                            ky = 0;
+                            plan_tile(k, 0);
+                        } else if (tails && k == n_mine) {
+                            if (pr == 0)
+                                post_claim();
+                            pending = true;
+                        }
+                    }
+                }
+            }
+        };
+        // TAIL2 tail step: K-blocks t and t + 1 (the second past the last
+        // K-block on an odd stage count: its loads land as zeros, unread).
+        auto issue_tail2 = [&](int buf) {
+            const int t = (ky * a.k_w + kx) * a.n_cblk + cblk;
+            const bool two = t + 1 < S;
+            int cb2 = cblk + 1, kx2 = kx, ky2 = ky;
+            if (cb2 == a.n_cblk) {
+                cb2 = 0;
+                if (++kx2 == a.k_w) {
+                    kx2 = 0;
+                    ++ky2;
+                }
+            }
+#pragma unroll
+            for (int jj = 0; jj < B_MINE; ++jj)
+                dma16(a.wpack, a.w_bytes, p_woff[jj], unsigned(t) * w_stage_bytes,
+                      b_base + buf * B_BYTES + (jj * NPROD + pr) * 1024);
+            const int dy = ky * a.d_h, dx = kx * a.d_w, cbase = cblk * CS;
+            const int dy2 = ky2 * a.d_h, dx2 = kx2 * a.d_w, cbase2 = cb2 * CS;
+            const int shift = (dy * a.w + dx) * row_elems + cbase;
+            const int shift2 = (dy2 * a.w + dx2) * row_elems + cbase2;
+#pragma unroll
+            for (int ii = 0; ii < A_MINE; ++ii) {
+                const int i = ii * NPROD + pr;  // ii >= A_MINE / 2: i >= 8; ii >= A_MINE / 4: i >= 4
+                if (ii >= A_MINE / 2) {
+                    // K-block t + 1's weights, to the upper half of the slot's activation region
+                    dma16(a.wpack, a.w_bytes, two ? p_woff[ii - A_MINE / 2] : 0x80000000u,
+                          two ? unsigned(t + 1) * w_stage_bytes : 0u, a_base + buf * A_BYTES + i * 1024);
+                } else {
+                    const bool second = ii >= A_MINE / 4;
+                    const int ddy = second ? dy2 : dy, ddx = second ? dx2 : dx;
+                    const bool inside = ((unsigned)(p_iy[ii] + ddy) < (unsigned)a.h) &
+                                        ((unsigned)(p_ix[ii] + ddx) < (unsigned)a.w) &
+                                        ((second ? cbase2 : cbase) < p_cl[ii]) & (!second || two);
+                    const unsigned off = inside ? unsigned(p_off[ii] + (second ? shift2 : shift) * ES) : 0x80000000u;
+                    dma16(xt, x_bytes, off, 0u, a_base + buf * A_BYTES + i * 1024);
+                }
+            }
+            // the cursor one or two K-blocks on; the tail block is a
+            // work-group's last item, so its end only moves k past it
+            bool end = false;
+            for (int r = 0; r < (two ? 2 : 1); ++r) {
+                if (++cblk == a.n_cblk) {
+                    cblk = 0;
+                    if (++kx == a.k_w) {
+                        kx = 0;
+                        end = ++ky == a.k_h;
+                    }
+                }
+            }
+            if (end)
+                ++k;
+        };
         auto issue = [&](int g) {
             const int buf = g & (NBUF - 1);
+            if constexpr (TAIL2) {
+                if (k >= n_mine) {
+                    issue_tail2(buf);
+                    return;
+                }
+            }
             const int t = (ky * a.k_w + kx) * a.n_cblk + cblk;  // stage within the tile
 #pragma unroll
             for (int jj = 0; jj < B_MINE; ++jj) {
@@ -576,23 +668,7 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
                     *reinterpret_cast<u32x4 *>(a_lds + buf * A_BYTES + i * 1024 + lane * 16) = v;
                 }
             }
-            if (++cblk == a.n_cblk) {
-                cblk = 0;
-                if (++kx == a.k_w) {
-                    kx = 0;
-                    if (++ky == a.k_h) {
-                        ++k;
-                        if (k < n_items) {
-                            ky = 0;
-                            plan_tile(k, 0);
-                        } else if (tails && k == n_mine) {
-                            if (pr == 0)
-                                post_claim();
-                            pending = true;
-                        }
-                    }
-                }
-            }
+            advance();
         };
         // Waits until all but this producer's DMAs of the `later` most
         // recently issued stages have landed.
@@ -610,7 +686,7 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
         };
         // steps of the items known so far (claims add to them as the
         // cursor reaches the end of the tiles)
-        auto total = [&]() { return n_items * S; };
+        auto total = [&]() { return n_mine * S + (n_items - n_mine) * ST; };
         // prologue: steps 0..2; step 0 lands before the first barrier
         for (int g = 0; g < LOOKAHEAD && g < total(); ++g)
             issue(g);
@@ -948,6 +1024,46 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
         rd_ker(nb_, 1, wk[1]);
         tail_group(3, wk[3]);
         __builtin_amdgcn_sched_barrier(0);
+        slot = ns;
+    };
+    // TAIL2 tail step: the slot's K-block t (activation rows 0..31, the
+    // weight region) and, with `two`, K-block t + 1 (rows 32..63, weights in
+    // the activation region's upper half); every fragment is read after the
+    // previous step's barrier, the slot is free after this one's.
+    auto step_tail2 = [&](bool two) {
+        const int ns = slot + 1 == NBUF ? 0 : slot + 1;
+        const unsigned char *const ab = a_lds + unsigned(slot) * A_BYTES;
+        const unsigned char *const bb = b_lds + unsigned(slot) * B_BYTES;
+        u32x4 dv0;
+        if constexpr (DEFER)
+            dv0 = drain_read(d_next);
+        auto kblock = [&](const unsigned char *act, const unsigned char *ker) {
+            u32x4 x[4], w[4][NB];
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+                const int q = wm ^ m;
+                x[m] = *reinterpret_cast<const u32x4 *>(act + l32 * 128 + (((2 * q + khalf) ^ swz<8>(l32)) * 16));
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb)
+                    w[m][nb] = *reinterpret_cast<const u32x4 *>(ker + b_rd[0][m] + nb * 32 * CPQ * 16);
+            }
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+                const unsigned fl = ((kHamiltonNeg >> (4 * wm + (wm ^ m))) & 1u) ? Elem<T>::sign : 0u;
+                const u32x4 xs = x[m] ^ fl;
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb)
+                    mfma_step<T>(acc[0][nb][0], w[m][nb], xs);
+            }
+        };
+        kblock(ab, bb);
+        if (two)
+            kblock(ab + 32 * 128, ab + A_BYTES / 2);
+        if constexpr (DEFER) {
+            drain_store(d_next, dv0);
+            d_next = d_next < N_DRAIN ? d_next + 1 : N_DRAIN;
+        }
+        __syncthreads();
         slot = ns;
     };
     // One tile: its S steps, two per iteration (activation sets alternate);
@@ -1605,9 +1721,14 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
 #pragma unroll
                     for (int e = 0; e < 16; ++e)
                         acc[0][nb][0][e] = 0.0f;
-                // its first stage was read as a tile's
-                rd_act_tail(unsigned(slot) * A_BYTES, xa0);
-                run_tile_allp(step_tail);
+                if constexpr (TAIL2) {
+                    for (int st = 0; st < ST; ++st)
+                        step_tail2(2 * st + 1 < S);
+                } else {
+                    // its first stage was read as a tile's
+                    rd_act_tail(unsigned(slot) * A_BYTES, xa0);
+                    run_tile_allp(step_tail);
+                }
                 if (defer) {
                     for (; d_next < N_DRAIN; ++d_next)
                         drain_store(d_next, drain_read(d_next));
