@@ -97,9 +97,10 @@ struct KArgs {
     int m_tiles, n_tiles;
     // Work split of a persistent launch: the first full_tiles tiles are
     // dealt to the work-groups (full_tiles = m_tiles * n_tiles unless
-    // tail_blocks is non-zero).  tail_blocks (all-components waves, Hamilton
-    // form, one N-tile, full_tiles a multiple of the grid of at least one
-    // tile per work-group, tail_blocks <= grid): the 32-pixel blocks past
+    // tail_blocks is non-zero).  tail_blocks (the 64-channel all-components
+    // tile with DMA loads, Hamilton form, one N-tile, full_tiles a multiple
+    // of the grid of at least one tile and 8 steps per work-group,
+    // tail_blocks <= grid): the 32-pixel blocks past
     // those tiles; each work-group claims one once its tiles are nearly
     // done, so the first to get there take them, and its four waves then
     // compute one output component of the block each.  claim (tail_blocks >
@@ -341,8 +342,9 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
     constexpr int PER_STAGE = (A_INSTR + NPROD - 1) / NPROD + (B_INSTR + NPROD - 1) / NPROD;
     constexpr int LOOKAHEAD = 3;                // stages issued ahead of the one being read
     constexpr int N_MFMA = MB * NB * (ES == 2 ? 1 : 4);  // MFMA instructions per k-step
-    // Tail blocks of the 64-channel DMA tile (two producers) carry two
-    // K-blocks per ring slot: a tail stage fills only rows 0..31 of the slot's
+    // Tail blocks (see KArgs) are taken by the 64-channel DMA tile (two
+    // producers) only, and carry two K-blocks per ring slot: a tail stage
+    // fills only rows 0..31 of the slot's
     // activation region, so K-block t's activations go to rows 0..31, K-block
     // t+1's to rows 32..63 and K-block t+1's weights (laid out as in the
     // weight region) to the region's upper half, which the A instructions
@@ -416,7 +418,7 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
     if (n_mine == 0)
         return;  // the whole work-group leaves: no barrier is pending
     auto tile_of = [&](int k) { return x_lo + xslot + k * cnt_x; };
-    const bool tails = ALLP && FORM == kFormHamilton && a.tail_blocks > 0;
+    const bool tails = TAIL2 && a.tail_blocks > 0;
     // first pixel of tail block c
     auto tail_m0 = [&](int c) { return ((BM / WTM) * a.full_tiles + c) * WTM; };
     const int S = a.stages;
@@ -636,8 +638,7 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
             for (int ii = 0; ii < A_MINE; ++ii) {
                 const int i = ii * NPROD + pr;
                 const bool inside = ((unsigned)(p_iy[ii] + dy) < (unsigned)a.h) &
-                                    ((unsigned)(p_ix[ii] + dx) < (unsigned)a.w) & (cbase < p_cl[ii]) &
-                                    (k < n_mine || i < WTM / 8);
+                                    ((unsigned)(p_ix[ii] + dx) < (unsigned)a.w) & (cbase < p_cl[ii]);
                 if constexpr (VEC) {
                     const unsigned off = inside ? unsigned(p_off[ii] + shift * ES) : 0x80000000u;
                     dma16(xt, x_bytes, off, 0u, a_base + buf * A_BYTES + i * 1024);
@@ -979,53 +980,10 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
         __builtin_amdgcn_sched_barrier(0);
         slot = ns;
     };
-    // Tail block (ALLP, Hamilton form): the work-group's 32 pixels sit in
-    // rows 0..31 of the stage and wave wm computes output component p = wm
-    // alone, block (p, q = p xor m) of each kernel group m: activation set
-    // entry m holds input component p xor m, and t_flip[m] the sign of eq. 6
-    // for that block (a quarter of a tile's MFMAs per wave).
-    auto rd_act_tail = [&](unsigned off, u32x4 (&dst)[4][MB]) {
-#pragma unroll
-        for (int m = 0; m < 4; ++m) {
-            const int q = wm ^ m;
-            dst[m][0] = *reinterpret_cast<const u32x4 *>(a_lds + off + l32 * 128 +
-                                                        (((2 * q + khalf) ^ swz<8>(l32)) * 16));
-        }
-    };
-    auto step_tail = [&](const u32x4 (&cur)[4][MB], u32x4 (&nxt)[4][MB]) {
-        const int ns = (slot + 1) & (NBUF - 1);
-        const unsigned cb = unsigned(slot) * B_BYTES;
-        const unsigned na = unsigned(ns) * A_BYTES, nb_ = unsigned(ns) * B_BYTES;
-        auto tail_group = [&](int m, const u32x4 (&w)[NB]) {
-            const unsigned fl = ((kHamiltonNeg >> (4 * wm + (wm ^ m))) & 1u) ? Elem<T>::sign : 0u;
-            const u32x4 x = cur[m][0] ^ fl;
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb)
-                mfma_step<T>(acc[0][nb][0], w[nb], x);
-        };
-        u32x4 dv0;
-        if constexpr (DEFER)
-            dv0 = drain_read(d_next);
-        __builtin_amdgcn_sched_barrier(0);
-        rd_ker(cb, 2, wk[2]);
-        tail_group(0, wk[0]);
-        rd_ker(cb, 3, wk[3]);
-        tail_group(1, wk[1]);
-        __builtin_amdgcn_sched_barrier(0);
-        if constexpr (DEFER) {
-            drain_store(d_next, dv0);
-            d_next = d_next < N_DRAIN ? d_next + 1 : N_DRAIN;
-        }
-        __builtin_amdgcn_sched_barrier(0);
-        __syncthreads();
-        rd_act_tail(na, nxt);
-        rd_ker(nb_, 0, wk[0]);
-        tail_group(2, wk[2]);
-        rd_ker(nb_, 1, wk[1]);
-        tail_group(3, wk[3]);
-        __builtin_amdgcn_sched_barrier(0);
-        slot = ns;
-    };
+    // Tail block: the work-group's 32 pixels and wave wm computes output
+    // component p = wm alone, block (p, q = p xor m) of each kernel group m
+    // (a quarter of a tile's MFMAs per wave), with the sign of eq. 6 for that
+    // block.
     // TAIL2 tail step: the slot's K-block t (activation rows 0..31, the
     // weight region) and, with `two`, K-block t + 1 (rows 32..63, weights in
     // the activation region's upper half); every fragment is read after the
@@ -1707,7 +1665,7 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
     // pixels (all four waves read the same activation rows).  The claim was
     // posted before the producers' barrier of step n_mine * S - 4 and is
     // read here after the barrier of step n_mine * S - 1.
-    if constexpr (ALLP && FORM == kFormHamilton) {
+    if constexpr (TAIL2) {
         if (tails) {
             const unsigned v = __builtin_amdgcn_readfirstlane(
                 __hip_atomic_load(a.claim + 1 + bid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM));
@@ -1721,14 +1679,8 @@ __global__ __launch_bounds__(64 * (WAVES_M * WAVES_N + producer_waves<T, MB, NB,
 #pragma unroll
                     for (int e = 0; e < 16; ++e)
                         acc[0][nb][0][e] = 0.0f;
-                if constexpr (TAIL2) {
-                    for (int st = 0; st < ST; ++st)
-                        step_tail2(2 * st + 1 < S);
-                } else {
-                    // its first stage was read as a tile's
-                    rd_act_tail(unsigned(slot) * A_BYTES, xa0);
-                    run_tile_allp(step_tail);
-                }
+                for (int st = 0; st < ST; ++st)
+                    step_tail2(2 * st + 1 < S);
                 if (defer) {
                     for (; d_next < N_DRAIN; ++d_next)
                         drain_store(d_next, drain_read(d_next));
@@ -2218,7 +2170,7 @@ AxisPhase axis_phase(int k, int p, int s, int in, int r)
 // pass that interleaves the phases into dX.
 hipError_t backward_data_phases(const ConvGeom &g, DType dt, const void *dy, const void *w_r, const void *w_i,
                                 const void *w_j, const void *w_k, void *dx, void *wpack, void *stage,
-                                hipStream_t stream, bool sep)
+                                hipStream_t stream, bool sep, ConvClaim *claim)
 {
     const size_t es = dt == DType::BF16 ? 2 : 4;
     const int row = 4 * g.c_in;
@@ -2260,7 +2212,7 @@ hipError_t backward_data_phases(const ConvGeom &g, DType dt, const void *dy, con
                 return e;
             e = qconv2d_run(qconv2d_plan(t, dt, sep ? ConvForm::SeparableGradData : ConvForm::Hamilton), pg, t, dt,
                             dy, wp, nullptr, static_cast<unsigned char *>(stage) + size_t(off) * es, nullptr,
-                            nullptr, stream);
+                            nullptr, stream, false, claim);
             if (e != hipSuccess)
                 return e;
             pm.hp[ph] = ay.size;
@@ -2294,7 +2246,7 @@ hipError_t backward_data_phases(const ConvGeom &g, DType dt, const void *dy, con
 
 hipError_t qconv2d_backward_data_run(const ConvGeom &g, DType dt, const void *dy, const void *w_r, const void *w_i,
                                      const void *w_j, const void *w_k, void *dx, void *wpack, void *stage,
-                                     hipStream_t stream, bool sep)
+                                     hipStream_t stream, bool sep, ConvClaim *claim)
 {
     const ConvGeom t = qconv2d_grad_data_geom(g);
     if (t.p_h < 0 || t.p_w < 0 || t.h < 1 || t.w < 1)
@@ -2307,7 +2259,7 @@ hipError_t qconv2d_backward_data_run(const ConvGeom &g, DType dt, const void *dy
     if (e != hipSuccess)
         return e;
     if ((g.s_h != 1 || g.s_w != 1) && g.d_h == 1 && g.d_w == 1 && g.s_h * g.s_w <= kMaxPhases)
-        return backward_data_phases(g, dt, dy, w_r, w_i, w_j, w_k, dx, wpack, stage, stream, sep);
+        return backward_data_phases(g, dt, dy, w_r, w_i, w_j, w_k, dx, wpack, stage, stream, sep, claim);
     const void *z = dy;
     if (g.s_h != 1 || g.s_w != 1) {
         const int row = 4 * g.c_out;
@@ -2339,7 +2291,7 @@ hipError_t qconv2d_backward_data_run(const ConvGeom &g, DType dt, const void *dy
         z = stage;
     }
     return qconv2d_run(qconv2d_plan(t, dt, sep ? ConvForm::SeparableGradData : ConvForm::Hamilton), pg, t, dt, z,
-                       wpack, nullptr, dx, nullptr, nullptr, stream);
+                       wpack, nullptr, dx, nullptr, nullptr, stream, false, claim);
 }
 
 bool qconv2d_writes_stats(const ConvPlan &plan, const ConvGeom &g, DType dt)
@@ -2358,7 +2310,7 @@ size_t qconv2d_claim_bytes()
 
 hipError_t qconv2d_run(const ConvPlan &plan, const PackGeom &pg, const ConvGeom &g, DType dt,
                        const void *x, const void *wpack, const void *bias, void *out,
-                       float *stats, const ConvFold *fold, hipStream_t stream, bool poincare, const ConvClaim *claim)
+                       float *stats, const ConvFold *fold, hipStream_t stream, bool poincare, ConvClaim *claim)
 {
     if (plan.id < 0 || plan.id >= kNumKernels)
         return hipErrorInvalidValue;
@@ -2424,15 +2376,23 @@ hipError_t qconv2d_run(const ConvPlan &plan, const PackGeom &pg, const ConvGeom 
     a.full_tiles = int(tiles);
     a.tail_blocks = 0;
     a.claim = claim != nullptr ? claim->buf : nullptr;
-    // 1..65535: never the zero of a mailbox that was never written
-    a.epoch = claim != nullptr ? claim->epoch % 0xffffu + 1u : 0u;
-    if (k.allp && plan.n_tiles == 1 && a.claim != nullptr && blocks <= unsigned(kClaimMaxGroups)) {
+    // 1..65535: never the zero of a mailbox that was never written; each
+    // launch on the buffer takes the next tag
+    a.epoch = claim != nullptr ? claim->epoch++ % 0xffffu + 1u : 0u;
+    // Only the 64-channel tile with DMA loads takes them (two K-blocks per
+    // tail stage): on the 32-channel tile a tail block costs about two
+    // thirds of a tile and the claim then outweighs the gain (measured:
+    // the four phase convolutions of a 3x3 stride-2 input gradient 183 ->
+    // 191 us).
+    const bool tail_kernel = k.allp && k.bnc == 64 && !poincare && (g.c_in % epc) == 0;
+    if (tail_kernel && plan.n_tiles == 1 && a.claim != nullptr && blocks <= unsigned(kClaimMaxGroups)) {
         const long long blk = (a.m + 31) / 32;
         const long long full = blk / (4LL * blocks);
         const long long rest = blk - full * 4 * blocks;
-        // (at least 4 steps of tiles per work-group: the first claim then
-        // falls after the producers' first barrier)
-        if (full >= 1 && rest > 0 && rest <= blocks && full * a.stages >= 4) {
+        // (at least 8 steps of tiles per work-group: the first claim then
+        // falls after the producers' first barrier, and the tiles outweigh
+        // the claim)
+        if (full >= 1 && rest > 0 && rest <= blocks && full * a.stages >= 8) {
             a.full_tiles = int(full * blocks);
             a.tail_blocks = int(rest);
         }

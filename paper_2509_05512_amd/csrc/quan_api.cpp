@@ -114,9 +114,13 @@ int iqbn_flags(void *stream, unsigned **out)
 int conv_claim(void *stream, quan::ConvClaim *out)
 {
     void *p = nullptr;
-    if (int rc = workspace(stream, kConvClaim, quan::qconv2d_claim_bytes(), &p, &out->epoch))
+    unsigned uses = 0;
+    if (int rc = workspace(stream, kConvClaim, quan::qconv2d_claim_bytes(), &p, &uses))
         return rc;
     out->buf = static_cast<unsigned *>(p);
+    // each call's launches (up to 16 output phases of an input gradient)
+    // take tags from a range of their own
+    out->epoch = uses * 17u;
     return QUAN_OK;
 }
 
@@ -711,8 +715,11 @@ int backward_data(const char *name, bool sep, const void *dy, const void *w_r, c
         if (int rc = workspace(stream, kGradStage, sb, &stage))
             return rc;
     }
+    quan::ConvClaim claim{};
+    if (int rc = conv_claim(stream, &claim))
+        return rc;
     const hipError_t e = quan::qconv2d_backward_data_run(g, dt, dy, w_r, w_i, w_j, w_k, dx, wpack, stage,
-                                                         static_cast<hipStream_t>(stream), sep);
+                                                         static_cast<hipStream_t>(stream), sep, &claim);
     if (e != hipSuccess)
         return fail_hip(e, "backward data launch");
     return QUAN_OK;

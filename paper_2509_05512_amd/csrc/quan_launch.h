@@ -85,8 +85,8 @@ bool qconv2d_writes_stats(const ConvPlan &plan, const ConvGeom &g, DType dt);
 // `claim` (optional): buf, qconv2d_claim_bytes() of device memory, zero
 // before the first launch that uses it, which every launch leaves zero
 // again (the launches that use one buffer must not overlap: one buffer per
-// stream); epoch, a tag that differs between consecutive launches on the
-// buffer.  With it a layer whose last round of tiles would leave
+// stream); epoch, the tag of the next launch on the buffer, which each
+// launch advances.  With it a layer whose last round of tiles would leave
 // work-groups idle ends in 32-pixel tail blocks that the work-groups claim
 // as they finish; NULL: whole tiles only.
 struct ConvClaim {
@@ -96,7 +96,7 @@ struct ConvClaim {
 hipError_t qconv2d_run(const ConvPlan &plan, const PackGeom &pg, const ConvGeom &g, DType dt,
                        const void *x, const void *wpack, const void *bias, void *out,
                        float *stats, const ConvFold *fold, hipStream_t stream, bool poincare = false,
-                       const ConvClaim *claim = nullptr);
+                       ConvClaim *claim = nullptr);
 size_t qconv2d_claim_bytes();
 
 // The stem layer (g.c_in == 1, bf16) as its own kernel: rgb is the colour
@@ -122,7 +122,7 @@ ConvGeom qconv2d_grad_data_geom(const ConvGeom &g);
 size_t qconv2d_grad_data_stage_bytes(const ConvGeom &g, DType dt);
 hipError_t qconv2d_backward_data_run(const ConvGeom &g, DType dt, const void *dy, const void *w_r, const void *w_i,
                                      const void *w_j, const void *w_k, void *dx, void *wpack, void *stage,
-                                     hipStream_t stream, bool sep = false);
+                                     hipStream_t stream, bool sep = false, ConvClaim *claim = nullptr);
 
 // Weight and bias gradients of the Hamilton convolution for dL/dY = dy:
 // dw_r..dw_k [c_out][c_in][k_h][k_w] and db [4][c_out] (NULL: skipped), all

@@ -2,11 +2,14 @@
 round of 128-pixel tiles would leave work-groups idle: those layers end in
 32-pixel tail blocks, which the work-groups claim (one each, through a
 per-stream counter) as they finish their tiles, each wave computing one
-output component of the block.  With 256 compute units (one work-group
-each) a layer takes tail blocks when its 32-pixel blocks number at least
-4 x 256 and leave a remainder of 1..256 past a whole number of rounds; the
-cases below are sized for that (on another device they are plain parity
-cases).
+output component of the block, two K-blocks per ring slot.  With 256
+compute units (one work-group each) a layer takes tail blocks when it runs
+on the 64-channel tile with DMA loads (33..64 output channels, input
+channels a multiple of 8 in bf16), its 32-pixel blocks number at least
+4 x 256 and leave a remainder of 1..256 past a whole number of rounds, and
+each work-group's tiles hold at least 8 K steps; the cases below are sized
+for that, except those marked as whole tiles (on another device they are
+all plain parity cases).
 
 Every case is compared in full against the oracle: the bias epilogue (64-
 and 32-channel tiles, a channel count without whole 16-byte output chunks,
@@ -27,25 +30,28 @@ pytestmark = pytest.mark.gpu
 BF16 = torch.bfloat16
 
 
-def tail_blocks(pixels, work_groups=256):
-    """Tail blocks the launch takes for a layer of `pixels` output pixels
-    (the host's rule), for the case labels."""
+def tail_blocks(pixels, steps, work_groups=256):
+    """Tail blocks the launch takes for a layer of `pixels` output pixels and
+    `steps` K steps per tile on the 64-channel DMA tile (the host's rule),
+    for the case labels."""
     blk = -(-pixels // 32)
     full = blk // (4 * work_groups)
     rest = blk - 4 * work_groups * full
-    return rest if full >= 1 and 0 < rest <= work_groups else 0
+    return rest if full >= 1 and 0 < rest <= work_groups and full * steps >= 8 else 0
 
 
 # (N, Cin, Cout, H, W, k, stride, pad)
 CONV_CASES = [
-    (8, 16, 64, 66, 66, 3, 1, 1),     # 1089 blocks: 65 tail blocks
-    (8, 16, 32, 66, 66, 3, 1, 1),     # 32-channel tile
+    (8, 16, 64, 66, 66, 3, 1, 1),     # 1089 blocks: 65 tail blocks, nine K steps (odd: last step one K-block)
+    (8, 16, 32, 66, 66, 3, 1, 1),     # 32-channel tile: whole tiles
     (8, 16, 36, 66, 66, 3, 1, 1),     # c_out % 8 != 0: direct stores
     (8, 8, 64, 41, 100, 3, 1, 1),     # 1025 blocks: one tail block
-    (8, 64, 64, 64, 80, 1, 1, 0),     # 1280 blocks: a tail block per work-group; 1x1
+    (8, 16, 64, 64, 80, 3, 1, 1),     # 1280 blocks: a tail block per work-group
+    (8, 64, 64, 64, 80, 1, 1, 0),     # 1x1, four K steps per tile: whole tiles
     (8, 16, 64, 92, 92, 3, 1, 1),     # 2116 blocks: two full rounds, 68 tail blocks
     (8, 16, 64, 131, 131, 3, 2, 1),   # stride 2 to 66 x 66
     (8, 16, 64, 65, 67, 3, 1, 1),     # 34840 pixels: ragged last tail block
+    (8, 32, 64, 66, 66, 3, 1, 1),     # 18 K steps (even)
 ]
 
 
@@ -62,7 +68,9 @@ def _inputs(case, seed):
 def _label(case):
     N, Cin, Cout, H, W, k, s, p = case
     ho, wo = quan.conv_out_size(H, k, s, p, 1), quan.conv_out_size(W, k, s, p, 1)
-    return f"{case} tail_blocks={tail_blocks(N * ho * wo)}"
+    steps = k * k * -(-Cin // 16)
+    dma_64 = 32 < Cout <= 64 and Cin % 8 == 0
+    return f"{case} tail_blocks={tail_blocks(N * ho * wo, steps) if dma_64 else 0}"
 
 
 @pytest.mark.parametrize("case", CONV_CASES, ids=[str(c) for c in CONV_CASES])
@@ -141,9 +149,10 @@ def test_tail_blocks_inference(relu):
 def test_tail_blocks_poincare_stem():
     """A 5x5 stem of 64 quaternion channels (past the dedicated stem
     kernel's weight table, so the implicit-GEMM kernel with the map of eq. 4
-    in its loads runs it) on 8 images of 66 x 66: 65 tail blocks."""
+    in its loads runs it) on 8 images of 66 x 66, a size with a partial last
+    round: the stem variant (element loads) runs whole tiles."""
     N, H, W, Cout, k, p = 8, 66, 66, 64, 5, 2
-    say(f"tail blocks poincare stem tail_blocks={tail_blocks(N * H * W)}")
+    say("tail-sized poincare stem")
     rng = np.random.default_rng(5)
     rgb = torch.from_numpy(rng.uniform(0.0, 1.0, (N, 3, H, W)).astype(np.float32)).to(BF16)
     w = torch.from_numpy((rng.standard_normal((4, Cout, 1, k, k)) / np.sqrt(4 * k * k)).astype(np.float32)).to(BF16)
@@ -210,3 +219,35 @@ def test_tail_blocks_two_streams():
     assert_close(f64(o1.cpu()), r1, BF16, "stream 1, first")
     assert_close(f64(o2.cpu()), r2, BF16, "stream 2")
     assert_close(f64(o3.cpu()), r1, BF16, "stream 1, second")
+
+
+# (N, Cin, Cout, H, W, k, stride, pad) of the forward layer: input gradients
+# whose stride-1 convolutions (one per output phase of a strided layer) end
+# in tail blocks
+GRAD_CASES = [
+    (8, 16, 64, 132, 132, 3, 2, 1),   # four phases of 8 x 66 x 66 pixels into 16 channels: whole tiles
+    (8, 64, 32, 132, 132, 3, 2, 1),   # into 64 channels: the 2 x 2-tap phase (8 K steps) takes tail blocks
+    (8, 64, 16, 66, 66, 3, 1, 1),     # stride 1: one gradient convolution of 34848 pixels, tail blocks
+]
+
+
+@pytest.mark.parametrize("case", GRAD_CASES, ids=[str(c) for c in GRAD_CASES])
+def test_tail_blocks_input_gradient(case):
+    """quan_qconv2d_backward_data on layers whose gradient convolutions take
+    tail blocks, against the oracle's input gradient in full."""
+    N, Cin, Cout, H, W, k, s, p = case
+    say(f"tail blocks input gradient {case}")
+    rng = np.random.default_rng(sum(case))
+    Ho, Wo = quan.conv_out_size(H, k, s, p, 1), quan.conv_out_size(W, k, s, p, 1)
+    w = torch.from_numpy(rng.standard_normal((4, Cout, Cin, k, k), dtype=np.float32)
+                         / np.float32(np.sqrt(4 * Cin * k * k))).to(BF16)
+    dy = torch.from_numpy(rng.standard_normal((N, 4, Cout, Ho, Wo), dtype=np.float32)).to(BF16)
+    dev = torch.device("cuda:0")
+    dx = quan.empty_qmap(N, Cin, H, W, BF16, dev)
+    dx.fill_(float("nan"))
+    quan.quan_qconv2d_backward_data(quan.to_device_layout(dy.to(dev)), *[w[q].contiguous().to(dev) for q in range(4)],
+                                    (H, W), stride=s, pad=p, dx=dx)
+    torch.cuda.synchronize()
+    x0 = np.zeros((N, 4, Cin, H, W))
+    ref, _, _ = oracle.qconv2d_backward(x0, f64(w), f64(dy), s, p, 1)
+    assert_close(f64(dx.cpu()), ref, BF16, f"tail dX {case}")
