@@ -184,9 +184,12 @@ def time_separable_backward(layers, quan, steps):
     g = torch.Generator(device="cpu").manual_seed(7)
     grads = [quan.to_device_layout(torch.randn(tuple(ly["y"].shape), generator=g).to(ly["y"].dtype)
                                    .to(ly["y"].device)) for ly in layers]
-    e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    # events of every step, one synchronisation at the end: the host queues
+    # ahead, so no interval holds the host's own dispatch time
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps + 1)]
 
-    def once():
+    def once(e):
+        e[0].record()
         for ly, dy in zip(layers, grads):
             L = ly["spec"]
             quan.quan_qconv2d_separable_backward_data(dy, *ly["w"], (ly["x"].shape[3], ly["x"].shape[4]),
@@ -196,16 +199,13 @@ def time_separable_backward(layers, quan, steps):
             L = ly["spec"]
             quan.quan_qconv2d_separable_backward_weight(ly["x"], dy, (L.k, L.k), stride=L.stride, pad=L.pad,
                                                         dilation=L.dilation)
-    once()
-    torch.cuda.synchronize()
-    tot = [0.0, 0.0]
-    for _ in range(steps):
-        e[0].record()
-        once()
         e[2].record()
-        torch.cuda.synchronize()
-        tot[0] += e[0].elapsed_time(e[1]) * 1e3
-        tot[1] += e[1].elapsed_time(e[2]) * 1e3
+    once(evs[0])
+    torch.cuda.synchronize()
+    for s in range(steps):
+        once(evs[s + 1])
+    torch.cuda.synchronize()
+    tot = [sum(e[0].elapsed_time(e[1]) for e in evs[1:]) * 1e3, sum(e[1].elapsed_time(e[2]) for e in evs[1:]) * 1e3]
     return [t / steps for t in tot]
 
 
@@ -243,33 +243,32 @@ def time_backward(layers, quan, steps, eps):
     g = torch.Generator(device="cpu").manual_seed(6)
     grads = [quan.to_device_layout(torch.randn(tuple(ly["z"].shape), generator=g).to(ly["z"].dtype)
                                    .to(ly["z"].device)) for ly in layers]
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in layers]
+    # events of every step, one synchronisation at the end: the host queues
+    # ahead, so no interval holds the host's own dispatch time
+    evs = [[[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in layers] for _ in range(steps + 1)]
 
-    def once(record):
+    def once(step_evs):
         for li in reversed(range(len(layers))):
             ly, L = layers[li], layers[li]["spec"]
-            ev = evs[li]
-            if record:
-                ev[0].record()
+            ev = step_evs[li]
+            ev[0].record()
             dy, _, _ = quan.quan_iqbn_backward(ly["y"], grads[li], ly["mean"], ly["var"], ly["gamma"],
                                                y=ly["z"] if L.relu else None, eps=eps)
-            if record:
-                ev[1].record()
+            ev[1].record()
             quan.quan_qconv2d_backward_data(dy, *ly["w"], (ly["x"].shape[3], ly["x"].shape[4]), stride=L.stride,
                                             pad=L.pad, dilation=L.dilation)
-            if record:
-                ev[2].record()
+            ev[2].record()
             quan.quan_qconv2d_backward_weight(ly["x"], dy, (L.k, L.k), stride=L.stride, pad=L.pad,
                                               dilation=L.dilation)
-            if record:
-                ev[3].record()
-    once(False)
+            ev[3].record()
+    once(evs[0])
+    torch.cuda.synchronize()
+    for s in range(steps):
+        once(evs[s + 1])
     torch.cuda.synchronize()
     tot = [0.0, 0.0, 0.0]
-    for _ in range(steps):
-        once(True)
-        torch.cuda.synchronize()
-        for ev in evs:
+    for step_evs in evs[1:]:
+        for ev in step_evs:
             for i in range(3):
                 tot[i] += ev[i].elapsed_time(ev[i + 1]) * 1e3
     return [t / steps for t in tot]
@@ -646,7 +645,8 @@ def main():
         },
         "step": "per layer: pack the four kernels, then quan_qconv2d_iqbn_forward with "
                 "QUAN_STATS_AUTO (the plain convolution and the one-launch IQBN where the "
-                "tensor takes it, else IQBN statistics in the convolution's epilogue)",
+                "tensor takes it and holds at least 64 MiB, else IQBN statistics in the "
+                "convolution's epilogue)",
         "stats_epilogue_us_per_step": round(mode_ms["epilogue"] * 1e3, 3),
         "stats_pass_us_per_step": round(pass_ms * 1e3, 3),
         "inference_us_per_step": round(inference_ms * 1e3, 3),

@@ -316,9 +316,10 @@ enum quan_stats_mode {
  *           100 MB on MI355X), one launch that reads out once and writes it
  *           once; otherwise three launches that read it twice.
  *           QUAN_STATS_AUTO picks the pass where that one launch applies
- *           (measured on MI355X: 261 against 270 us for the 64 x 56 x 56,
- *           64-channel layer) and the epilogue elsewhere.  All modes are
- *           deterministic.
+ *           to a tensor of at least 64 MiB (measured on MI355X: 262.7
+ *           against 267.5 us for the 64 x 56 x 56, 64-channel layer's 103
+ *           MB; 52 MB layers are faster with the epilogue) and the epilogue
+ *           elsewhere.  All modes are deterministic.
  */
 QUAN_API int quan_qconv2d_iqbn_forward(const void *x, const void *packed, const void *bias,
                                        int32_t stride_h, int32_t stride_w,
