@@ -12,7 +12,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libquan.so")
-SOURCES = ["qconv2d_gfx950.hip", "qconv2d_wgrad_gfx950.hip", "stem_gfx950.hip", "iqbn_gfx950.hip",
+SOURCES = ["qconv2d_gfx950.hip", "qconv2d_pointwise_gfx950.hip", "qconv2d_wgrad_gfx950.hip", "stem_gfx950.hip", "iqbn_gfx950.hip",
            "poincare_gfx950.hip", "quan_noalloc.hip", "quan_api.cpp"]
 ARCH = "gfx950"
 

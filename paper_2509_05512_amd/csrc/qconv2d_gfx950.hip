@@ -45,6 +45,7 @@
 #include <mutex>
 #include <type_traits>
 
+#include "gfx950_dma.h"
 #include "quan_launch.h"
 
 namespace quan {
@@ -207,48 +208,6 @@ __device__ __forceinline__ void interleave_kstep()
     }
     if constexpr (NDSR > NMFMA * RPM)
         __builtin_amdgcn_sched_group_barrier(kSchedDsRead, NDSR - NMFMA * RPM, 0);
-}
-
-// Raw buffer resource over [base, base + bytes): loads past the end return
-// zero.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, unsigned bytes)
-{
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, 0x00020000);
-}
-
-// LDS address of a __shared__ pointer, as the 32-bit value M0 takes.
-__device__ __forceinline__ unsigned lds_addr(const void *p)
-{
-    return __builtin_amdgcn_readfirstlane(
-        (unsigned)(size_t)(const __attribute__((address_space(3))) void *)p);
-}
-
-// One 16-byte chunk per lane from byte offset voff + soff of the buffer
-// [base, base + bytes) straight into LDS at m0 + 16 * lane; offsets past the
-// end land as zeros.  The compiler does not see this load: the issuing wave
-// waits for it with s_waitcnt vmcnt, and no wave that issues these reads LDS
-// (an outstanding LDS DMA holds back the issuing wave's own LDS reads).  The
-// scalar operands go through readfirstlane so they sit in SGPRs even where
-// the compiler kept a copy in a VGPR.
-__device__ __forceinline__ void dma16(const void *base, unsigned bytes, unsigned voff, unsigned soff,
-                                      unsigned m0)
-{
-    const unsigned long long b = (unsigned long long)base;
-    const unsigned lo = __builtin_amdgcn_readfirstlane(unsigned(b));
-    const unsigned hi = __builtin_amdgcn_readfirstlane(unsigned(b >> 32));
-    const __amdgpu_buffer_rsrc_t rsrc =
-        make_rsrc((const void *)(((unsigned long long)hi << 32) | lo), __builtin_amdgcn_readfirstlane(bytes));
-    asm volatile("s_mov_b32 m0, %3\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds" ::"v"(voff),
-                 "s"(rsrc), "s"(__builtin_amdgcn_readfirstlane(soff)), "s"(__builtin_amdgcn_readfirstlane(m0))
-                 : "memory");
-}
-
-template <int N>
-__device__ __forceinline__ void wait_vmcnt()
-{
-    static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
-    // vmcnt[3:0] | expcnt (7) | lgkmcnt (15) | vmcnt[5:4]
-    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
 
 // One work-group: WAVES_M x WAVES_N compute waves, each MB x NB blocks of 32
@@ -2041,6 +2000,21 @@ ConvPlan qconv2d_plan(const ConvGeom &g, DType dt, ConvForm form)
 {
     const bool sep = form != ConvForm::Hamilton;
     const int64_t m = g.m();
+    if (form == ConvForm::Hamilton && qconv2d_pointwise_takes(g, dt)) {
+        // 1x1 layers stream through the pointwise kernel
+        ConvPlan p;
+        p.id = -1;
+        p.pointwise = true;
+        p.group_stages = qconv2d_pointwise_group_stages(m, device_cus());
+        p.bm = qconv2d_pointwise_stage_pixels();
+        p.bnc = g.c_out;
+        p.n_tiles = 1;
+        p.m_tiles = int((m + p.bm - 1) / p.bm);
+        p.stat_rows = p.bm * p.group_stages;
+        p.stat_tiles = int((m + p.stat_rows - 1) / p.stat_rows);
+        p.name = "bf16_pointwise";
+        return p;
+    }
     const int pk = dt == DType::BF16 ? 16 : 8;
     const int stages = g.k_h * g.k_w * ((g.c_in + pk - 1) / pk);
     int id = -1;
@@ -2064,6 +2038,8 @@ ConvPlan qconv2d_plan(const ConvGeom &g, DType dt, ConvForm form)
     const KernelEntry &k = kKernels[id];
     ConvPlan p;
     p.id = id;
+    p.pointwise = false;
+    p.group_stages = 0;
     p.bm = k.bm;
     p.bnc = k.bnc;
     p.n_tiles = (g.c_out + k.bnc - 1) / k.bnc;
@@ -2296,6 +2272,8 @@ hipError_t qconv2d_backward_data_run(const ConvGeom &g, DType dt, const void *dy
 
 bool qconv2d_writes_stats(const ConvPlan &plan, const ConvGeom &g, DType dt)
 {
+    if (plan.pointwise)
+        return qconv2d_pointwise_takes(g, dt);
     if (plan.id < 0 || plan.id >= kNumKernels)
         return false;
     const KernelEntry &k = kKernels[plan.id];
@@ -2312,6 +2290,12 @@ hipError_t qconv2d_run(const ConvPlan &plan, const PackGeom &pg, const ConvGeom 
                        const void *x, const void *wpack, const void *bias, void *out,
                        float *stats, const ConvFold *fold, hipStream_t stream, bool poincare, ConvClaim *claim)
 {
+    if (plan.pointwise) {
+        if (poincare)
+            return hipErrorInvalidValue;
+        return qconv2d_pointwise_run(g, pg, plan.group_stages, x, wpack, bias, out, stats, plan.stat_tiles, fold,
+                                     stream);
+    }
     if (plan.id < 0 || plan.id >= kNumKernels)
         return hipErrorInvalidValue;
     const KernelEntry &k = kKernels[plan.id];

@@ -46,6 +46,10 @@ struct ConvPlan {
     int stat_rows;       // output pixels per IQBN statistics partial
     int stat_tiles;      // statistics partials per column: ceil(m / stat_rows)
     const char *name;
+    // the pointwise streaming kernel (qconv2d_pointwise_run) instead of the
+    // implicit-GEMM kernel table: group_stages 32-pixel stages per work-group
+    bool pointwise;
+    int group_stages;
 };
 
 // What a convolution launch computes: the Hamilton product (eq. 5), the
@@ -98,6 +102,18 @@ hipError_t qconv2d_run(const ConvPlan &plan, const PackGeom &pg, const ConvGeom 
                        float *stats, const ConvFold *fold, hipStream_t stream, bool poincare = false,
                        ConvClaim *claim = nullptr);
 size_t qconv2d_claim_bytes();
+
+// The pointwise streaming kernel (1x1 kernel, no padding, any stride; bf16,
+// 32 or 64 input and output channels, input under 2 GiB): whether it takes
+// the layer; its stages per work-group on `cus` compute units; the launch
+// (stats with stat_tiles == the number of work-groups, one partial per
+// work-group run of 32 * group_stages pixels; or fold; or neither).
+bool qconv2d_pointwise_takes(const ConvGeom &g, DType dt);
+int qconv2d_pointwise_group_stages(int64_t m, int cus);
+int qconv2d_pointwise_stage_pixels();
+hipError_t qconv2d_pointwise_run(const ConvGeom &g, const PackGeom &pg, int group_stages, const void *x,
+                                 const void *wpack, const void *bias, void *out, float *stats, int stat_tiles,
+                                 const ConvFold *fold, hipStream_t stream);
 
 // The stem layer (g.c_in == 1, bf16) as its own kernel: rgb is the colour
 // planes [n][3][h][w], mapped to quaternions by eq. 4 as they are loaded;

@@ -14,9 +14,10 @@ all plain parity cases).
 Every case is compared in full against the oracle: the bias epilogue (64-
 and 32-channel tiles, a channel count without whole 16-byte output chunks,
 one tail block, a tail block for every work-group, two full rounds before
-the tail, stride 2, a 1x1 layer), the IQBN statistics gathered in the
-epilogue with a ragged last block, the folded inference epilogue, and the
-Poincare stem with the map in the kernel's loads."""
+the tail, stride 2, and a 1x1 layer, which the pointwise kernel takes), the
+IQBN statistics gathered in the epilogue with a ragged last block, the
+folded inference epilogue, and the Poincare stem with the map in the
+kernel's loads."""
 import numpy as np
 import pytest
 import torch
@@ -47,7 +48,7 @@ CONV_CASES = [
     (8, 16, 36, 66, 66, 3, 1, 1),     # c_out % 8 != 0: direct stores
     (8, 8, 64, 41, 100, 3, 1, 1),     # 1025 blocks: one tail block
     (8, 16, 64, 64, 80, 3, 1, 1),     # 1280 blocks: a tail block per work-group
-    (8, 64, 64, 64, 80, 1, 1, 0),     # 1x1, four K steps per tile: whole tiles
+    (8, 64, 64, 64, 80, 1, 1, 0),     # 1x1: the pointwise streaming kernel (no tail blocks)
     (8, 16, 64, 92, 92, 3, 1, 1),     # 2116 blocks: two full rounds, 68 tail blocks
     (8, 16, 64, 131, 131, 3, 2, 1),   # stride 2 to 66 x 66
     (8, 16, 64, 65, 67, 3, 1, 1),     # 34840 pixels: ragged last tail block
