@@ -50,24 +50,32 @@ OTHER_CONFIGS = ["detection_pair", "deep_stack"]
 # from rocprofv3 --pmc FETCH_SIZE and WRITE_SIZE runs of this benchmark, each
 # scaled by what the same counter reads for a 512 MiB device copy (FETCH x2.0,
 # WRITE x1.0); the runs are summarised in profiles/qconv2d_<workload>_hbm.md.
-# A figure is reported only while the kernel source is the one it was
-# measured on (sha256 prefix).
+# A figure is reported only while the kernel sources are the ones it was
+# measured on (sha256 prefix of the convolution sources, concatenated).
 CONV_TRAFFIC = {
     "imagenet_stage": {"bytes": 219475259, "kernel_sha256": "b910a265452d710e"},
     "detection_pair": {"bytes": 277185907, "kernel_sha256": "b910a265452d710e"},
     "deep_stack": {"bytes": 260089605, "kernel_sha256": "b910a265452d710e"},
 }
-CONV_SOURCE = os.path.join(ROOT, "paper_2509_05512_amd", "csrc", "qconv2d_gfx950.hip")
+CONV_SOURCES = [os.path.join(ROOT, "paper_2509_05512_amd", "csrc", f)
+                for f in ("qconv2d_gfx950.hip", "qconv2d_pointwise_gfx950.hip", "gfx950_dma.h")]
+
+
+def conv_source_sha():
+    """sha256 prefix of the convolution kernels' sources, concatenated."""
+    import hashlib
+    h = hashlib.sha256()
+    for path in CONV_SOURCES:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def conv_traffic(workload):
-    import hashlib
     entry = CONV_TRAFFIC.get(workload)
     if entry is None:
         return None
-    with open(CONV_SOURCE, "rb") as f:
-        sha = hashlib.sha256(f.read()).hexdigest()[:16]
-    return entry["bytes"] if sha == entry["kernel_sha256"] else None
+    return entry["bytes"] if conv_source_sha() == entry["kernel_sha256"] else None
 
 
 def parse_args():
@@ -401,9 +409,16 @@ def layer_records(wl, dims, conv_ms, iqbn_ms, cold_us, pack_ms=None):
              "h_out": d["ho"], "w_out": d["wo"]}
         if pack_ms is not None:
             r["pack_us"] = round(pack_ms[li] * 1e3, 3)
+        # the least HBM traffic of the layer: its input and output once, the
+        # four kernels once
+        conv_bytes = (wl.n * d["h"] * d["w"] * 4 * L.c_in + wl.n * d["ho"] * d["wo"] * 4 * L.c_out
+                      + 4 * L.c_out * L.c_in * L.k * L.k) * esz
+        conv_gbps = conv_bytes / (conv_ms[li] * 1e-3) / 1e9
         r.update({
             "qconv2d_us": round(conv_ms[li] * 1e3, 3), "qconv2d_tflops": round(tf, 2),
             "qconv2d_frac_mfma_peak": round(tf / peak, 4),
+            "qconv2d_algorithmic_gbps": round(conv_gbps, 1),
+            "qconv2d_frac_hbm_peak": round(conv_gbps / HBM_PEAK_GBPS, 4),
             "iqbn_cold_us": round(cold_us[li], 3),
             "iqbn_cold_gbps": round(nbytes / (cold_us[li] * 1e-6) / 1e9, 1),
             "iqbn_cold_frac_hbm_peak": round(nbytes / (cold_us[li] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),

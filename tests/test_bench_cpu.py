@@ -27,7 +27,7 @@ def test_traffic_only_for_the_profiled_source(tmp_path, monkeypatch):
     src = tmp_path / "kernel.hip"
     src.write_text("// one version\n")
     sha = hashlib.sha256(src.read_bytes()).hexdigest()[:16]
-    monkeypatch.setattr(bench, "CONV_SOURCE", str(src))
+    monkeypatch.setattr(bench, "CONV_SOURCES", [str(src)])
     monkeypatch.setattr(bench, "CONV_TRAFFIC", {"w": {"bytes": 123, "kernel_sha256": sha}})
     assert bench.conv_traffic("w") == 123
     assert bench.conv_traffic("other workload") is None
