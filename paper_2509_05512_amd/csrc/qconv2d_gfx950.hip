@@ -1723,6 +1723,58 @@ __global__ __launch_bounds__(256) void qconv2d_pack(const T *__restrict__ w0, co
 // Scatters dY [n][ho][wo][row] into the zero-filled z [n][hz][wz][row] at
 // rows and columns (oy * s_h, ox * s_w): the input of the input-gradient
 // convolution of a strided layer.  One thread per VW elements.
+// The forward pack of bf16 kernels whose input channels come in whole
+// 8-channel octets, TAPS taps: one thread per (channel block, kernel, output
+// row, octet).  The thread's source is 8 x TAPS consecutive elements
+// ([o][c..c+7][taps]), read as TAPS 16-byte pieces; it writes one 16-byte
+// piece per tap (the octet's 8 channels at that tap), consecutive threads
+// writing consecutive pieces.  Sources must be 16-byte aligned.
+template <int TAPS>
+__global__ __launch_bounds__(64) void qconv2d_pack_octets(const __bf16 *__restrict__ w0, const __bf16 *__restrict__ w1,
+                                                          const __bf16 *__restrict__ w2, const __bf16 *__restrict__ w3,
+                                                          __bf16 *__restrict__ wp, int c_in, int c_out, int n_cblk,
+                                                          int cout_pad, int threads)
+{
+    const int t = blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= threads)
+        return;
+    const int g = t & 1;
+    int r = t >> 1;
+    const int o = r % cout_pad;
+    r /= cout_pad;
+    const int ws = r & 3;
+    const int cblk = r >> 2;
+    const int c = cblk * 16 + 8 * g;
+    const __bf16 *src = ws == 0 ? w0 : ws == 1 ? w1 : ws == 2 ? w2 : w3;
+    unsigned d[4 * TAPS];
+    if (o < c_out && c < c_in) {
+        const u32x4 *p = reinterpret_cast<const u32x4 *>(src + (size_t(o) * c_in + c) * TAPS);
+#pragma unroll
+        for (int i = 0; i < TAPS; ++i) {
+            const u32x4 v = p[i];
+            d[4 * i + 0] = v[0];
+            d[4 * i + 1] = v[1];
+            d[4 * i + 2] = v[2];
+            d[4 * i + 3] = v[3];
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < 4 * TAPS; ++i)
+            d[i] = 0u;
+    }
+    // element e * TAPS + tap of the source is channel c + e at that tap
+    auto half = [&](int i) { return (d[i / 2] >> (16 * (i % 2))) & 0xffffu; };
+#pragma unroll
+    for (int tap = 0; tap < TAPS; ++tap) {
+        u32x4 v;
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            v[k] = half((2 * k) * TAPS + tap) | (half((2 * k + 1) * TAPS + tap) << 16);
+        *reinterpret_cast<u32x4 *>(wp + ((size_t(tap) * n_cblk + cblk) * 4 + ws) * cout_pad * 16 + size_t(o) * 16 +
+                                   8 * g) = v;
+    }
+}
+
 template <typename T, int VW>
 __global__ __launch_bounds__(256) void qconv2d_grad_dilate(const T *__restrict__ dy, T *__restrict__ z, int ho,
                                                            int wo, int hz, int wz, int s_h, int s_w, int row_vecs,
@@ -2061,6 +2113,22 @@ hipError_t pack_weights(const PackGeom &pg, int c_in, int c_out, int k_h, int k_
 {
     const int total = int(pg.bytes / (dt == DType::BF16 ? 2 : 4));
     const int blocks = (total + 255) / 256;
+    const bool aligned16 = ((reinterpret_cast<uintptr_t>(w_r) | reinterpret_cast<uintptr_t>(w_i) |
+                             reinterpret_cast<uintptr_t>(w_j) | reinterpret_cast<uintptr_t>(w_k)) & 15) == 0;
+    if (MODE == kPackForward && dt == DType::BF16 && c_in % 8 == 0 && aligned16 && pg.pk == 16 &&
+        (k_h * k_w == 9 || k_h * k_w == 1)) {
+        const int threads = pg.n_cblk * 4 * pg.cout_pad * 2;
+        const int b64 = (threads + 63) / 64;
+        if (k_h * k_w == 9)
+            hipLaunchKernelGGL((qconv2d_pack_octets<9>), dim3(b64), dim3(64), 0, stream, (const __bf16 *)w_r,
+                               (const __bf16 *)w_i, (const __bf16 *)w_j, (const __bf16 *)w_k, (__bf16 *)wpack, c_in,
+                               c_out, pg.n_cblk, pg.cout_pad, threads);
+        else
+            hipLaunchKernelGGL((qconv2d_pack_octets<1>), dim3(b64), dim3(64), 0, stream, (const __bf16 *)w_r,
+                               (const __bf16 *)w_i, (const __bf16 *)w_j, (const __bf16 *)w_k, (__bf16 *)wpack, c_in,
+                               c_out, pg.n_cblk, pg.cout_pad, threads);
+        return hipGetLastError();
+    }
     if (full_kh == 0) {
         full_kh = k_h;
         full_kw = k_w;
