@@ -4,9 +4,10 @@
 One step = one pass of the whole hot path over one batch of a workload: for
 every layer, pack the four real kernels, then the quaternion (Hamilton)
 convolution with IQBN (+ReLU where the layer has it) behind it
-(quan_qconv2d_iqbn_forward with the library's default statistics mode: the
-one-launch IQBN after the plain convolution where the tensor takes it, else
-per-tile statistics in the convolution's epilogue), through libquan's C ABI
+(quan_qconv2d_iqbn_forward with the library's default statistics mode: a
+separate IQBN pass after the plain convolution where the tensor takes the
+one-launch or the merged two-launch form, else per-tile statistics in the
+convolution's epilogue), through libquan's C ABI
 on torch's current stream.  Inputs are seeded synthetic tensors already
 resident in HBM when the timed region starts.  The same steps are then timed
 with each statistics mode forced (epilogue, separate pass) and in inference
@@ -659,9 +660,10 @@ def main():
             "useful_gflop_per_step": round(step_flops / 1e9, 3),
         },
         "step": "per layer: pack the four kernels, then quan_qconv2d_iqbn_forward with "
-                "QUAN_STATS_AUTO (the plain convolution and the one-launch IQBN where the "
-                "tensor takes it and holds at least 64 MiB, else IQBN statistics in the "
-                "convolution's epilogue)",
+                "QUAN_STATS_AUTO (the plain convolution and then IQBN in one launch where "
+                "the tensor takes it and holds at least 64 MiB, or in two launches with the "
+                "finalize merged into the normalization on tensors of up to 32 MiB with wide "
+                "rows; else IQBN statistics in the convolution's epilogue)",
         "stats_epilogue_us_per_step": round(mode_ms["epilogue"] * 1e3, 3),
         "stats_pass_us_per_step": round(pass_ms * 1e3, 3),
         "inference_us_per_step": round(inference_ms * 1e3, 3),

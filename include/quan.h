@@ -311,15 +311,20 @@ enum quan_stats_mode {
  *           them (fewer than 32 output channels, or c_out not a multiple of
  *           8 for bf16 / 4 for fp32) use the separate pass instead.
  *           QUAN_STATS_PASS runs the plain convolution and then
- *           quan_iqbn_forward's normalisation on out: on tensors of 16 MiB
- *           or more that one work-group per compute unit can hold (about
- *           100 MB on MI355X), one launch that reads out once and writes it
- *           once; otherwise three launches that read it twice.
- *           QUAN_STATS_AUTO picks the pass where that one launch applies
- *           to a tensor of at least 64 MiB (measured on MI355X: 262.7
- *           against 267.5 us for the 64 x 56 x 56, 64-channel layer's 103
- *           MB; 52 MB layers are faster with the epilogue) and the epilogue
- *           elsewhere.  All modes are deterministic.
+ *           quan_iqbn_forward's normalisation on out: on tensors of up to
+ *           32 MiB whose rows hold at least 193 reals (4 c_out), two
+ *           launches (statistics, then the normalisation with the finalize
+ *           merged in); on other tensors of 16 MiB or more that one
+ *           work-group per compute unit can hold (about 100 MB on MI355X),
+ *           one launch that reads out once and writes it once; otherwise
+ *           three launches that read it twice.
+ *           QUAN_STATS_AUTO picks the pass where it takes two launches, or
+ *           one launch on a tensor of at least 64 MiB (measured on MI355X:
+ *           133.0 against 137.3 us for the 32 x 14 x 14, 256-channel
+ *           layer's 12.8 MB; 262.7 against 267.5 us for the 64 x 56 x 56,
+ *           64-channel layer's 103 MB; 52 MB layers are faster with the
+ *           epilogue), and the epilogue elsewhere.  All modes are
+ *           deterministic.
  */
 QUAN_API int quan_qconv2d_iqbn_forward(const void *x, const void *packed, const void *bias,
                                        int32_t stride_h, int32_t stride_w,

@@ -20,6 +20,12 @@
 //                     column exact (a folded x * scale + shift would cancel
 //                     two terms of size |mean| * scale).
 //
+// Tensors of up to 32 MiB whose rows span at least four 64-column groups
+// take two launches instead: iqbn_stats over blocks of 64 columns (at most
+// 64 partials per column), then iqbn_merge_affine, which merges the partials
+// inside the normalization pass while its first loads of x are in flight.
+// Larger tensors take the one-launch form below where it fits.
+//
 // After a convolution that wrote per-tile statistics of its output (fused
 // into its epilogue), iqbn_finalize_tiles replaces passes 1 and 2: the
 // normalization then costs one read and one write of the tensor.
@@ -97,6 +103,66 @@ Layout make_layout(int64_t pixels, int c, int vw, int cap = kMaxBlocks)
     return l;
 }
 
+// Merged finalize and normalization, for tensors whose columns have few
+// statistics partials: the finalize step runs inside the normalization pass
+// instead of a launch of its own.  A block covers kMergeCols columns of a run
+// of rows; it issues the loads of its first rows, merges its columns'
+// partials in fp64 (a fixed order, the same in every block of the column
+// group) while those loads are in flight, and then normalises its rows.
+constexpr int kMergeCols = 64;
+constexpr int kMergeMaxParts = 64;                   // statistics blocks per column
+constexpr int kMergeSlices = kThreads / kMergeCols;  // merge threads per column
+constexpr int kMergeBlocks = 256;                    // target blocks per launch
+constexpr int64_t kMergeMaxBytes = int64_t(32) << 20;
+
+// Column-group layout of the merged path: kMergeCols columns per block,
+// blocks_x runs of rows per column group (grid (blocks, col_groups), so that
+// consecutive blocks, which the XCDs take in turn, stream different rows).
+Layout make_layout_narrow(int64_t pixels, int c, int vw, int blocks_x)
+{
+    Layout l;
+    l.pixels = pixels;
+    l.row_len = 4 * c;
+    l.vw = vw;
+    l.chunks = l.row_len / vw;
+    const int want_cg = kMergeCols / vw;
+    l.cg = l.chunks < want_cg ? l.chunks : want_cg;
+    l.rpi = kThreads / l.cg;
+    l.col_groups = (l.chunks + l.cg - 1) / l.cg;
+    if (blocks_x < 1)
+        blocks_x = 1;
+    l.rows_per_block = (pixels + blocks_x - 1) / blocks_x;
+    l.blocks = int((pixels + l.rows_per_block - 1) / l.rows_per_block);
+    return l;
+}
+
+// Row blocks per column group of the merged path: about kMergeBlocks blocks
+// in all, at most kMergeMaxParts, and at least one row per thread.
+int merge_blocks_x(int64_t pixels, int c, int vw)
+{
+    const Layout l = make_layout_narrow(pixels, c, vw, 1);
+    int64_t bx = (kMergeBlocks + l.col_groups - 1) / l.col_groups;
+    const int64_t by_rows = (pixels + l.rpi - 1) / l.rpi;
+    if (bx > by_rows)
+        bx = by_rows;
+    if (bx > kMergeMaxParts)
+        bx = kMergeMaxParts;
+    return bx < 1 ? 1 : int(bx);
+}
+
+// Whether IQBN takes the merged path: a tensor of at most kMergeMaxBytes
+// whose rows span at least four column groups (so the launch has enough
+// blocks).  Measured on MI355X, cold: 12.8 MB (6272 rows of 1024 columns)
+// 16.4 us against 23.4 for three launches; 25.7 MB 21.7 us against 27.7 for
+// the one-launch form; at 52 MB the one-launch form is ahead (35.0 against
+// 38.4 us with up to 128 partials per column), and at 103 MB (54.6 against
+// 63.0).
+bool merge_takes(int64_t pixels, int c, int vw, int elem)
+{
+    const Layout l = make_layout_narrow(pixels, c, vw, 1);
+    return pixels * l.row_len * elem <= kMergeMaxBytes && l.col_groups >= 4;
+}
+
 int vec_width(int c, DType dt)
 {
     const int epc = dt == DType::BF16 ? 8 : 4;
@@ -105,7 +171,7 @@ int vec_width(int c, DType dt)
 
 template <typename T, int VW>
 __global__ __launch_bounds__(kThreads) void iqbn_stats(const T *__restrict__ x, Layout l,
-                                                       float *__restrict__ part)
+                                                       float *__restrict__ part, float *__restrict__ kout)
 {
     __shared__ float red[2][kThreads][VW];
     const int tid = threadIdx.x;
@@ -174,15 +240,24 @@ __global__ __launch_bounds__(kThreads) void iqbn_stats(const T *__restrict__ x, 
                 t2[e] += red[1][j * l.cg + cl][e];
             }
         }
-        // Partials are column-major, [2][L][blocks]: the finalize pass reads
-        // one column's partials with consecutive lanes.
+        // Partials are column-major, [2][L][blocks], for iqbn_finalize (it
+        // reads one column's partials with consecutive lanes), or, with
+        // kout given, block-major, [2][blocks][L], for iqbn_merge_affine
+        // (consecutive lanes take consecutive columns).
         const size_t stride2 = size_t(l.row_len) * l.blocks;
 #pragma unroll
         for (int e = 0; e < VW; ++e) {
-            const size_t idx = size_t(col * VW + e) * l.blocks + blockIdx.x;
+            const size_t idx = kout != nullptr ? size_t(blockIdx.x) * l.row_len + col * VW + e
+                                               : size_t(col * VW + e) * l.blocks + blockIdx.x;
             part[idx] = t1[e];
             part[stride2 + idx] = t2[e];
         }
+        // the shifts K, for a finalize that cannot read x's row 0 (the
+        // merged pass normalises in place)
+        if (kout != nullptr && blockIdx.x == 0)
+#pragma unroll
+            for (int e = 0; e < VW; ++e)
+                kout[col * VW + e] = k[e];
     }
 }
 
@@ -415,6 +490,142 @@ __global__ __launch_bounds__(kThreads) void iqbn_affine(const T *x, T *out, Layo
     }
 }
 
+// The merged finalize + normalization (see kMergeCols), after iqbn_stats
+// with block-major partials: part[b][col] = s1 of block b, part[n_part][...]
+// the s2, then the shifts K (part + 2 L n_part).  Merge thread t takes
+// column t % kMergeCols (so a wave's loads are 64 consecutive floats) and
+// blocks t / kMergeCols + kMergeSlices i; the slices are added in slice
+// order, in fp64, the same in every block.  The blocks of row block 0 also
+// write mean and var.  In place (x == out) is allowed: a block reads and
+// writes only its own rows, and K comes from the partials.
+struct MergeArgs {
+    const float *part;
+    int n_part;
+    const float *gamma;
+    const float *beta;
+    float eps;
+    float *mean;
+    float *var;
+};
+
+template <typename T, int VW, bool RELU>
+__global__ __launch_bounds__(kThreads) void iqbn_merge_affine(const T *x, T *out, Layout l, MergeArgs a)
+{
+    constexpr int MP = kMergeMaxParts / kMergeSlices;
+    __shared__ double red[2][kMergeSlices][kMergeCols];
+    __shared__ float coef[3][kMergeCols];
+    const int tid = threadIdx.x;
+    const int cl = tid % l.cg, rl = tid / l.cg;
+    const int chunk = blockIdx.y * l.cg + cl;
+    const bool active = rl < l.rpi && chunk < l.chunks;
+    const int64_t r0 = int64_t(blockIdx.x) * l.rows_per_block;
+    int64_t r1 = r0 + l.rows_per_block;
+    if (r1 > l.pixels)
+        r1 = l.pixels;
+    const int64_t step = l.rpi;
+    const T *src = x + chunk * VW;
+    T *dst = out + chunk * VW;
+
+    // the block's first rows, in flight during the merge
+    int64_t r = r0 + rl;
+    Vec<T, VW> v[4];
+    if (active) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (r + u * step < r1)
+                v[u] = *reinterpret_cast<const Vec<T, VW> *>(src + (r + u * step) * l.row_len);
+    }
+
+    // merge: wave sl is slice sl (its branches are wave-uniform)
+    const int j = tid % kMergeCols, sl = tid / kMergeCols;
+    const int col0 = blockIdx.y * l.cg * VW;
+    const int col = col0 + j;
+    const bool mcol = j < l.cg * VW && col < l.row_len;
+    const int cc = mcol ? col : col0;
+    const size_t plane = size_t(a.n_part) * l.row_len;
+    float pv[MP], qv[MP];
+#pragma unroll
+    for (int i = 0; i < MP; ++i) {
+        const int b = sl + kMergeSlices * i;
+        pv[i] = 0.0f;
+        qv[i] = 0.0f;
+        if (b < a.n_part) {
+            pv[i] = a.part[size_t(b) * l.row_len + cc];
+            qv[i] = a.part[plane + size_t(b) * l.row_len + cc];
+        }
+    }
+    double s1 = 0.0, s2 = 0.0;
+#pragma unroll
+    for (int i = 0; i < MP; ++i) {
+        if (sl + kMergeSlices * i < a.n_part) {
+            s1 += double(pv[i]);
+            s2 += double(qv[i]);
+        }
+    }
+    red[0][sl][j] = s1;
+    red[1][sl][j] = s2;
+    __syncthreads();
+    if (sl == 0 && mcol) {
+        double t1 = 0.0, t2 = 0.0;
+#pragma unroll
+        for (int w = 0; w < kMergeSlices; ++w) {
+            t1 += red[0][w][j];
+            t2 += red[1][w][j];
+        }
+        const double n = double(l.pixels);
+        const double d = t1 / n;  // mean - K
+        double var = t2 / n - d * d;
+        if (var < 0.0)
+            var = 0.0;
+        const double mu = double(a.part[2 * plane + col]) + d;
+        const double sc = double(a.gamma[col]) / sqrt(var + double(a.eps));
+        coef[0][j] = float(mu);
+        coef[1][j] = float(sc);
+        coef[2][j] = a.beta[col];
+        if (blockIdx.x == 0) {
+            a.mean[col] = float(mu);
+            a.var[col] = float(var);
+        }
+    }
+    __syncthreads();
+    if (!active)
+        return;
+    float mu[VW], sc[VW], be[VW];
+#pragma unroll
+    for (int e = 0; e < VW; ++e) {
+        mu[e] = coef[0][cl * VW + e];
+        sc[e] = coef[1][cl * VW + e];
+        be[e] = coef[2][cl * VW + e];
+    }
+    auto norm = [&](const Vec<T, VW> &in) {
+        Vec<T, VW> o;
+#pragma unroll
+        for (int e = 0; e < VW; ++e) {
+            float y = fmaf(float(in.v[e]) - mu[e], sc[e], be[e]);
+            if (RELU)
+                y = fmaxf(y, 0.0f);
+            o.v[e] = T(y);
+        }
+        return o;
+    };
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+        if (r + u * step < r1)
+            store_stream(reinterpret_cast<Vec<T, VW> *>(dst + (r + u * step) * l.row_len), norm(v[u]));
+    r += 4 * step;
+    for (; r + 3 * step < r1; r += 4 * step) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            v[u] = *reinterpret_cast<const Vec<T, VW> *>(src + (r + u * step) * l.row_len);
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            store_stream(reinterpret_cast<Vec<T, VW> *>(dst + (r + u * step) * l.row_len), norm(v[u]));
+    }
+    for (; r < r1; r += step)
+        store_stream(reinterpret_cast<Vec<T, VW> *>(dst + r * l.row_len),
+                     norm(*reinterpret_cast<const Vec<T, VW> *>(src + r * l.row_len)));
+}
+
 // ------------------------ one-launch resident IQBN ------------------------
 // Where the tensor fits in the registers and LDS of one work-group per
 // compute unit (up to about 100 MB on 256 CUs), IQBN runs as ONE launch that
@@ -456,7 +667,8 @@ constexpr long kSpinLimit = 1L << 20;
 // Below 16 MiB the three launches are as fast (measured on MI355X: 12.8 MB
 // tensors take 21-24 us either way, 16.8 MB 22.1 against 23.7, 52 MB 34.4
 // against 37.7, 103 MB 54.6 against 59.4, cold), so only larger tensors rely
-// on all work-groups being resident together.
+// on all work-groups being resident together; up to 32 MiB the merged
+// two-launch form (merge_takes) is ahead where it applies.
 constexpr int64_t kResMinBytes = int64_t(16) << 20;
 
 typedef unsigned int res_u32x4 __attribute__((ext_vector_type(4)));
@@ -1156,12 +1368,27 @@ hipError_t launch_all(const void *x, const float *gamma, const float *beta, floa
                       void *out, float *mean, float *var, int64_t pixels, int c, void *work,
                       hipStream_t stream)
 {
-    const Layout l = make_layout(pixels, c, VW);
-    float *part = static_cast<float *>(work);
-    float *affine = part + size_t(l.blocks) * 2 * l.row_len;
     const T *xt = static_cast<const T *>(x);
+    float *part = static_cast<float *>(work);
+    if (merge_takes(pixels, c, VW, int(sizeof(T)))) {
+        // two launches: statistics, then the merged finalize + normalization
+        const Layout l = make_layout_narrow(pixels, c, VW, merge_blocks_x(pixels, c, VW));
+        const dim3 grid(l.blocks, l.col_groups);
+        hipLaunchKernelGGL((iqbn_stats<T, VW>), grid, dim3(kThreads), 0, stream, xt, l, part,
+                           part + size_t(l.blocks) * 2 * l.row_len);
+        const MergeArgs a = {part, l.blocks, gamma, beta, eps, mean, var};
+        if (relu)
+            hipLaunchKernelGGL((iqbn_merge_affine<T, VW, true>), grid, dim3(kThreads), 0, stream, xt,
+                               static_cast<T *>(out), l, a);
+        else
+            hipLaunchKernelGGL((iqbn_merge_affine<T, VW, false>), grid, dim3(kThreads), 0, stream, xt,
+                               static_cast<T *>(out), l, a);
+        return hipGetLastError();
+    }
+    const Layout l = make_layout(pixels, c, VW);
+    float *affine = part + size_t(l.blocks) * 2 * l.row_len;
     const dim3 grid(l.blocks, l.col_groups);
-    hipLaunchKernelGGL((iqbn_stats<T, VW>), grid, dim3(kThreads), 0, stream, xt, l, part);
+    hipLaunchKernelGGL((iqbn_stats<T, VW>), grid, dim3(kThreads), 0, stream, xt, l, part, nullptr);
     const int fin_blocks = (l.row_len + kThreads / 64 - 1) / (kThreads / 64);
     hipLaunchKernelGGL((iqbn_finalize<T>), dim3(fin_blocks), dim3(kThreads), 0, stream, xt, l, part,
                        gamma, beta, eps, mean, var, affine);
@@ -1257,10 +1484,15 @@ hipError_t iqbn_from_tiles_run(const float *part, int m_tiles, int tile_rows, co
                                        pixels, c, affine, stream);
 }
 
+bool iqbn_merged(int64_t pixels, int c, DType dt)
+{
+    return merge_takes(pixels, c, vec_width(c, dt), dt == DType::BF16 ? 2 : 4);
+}
+
 bool iqbn_one_launch(int64_t pixels, int c, DType dt)
 {
     ResPlan rp;
-    return resident_plan(pixels, c, dt, &rp);
+    return !merge_takes(pixels, c, vec_width(c, dt), dt == DType::BF16 ? 2 : 4) && resident_plan(pixels, c, dt, &rp);
 }
 
 size_t iqbn_barrier_bytes()
@@ -1284,6 +1516,11 @@ size_t iqbn_workspace_bytes(int64_t pixels, int c)
         const size_t b = (size_t(l.blocks) * 2 + 3) * size_t(l.row_len) * sizeof(float);
         if (b > best)
             best = b;
+        // the merged path: partials and the shifts K
+        const Layout ln = make_layout_narrow(pixels, c, vw, merge_blocks_x(pixels, c, vw));
+        const size_t bn = (size_t(ln.blocks) * 2 + 1) * size_t(ln.row_len) * sizeof(float);
+        if (bn > best)
+            best = bn;
     }
     return best;
 }
@@ -1312,12 +1549,13 @@ hipError_t iqbn_run(const void *x, const float *gamma, const float *beta, float 
                     unsigned *flags, hipStream_t stream)
 {
     ResPlan rp;
-    if (flags != nullptr && resident_plan(pixels, c, dt, &rp))
+    const int vw = vec_width(c, dt);
+    const bool merged = merge_takes(pixels, c, vw, dt == DType::BF16 ? 2 : 4);
+    if (!merged && flags != nullptr && resident_plan(pixels, c, dt, &rp))
         return dt == DType::BF16 ? launch_resident<__bf16>(rp, x, gamma, beta, eps, relu, out, mean, var, pixels,
                                                            c, work, flags, stream)
                                  : launch_resident<float>(rp, x, gamma, beta, eps, relu, out, mean, var, pixels, c,
                                                           work, flags, stream);
-    const int vw = vec_width(c, dt);
     if (dt == DType::BF16) {
         if (vw == 8)
             return launch_all<__bf16, 8>(x, gamma, beta, eps, relu, out, mean, var, pixels, c, work, stream);

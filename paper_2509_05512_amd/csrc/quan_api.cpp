@@ -519,17 +519,18 @@ QUAN_API int quan_qconv2d_iqbn_forward(const void *x, const void *packed, const 
     if (int rc = conv_claim(stream, &claim))
         return rc;
     hipError_t e;
-    // AUTO: a one-launch IQBN pass after the plain convolution where the
-    // tensor takes it and is large enough for its fixed cost (two grid
+    // AUTO: an IQBN pass after the plain convolution where the tensor takes
+    // the one-launch form and is large enough for its fixed cost (two grid
     // barriers and a merge) to matter less than the epilogue's statistics
-    // work, else the epilogue.  Measured per step on MI355X: 103 MB tensors
-    // (64 x 56 x 56, 64 channels) 262.7 us with the pass against 267.5 with
-    // the epilogue; 52 MB (16 x 80 x 80, 64 channels, two layers) 162.3
-    // against 160.1.
+    // work, or takes the merged two-launch form; else the epilogue.
+    // Measured per layer on MI355X: 103 MB tensors (64 x 56 x 56, 64
+    // channels) 262.7 us with the pass against 267.5 with the epilogue; 52 MB
+    // (16 x 80 x 80, 64 channels, two layers) 162.3 against 160.1; 12.8 MB
+    // (32 x 14 x 14, 256 channels, merged form) 133.0 against 137.3.
     constexpr int64_t kPassMinBytes = int64_t(64) << 20;
     const bool big = pixels * 4 * c_out * int64_t(elem_size(dtype)) >= kPassMinBytes;
-    const bool epilogue = stats == QUAN_STATS_EPILOGUE ||
-                          (stats == QUAN_STATS_AUTO && !(big && quan::iqbn_one_launch(pixels, c_out, dt)));
+    const bool pass = (big && quan::iqbn_one_launch(pixels, c_out, dt)) || quan::iqbn_merged(pixels, c_out, dt);
+    const bool epilogue = stats == QUAN_STATS_EPILOGUE || (stats == QUAN_STATS_AUTO && !pass);
     if (epilogue && quan::qconv2d_writes_stats(plan, g, dt)) {
         // statistics gathered in the convolution's epilogue
         if (int rc = workspace(stream, kIqbnPartials, quan::iqbn_tile_stats_bytes(plan.stat_tiles, c_out), &work))

@@ -170,6 +170,9 @@ size_t iqbn_barrier_bytes();
 // Whether iqbn_run (given flags) normalises this tensor in one launch that
 // reads it once, on the current device.
 bool iqbn_one_launch(int64_t pixels, int c, DType dt);
+// Whether iqbn_run takes two launches with the finalize merged into the
+// normalization (small tensors with wide rows).
+bool iqbn_merged(int64_t pixels, int c, DType dt);
 hipError_t iqbn_run(const void *x, const float *gamma, const float *beta, float eps, bool relu,
                     void *out, float *mean, float *var, int64_t pixels, int c, DType dt,
                     void *work, unsigned *flags, hipStream_t stream);

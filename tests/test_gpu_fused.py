@@ -33,6 +33,8 @@ CASES = [
     (2, 8, 16, 9, 9, 3, 1, 1, True, "bf16"),       # 16 channels: separate IQBN passes
     (2, 8, 36, 6, 6, 3, 1, 1, False, "bf16"),      # c_out % 8 != 0: separate passes
     (2, 4, 4, 16, 16, 3, 1, 1, False, "fp32"),     # fp32: separate passes
+    (2, 16, 64, 64, 64, 3, 1, 1, True, "bf16"),    # 256 statistics runs of 32 rows; pass: merged finalize
+    (1, 16, 64, 65, 63, 3, 1, 1, False, "bf16"),   # 4095 rows: a ragged last statistics run
 ]
 
 

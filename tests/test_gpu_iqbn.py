@@ -26,6 +26,8 @@ SHAPES = [
     (64, 8, 32, 16),       # many rows, many blocks
     (32, 256, 14, 14),     # the deep-stack layer
     (64, 16, 32, 32),      # 86 statistics blocks per column group
+    (2, 65, 5, 7),         # 4C = 260: bf16 scalar columns in 64-column groups, a short last group
+    (16, 64, 24, 20),      # 256 columns, 7680 rows: 8 row blocks of the merged normalization
 ]
 
 
@@ -79,11 +81,14 @@ def test_iqbn_large_offset_does_not_cancel(dtype):
     assert_close(f64(out), ref, dt, "out")
 
 
+@pytest.mark.parametrize("shape", [(3, 16, 10, 10), (4, 96, 9, 10)], ids=str)
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
-def test_iqbn_in_place(dtype):
-    say(f"iqbn in-place {dtype}")
+def test_iqbn_in_place(dtype, shape):
+    """In place, with the finalize in its own launch (16 channels) and merged
+    into the normalization (96 channels: six 64-column groups)."""
+    say(f"iqbn in-place {dtype} {shape}")
     dt = DT[dtype]
-    x, g, b = _case((3, 16, 10, 10), dt, seed=4)
+    x, g, b = _case(shape, dt, seed=4)
     out, mean, var = _run(x, g, b, 1e-5, True, inplace=True)
     ref, _, _ = oracle.iqbn(f64(x), f64(g), f64(b), 1e-5, True)
     assert_close(f64(out), ref, dt, "in-place out")
@@ -146,21 +151,22 @@ def test_iqbn_repeated_calls_reuse_counters():
                 assert torch.equal(first[0], out.cpu()) and torch.equal(first[2], var.cpu())
 
 
-# ---- the one-launch form (tensors of 16 MiB and more that fit the registers
-# and LDS of one work-group per compute unit) --------------------------------
+# ---- the one-launch form (tensors that fit the registers and LDS of one
+# work-group per compute unit: above 32 MiB, or from 16 MiB where the rows
+# span fewer than four 64-column groups) -------------------------------------
 
 def _cus():
     return torch.cuda.get_device_properties(0).multi_processor_count
 
 
-# (N, C, H, W), dtype, relu: 16 MiB and up; narrow rows (8 chunks), 256-byte
-# rows with 32 and 64 chunks, 4 KB and 8 KB rows (several columns merged per
-# work-group), the detection-pair layer and the full ImageNet-stage layer
+# (N, C, H, W), dtype, relu: narrow rows (8 chunks, 16 MiB), 512-byte and
+# 1 KB rows (32 and 64 chunks), 4 KB and 8 KB rows (several columns merged
+# per work-group), the detection-pair layer and the full ImageNet-stage layer
 RESIDENT = [
     ((128, 16, 32, 32), "bf16", True),
-    ((32, 64, 32, 32), "bf16", False),
-    ((16, 64, 32, 32), "fp32", True),
-    ((4, 512, 32, 32), "bf16", False),
+    ((64, 64, 32, 32), "bf16", False),
+    ((32, 64, 32, 32), "fp32", True),
+    ((8, 512, 32, 32), "bf16", False),
     ((2, 1024, 32, 64), "bf16", True),
     ((16, 64, 80, 80), "bf16", False),
     ((64, 64, 56, 56), "bf16", True),
@@ -172,6 +178,27 @@ def test_iqbn_one_launch_matches_oracle(shape, dtype, relu):
     say(f"iqbn one-launch {dtype} {shape} relu={relu}")
     dt = DT[dtype]
     x, g, b = _case(shape, dt, seed=sum(shape) + 5)
+    out, mean, var = _run(x, g, b, 1e-5, relu)
+    ref, rmean, rvar = oracle.iqbn(f64(x), f64(g), f64(b), 1e-5, relu)
+    assert_close(f64(mean), rmean, dt, "mean")
+    assert_close(f64(var), rvar, dt, "var")
+    assert_close(f64(out), ref, dt, "out")
+
+
+# 16 MiB tensors with four or more 64-column groups: the merged two-launch
+# form (statistics, then the finalize merged into the normalization)
+MERGED = [
+    ((32, 64, 32, 32), "bf16", False),
+    ((16, 64, 32, 32), "fp32", True),
+    ((4, 512, 32, 32), "bf16", True),
+]
+
+
+@pytest.mark.parametrize("shape,dtype,relu", MERGED, ids=[f"{s}-{d}-relu{int(r)}" for s, d, r in MERGED])
+def test_iqbn_merged_16mib_matches_oracle(shape, dtype, relu):
+    say(f"iqbn merged {dtype} {shape} relu={relu}")
+    dt = DT[dtype]
+    x, g, b = _case(shape, dt, seed=sum(shape) + 6)
     out, mean, var = _run(x, g, b, 1e-5, relu)
     ref, rmean, rvar = oracle.iqbn(f64(x), f64(g), f64(b), 1e-5, relu)
     assert_close(f64(mean), rmean, dt, "mean")
@@ -200,7 +227,7 @@ def test_iqbn_one_launch_in_place_and_repeatable(dtype):
     advance by two per call)."""
     say(f"iqbn one-launch in-place {dtype}")
     dt = DT[dtype]
-    x, g, b = _case((32, 64, 32, 32), dt, seed=91)
+    x, g, b = _case((64, 64, 32, 32), dt, seed=91)
     o1, m1, v1 = _run(x, g, b, 1e-5, True, inplace=True)
     ref, rmean, rvar = oracle.iqbn(f64(x), f64(g), f64(b), 1e-5, True)
     assert_close(f64(o1), ref, dt, "in-place out")
