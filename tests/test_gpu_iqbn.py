@@ -105,11 +105,15 @@ def test_iqbn_constant_input_gives_beta():
     assert torch.allclose(out.cpu(), b[None, :, :, None, None].expand(2, 4, 6, 5, 5), atol=1e-6)
 
 
+@pytest.mark.parametrize("shape", [(16, 32, 14, 14), (16, 64, 14, 14)], ids=str)
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
-def test_iqbn_deterministic(dtype):
-    say(f"iqbn determinism {dtype}")
+def test_iqbn_deterministic(dtype, shape):
+    """Bit-identical across calls: three launches (128 columns) and the
+    merged two launches (256 columns: every block of a column group merges
+    the partials itself, in one fixed order)."""
+    say(f"iqbn determinism {dtype} {shape}")
     dt = DT[dtype]
-    x, g, b = _case((16, 32, 14, 14), dt, seed=8)
+    x, g, b = _case(shape, dt, seed=8)
     o1, m1, v1 = _run(x, g, b, 1e-5, False)
     o2, m2, v2 = _run(x, g, b, 1e-5, False)
     assert torch.equal(o1.cpu(), o2.cpu()) and torch.equal(m1.cpu(), m2.cpu()) \
